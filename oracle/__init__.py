@@ -1,0 +1,175 @@
+"""Python access to the CPU oracle of the masked MoE layer (fp64).
+
+TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the benchmark's
+CPU-baseline leg use this package; the product package never imports it.
+The arithmetic lives in ``flexmoe_oracle.c`` (plain C, fp64 accumulation);
+this module only marshals NumPy arrays.  See that file's header for what is
+computed and which passages of the paper each function follows.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "flexmoe_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+# A test that checks the pins against deliberately broken copies of the
+# oracle points this at such a copy (built in a temporary directory).
+_LIB_OVERRIDE = os.environ.get("FLEXMOE_ORACLE_LIB")
+
+F32 = 0
+BF16 = 1
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with gcc (OpenMP over independent tokens/rows)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-Wall",
+               "-o", tmp, _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if _LIB_OVERRIDE:
+            L = ctypes.CDLL(_LIB_OVERRIDE)
+        else:
+            if not os.path.exists(_LIB):
+                build()
+            L = ctypes.CDLL(_LIB)
+        p = ctypes.c_void_p
+        i = ctypes.c_int
+        L.oracle_route.argtypes = [i, i, i, p, i, p, p]
+        L.oracle_dispatch.argtypes = [i, i, i, p, p, p, p, p, p]
+        L.oracle_layer_forward.argtypes = [i] * 8 + [p] * 16
+        L.oracle_rank_reorder.argtypes = [i, i, i, i] + [p] * 8
+        L.oracle_keep_from_ratio.argtypes = [ctypes.c_double, i]
+        for f in (L.oracle_route, L.oracle_dispatch, L.oracle_layer_forward,
+                  L.oracle_rank_reorder, L.oracle_keep_from_ratio):
+            f.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _ptr(a: Optional[np.ndarray]):
+    if a is None:
+        return None
+    assert a.flags["C_CONTIGUOUS"]
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _dtype_of(a: np.ndarray) -> int:
+    if a.dtype == np.float32:
+        return F32
+    if a.dtype == np.uint16:
+        return BF16
+    raise TypeError("x / weights must be float32 or uint16 (bf16 bits), got %s" % a.dtype)
+
+
+def route(logits: np.ndarray, k: int, norm_topk: int):
+    """Top-k expert ids [T][k] (int32) and router weights [T][k] (fp64)."""
+    logits = np.ascontiguousarray(logits, dtype=np.float32)
+    T, E = logits.shape
+    idx = np.empty((T, k), dtype=np.int32)
+    w = np.empty((T, k), dtype=np.float64)
+    rc = lib().oracle_route(T, E, k, _ptr(logits), int(norm_topk), _ptr(idx), _ptr(w))
+    if rc != 0:
+        raise ValueError("oracle_route failed (%d)" % rc)
+    return idx, w
+
+
+def dispatch(idx: np.ndarray, keep: np.ndarray, E: int):
+    """counts [E], offsets [E+1], perm [P], pos [T*k]."""
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    keep = np.ascontiguousarray(keep, dtype=np.int32)
+    T, k = idx.shape
+    counts = np.empty(E, dtype=np.int32)
+    offsets = np.empty(E + 1, dtype=np.int32)
+    perm = np.empty(T * k, dtype=np.int32)
+    pos = np.empty(T * k, dtype=np.int32)
+    P = lib().oracle_dispatch(T, E, k, _ptr(idx), _ptr(keep), _ptr(counts), _ptr(offsets),
+                              _ptr(perm), _ptr(pos))
+    if P < 0:
+        raise ValueError("oracle_dispatch failed")
+    return counts, offsets, perm[:P].copy(), pos
+
+
+def layer_forward(x, logits, w_gate, w_up, w_down, keep, top_k, norm_topk,
+                  ws_gate=None, ws_up=None, ws_down=None, want_route=False):
+    """Masked MoE layer: y [T][d] fp64 (unrounded).
+
+    x [T][d]; logits [T][E] fp32; w_gate/w_up [E][I][d]; w_down [E][d][I];
+    keep [E] int32; shared weights [I_s][d], [I_s][d], [d][I_s] or None.
+    x and weights are float32 or uint16 bf16 bits (all the same type).
+    """
+    x = np.ascontiguousarray(x)
+    dtype = _dtype_of(x)
+    logits = np.ascontiguousarray(logits, dtype=np.float32)
+    T, d = x.shape
+    E, I, d2 = w_gate.shape
+    assert d2 == d and logits.shape == (T, E)
+    for a in (w_gate, w_up, w_down):
+        assert _dtype_of(a) == dtype
+    assert w_down.shape == (E, d, I)
+    I_s = 0
+    if ws_gate is not None:
+        I_s = ws_gate.shape[0]
+        assert ws_up.shape == (I_s, d) and ws_down.shape == (d, I_s)
+    keep = np.ascontiguousarray(keep, dtype=np.int32)
+    y = np.empty((T, d), dtype=np.float64)
+    A = T * top_k
+    idx = np.empty((T, top_k), dtype=np.int32)
+    w = np.empty((T, top_k), dtype=np.float64)
+    counts = np.empty(E, dtype=np.int32)
+    offsets = np.empty(E + 1, dtype=np.int32)
+    perm = np.empty(max(A, 1), dtype=np.int32)
+    pos = np.empty(max(A, 1), dtype=np.int32)
+    rc = lib().oracle_layer_forward(
+        T, d, E, I, top_k, I_s, dtype, int(norm_topk), _ptr(x), _ptr(logits),
+        _ptr(np.ascontiguousarray(w_gate)), _ptr(np.ascontiguousarray(w_up)),
+        _ptr(np.ascontiguousarray(w_down)), _ptr(keep),
+        _ptr(None if ws_gate is None else np.ascontiguousarray(ws_gate)),
+        _ptr(None if ws_up is None else np.ascontiguousarray(ws_up)),
+        _ptr(None if ws_down is None else np.ascontiguousarray(ws_down)),
+        _ptr(y), _ptr(idx), _ptr(w), _ptr(counts), _ptr(offsets), _ptr(perm), _ptr(pos))
+    if rc != 0:
+        raise ValueError("oracle_layer_forward failed (%d)" % rc)
+    if not want_route:
+        return y
+    P = int(offsets[E]) if T > 0 else 0
+    return y, dict(idx=idx, w=w, counts=counts, offsets=offsets, perm=perm[:P].copy(),
+                   pos=pos[:A].copy())
+
+
+def rank_reorder(scores, w_gate, w_up, w_down):
+    """Eq. 3 reorder: returns (w_gate_r, w_up_r, w_down_r, perm [E][I])."""
+    scores = np.ascontiguousarray(scores, dtype=np.float32)
+    E, I = scores.shape
+    dtype = _dtype_of(w_gate)
+    d = w_gate.shape[2]
+    wg_r = np.empty_like(w_gate)
+    wu_r = np.empty_like(w_up)
+    wd_r = np.empty_like(w_down)
+    perm = np.empty((E, I), dtype=np.int32)
+    rc = lib().oracle_rank_reorder(E, I, d, dtype, _ptr(scores), _ptr(np.ascontiguousarray(w_gate)),
+                                   _ptr(np.ascontiguousarray(w_up)), _ptr(np.ascontiguousarray(w_down)),
+                                   _ptr(wg_r), _ptr(wu_r), _ptr(wd_r), _ptr(perm))
+    if rc != 0:
+        raise ValueError("oracle_rank_reorder failed (%d)" % rc)
+    return wg_r, wu_r, wd_r, perm
+
+
+def keep_from_ratio(r: float, I: int) -> int:
+    return int(lib().oracle_keep_from_ratio(float(r), int(I)))

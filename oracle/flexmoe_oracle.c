@@ -1,0 +1,361 @@
+/*
+ * CPU oracle for the prefix-masked MoE layer forward of FlexMoE.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the checker: the parity tests, the
+ * smoke check and the CPU-baseline leg of the benchmark call it; the product
+ * library never links it, includes it or calls it.  It shares no code with the
+ * GPU path.  Everything is plain, slow and written to be checked by eye
+ * against the paper: fp64 accumulation, one loop per sum, no blocking.
+ *
+ * What is computed (paper, Sec. 3 and App. C):
+ *   - the expert FFN  FFN(h) = W_down (phi(W_gate h) * W_up h), phi = SiLU (Eq. 1);
+ *   - the prefix-sliced expert of Eq. 4: only the first k_e ranked channels
+ *     take part, channels c >= k_e are never touched;
+ *   - the routed layer in the per-expert loop form of the naive online
+ *     clipped FFN (App. C.1, Algorithm 1): for each active expert gather its
+ *     tokens, run the sliced FFN, weight by the router score and add into Y;
+ *   - the channel reorder of Eq. 3 (Sec. 3.1): a descending sort of the
+ *     saliency scores gives pi; gate/up rows and down columns are permuted
+ *     consistently;
+ *   - k = ceil(r * d_ff) for a retention ratio r (Sec. 3.1, after Eq. 3).
+ *
+ * Readings where the paper is silent (each listed with its reason in the
+ * design notes):
+ *   - router: softmax over all E fp32 logits, top-k selected on the raw
+ *     logits ordered by (logit descending, expert id ascending); NaN logits
+ *     order after every number; with norm_topk the k selected probabilities
+ *     are divided by their sum;
+ *   - dispatch order inside one expert: ascending assignment id a = t*k + j;
+ *   - k_e = 0: the expert keeps its routing slot and weight, contributes
+ *     exactly 0 and is left out of the permutation;
+ *   - the router weight multiplies the expert output after the down
+ *     projection (Algorithm 1 and Algorithm 2 both do this);
+ *   - one optional shared expert, unpruned, added with weight 1;
+ *   - reorder ties keep the lower original channel index first; NaN scores
+ *     order after every number.
+ *
+ * Layouts (row-major):  x [T][d]; logits [T][E] fp32;
+ *   w_gate, w_up [E][I][d];  w_down [E][d][I]  (row = hidden unit, column =
+ *   channel);  shared ws_gate, ws_up [I_s][d], ws_down [d][I_s].
+ * Element type of x and weights: dtype 0 = fp32, 1 = bf16 (raw bits).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORACLE_F32 0
+#define ORACLE_BF16 1
+
+/* Exact decode of one stored element to double (bf16 -> fp32 is a shift). */
+static double elem(const void *base, int dtype, size_t i)
+{
+    if (dtype == ORACLE_F32)
+        return (double)((const float *)base)[i];
+    uint32_t bits = ((uint32_t)((const uint16_t *)base)[i]) << 16;
+    float f;
+    memcpy(&f, &bits, sizeof f);
+    return (double)f;
+}
+
+static void store(void *base, int dtype, size_t i, const void *src, size_t j)
+{
+    if (dtype == ORACLE_F32)
+        ((float *)base)[i] = ((const float *)src)[j];
+    else
+        ((uint16_t *)base)[i] = ((const uint16_t *)src)[j];
+}
+
+/* Routing order: does (va, ia) come before (vb, ib)?  Larger logit first,
+ * equal logits -> lower expert id first, NaN after every number. */
+static int route_before(float va, int ia, float vb, int ib)
+{
+    int na = isnan(va), nb = isnan(vb);
+    if (na != nb)
+        return nb;
+    if (!na && va != vb)
+        return va > vb;
+    return ia < ib;
+}
+
+/* Per token: top-k experts by logit and their router weights.
+ * idx [T][k], w [T][k] (fp64). */
+int oracle_route(int T, int E, int k, const float *logits, int norm_topk,
+                 int32_t *idx, double *w)
+{
+    if (T < 0 || E < 1 || k < 1 || k > E || !logits || !idx || !w)
+        return -1;
+    char *taken = (char *)malloc((size_t)E);
+    if (!taken)
+        return -1;
+    for (int t = 0; t < T; ++t) {
+        const float *l = logits + (size_t)t * E;
+        memset(taken, 0, (size_t)E);
+        /* selection: k rounds, each picks the first not-yet-taken expert in
+         * routing order */
+        for (int j = 0; j < k; ++j) {
+            int best = -1;
+            for (int e = 0; e < E; ++e) {
+                if (taken[e])
+                    continue;
+                if (best < 0 || route_before(l[e], e, l[best], best))
+                    best = e;
+            }
+            taken[best] = 1;
+            idx[(size_t)t * k + j] = best;
+        }
+        /* softmax over all E experts, shifted by the largest logit */
+        double m = -INFINITY;
+        for (int e = 0; e < E; ++e)
+            if ((double)l[e] > m)
+                m = (double)l[e];
+        double z = 0.0;
+        for (int e = 0; e < E; ++e)
+            z += exp((double)l[e] - m);
+        double s = 0.0;
+        for (int j = 0; j < k; ++j) {
+            int e = idx[(size_t)t * k + j];
+            w[(size_t)t * k + j] = exp((double)l[e] - m) / z;
+            s += w[(size_t)t * k + j];
+        }
+        if (norm_topk)
+            for (int j = 0; j < k; ++j)
+                w[(size_t)t * k + j] /= s;
+    }
+    free(taken);
+    return 0;
+}
+
+/* Stable counting sort of the T*k assignments by expert id, active experts
+ * only (k_e > 0).  counts [E] = raw n_e of every expert; offsets [E+1] over
+ * active experts; perm [P] = assignment ids; pos [T*k] = slot in perm or -1.
+ * Returns P (number of active assignments) or -1. */
+int oracle_dispatch(int T, int E, int k, const int32_t *idx, const int32_t *keep,
+                    int32_t *counts, int32_t *offsets, int32_t *perm, int32_t *pos)
+{
+    if (T < 0 || E < 1 || k < 1 || !idx || !keep || !counts || !offsets)
+        return -1;
+    size_t A = (size_t)T * k;
+    for (int e = 0; e < E; ++e)
+        counts[e] = 0;
+    for (size_t a = 0; a < A; ++a) {
+        if (idx[a] < 0 || idx[a] >= E)
+            return -1;
+        counts[idx[a]]++;
+    }
+    offsets[0] = 0;
+    for (int e = 0; e < E; ++e)
+        offsets[e + 1] = offsets[e] + (keep[e] > 0 ? counts[e] : 0);
+    int32_t *fill = (int32_t *)calloc((size_t)E, sizeof(int32_t));
+    if (!fill)
+        return -1;
+    for (size_t a = 0; a < A; ++a) {
+        int e = idx[a];
+        if (keep[e] > 0) {
+            int32_t p = offsets[e] + fill[e]++;
+            if (perm)
+                perm[p] = (int32_t)a;
+            if (pos)
+                pos[a] = p;
+        } else if (pos) {
+            pos[a] = -1;
+        }
+    }
+    free(fill);
+    return offsets[E];
+}
+
+/* One prefix-sliced SwiGLU expert applied to one token (Eq. 4):
+ *   g_c = <W_gate[c], x>, u_c = <W_up[c], x>, h_c = silu(g_c) * u_c  (c < kk)
+ *   out[n] = sum_{c < kk} h_c * W_down[n][c]
+ * wg/wu point at the expert's [I][d] blocks, wd at its [d][ld_down] block. */
+static void sliced_ffn(int d, int kk, int ld_down, int dtype, const void *x, size_t x_off,
+                       const void *wg, const void *wu, const void *wd, size_t w_off,
+                       size_t wd_off, double *h, double *out)
+{
+    for (int c = 0; c < kk; ++c) {
+        double g = 0.0, u = 0.0;
+        for (int i = 0; i < d; ++i) {
+            double xi = elem(x, dtype, x_off + i);
+            g += elem(wg, dtype, w_off + (size_t)c * d + i) * xi;
+            u += elem(wu, dtype, w_off + (size_t)c * d + i) * xi;
+        }
+        h[c] = g / (1.0 + exp(-g)) * u;
+    }
+    for (int n = 0; n < d; ++n) {
+        double acc = 0.0;
+        for (int c = 0; c < kk; ++c)
+            acc += h[c] * elem(wd, dtype, wd_off + (size_t)n * ld_down + c);
+        out[n] = acc;
+    }
+}
+
+/* Masked MoE layer forward.  y [T][d] fp64, unrounded.  The routing and
+ * dispatch results are returned through the optional pointers (NULL = skip):
+ * idx/w [T][k], counts [E], offsets [E+1], perm [T*k], pos [T*k].
+ * Returns 0, or -1 on bad arguments, -3 on a keep count outside [0, I]. */
+int oracle_layer_forward(int T, int d, int E, int I, int k, int I_s, int dtype,
+                         int norm_topk, const void *x, const float *logits,
+                         const void *w_gate, const void *w_up, const void *w_down,
+                         const int32_t *keep, const void *ws_gate, const void *ws_up,
+                         const void *ws_down, double *y, int32_t *idx_out, double *w_out,
+                         int32_t *counts_out, int32_t *offsets_out, int32_t *perm_out,
+                         int32_t *pos_out)
+{
+    if (T < 0 || d < 1 || E < 1 || I < 1 || k < 1 || k > E || I_s < 0 || !y || !keep)
+        return -1;
+    if (dtype != ORACLE_F32 && dtype != ORACLE_BF16)
+        return -1;
+    for (int e = 0; e < E; ++e)
+        if (keep[e] < 0 || keep[e] > I)
+            return -3;
+    if (T == 0)
+        return 0;
+    size_t A = (size_t)T * k;
+    int32_t *idx = (int32_t *)malloc(A * sizeof(int32_t));
+    double *w = (double *)malloc(A * sizeof(double));
+    int32_t *counts = (int32_t *)malloc((size_t)E * sizeof(int32_t));
+    int32_t *offsets = (int32_t *)malloc((size_t)(E + 1) * sizeof(int32_t));
+    int32_t *perm = (int32_t *)malloc(A * sizeof(int32_t));
+    int32_t *pos = (int32_t *)malloc(A * sizeof(int32_t));
+    double *O = (double *)malloc(A * (size_t)d * sizeof(double));
+    int rc = -1;
+    if (!idx || !w || !counts || !offsets || !perm || !pos || !O)
+        goto done;
+
+    /* step 1: routing (the router is an input of Algorithm 1) */
+    if (oracle_route(T, E, k, logits, norm_topk, idx, w) != 0)
+        goto done;
+    /* step 2: group the routed assignments by expert, skipping k_e = 0 */
+    int P = oracle_dispatch(T, E, k, idx, keep, counts, offsets, perm, pos);
+    if (P < 0)
+        goto done;
+
+    /* step 3: for each active expert, its sliced FFN on each routed token */
+    for (int e = 0; e < E; ++e) {
+        int kk = keep[e];
+        if (kk == 0)
+            continue;
+#pragma omp parallel for schedule(dynamic, 1)
+        for (int p = offsets[e]; p < offsets[e + 1]; ++p) {
+            double *h = (double *)malloc((size_t)kk * sizeof(double));
+            int t = perm[p] / k;
+            sliced_ffn(d, kk, I, dtype, x, (size_t)t * d, w_gate, w_up, w_down,
+                       (size_t)e * I * d, (size_t)e * d * I, h, O + (size_t)p * d);
+            free(h);
+        }
+    }
+
+    /* step 4: weight by router score after the down projection and add into
+     * Y in ascending slot order; then the shared expert with weight 1 */
+#pragma omp parallel for schedule(static)
+    for (int t = 0; t < T; ++t) {
+        double *yt = y + (size_t)t * d;
+        for (int n = 0; n < d; ++n)
+            yt[n] = 0.0;
+        for (int j = 0; j < k; ++j) {
+            int32_t p = pos[(size_t)t * k + j];
+            if (p < 0)
+                continue;
+            double wt = w[(size_t)t * k + j];
+            for (int n = 0; n < d; ++n)
+                yt[n] += wt * O[(size_t)p * d + n];
+        }
+        if (I_s > 0) {
+            double *h = (double *)malloc((size_t)I_s * sizeof(double));
+            double *s = (double *)malloc((size_t)d * sizeof(double));
+            sliced_ffn(d, I_s, I_s, dtype, x, (size_t)t * d, ws_gate, ws_up, ws_down, 0, 0, h, s);
+            for (int n = 0; n < d; ++n)
+                yt[n] += s[n];
+            free(h);
+            free(s);
+        }
+    }
+
+    if (idx_out)
+        memcpy(idx_out, idx, A * sizeof(int32_t));
+    if (w_out)
+        memcpy(w_out, w, A * sizeof(double));
+    if (counts_out)
+        memcpy(counts_out, counts, (size_t)E * sizeof(int32_t));
+    if (offsets_out)
+        memcpy(offsets_out, offsets, (size_t)(E + 1) * sizeof(int32_t));
+    if (perm_out)
+        memcpy(perm_out, perm, (size_t)P * sizeof(int32_t));
+    if (pos_out)
+        memcpy(pos_out, pos, A * sizeof(int32_t));
+    rc = 0;
+done:
+    free(idx);
+    free(w);
+    free(counts);
+    free(offsets);
+    free(perm);
+    free(pos);
+    free(O);
+    return rc;
+}
+
+/* Eq. 3: sort scores in descending order to get pi, then
+ *   W~_gate = P W_gate (rows), W~_up = P W_up (rows), W~_down = W_down P^T
+ * (columns).  Ranked channel c holds original channel pi[c]. */
+static const float *g_sort_scores;
+static int rank_cmp(const void *pa, const void *pb)
+{
+    int a = *(const int32_t *)pa, b = *(const int32_t *)pb;
+    float va = g_sort_scores[a], vb = g_sort_scores[b];
+    int na = isnan(va), nb = isnan(vb);
+    if (na != nb)
+        return na ? 1 : -1;
+    if (!na && va != vb)
+        return va > vb ? -1 : 1;
+    return a < b ? -1 : (a > b);
+}
+
+int oracle_rank_reorder(int E, int I, int d, int dtype, const float *scores,
+                        const void *w_gate, const void *w_up, const void *w_down,
+                        void *w_gate_r, void *w_up_r, void *w_down_r, int32_t *perm_out)
+{
+    if (E < 1 || I < 1 || d < 1 || !scores || !w_gate || !w_up || !w_down || !w_gate_r ||
+        !w_up_r || !w_down_r)
+        return -1;
+    int32_t *pi = (int32_t *)malloc((size_t)I * sizeof(int32_t));
+    if (!pi)
+        return -1;
+    for (int e = 0; e < E; ++e) {
+        for (int c = 0; c < I; ++c)
+            pi[c] = c;
+        g_sort_scores = scores + (size_t)e * I;
+        qsort(pi, (size_t)I, sizeof(int32_t), rank_cmp);
+        for (int c = 0; c < I; ++c) {
+            size_t src = ((size_t)e * I + pi[c]) * d, dst = ((size_t)e * I + c) * d;
+            for (int i = 0; i < d; ++i) {
+                store(w_gate_r, dtype, dst + i, w_gate, src + i);
+                store(w_up_r, dtype, dst + i, w_up, src + i);
+            }
+        }
+        for (int n = 0; n < d; ++n)
+            for (int c = 0; c < I; ++c)
+                store(w_down_r, dtype, ((size_t)e * d + n) * I + c, w_down,
+                      ((size_t)e * d + n) * I + pi[c]);
+        if (perm_out)
+            memcpy(perm_out + (size_t)e * I, pi, (size_t)I * sizeof(int32_t));
+    }
+    free(pi);
+    return 0;
+}
+
+/* k = ceil(r * d_ff) (Sec. 3.1).  A slack of 1e-9 absorbs the representation
+ * error of decimal ratios such as 0.7 in binary floating point.
+ * Returns -1 for r outside [0, 1], NaN or I < 1. */
+int oracle_keep_from_ratio(double r, int I)
+{
+    if (!(r >= 0.0 && r <= 1.0) || I < 1)
+        return -1;
+    double k = ceil(r * (double)I - 1e-9);
+    if (k < 0)
+        k = 0;
+    if (k > I)
+        k = I;
+    return (int)k;
+}
