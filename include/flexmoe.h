@@ -1,0 +1,158 @@
+/*
+ * flexmoe.h -- C ABI of the FlexMoE masked MoE-layer forward for MI355X (gfx950).
+ *
+ * The library computes one MoE layer in which every routed expert e runs only
+ * the first k_e channels of its importance-ranked intermediate dimension
+ * (FlexMoE, Sec. 3.1, Eq. 4).  Ranking is a one-time channel permutation of
+ * the expert weights (Eq. 3); a budget is the per-expert keep-count array
+ * k[E] (the hardened action mask of Eqs. 9-10 expressed as channel counts).
+ * Switching budgets rewrites only that array: no weight is moved, which is the
+ * online clipping mode of Sec. 4.4 (Table 3).
+ *
+ * General rules for every entry point
+ *   - All pointers except the descriptor, the host keep table of
+ *     flexmoe_set_budget and the debug-output struct are DEVICE pointers of the
+ *     current HIP device.  The caller owns and allocates every buffer,
+ *     including the forward workspace; the library allocates nothing and keeps
+ *     no device state between calls.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
+ *     work is enqueued on it; no call synchronises the host.
+ *   - Return value 0 = success, otherwise one of the negative FLEXMOE_E* codes;
+ *     flexmoe_last_error() then returns a message (thread-local).  Argument
+ *     checks happen on the host before any device work: a call that returns
+ *     an argument error has enqueued nothing.  Device-resident data (logits,
+ *     keep counts) is not inspected by the host; keep counts read on the device
+ *     are clamped to [0, I] so that no access leaves its buffer.
+ *
+ * Element types: dtype FLEXMOE_F32 (x, weights and y in fp32) or FLEXMOE_BF16
+ * (x, weights and y in bf16).  Router logits are always fp32.  Accumulation is
+ * fp32; in bf16 mode the SwiGLU activations are rounded to bf16 before the
+ * down projection and y is rounded once at the end (round to nearest even).
+ *
+ * Shape rules (FLEXMOE_ESHAPE otherwise): d, I and I_shared are multiples of
+ * 8; 1 <= E <= 256; 1 <= top_k <= min(E, 16); 0 <= T <= max_tokens.
+ */
+#ifndef FLEXMOE_H
+#define FLEXMOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    FLEXMOE_OK = 0,
+    FLEXMOE_EINVAL = -1,     /* null pointer, negative count, bad flag value   */
+    FLEXMOE_ESHAPE = -2,     /* dimension rule broken, T > max_tokens           */
+    FLEXMOE_EKEEP = -3,      /* a host keep count outside [0, I]                */
+    FLEXMOE_EWORKSPACE = -4, /* workspace missing or smaller than required      */
+    FLEXMOE_EDTYPE = -5,     /* dtype is neither FLEXMOE_F32 nor FLEXMOE_BF16   */
+    FLEXMOE_EHIP = -6        /* a HIP call or kernel launch failed              */
+};
+
+typedef enum { FLEXMOE_F32 = 0, FLEXMOE_BF16 = 1 } flexmoe_dtype;
+
+/* Static description of one MoE layer. */
+typedef struct flexmoe_layer_desc {
+    int32_t d;          /* hidden size                                          */
+    int32_t E;          /* routed experts                                       */
+    int32_t I;          /* intermediate channels per routed expert (d_ff)       */
+    int32_t top_k;      /* experts per token                                    */
+    int32_t I_shared;   /* channels of the one unpruned shared expert, 0 = none */
+    int32_t dtype;      /* flexmoe_dtype of x, weights and y                    */
+    int32_t norm_topk;  /* 1: router weights renormalised over the top-k;
+                           0: raw softmax probabilities                         */
+    int32_t max_tokens; /* largest T a forward will be called with              */
+} flexmoe_layer_desc;
+
+/* Optional copies of the routing and dispatch results (device pointers; any
+ * field may be NULL).  They are written on `stream` at the end of a forward.
+ *   topk_idx [T][top_k] int32  expert ids, slot j = j-th largest logit
+ *   topk_w   [T][top_k] fp32   router weights
+ *   counts   [E]        int32  tokens routed to each expert (k_e = 0 included)
+ *   offsets  [E+1]      int32  segment starts of the active experts (k_e > 0)
+ *                              in perm; offsets[E] = P
+ *   perm     [T*top_k]  int32  assignment ids a = t*top_k + j grouped by
+ *                              expert, ascending a inside an expert; entries
+ *                              at and past P are unspecified
+ *   pos      [T*top_k]  int32  slot of assignment a in perm, -1 if k_e = 0 */
+typedef struct flexmoe_route_out {
+    int32_t *topk_idx;
+    float *topk_w;
+    int32_t *counts;
+    int32_t *offsets;
+    int32_t *perm;
+    int32_t *pos;
+} flexmoe_route_out;
+
+/* Bytes of device workspace flexmoe_layer_forward needs for T tokens
+ * (T <= desc->max_tokens).  Returns 0 and sets the last error when the
+ * descriptor or T is invalid.  A workspace sized for max_tokens serves every
+ * smaller T. */
+size_t flexmoe_workspace_bytes(const flexmoe_layer_desc *desc, int32_t T);
+
+/* One-time channel ranking and reorder (Sec. 3.1, Eq. 3).
+ *   scores  [E][I] fp32   channel saliency (Eq. 2); larger = more important
+ *   w_gate, w_up [E][I][d]  original weights, rows = channels
+ *   w_down  [E][d][I]       original weights, columns = channels
+ *   w_gate_r, w_up_r [E][I][d], w_down_r [E][d][I]  ranked outputs (must not
+ *                           overlap the inputs)
+ *   perm    [E][I] int32  output: ranked channel c holds original channel
+ *                         perm[e][c]
+ * The order is a stable descending sort of the scores: equal scores keep the
+ * lower original index first; NaN scores order after every number.  The same
+ * permutation is applied to gate rows, up rows and down columns, so the
+ * unpruned expert function is unchanged.  Uses desc->d, E, I and dtype. */
+int flexmoe_rank_reorder(const flexmoe_layer_desc *desc, const float *scores,
+                         const void *w_gate, const void *w_up, const void *w_down,
+                         void *w_gate_r, void *w_up_r, void *w_down_r, int32_t *perm,
+                         void *stream);
+
+/* Budget switch: validates 0 <= keep_host[e] <= I for every e on the host, then
+ * writes the E counts into keep_dev [E] on `stream` (one small kernel whose
+ * arguments carry the table, so keep_host may be reused as soon as the call
+ * returns).  A forward queued later on the same stream sees the new budget.
+ * Holding several device keep tables and passing a different keep_dev pointer
+ * to the forward is an equally valid zero-copy switch. */
+int flexmoe_set_budget(const flexmoe_layer_desc *desc, int32_t *keep_dev,
+                       const int32_t *keep_host, void *stream);
+
+/* Masked MoE-layer forward (Eq. 4 inside a top-k MoE layer; App. C.3).
+ *   x        [T][d]            hidden states (dtype)
+ *   logits   [T][E] fp32       router logits
+ *   w_gate_r, w_up_r [E][I][d] ranked weights; channel c of expert e is used
+ *                              iff c < keep_dev[e]
+ *   w_down_r [E][d][I]         ranked down projection (columns = channels)
+ *   keep_dev [E] int32         keep counts k_e (k_e = 0: the expert is skipped
+ *                              and contributes exactly 0)
+ *   ws_gate, ws_up [I_shared][d], ws_down [d][I_shared]  shared expert
+ *                              (NULL iff I_shared = 0), added with weight 1
+ *   y        [T][d]            output (dtype)
+ *   workspace / workspace_bytes  device scratch of at least
+ *                              flexmoe_workspace_bytes(desc, T) bytes, 256-byte
+ *                              aligned; its contents are clobbered
+ *   dbg                        optional routing/dispatch copies (may be NULL)
+ * Routing: softmax over all E logits; the top_k experts by (logit descending,
+ * expert id ascending; NaN last) are selected; with norm_topk their weights are
+ * divided by their sum.  y[t] = sum_j w[t][j] * FFN_{e_j}^{(k_e)}(x[t]) + shared.
+ * T = 0 is a valid no-op.  Deterministic: the same inputs give the same bits. */
+int flexmoe_layer_forward(const flexmoe_layer_desc *desc, int32_t T, const void *x,
+                          const float *logits, const void *w_gate_r, const void *w_up_r,
+                          const void *w_down_r, const int32_t *keep_dev, const void *ws_gate,
+                          const void *ws_up, const void *ws_down, void *y, void *workspace,
+                          size_t workspace_bytes, const flexmoe_route_out *dbg, void *stream);
+
+/* k = ceil(r * I) for a retention ratio r in [0, 1] (Sec. 3.1).  A slack of
+ * 1e-9 absorbs the binary representation error of decimal ratios (0.7 * 1000
+ * gives 700).  Returns -1 for r outside [0, 1], NaN, or I < 1. */
+int flexmoe_keep_from_ratio(double r, int32_t I);
+
+/* Message for the last non-zero return on this thread ("" if none). */
+const char *flexmoe_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FLEXMOE_H */

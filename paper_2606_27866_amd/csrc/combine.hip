@@ -1,0 +1,56 @@
+// Weighted combine (App. C.3: router-weight scaling and scatter-add, done as
+// a deterministic gather).  For token t:
+//   y[t] = sum_{j < top_k, pos[t][j] >= 0} w[t][j] * O[pos[t][j]] + S[t]
+// summed in ascending slot order in fp32, then rounded once to the output
+// type.  Assignments of experts with k_e = 0 have pos = -1 and add nothing.
+#include "kernels.h"
+
+namespace flexmoe {
+
+template <typename OutT>
+__global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ O,
+                                                      const float* __restrict__ Os,
+                                                      const int32_t* __restrict__ pos,
+                                                      const float* __restrict__ wts, int k, int d,
+                                                      int has_shared, OutT* __restrict__ y) {
+    const int t = blockIdx.x;
+    for (int n = threadIdx.x * 4; n < d; n += blockDim.x * 4) {
+        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int j = 0; j < k; ++j) {
+            const int p = pos[(size_t)t * k + j];
+            if (p < 0) continue;
+            const float w = wts[(size_t)t * k + j];
+            const float4 o = *reinterpret_cast<const float4*>(O + (size_t)p * d + n);
+            acc.x += w * o.x;
+            acc.y += w * o.y;
+            acc.z += w * o.z;
+            acc.w += w * o.w;
+        }
+        if (has_shared) {
+            const float4 sv = *reinterpret_cast<const float4*>(Os + (size_t)t * d + n);
+            acc.x += sv.x;
+            acc.y += sv.y;
+            acc.z += sv.z;
+            acc.w += sv.w;
+        }
+        if constexpr (sizeof(OutT) == 4) {
+            *reinterpret_cast<float4*>(y + (size_t)t * d + n) = acc;
+        } else {
+            const uint32_t lo = (uint32_t)f32_to_bf16(acc.x) | ((uint32_t)f32_to_bf16(acc.y) << 16);
+            const uint32_t hi = (uint32_t)f32_to_bf16(acc.z) | ((uint32_t)f32_to_bf16(acc.w) << 16);
+            *reinterpret_cast<uint2*>(y + (size_t)t * d + n) = make_uint2(lo, hi);
+        }
+    }
+}
+
+hipError_t launch_combine(const float* O, const float* Os, const int32_t* pos, const float* wts,
+                          int T, int k, int d, int has_shared, int dtype, void* y, hipStream_t s) {
+    if (T <= 0) return hipSuccess;
+    if (dtype == 0)
+        combine_kernel<float><<<T, 256, 0, s>>>(O, Os, pos, wts, k, d, has_shared, (float*)y);
+    else
+        combine_kernel<bf16_t><<<T, 256, 0, s>>>(O, Os, pos, wts, k, d, has_shared, (bf16_t*)y);
+    return hipGetLastError();
+}
+
+}  // namespace flexmoe

@@ -1,0 +1,108 @@
+// Shared definitions of the FlexMoE HIP kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace flexmoe {
+
+constexpr int kWave = 64;
+constexpr int kMaxExperts = 256;
+constexpr int kMaxTopK = 16;
+constexpr int kRouteTokens = 64;   // tokens per routing block (= dispatch chunk)
+
+typedef uint16_t bf16_t;           // raw bf16 bits in memory
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t b) {
+    return __uint_as_float(((uint32_t)b) << 16);
+}
+
+// Round to nearest even; NaN becomes a quiet NaN.
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (bf16_t)(u >> 16);
+}
+
+// x * sigmoid(x) in fp32 via the hardware exp2.  For x -> -inf the quotient
+// tends to -0, for x -> +inf to x.
+__device__ __forceinline__ float silu_fast(float x) {
+    float e = __builtin_amdgcn_exp2f(-x * 1.4426950408889634f);
+    return x / (1.0f + e);
+}
+
+__host__ __device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+// Per-segment metadata written by the dispatch kernel.  Segments 0..E-1 are
+// the routed experts (rows grouped by the dispatch permutation); segment E is
+// the shared expert when the layer has one (rows = tokens).
+struct SegMeta {
+    int32_t row0;   // first row of the segment in the routed row space
+    int32_t rows;   // rows of the segment (0 for inactive experts)
+    int32_t kk;     // channels of the segment (k_e, or I_shared)
+    int32_t pad;
+};
+
+// Tile shapes of one GEMM-kernel family; the dispatch kernel builds the tile
+// tables with the same numbers the GEMM kernels use.
+struct TileShape {
+    int32_t bm1, bn1;   // gate/up GEMM: rows x channels per tile
+    int32_t bm2, bn2;   // down GEMM: rows x output columns per tile
+};
+
+// Wave-wide inclusive prefix sum of an int (64 lanes).
+__device__ __forceinline__ int wave_incl_scan(int v) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        int n = __shfl_up(v, o, 64);
+        if (lane >= o) v += n;
+    }
+    return v;
+}
+
+__device__ __forceinline__ int wave_sum(int v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+__device__ __forceinline__ float wave_sum_f(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+}  // namespace flexmoe
+
+namespace flexmoe {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Segment owning tile L: the largest s with tstart[s] <= L (segments with no
+// tiles share their start with the next one and are skipped).  The table is
+// uniform across the block, so this runs on scalar loads.
+__device__ __forceinline__ int find_segment(const int32_t* tstart, int nseg, int L) {
+    int lo = 0, hi = nseg - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (tstart[mid] <= L) lo = mid;
+        else hi = mid - 1;
+    }
+    return lo;
+}
+
+// Zero the bf16 elements at positions >= nvalid of an 8-element vector.
+__device__ __forceinline__ u32x4 mask_tail_bf16(u32x4 v, int nvalid) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        if (2 * i >= nvalid) v[i] = 0u;
+        else if (2 * i + 1 >= nvalid) v[i] &= 0xffffu;
+    }
+    return v;
+}
+
+}  // namespace flexmoe

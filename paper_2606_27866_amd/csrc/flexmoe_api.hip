@@ -1,0 +1,277 @@
+// Host side of the FlexMoE C ABI: argument checks, workspace carving and the
+// launch sequence of one masked MoE-layer forward (include/flexmoe.h).
+//
+//   route -> dispatch scan -> dispatch scatter -> gate/up GEMM -> down GEMM
+//   -> combine
+//
+// All launches go to the caller's stream.  The host never reads routing
+// results back: tile counts live on the device and the GEMM grids are sized
+// by an upper bound computed from (T, E, I, I_shared); surplus workgroups
+// exit at once.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <cmath>
+
+#include "../../include/flexmoe.h"
+#include "kernels.h"
+
+using namespace flexmoe;
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+    return fail(FLEXMOE_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
+
+int check_desc(const flexmoe_layer_desc* D) {
+    if (!D) return fail(FLEXMOE_EINVAL, "desc is NULL");
+    if (D->dtype != FLEXMOE_F32 && D->dtype != FLEXMOE_BF16)
+        return fail(FLEXMOE_EDTYPE, "dtype %d is neither FLEXMOE_F32 nor FLEXMOE_BF16", D->dtype);
+    if (D->norm_topk != 0 && D->norm_topk != 1)
+        return fail(FLEXMOE_EINVAL, "norm_topk must be 0 or 1 (got %d)", D->norm_topk);
+    if (D->d < 8 || D->d % 8) return fail(FLEXMOE_ESHAPE, "d = %d must be a positive multiple of 8", D->d);
+    if (D->I < 8 || D->I % 8) return fail(FLEXMOE_ESHAPE, "I = %d must be a positive multiple of 8", D->I);
+    if (D->I_shared < 0 || D->I_shared % 8)
+        return fail(FLEXMOE_ESHAPE, "I_shared = %d must be 0 or a positive multiple of 8", D->I_shared);
+    if (D->E < 1 || D->E > kMaxExperts)
+        return fail(FLEXMOE_ESHAPE, "E = %d outside [1, %d]", D->E, kMaxExperts);
+    if (D->top_k < 1 || D->top_k > D->E || D->top_k > kMaxTopK)
+        return fail(FLEXMOE_ESHAPE, "top_k = %d outside [1, min(E, %d)]", D->top_k, kMaxTopK);
+    if (D->max_tokens < 0) return fail(FLEXMOE_ESHAPE, "max_tokens = %d is negative", D->max_tokens);
+    // every row index and tile count below stays inside int32
+    const long long A = (long long)D->max_tokens * D->top_k;
+    if (A + D->max_tokens > (1LL << 30))
+        return fail(FLEXMOE_ESHAPE, "max_tokens * (top_k + 1) exceeds 2^30");
+    return FLEXMOE_OK;
+}
+
+struct Layout {
+    size_t idx, wts, blockcnt, blockbase, counts, offsets, perm, pos, seg, t1, t2, H, Hs, O, Os;
+    size_t total;
+};
+
+int num_chunks(int T) { return ceil_div(T, kRouteTokens); }
+
+Layout layout(const flexmoe_layer_desc& D, int T) {
+    const size_t A = (size_t)T * D.top_k;
+    const size_t NB = (size_t)num_chunks(T);
+    const size_t nseg = (size_t)D.E + (D.I_shared > 0 ? 1 : 0);
+    const size_t es = D.dtype == FLEXMOE_BF16 ? 2 : 4;
+    Layout L{};
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t o = off;
+        off += align256(bytes);
+        return o;
+    };
+    L.idx = take(A * 4);
+    L.wts = take(A * 4);
+    L.blockcnt = take((size_t)D.E * NB * 4);
+    L.blockbase = take((size_t)D.E * NB * 4);
+    L.counts = take((size_t)D.E * 4);
+    L.offsets = take(((size_t)D.E + 1) * 4);
+    L.perm = take(A * 4);
+    L.pos = take(A * 4);
+    L.seg = take(nseg * sizeof(SegMeta));
+    L.t1 = take((nseg + 1) * 4);
+    L.t2 = take((nseg + 1) * 4);
+    L.H = take(A * (size_t)D.I * es);
+    L.Hs = take((size_t)T * D.I_shared * es);
+    L.O = take(A * (size_t)D.d * 4);
+    L.Os = take(D.I_shared > 0 ? (size_t)T * D.d * 4 : 0);
+    L.total = off;
+    return L;
+}
+
+// Upper bound on the number of row tiles of height bm over all routed
+// segments: sum_e ceil(n_e/bm) <= ceil(A/bm) + E - 1, and <= E*ceil(T/bm)
+// because a token routes to an expert at most once.
+long long routed_row_tiles_ub(int T, int E, int k, int bm) {
+    const long long A = (long long)T * k;
+    const long long a = (A + bm - 1) / bm + E - 1;
+    const long long b = (long long)E * ((T + bm - 1) / bm);
+    return a < b ? a : b;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* flexmoe_last_error(void) { return g_err; }
+
+int flexmoe_keep_from_ratio(double r, int32_t I) {
+    if (!(r >= 0.0 && r <= 1.0) || I < 1) {
+        fail(FLEXMOE_EINVAL, "ratio %g outside [0, 1] or I = %d < 1", r, I);
+        return -1;
+    }
+    double k = std::ceil(r * (double)I - 1e-9);
+    if (k < 0) k = 0;
+    if (k > I) k = I;
+    return (int)k;
+}
+
+size_t flexmoe_workspace_bytes(const flexmoe_layer_desc* desc, int32_t T) {
+    if (check_desc(desc) != FLEXMOE_OK) return 0;
+    if (T < 0 || T > desc->max_tokens) {
+        fail(FLEXMOE_ESHAPE, "T = %d outside [0, max_tokens = %d]", T, desc->max_tokens);
+        return 0;
+    }
+    return layout(*desc, T).total;
+}
+
+int flexmoe_set_budget(const flexmoe_layer_desc* desc, int32_t* keep_dev, const int32_t* keep_host,
+                       void* stream) {
+    int rc = check_desc(desc);
+    if (rc) return rc;
+    if (!keep_dev || !keep_host) return fail(FLEXMOE_EINVAL, "keep_dev / keep_host is NULL");
+    KeepArgs args;
+    for (int e = 0; e < desc->E; ++e) {
+        if (keep_host[e] < 0 || keep_host[e] > desc->I)
+            return fail(FLEXMOE_EKEEP, "keep[%d] = %d outside [0, I = %d]", e, keep_host[e], desc->I);
+        args.v[e] = keep_host[e];
+    }
+    for (int e = desc->E; e < kMaxExperts; ++e) args.v[e] = 0;
+    set_keep_kernel<<<1, kMaxExperts, 0, (hipStream_t)stream>>>(keep_dev, args, desc->E);
+    const hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return hip_fail(err, "set_budget launch");
+    return FLEXMOE_OK;
+}
+
+int flexmoe_rank_reorder(const flexmoe_layer_desc* desc, const float* scores, const void* w_gate,
+                         const void* w_up, const void* w_down, void* w_gate_r, void* w_up_r,
+                         void* w_down_r, int32_t* perm, void* stream) {
+    int rc = check_desc(desc);
+    if (rc) return rc;
+    if (!scores || !w_gate || !w_up || !w_down || !w_gate_r || !w_up_r || !w_down_r || !perm)
+        return fail(FLEXMOE_EINVAL, "rank_reorder: a pointer is NULL");
+    const int es = desc->dtype == FLEXMOE_BF16 ? 2 : 4;
+    const hipError_t err = launch_rank_reorder(scores, w_gate, w_up, w_down, w_gate_r, w_up_r,
+                                               w_down_r, perm, desc->E, desc->I, desc->d, es,
+                                               (hipStream_t)stream);
+    if (err != hipSuccess) return hip_fail(err, "rank_reorder launch");
+    return FLEXMOE_OK;
+}
+
+int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void* x,
+                          const float* logits, const void* w_gate_r, const void* w_up_r,
+                          const void* w_down_r, const int32_t* keep_dev, const void* ws_gate,
+                          const void* ws_up, const void* ws_down, void* y, void* workspace,
+                          size_t workspace_bytes, const flexmoe_route_out* dbg, void* stream) {
+    int rc = check_desc(desc);
+    if (rc) return rc;
+    const flexmoe_layer_desc& D = *desc;
+    if (T < 0) return fail(FLEXMOE_EINVAL, "T = %d is negative", T);
+    if (T > D.max_tokens) return fail(FLEXMOE_ESHAPE, "T = %d exceeds max_tokens = %d", T, D.max_tokens);
+    if (T == 0) return FLEXMOE_OK;
+    if (!x || !logits || !w_gate_r || !w_up_r || !w_down_r || !keep_dev || !y)
+        return fail(FLEXMOE_EINVAL, "forward: an input/output pointer is NULL");
+    for (const void* ptr : {x, w_gate_r, w_up_r, w_down_r, ws_gate, ws_up, ws_down, (const void*)y})
+        if (((uintptr_t)ptr) & 15) return fail(FLEXMOE_EINVAL, "x, weights and y must be 16-byte aligned");
+    if (((uintptr_t)logits) & 3 || ((uintptr_t)keep_dev) & 3)
+        return fail(FLEXMOE_EINVAL, "logits and keep_dev must be 4-byte aligned");
+    const bool has_shared = D.I_shared > 0;
+    if (has_shared != (ws_gate && ws_up && ws_down) || (!has_shared && (ws_gate || ws_up || ws_down)))
+        return fail(FLEXMOE_EINVAL, "shared weights must be given iff I_shared > 0");
+    const Layout L = layout(D, T);
+    if (!workspace || workspace_bytes < L.total)
+        return fail(FLEXMOE_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace_bytes, L.total);
+    if (((uintptr_t)workspace) & 255) return fail(FLEXMOE_EWORKSPACE, "workspace is not 256-byte aligned");
+
+    hipStream_t s = (hipStream_t)stream;
+    char* ws = (char*)workspace;
+    int32_t* idx = (int32_t*)(ws + L.idx);
+    float* wts = (float*)(ws + L.wts);
+    int32_t* blockcnt = (int32_t*)(ws + L.blockcnt);
+    int32_t* blockbase = (int32_t*)(ws + L.blockbase);
+    int32_t* counts = (int32_t*)(ws + L.counts);
+    int32_t* offsets = (int32_t*)(ws + L.offsets);
+    int32_t* perm = (int32_t*)(ws + L.perm);
+    int32_t* pos = (int32_t*)(ws + L.pos);
+    SegMeta* seg = (SegMeta*)(ws + L.seg);
+    int32_t* t1 = (int32_t*)(ws + L.t1);
+    int32_t* t2 = (int32_t*)(ws + L.t2);
+    float* O = (float*)(ws + L.O);
+    float* Os = (float*)(ws + L.Os);
+    const int NB = num_chunks(T);
+    const int nseg = D.E + (has_shared ? 1 : 0);
+    const bool bf16 = D.dtype == FLEXMOE_BF16;
+    const TileShape ts = bf16 ? TileShape{kBf16BM1, kBf16BN1, kBf16BM2, kBf16BN2}
+                              : TileShape{kF32BM, kF32BN, kF32BM, kF32BN};
+
+    route_kernel<<<NB, 256, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, idx, wts, blockcnt, NB);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return hip_fail(err, "route launch");
+    dispatch_scan_kernel<<<D.E, 256, 0, s>>>(blockcnt, NB, blockbase, counts);
+    if ((err = hipGetLastError()) != hipSuccess) return hip_fail(err, "dispatch scan launch");
+    dispatch_scatter_kernel<<<NB, 64, 0, s>>>(idx, keep_dev, counts, blockbase, T, D.E, D.top_k, D.I,
+                                              D.I_shared, D.d, NB, ts, perm, pos, offsets, seg, t1, t2);
+    if ((err = hipGetLastError()) != hipSuccess) return hip_fail(err, "dispatch scatter launch");
+
+    // grid upper bounds from host-known sizes
+    const long long rt1 = routed_row_tiles_ub(T, D.E, D.top_k, ts.bm1);
+    const long long rt2 = routed_row_tiles_ub(T, D.E, D.top_k, ts.bm2);
+    long long g1 = rt1 * ceil_div(D.I, ts.bn1);
+    long long g2 = rt2 * ceil_div(D.d, ts.bn2);
+    if (has_shared) {
+        g1 += (long long)ceil_div(T, ts.bm1) * ceil_div(D.I_shared, ts.bn1);
+        g2 += (long long)ceil_div(T, ts.bm2) * ceil_div(D.d, ts.bn2);
+    }
+    if (g1 > 0x7fffffffLL || g2 > 0x7fffffffLL) return fail(FLEXMOE_ESHAPE, "tile grid too large");
+
+    if (bf16) {
+        Gemm1Params<bf16_t> p1{(const bf16_t*)x, (const bf16_t*)w_gate_r, (const bf16_t*)w_up_r,
+                               (const bf16_t*)ws_gate, (const bf16_t*)ws_up, perm, seg, t1,
+                               (bf16_t*)(ws + L.H), (bf16_t*)(ws + L.Hs), D.d, D.I, D.I_shared, D.E,
+                               D.top_k, nseg, T};
+        if ((err = launch_gemm1_bf16(p1, (int)g1, s)) != hipSuccess) return hip_fail(err, "gate/up GEMM launch");
+        Gemm2Params<bf16_t> p2{(const bf16_t*)(ws + L.H), (const bf16_t*)(ws + L.Hs),
+                               (const bf16_t*)w_down_r, (const bf16_t*)ws_down, seg, t2, O, Os, D.d,
+                               D.I, D.I_shared, D.E, nseg};
+        if ((err = launch_gemm2_bf16(p2, (int)g2, s)) != hipSuccess) return hip_fail(err, "down GEMM launch");
+    } else {
+        Gemm1Params<float> p1{(const float*)x, (const float*)w_gate_r, (const float*)w_up_r,
+                              (const float*)ws_gate, (const float*)ws_up, perm, seg, t1,
+                              (float*)(ws + L.H), (float*)(ws + L.Hs), D.d, D.I, D.I_shared, D.E,
+                              D.top_k, nseg, T};
+        if ((err = launch_gemm1_f32(p1, (int)g1, s)) != hipSuccess) return hip_fail(err, "gate/up GEMM launch");
+        Gemm2Params<float> p2{(const float*)(ws + L.H), (const float*)(ws + L.Hs),
+                              (const float*)w_down_r, (const float*)ws_down, seg, t2, O, Os, D.d, D.I,
+                              D.I_shared, D.E, nseg};
+        if ((err = launch_gemm2_f32(p2, (int)g2, s)) != hipSuccess) return hip_fail(err, "down GEMM launch");
+    }
+    if ((err = launch_combine(O, Os, pos, wts, T, D.top_k, D.d, has_shared ? 1 : 0, D.dtype, y, s)) != hipSuccess)
+        return hip_fail(err, "combine launch");
+
+    if (dbg) {
+        const size_t A = (size_t)T * D.top_k;
+        struct {
+            void* dst;
+            const void* src;
+            size_t bytes;
+        } cp[] = {{dbg->topk_idx, idx, A * 4},          {dbg->topk_w, wts, A * 4},
+                  {dbg->counts, counts, (size_t)D.E * 4}, {dbg->offsets, offsets, ((size_t)D.E + 1) * 4},
+                  {dbg->perm, perm, A * 4},              {dbg->pos, pos, A * 4}};
+        for (auto& c : cp) {
+            if (!c.dst) continue;
+            if ((err = hipMemcpyAsync(c.dst, c.src, c.bytes, hipMemcpyDeviceToDevice, s)) != hipSuccess)
+                return hip_fail(err, "debug copy");
+        }
+    }
+    return FLEXMOE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,72 @@
+// Kernel declarations and argument blocks of the FlexMoE HIP library.
+#pragma once
+
+#include "common.h"
+
+namespace flexmoe {
+
+struct KeepArgs {
+    int32_t v[kMaxExperts];
+};
+
+// Gate/up GEMM with fused SwiGLU:
+//   H[row][c] = silu(<W_gate[c], x_t>) * <W_up[c], x_t>,  c < k_s
+// over every segment s (routed experts, then the shared expert).
+template <typename T>
+struct Gemm1Params {
+    const T* x;                 // [T][d]
+    const T* wg;                // routed gate [E][I][d]
+    const T* wu;                // routed up   [E][I][d]
+    const T* sg;                // shared gate [I_s][d]
+    const T* su;                // shared up   [I_s][d]
+    const int32_t* perm;        // grouped row -> assignment id
+    const SegMeta* seg;         // [nseg]
+    const int32_t* tstart;      // [nseg+1] first tile of each segment
+    T* H;                       // routed activations [A][I]
+    T* Hs;                      // shared activations [T][I_s]
+    int d, I, Is, E, top_k, nseg, tokens;
+};
+
+// Down GEMM: O[row][n] = sum_{c < k_s} H[row][c] * W_down[n][c].
+template <typename T>
+struct Gemm2Params {
+    const T* H;
+    const T* Hs;
+    const T* wd;                // routed down [E][d][I]
+    const T* sd;                // shared down [d][I_s]
+    const SegMeta* seg;
+    const int32_t* tstart;
+    float* O;                   // routed rows [A][d]
+    float* Os;                  // shared rows [T][d]
+    int d, I, Is, E, nseg;
+};
+
+// Tile shapes of the kernel families (the dispatch kernel builds tile tables
+// with these numbers).
+constexpr int kBf16BM1 = 128, kBf16BN1 = 64, kBf16BM2 = 128, kBf16BN2 = 128;
+constexpr int kF32BM = 64, kF32BN = 64;
+
+__global__ void route_kernel(const float* logits, int T, int E, int k, int norm_topk, int32_t* idx,
+                             float* wts, int32_t* blockcnt, int NB);
+__global__ void dispatch_scan_kernel(const int32_t* blockcnt, int NB, int32_t* blockbase,
+                                     int32_t* counts);
+__global__ void dispatch_scatter_kernel(const int32_t* idx, const int32_t* keep,
+                                        const int32_t* counts, const int32_t* blockbase, int T,
+                                        int E, int k, int I, int I_shared, int d, int NB,
+                                        TileShape ts, int32_t* perm, int32_t* pos,
+                                        int32_t* offsets, SegMeta* seg, int32_t* t1start,
+                                        int32_t* t2start);
+__global__ void set_keep_kernel(int32_t* keep, KeepArgs t, int E);
+
+// Launchers (defined next to their kernels).  Each returns the launch status.
+hipError_t launch_gemm1_bf16(const Gemm1Params<bf16_t>& p, int grid, hipStream_t s);
+hipError_t launch_gemm2_bf16(const Gemm2Params<bf16_t>& p, int grid, hipStream_t s);
+hipError_t launch_gemm1_f32(const Gemm1Params<float>& p, int grid, hipStream_t s);
+hipError_t launch_gemm2_f32(const Gemm2Params<float>& p, int grid, hipStream_t s);
+hipError_t launch_combine(const float* O, const float* Os, const int32_t* pos, const float* wts,
+                          int T, int k, int d, int has_shared, int dtype, void* y, hipStream_t s);
+hipError_t launch_rank_reorder(const float* scores, const void* wg, const void* wu,
+                               const void* wd, void* wg_r, void* wu_r, void* wd_r,
+                               int32_t* perm, int E, int I, int d, int esize, hipStream_t s);
+
+}  // namespace flexmoe

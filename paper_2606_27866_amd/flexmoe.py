@@ -1,0 +1,199 @@
+"""ctypes binding of libflexmoe.so (include/flexmoe.h).
+
+Argument marshalling only: every step of the layer runs in the HIP library.
+Functions keep the C names; device buffers are passed as torch CUDA tensors
+(their data pointers), the stream defaults to torch's current stream.  There
+is no fallback: if the library is missing or a call fails, an exception is
+raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+from .build import LIB
+
+FLEXMOE_F32 = 0
+FLEXMOE_BF16 = 1
+
+ERRORS = {
+    -1: "FLEXMOE_EINVAL",
+    -2: "FLEXMOE_ESHAPE",
+    -3: "FLEXMOE_EKEEP",
+    -4: "FLEXMOE_EWORKSPACE",
+    -5: "FLEXMOE_EDTYPE",
+    -6: "FLEXMOE_EHIP",
+}
+
+EXPORTED = ("flexmoe_workspace_bytes", "flexmoe_rank_reorder", "flexmoe_set_budget",
+            "flexmoe_layer_forward", "flexmoe_keep_from_ratio", "flexmoe_last_error")
+
+
+class FlexMoEError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__("%s (%d): %s" % (ERRORS.get(code, "?"), code, msg))
+        self.code = code
+
+
+class flexmoe_layer_desc(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("d", "E", "I", "top_k", "I_shared", "dtype", "norm_topk", "max_tokens")]
+
+
+class flexmoe_route_out(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in
+                ("topk_idx", "topk_w", "counts", "offsets", "perm", "pos")]
+
+
+_lib = None
+
+
+def lib():
+    """Load libflexmoe.so (built in-tree by build.py); raise if it is absent."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB):
+            raise RuntimeError("libflexmoe.so is not built (%s); run "
+                               "`python -m paper_2606_27866_amd.build`" % LIB)
+        L = ctypes.CDLL(LIB)
+        vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+        D = ctypes.POINTER(flexmoe_layer_desc)
+        L.flexmoe_workspace_bytes.argtypes = [D, i32]
+        L.flexmoe_workspace_bytes.restype = sz
+        L.flexmoe_rank_reorder.argtypes = [D] + [vp] * 9
+        L.flexmoe_rank_reorder.restype = ctypes.c_int
+        L.flexmoe_set_budget.argtypes = [D, vp, vp, vp]
+        L.flexmoe_set_budget.restype = ctypes.c_int
+        L.flexmoe_layer_forward.argtypes = [D, i32] + [vp] * 11 + [sz, ctypes.POINTER(flexmoe_route_out), vp]
+        L.flexmoe_layer_forward.restype = ctypes.c_int
+        L.flexmoe_keep_from_ratio.argtypes = [ctypes.c_double, i32]
+        L.flexmoe_keep_from_ratio.restype = ctypes.c_int
+        L.flexmoe_last_error.argtypes = []
+        L.flexmoe_last_error.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise FlexMoEError(rc, lib().flexmoe_last_error().decode())
+
+
+def _p(t) -> Optional[int]:
+    """Device pointer of a tensor (or None)."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is not None:
+        return stream if isinstance(stream, int) else stream.cuda_stream
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+def make_desc(d, E, I, top_k, I_shared=0, dtype=FLEXMOE_BF16, norm_topk=1, max_tokens=0):
+    return flexmoe_layer_desc(d, E, I, top_k, I_shared, dtype, norm_topk, max_tokens)
+
+
+def flexmoe_last_error() -> str:
+    return lib().flexmoe_last_error().decode()
+
+
+def flexmoe_keep_from_ratio(r: float, I: int) -> int:
+    return int(lib().flexmoe_keep_from_ratio(float(r), int(I)))
+
+
+def flexmoe_workspace_bytes(desc: flexmoe_layer_desc, T: int) -> int:
+    n = lib().flexmoe_workspace_bytes(ctypes.byref(desc), int(T))
+    if n == 0:
+        raise FlexMoEError(-2, flexmoe_last_error())
+    return int(n)
+
+
+def flexmoe_set_budget(desc, keep_dev, keep_host: Sequence[int], stream=None):
+    kh = np.ascontiguousarray(np.asarray(keep_host, dtype=np.int32))
+    _check(lib().flexmoe_set_budget(ctypes.byref(desc), _p(keep_dev),
+                                    kh.ctypes.data_as(ctypes.c_void_p), _stream(stream)))
+
+
+def flexmoe_rank_reorder(desc, scores, w_gate, w_up, w_down, w_gate_r, w_up_r, w_down_r, perm,
+                         stream=None):
+    _check(lib().flexmoe_rank_reorder(ctypes.byref(desc), _p(scores), _p(w_gate), _p(w_up),
+                                      _p(w_down), _p(w_gate_r), _p(w_up_r), _p(w_down_r), _p(perm),
+                                      _stream(stream)))
+
+
+def flexmoe_layer_forward(desc, T, x, logits, w_gate_r, w_up_r, w_down_r, keep_dev, ws_gate,
+                          ws_up, ws_down, y, workspace, workspace_bytes=None, dbg=None,
+                          stream=None):
+    """dbg: optional dict with any of topk_idx, topk_w, counts, offsets, perm, pos tensors."""
+    if workspace_bytes is None:
+        workspace_bytes = workspace.numel() * workspace.element_size()
+    ro = None
+    if dbg:
+        ro = flexmoe_route_out(*[_p(dbg.get(n)) for n, _ in flexmoe_route_out._fields_])
+    _check(lib().flexmoe_layer_forward(
+        ctypes.byref(desc), int(T), _p(x), _p(logits), _p(w_gate_r), _p(w_up_r), _p(w_down_r),
+        _p(keep_dev), _p(ws_gate), _p(ws_up), _p(ws_down), _p(y), _p(workspace),
+        int(workspace_bytes), ctypes.byref(ro) if ro is not None else None, _stream(stream)))
+
+
+class Layer:
+    """Device-resident masked MoE layer: weights, keep table, workspace.
+
+    A thin holder around the C calls (no arithmetic): it allocates torch
+    buffers once and forwards with the library.
+    """
+
+    def __init__(self, d, E, I, top_k, I_shared=0, dtype=FLEXMOE_BF16, norm_topk=1,
+                 max_tokens=1, device="cuda"):
+        import torch
+        self.desc = make_desc(d, E, I, top_k, I_shared, dtype, norm_topk, max_tokens)
+        self.tdtype = torch.bfloat16 if dtype == FLEXMOE_BF16 else torch.float32
+        self.device = device
+        self.keep = torch.full((E,), I, dtype=torch.int32, device=device)
+        nbytes = flexmoe_workspace_bytes(self.desc, max_tokens)
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        self.w_gate = self.w_up = self.w_down = None
+        self.ws_gate = self.ws_up = self.ws_down = None
+
+    def set_weights(self, w_gate, w_up, w_down, ws_gate=None, ws_up=None, ws_down=None):
+        self.w_gate, self.w_up, self.w_down = w_gate, w_up, w_down
+        self.ws_gate, self.ws_up, self.ws_down = ws_gate, ws_up, ws_down
+
+    def set_budget(self, keep_host, stream=None):
+        flexmoe_set_budget(self.desc, self.keep, keep_host, stream)
+
+    def forward(self, x, logits, y=None, keep=None, dbg=None, stream=None):
+        import torch
+        T = x.shape[0]
+        if y is None:
+            y = torch.empty((T, self.desc.d), dtype=self.tdtype, device=self.device)
+        flexmoe_layer_forward(self.desc, T, x, logits, self.w_gate, self.w_up, self.w_down,
+                              self.keep if keep is None else keep, self.ws_gate, self.ws_up,
+                              self.ws_down, y, self.workspace, dbg=dbg, stream=stream)
+        return y
+
+
+def to_device(a: np.ndarray, device="cuda"):
+    """NumPy array (fp32, int32, or uint16 bf16 bits) -> torch CUDA tensor."""
+    import torch
+    if a.dtype == np.uint16:
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(device).view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(a)).to(device)
+
+
+def to_host(t) -> np.ndarray:
+    """torch tensor -> NumPy (bf16 becomes uint16 bits)."""
+    import torch
+    t = t.detach().cpu()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy().view(np.uint16)
+    return t.numpy()

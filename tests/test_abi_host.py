@@ -1,0 +1,115 @@
+"""C ABI checks that need no GPU: the library loads, exports every function
+declared in include/flexmoe.h, and rejects bad arguments on the host before
+any device work (no call here reaches a kernel launch)."""
+import ctypes
+import math
+import os
+import re
+from fractions import Fraction
+
+import pytest
+
+from paper_2606_27866_amd import flexmoe as fm
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "flexmoe.h")
+FAKE = 0x100000  # never dereferenced: every call below fails its host checks first
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(flexmoe_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    L = fm.lib()
+    names = declared_functions()
+    assert set(names) == set(fm.EXPORTED)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def good_desc(**kw):
+    a = dict(d=64, E=8, I=128, top_k=2, I_shared=0, dtype=fm.FLEXMOE_BF16, norm_topk=1,
+             max_tokens=100)
+    a.update(kw)
+    return fm.make_desc(**a)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=7), -5),
+    (dict(d=60), -2), (dict(d=0), -2), (dict(I=100), -2), (dict(I_shared=12), -2),
+    (dict(I_shared=-8), -2), (dict(E=0), -2), (dict(E=257), -2), (dict(top_k=0), -2),
+    (dict(top_k=9), -2), (dict(E=32, top_k=17), -2), (dict(max_tokens=-1), -2),
+    (dict(norm_topk=2), -1), (dict(max_tokens=1 << 29), -2),
+])
+def test_bad_descriptor(kw, code):
+    desc = good_desc(**kw)
+    assert fm.lib().flexmoe_workspace_bytes(ctypes.byref(desc), 1) == 0
+    with pytest.raises(fm.FlexMoEError) as ei:
+        fm.flexmoe_layer_forward(desc, 1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, None,
+                                 FAKE, FAKE, workspace_bytes=1 << 40, stream=0)
+    assert ei.value.code == code
+
+
+def test_workspace_monotone_in_T():
+    desc = good_desc(I_shared=64)
+    sizes = [fm.flexmoe_workspace_bytes(desc, T) for T in (0, 1, 2, 63, 64, 65, 100)]
+    assert sizes == sorted(sizes)
+    assert all(s % 256 == 0 for s in sizes)
+    with pytest.raises(fm.FlexMoEError):
+        fm.flexmoe_workspace_bytes(desc, 101)
+
+
+def test_forward_argument_errors():
+    desc = good_desc()
+    need = fm.flexmoe_workspace_bytes(desc, 10)
+    f = fm.flexmoe_layer_forward
+
+    def call(T=10, x=FAKE, ws=FAKE, nbytes=need, shared=(None, None, None), y=FAKE, keep=FAKE):
+        f(desc, T, x, FAKE, FAKE, FAKE, FAKE, keep, *shared, y, ws, workspace_bytes=nbytes, stream=0)
+
+    for kwargs, code in [(dict(x=None), -1), (dict(y=None), -1), (dict(keep=None), -1),
+                         (dict(T=-1), -1), (dict(T=101), -2), (dict(nbytes=need - 1), -4),
+                         (dict(ws=None), -4), (dict(ws=FAKE + 8), -4),
+                         (dict(shared=(FAKE, FAKE, FAKE)), -1)]:
+        with pytest.raises(fm.FlexMoEError) as ei:
+            call(**kwargs)
+        assert ei.value.code == code, kwargs
+        assert fm.flexmoe_last_error()
+    call(T=0)  # T = 0 is a valid no-op: nothing is launched
+
+
+def test_shared_weights_required_iff_shared_expert():
+    desc = good_desc(I_shared=64)
+    need = fm.flexmoe_workspace_bytes(desc, 4)
+    with pytest.raises(fm.FlexMoEError) as ei:
+        fm.flexmoe_layer_forward(desc, 4, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE,
+                                 FAKE, FAKE, workspace_bytes=need, stream=0)
+    assert ei.value.code == -1
+
+
+def test_set_budget_rejects_out_of_range_on_host():
+    desc = good_desc()
+    for bad in ([0] * 7 + [129], [-1] + [0] * 7):
+        with pytest.raises(fm.FlexMoEError) as ei:
+            fm.flexmoe_set_budget(desc, FAKE, bad, stream=0)
+        assert ei.value.code == -3
+    with pytest.raises(fm.FlexMoEError) as ei:
+        fm.flexmoe_set_budget(desc, None, [1] * 8, stream=0)
+    assert ei.value.code == -1
+
+
+def test_rank_reorder_null_pointer():
+    with pytest.raises(fm.FlexMoEError) as ei:
+        fm.flexmoe_rank_reorder(good_desc(), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, stream=0)
+    assert ei.value.code == -1
+
+
+def test_keep_from_ratio_matches_exact_ceil():
+    for I in (14336, 2560, 1408, 512, 1000, 7):
+        for r in ("0.1", "0.4", "0.7", "1.0", "0.25", "0.5", "0.75", "0", "0.333"):
+            assert fm.flexmoe_keep_from_ratio(float(r), I) == math.ceil(Fraction(r) * I)
+    assert fm.flexmoe_keep_from_ratio(-0.1, 10) == -1
+    assert fm.flexmoe_keep_from_ratio(float("nan"), 10) == -1

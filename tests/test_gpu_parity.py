@@ -1,0 +1,206 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Bars: routing ids, counts, offsets, dispatch permutation and inverse are
+bit-exact; router weights within 1e-6; y within 2e-2 * max|ref| for bf16
+inputs and 1e-5 * max|ref| in fp32 mode (oracle in fp64, unrounded).
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_27866_amd import flexmoe as fm
+from paper_2606_27866_amd import synth
+from tests.gpu_util import (BF16_TOL, F32_TOL, GpuLayer, check_route, check_y, mini_layer,
+                            oracle_ref, say)
+
+pytestmark = pytest.mark.gpu
+
+
+def gpu_layer_for(cfg, w, s, max_tokens=None):
+    return GpuLayer(cfg.d, cfg.E, cfg.I, cfg.top_k, cfg.I_shared, cfg.dtype, cfg.norm_topk,
+                    max_tokens or cfg.T, *w, *s)
+
+
+def test_native_library_is_the_one_loaded():
+    L = fm.lib()
+    assert L._name.endswith("paper_2606_27866_amd/libflexmoe.so")
+
+
+# --------------------------------------------------------------------------
+# tiny fp32 layer: every keep table, 1e-5
+# --------------------------------------------------------------------------
+def tiny_tables(cfg):
+    t = dict(synth.config_keep_tables(cfg))
+    t["edges_a"] = np.array([0, 1, 15, 16, 17, 63, 64, 65], np.int32)
+    t["edges_b"] = np.array([cfg.I - 1, cfg.I, 0, 1, 17, 100, 511, 512], np.int32)
+    t["one_channel"] = np.ones(cfg.E, np.int32)
+    return t
+
+
+def test_tiny_fp32_all_tables():
+    cfg = synth.CONFIGS["tiny_fp32"]
+    x, lg = synth.make_tokens(cfg)
+    w = synth.make_expert_weights(cfg)
+    g = gpu_layer_for(cfg, w, (None, None, None))
+    for name, keep in tiny_tables(cfg).items():
+        say("tiny_fp32 table", name, keep.tolist())
+        y, r = g.forward(x, lg, keep)
+        ref, rr = oracle_ref(cfg, x, lg, w, (None, None, None), keep)
+        check_route(r, rr)
+        check_y(y, ref, F32_TOL)
+
+
+def test_tiny_fp32_zero_budget_is_exact_zero():
+    cfg = synth.CONFIGS["tiny_fp32"]
+    x, lg = synth.make_tokens(cfg)
+    w = synth.make_expert_weights(cfg)
+    g = gpu_layer_for(cfg, w, (None, None, None))
+    y, r = g.forward(x, lg, np.zeros(cfg.E, np.int32))
+    assert np.all(y == 0.0)
+    assert np.all(r["pos"] == -1) and r["offsets"][-1] == 0
+
+
+# --------------------------------------------------------------------------
+# bf16 layers of several tiles with ragged tails
+# --------------------------------------------------------------------------
+MINIS = [
+    # name, T, d, E, I, k, I_s, norm
+    ("m_a", 300, 256, 8, 320, 2, 0, 1),
+    ("m_b", 200, 512, 60, 192, 4, 256, 0),
+    ("m_topk_eq_E", 129, 128, 16, 136, 16, 0, 1),
+    ("m_top1", 77, 64, 5, 64, 1, 0, 1),
+    ("m_256_experts", 100, 64, 256, 64, 8, 64, 0),
+    ("m_shared_wide", 150, 192, 6, 72, 2, 520, 1),
+]
+
+
+@pytest.mark.parametrize("spec", MINIS, ids=[m[0] for m in MINIS])
+def test_bf16_mini(spec):
+    name, T, d, E, I, k, I_s, norm = spec
+    cfg, x, lg, w, s = mini_layer(name, T, d, E, I, k, I_s, norm=norm, config_id=60 + MINIS.index(spec))
+    g = gpu_layer_for(cfg, w, s)
+    rng = np.random.default_rng(len(name))
+    tables = [np.full(E, I, np.int32), rng.integers(0, I + 1, size=E).astype(np.int32)]
+    edge = np.array([0, 1, 15, 16, 17, 63, 64, 65, I - 1, I], np.int32)
+    tables.append(np.minimum(np.resize(edge, E), I))
+    for keep in tables:
+        say(name, "keep", keep[:12].tolist())
+        y, r = g.forward(x, lg, keep)
+        ref, rr = oracle_ref(cfg, x, lg, w, s, keep)
+        check_route(r, rr)
+        check_y(y, ref, BF16_TOL)
+
+
+@pytest.mark.parametrize("T", [1, 2, 63, 64, 65, 129])
+def test_bf16_token_counts(T):
+    cfg, x, lg, w, s = mini_layer("t%d" % T, 129, 128, 8, 96, 2, 64, config_id=70)
+    x, lg = x[:T], lg[:T]
+    g = gpu_layer_for(cfg, w, s, max_tokens=129)
+    keep = np.array([96, 0, 17, 64, 65, 1, 96, 33], np.int32)
+    y, r = g.forward(x, lg, keep)
+    ref, rr = oracle_ref(cfg, x, lg, w, s, keep)
+    check_route(r, rr)
+    check_y(y, ref, BF16_TOL)
+
+
+def test_all_tokens_on_one_expert_and_ties():
+    cfg, x, lg, w, s = mini_layer("skew", 257, 128, 8, 128, 2, 0, config_id=71)
+    g = gpu_layer_for(cfg, w, s)
+    keep = np.array([128, 77, 0, 128, 5, 64, 128, 1], np.int32)
+    cases = {
+        "one_expert": lg + np.array([50, 0, 0, 0, 0, 0, 0, 0], np.float32),
+        "quantised_ties": np.round(lg * 2) / 2,
+        "all_equal": np.zeros_like(lg),
+        "nan_logit": np.where(np.arange(lg.shape[1])[None, :] == 3, np.float32(np.nan), lg),
+    }
+    for name, l2 in cases.items():
+        say("routing case", name)
+        l2 = np.ascontiguousarray(l2, np.float32)
+        y, r = g.forward(x, l2, keep)
+        ref, rr = oracle_ref(cfg, x, l2, w, s, keep)
+        np.testing.assert_array_equal(r["topk_idx"], rr["idx"])
+        np.testing.assert_array_equal(r["perm"], rr["perm"])
+        np.testing.assert_array_equal(r["pos"], rr["pos"])
+        if name != "nan_logit":
+            check_route(r, rr)
+            check_y(y, ref, BF16_TOL)
+
+
+def test_zero_budget_bf16_exact_zero_and_shared_only():
+    cfg, x, lg, w, s = mini_layer("zero", 100, 128, 8, 64, 2, 0, config_id=72)
+    g = gpu_layer_for(cfg, w, s)
+    y, _ = g.forward(x, lg, np.zeros(cfg.E, np.int32))
+    assert np.all(y == 0.0)
+    cfg2, x2, lg2, w2, s2 = mini_layer("zero_sh", 100, 128, 8, 64, 2, 96, config_id=73)
+    g2 = gpu_layer_for(cfg2, w2, s2)
+    y2, _ = g2.forward(x2, lg2, np.zeros(cfg2.E, np.int32))
+    ref = oracle.layer_forward(x2, lg2, *w2, np.zeros(cfg2.E, np.int32), cfg2.top_k, 1, *s2)
+    check_y(y2, ref, BF16_TOL)
+
+
+def test_deterministic_bits():
+    cfg, x, lg, w, s = mini_layer("det", 333, 256, 16, 128, 4, 128, config_id=74)
+    g = gpu_layer_for(cfg, w, s)
+    keep = np.arange(16, dtype=np.int32) * 8
+    y1, r1 = g.forward(x, lg, keep)
+    y2, r2 = g.forward(x, lg, keep)
+    assert np.array_equal(y1, y2)
+    for k in r1:
+        assert np.array_equal(r1[k], r2[k])
+
+
+def test_budget_switch_stream_ordered():
+    """Five nested tables set with flexmoe_set_budget between forwards queued
+    on one stream with no host sync in between: each output matches the
+    oracle for its own table."""
+    import torch
+    cfg, x, lg, w, s = mini_layer("switch", 256, 256, 8, 256, 2, 128, config_id=75)
+    g = gpu_layer_for(cfg, w, s)
+    fam = synth.nested_keep_family(cfg.E, cfg.I, seed=99, grid=16)
+    xd, ld = fm.to_device(x), fm.to_device(lg)
+    ys = []
+    for keep in fam:
+        g.layer.set_budget(keep)
+        ys.append(g.layer.forward(xd, ld))
+    torch.cuda.synchronize()
+    for keep, yd in zip(fam, ys):
+        y = synth.bf16_bits_to_f32(fm.to_host(yd)).astype(np.float64)
+        ref = oracle.layer_forward(x, lg, *w, keep, cfg.top_k, cfg.norm_topk, *s)
+        check_y(y, ref, BF16_TOL)
+    # zero-copy switch: a different device keep table per forward
+    tables = [fm.to_device(k) for k in fam]
+    outs = [g.layer.forward(xd, ld, keep=t) for t in tables]
+    torch.cuda.synchronize()
+    for a, b in zip(ys, outs):
+        assert torch.equal(a, b)
+
+
+# --------------------------------------------------------------------------
+# rank + reorder (Eq. 3)
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+def test_rank_reorder(dtype):
+    import torch
+    cfg, x, lg, w, s = mini_layer("rr", 64, 128, 6, 200, 2, 0, dtype=dtype, config_id=76)
+    rng = np.random.default_rng(3)
+    scores = np.abs(rng.standard_normal((cfg.E, cfg.I))).astype(np.float32)
+    scores[1] = np.round(scores[1] * 4) / 4  # ties
+    scores[2, 7] = np.nan
+    wg_r, wu_r, wd_r, perm = oracle.rank_reorder(scores, *w)
+    desc = fm.make_desc(cfg.d, cfg.E, cfg.I, cfg.top_k, 0, dtype, cfg.norm_topk, cfg.T)
+    dev = [fm.to_device(a) for a in w]
+    outs = [torch.empty_like(t) for t in dev]
+    pd = torch.empty((cfg.E, cfg.I), dtype=torch.int32, device="cuda")
+    fm.flexmoe_rank_reorder(desc, fm.to_device(scores), *dev, *outs, pd)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(pd.cpu().numpy(), perm)
+    for o, ref in zip(outs, (wg_r, wu_r, wd_r)):
+        assert np.array_equal(fm.to_host(o), ref)
+    # permutation invariance on the GPU: ranked full layer == original full layer
+    full = np.full(cfg.E, cfg.I, np.int32)
+    g0 = gpu_layer_for(cfg, w, s)
+    g1 = gpu_layer_for(cfg, (wg_r, wu_r, wd_r), s)
+    y0, _ = g0.forward(x, lg, full)
+    y1, _ = g1.forward(x, lg, full)
+    tol = F32_TOL if dtype == synth.F32 else BF16_TOL
+    check_y(y1, y0, tol)
