@@ -58,6 +58,11 @@ def lib():
         if not os.path.exists(LIB):
             raise RuntimeError("libflexmoe.so is not built (%s); run "
                                "`python -m paper_2606_27866_amd.build`" % LIB)
+        # torch ships its own HIP runtime (soname libamdhip64.so.7).  Loading
+        # torch first makes the library's libamdhip64.so.7 dependency resolve
+        # to that same runtime, so device pointers and streams are shared; a
+        # second runtime in the process would not see the GPU.
+        import torch  # noqa: F401
         L = ctypes.CDLL(LIB)
         vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
         D = ctypes.POINTER(flexmoe_layer_desc)

@@ -113,3 +113,13 @@ def test_keep_from_ratio_matches_exact_ceil():
             assert fm.flexmoe_keep_from_ratio(float(r), I) == math.ceil(Fraction(r) * I)
     assert fm.flexmoe_keep_from_ratio(-0.1, 10) == -1
     assert fm.flexmoe_keep_from_ratio(float("nan"), 10) == -1
+
+
+def test_one_hip_runtime_in_process():
+    """The library must share torch's HIP runtime (a second copy would not see
+    the GPU and could not use torch's pointers and streams)."""
+    fm.lib()
+    maps = open("/proc/self/maps").read()
+    hips = set(re.findall(r"\S*libamdhip64\S*", maps))
+    hsas = set(re.findall(r"\S*libhsa-runtime64\S*", maps))
+    assert len(hips) == 1 and len(hsas) == 1, (hips, hsas)
