@@ -1,0 +1,303 @@
+#!/usr/bin/env python3
+"""Benchmark of the masked MoE-layer forward (FlexMoE online clipping) on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--table NAME]
+
+A step is one flexmoe_layer_forward: routing, dispatch, the gate/up GEMM with
+fused SwiGLU (routed experts truncated to k_e channels, plus the shared
+expert), the down GEMM and the weighted combine.  Inputs are seeded synthetic
+tensors already resident in HBM; the weights are rotated over --copies
+device copies so that no step finds them in the 256 MB last-level cache.
+
+Prints ONE JSON line on stdout.  `value` is tokens/s of the whole layer;
+`roofline` describes the dominant kernel (the gate/up GEMM) with its
+algorithmic flops or bytes per launch over its average launch time, measured
+with HIP events around that kernel inside the timed region; `cpu_baseline` is
+the CPU oracle timed on a bounded sample of the same workload.  Per-budget
+results (the nested 100/80/60/40/20 % tables) go into `per_budget`.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3      # MI355X fp32 vector
+PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
+RIDGE = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="qwen15_moe_a27b")
+    ap.add_argument("--table", default=None, help="keep table (default: the workload's own, else kept100)")
+    ap.add_argument("--decode-T", type=int, default=1, help="tokens per step of the decode workload")
+    ap.add_argument("--copies", type=int, default=3, help="weight copies rotated over the steps")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-per-budget", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-baseline work")
+    return ap.parse_args()
+
+
+def kernel_src_hash():
+    h = hashlib.sha256()
+    for f in ("gemm_bf16.hip", "common.h", "kernels.h"):
+        h.update(open(os.path.join(ROOT, "paper_2606_27866_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(workload, table):
+    """HBM bytes per gate/up-GEMM launch from committed rocprofv3 counter
+    runs, or None if absent or taken on a different kernel source."""
+    path = os.path.join(ROOT, "profiles", "gate_up_gemm_traffic_%s.json" % workload)
+    if not os.path.exists(path):
+        return None
+    d = json.load(open(path))
+    if d.get("kernel_src_sha") != kernel_src_hash() or d.get("table") != table:
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+class Workload:
+    """Host inputs + device copies of one layer configuration."""
+
+    def __init__(self, cfg, table_name, copies, decode_T=None):
+        import torch
+        from paper_2606_27866_amd import flexmoe as fm
+        from paper_2606_27866_amd import synth
+        self.cfg, self.fm, self.synth, self.torch = cfg, fm, synth, torch
+        t0 = time.time()
+        self.tables = synth.config_keep_tables(cfg)
+        if table_name is None:
+            table_name = "own" if "own" in self.tables else "kept100"
+        self.table_name = table_name
+        self.decode = decode_T is not None
+        self.T = decode_T if self.decode else cfg.T
+        bias = synth.router_bias(cfg)
+        if self.decode:
+            self.batches = [synth.make_tokens(cfg, T=self.T, batch=b, bias=bias) for b in range(64)]
+        else:
+            self.batches = [synth.make_tokens(cfg, bias=bias)]
+        self.w = synth.make_expert_weights(cfg)
+        self.s = synth.make_shared_weights(cfg)
+        log("[bench] host inputs ready in %.1fs" % (time.time() - t0))
+        self.layer = fm.Layer(cfg.d, cfg.E, cfg.I, cfg.top_k, cfg.I_shared, cfg.dtype, cfg.norm_topk,
+                              max_tokens=self.T)
+        dev_w = [fm.to_device(a) for a in self.w]
+        dev_s = [fm.to_device(a) if a is not None else None for a in self.s]
+        self.copies = [(dev_w, dev_s)]
+        for _ in range(copies - 1):
+            self.copies.append(([t.clone() for t in dev_w], [t.clone() if t is not None else None for t in dev_s]))
+        self.xd = [(fm.to_device(x), fm.to_device(lg)) for x, lg in self.batches]
+        self.y = torch.empty((self.T, cfg.d), dtype=self.layer.tdtype, device="cuda")
+        self.keep_dev = {n: fm.to_device(t) for n, t in self.tables.items()}
+        torch.cuda.synchronize()
+        log("[bench] device buffers ready (%d weight copies) in %.1fs" % (copies, time.time() - t0))
+
+    def use_copy(self, i):
+        w, s = self.copies[i % len(self.copies)]
+        self.layer.set_weights(*w, *s)
+
+    def counts(self, batch, keep_name):
+        """Per-expert routed token counts n_e from the GPU's own dispatch."""
+        torch = self.torch
+        c = torch.empty(self.cfg.E, dtype=torch.int32, device="cuda")
+        x, lg = self.xd[batch]
+        self.use_copy(0)
+        self.layer.forward(x, lg, y=self.y, keep=self.keep_dev[keep_name], dbg={"counts": c})
+        torch.cuda.synchronize()
+        return c.cpu().numpy().astype(np.int64)
+
+    def algorithmic(self, n, keep):
+        """Flops and HBM bytes of the whole layer and of the gate/up GEMM."""
+        cfg = self.cfg
+        d, Is, T = cfg.d, cfg.I_shared, self.T
+        sw = 2 if cfg.dtype == self.synth.BF16 else 4
+        k = keep.astype(np.int64)
+        act = (n > 0) & (k > 0)
+        nk = int((n * k)[act].sum())
+        F = 6 * d * nk + 6 * d * T * Is
+        B = 3 * d * int(k[act].sum()) * sw + 3 * d * Is * sw + 2 * T * d * sw + 4 * T * cfg.E
+        F1 = 4 * d * (nk + T * Is)
+        B1 = 2 * d * (int(k[act].sum()) + Is) * sw + T * d * sw + (nk + T * Is) * sw
+        lw_keep = float((n * k).sum()) / max(1, int(n.sum()) * cfg.I)
+        return dict(F=F, B=B, F1=F1, B1=B1, load_weighted_keep=lw_keep)
+
+    def run(self, steps, keep_names, with_kernel_times=False):
+        """Time `steps` forwards; the keep table cycles over keep_names (one
+        budget switch per step when there are several)."""
+        torch, fm = self.torch, self.fm
+        switching = len(keep_names) > 1
+        if with_kernel_times:
+            fm.flexmoe_timing_enable(True)
+        torch.cuda.synchronize()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        ev0.record()
+        for i in range(steps):
+            self.use_copy(i)
+            if switching:
+                self.layer.set_budget(self.tables[keep_names[i % len(keep_names)]])
+                keep = None
+            else:
+                keep = self.keep_dev[keep_names[0]]
+            x, lg = self.xd[i % len(self.xd)]
+            self.layer.forward(x, lg, y=self.y, keep=keep)
+        ev1.record()
+        torch.cuda.synchronize()
+        ms = ev0.elapsed_time(ev1)
+        kt = None
+        if with_kernel_times:
+            kt = fm.flexmoe_timing_read()
+            fm.flexmoe_timing_enable(False)
+        return ms, kt
+
+
+def cpu_baseline(wl, keep, target_s):
+    """The oracle, untouched, on the first S tokens of the workload."""
+    import oracle
+    cfg = wl.cfg
+    x, lg = wl.batches[0]
+    s = wl.s
+
+    def run(S):
+        t0 = time.time()
+        oracle.layer_forward(x[:S], lg[:S], *wl.w, keep, cfg.top_k, cfg.norm_topk, *s)
+        return time.time() - t0
+
+    S0 = min(8, x.shape[0])
+    t0 = run(S0)
+    S = int(min(x.shape[0], max(S0, S0 * target_s / max(t0, 1e-3))))
+    t = run(S) if S != S0 else t0
+    return dict(value=S / t, unit="tokens/s", cores=oracle.num_threads(), kind="oracle",
+                sample="first %d of %d tokens of the workload, same weights and keep table, "
+                       "%.1f s (fp64 accumulation)" % (S, x.shape[0], t))
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the layer shards by tokens or experts; see the design notes). Run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2606_27866_amd import flexmoe as fm
+    from paper_2606_27866_amd import synth
+    torch.cuda.set_device(0)
+    fm.lib()
+    cfg = synth.CONFIGS[args.workload]
+    decode_T = args.decode_T if args.workload == "qwen2_57b_a14b_decode" else None
+    wl = Workload(cfg, args.table, args.copies, decode_T)
+    bf16 = cfg.dtype == synth.BF16
+
+    if wl.decode:
+        # decode: a pool of 64 batches, the 5 nested tables switching every step
+        names = ["kept%d" % int(round(f * 100)) for f in synth.NESTED_FRACTIONS]
+        per = []
+        for b in range(min(64, args.steps + args.warmup)):
+            n = wl.counts(b, names[b % len(names)])
+            per.append(wl.algorithmic(n, wl.tables[names[b % len(names)]]))
+        alg = {k: float(np.mean([p[k] for p in per])) for k in per[0]}
+        keep_names = names
+    else:
+        n = wl.counts(0, wl.table_name)
+        alg = wl.algorithmic(n, wl.tables[wl.table_name])
+        keep_names = [wl.table_name]
+
+    wl.run(args.warmup, keep_names)
+    ms, kt = wl.run(args.steps, keep_names, with_kernel_times=True)
+    ms_step = ms / args.steps
+    value = wl.T * args.steps / (ms / 1e3)
+    log("[bench] %s: %.4f ms/step, %.0f tokens/s" % (args.workload, ms_step, value))
+    for kname, (kms, cnt) in kt.items():
+        if cnt:
+            log("[bench]   %-17s %8.4f ms avg over %d launches" % (kname, kms / cnt, cnt))
+
+    gu_ms, gu_n = kt["gate_up"]
+    gu_avg = gu_ms / max(gu_n, 1)
+    intensity = alg["F1"] / alg["B1"]
+    peak_flops = PEAK_BF16_TFLOPS if bf16 else PEAK_F32_TFLOPS
+    if intensity >= RIDGE and not wl.decode:
+        roof = dict(bound="mfma", achieved=alg["F1"] / (gu_avg / 1e3) / 1e12, peak=peak_flops,
+                    unit="TFLOP/s")
+    else:
+        roof = dict(bound="hbm", achieved=alg["B1"] / (gu_avg / 1e3) / 1e9, peak=PEAK_HBM_GBS,
+                    unit="GB/s")
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = load_traffic(args.workload, wl.table_name) if not wl.decode else None
+    roof["kernel"] = "gate_up GEMM (gemm1_bf16_kernel)" if bf16 else "gate_up GEMM (gemm1_f32_kernel)"
+    roof["avg_launch_ms"] = gu_avg
+
+    layer_s = ms_step / 1e3
+    layer = dict(tflops=alg["F"] / layer_s / 1e12, frac_mfma=alg["F"] / layer_s / 1e12 / peak_flops,
+                 gbs=alg["B"] / layer_s / 1e9, frac_hbm=alg["B"] / layer_s / 1e9 / PEAK_HBM_GBS,
+                 flops_per_step=alg["F"], bytes_per_step=alg["B"],
+                 load_weighted_keep=alg["load_weighted_keep"],
+                 kernels_ms={k: v[0] / max(v[1], 1) for k, v in kt.items()})
+
+    per_budget = None
+    if not args.no_per_budget and not wl.decode:
+        per_budget = []
+        steps_b = max(5, args.steps // 2)
+        for name in ["kept%d" % int(round(f * 100)) for f in synth.NESTED_FRACTIONS]:
+            nb = wl.counts(0, name)
+            a = wl.algorithmic(nb, wl.tables[name])
+            wl.run(2, [name])
+            msb, _ = wl.run(steps_b, [name])
+            sb = msb / steps_b / 1e3
+            per_budget.append(dict(table=name, kept=synth.keep_fraction(wl.tables[name], cfg.I),
+                                   ms=sb * 1e3, tokens_per_s=wl.T / sb,
+                                   tflops=a["F"] / sb / 1e12,
+                                   frac_mfma=a["F"] / sb / 1e12 / peak_flops,
+                                   frac_hbm=a["B"] / sb / 1e9 / PEAK_HBM_GBS))
+            log("[bench]   budget %-7s %.4f ms  %.0f tok/s  %.1f TFLOP/s" %
+                (name, sb * 1e3, wl.T / sb, a["F"] / sb / 1e12))
+
+    cpu = None
+    if not args.no_cpu:
+        log("[bench] CPU oracle baseline ...")
+        cpu = cpu_baseline(wl, wl.tables[keep_names[0]], args.cpu_seconds)
+        log("[bench] CPU oracle: %.2f tokens/s on %d threads" % (cpu["value"], cpu["cores"]))
+
+    out = {
+        "metric": "masked MoE-layer tokens/s + % bf16 MFMA peak / % HBM BW, per budget",
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if bf16 else "f32",
+        "data": "synthetic (seeded PCG64; random-init weights of the layer's shape)",
+        "config": {"workload": args.workload, "T": wl.T, "d": cfg.d, "E": cfg.E, "I": cfg.I,
+                   "top_k": cfg.top_k, "I_shared": cfg.I_shared,
+                   "keep_table": "+".join(keep_names) if wl.decode else wl.table_name,
+                   "weight_copies": args.copies},
+        "roofline": roof,
+        "layer": layer,
+        "per_budget": per_budget,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

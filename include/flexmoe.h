@@ -23,6 +23,8 @@
  *     an argument error has enqueued nothing.  Device-resident data (logits,
  *     keep counts) is not inspected by the host; keep counts read on the device
  *     are clamped to [0, I] so that no access leaves its buffer.
+ *   - x, weights and y must be 16-byte aligned; logits and keep arrays 4-byte
+ *     aligned (FLEXMOE_EINVAL otherwise); the workspace 256-byte aligned.
  *
  * Element types: dtype FLEXMOE_F32 (x, weights and y in fp32) or FLEXMOE_BF16
  * (x, weights and y in bf16).  Router logits are always fp32.  Accumulation is
@@ -148,6 +150,30 @@ int flexmoe_layer_forward(const flexmoe_layer_desc *desc, int32_t T, const void 
  * 1e-9 absorbs the binary representation error of decimal ratios (0.7 * 1000
  * gives 700).  Returns -1 for r outside [0, 1], NaN, or I < 1. */
 int flexmoe_keep_from_ratio(double r, int32_t I);
+
+/* Per-kernel timing, a measurement aid for benchmarks.  flexmoe_timing_enable(1)
+ * clears the accumulators and makes every later forward record a HIP event
+ * pair around each of its kernels, on the forward's stream;
+ * flexmoe_timing_enable(0) stops recording.  flexmoe_timing_read waits for
+ * every recorded event, writes the summed durations (milliseconds) and launch
+ * counts per kernel into *out (indexed by FLEXMOE_K_*) and clears the
+ * accumulators.  Recording costs two event records per kernel; it creates
+ * events (host-side HIP objects) on first use and reuses them afterwards. */
+enum {
+    FLEXMOE_K_ROUTE = 0,          /* top-k routing + chunk histograms          */
+    FLEXMOE_K_DISPATCH_SCAN = 1,  /* per-expert scan of the histograms         */
+    FLEXMOE_K_DISPATCH_SCATTER = 2, /* stable permutation, segment/tile tables */
+    FLEXMOE_K_GATE_UP = 3,        /* gate/up GEMM with fused SwiGLU            */
+    FLEXMOE_K_DOWN = 4,           /* down GEMM                                 */
+    FLEXMOE_K_COMBINE = 5,        /* weighted combine + shared add             */
+    FLEXMOE_K_COUNT = 6
+};
+typedef struct flexmoe_kernel_times {
+    double ms[8];
+    int64_t launches[8];
+} flexmoe_kernel_times;
+int flexmoe_timing_enable(int on);
+int flexmoe_timing_read(flexmoe_kernel_times *out);
 
 /* Message for the last non-zero return on this thread ("" if none). */
 const char *flexmoe_last_error(void);

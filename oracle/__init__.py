@@ -56,8 +56,9 @@ def lib():
         L.oracle_layer_forward.argtypes = [i] * 8 + [p] * 16
         L.oracle_rank_reorder.argtypes = [i, i, i, i] + [p] * 8
         L.oracle_keep_from_ratio.argtypes = [ctypes.c_double, i]
+        L.oracle_num_threads.argtypes = []
         for f in (L.oracle_route, L.oracle_dispatch, L.oracle_layer_forward,
-                  L.oracle_rank_reorder, L.oracle_keep_from_ratio):
+                  L.oracle_rank_reorder, L.oracle_keep_from_ratio, L.oracle_num_threads):
             f.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -173,3 +174,7 @@ def rank_reorder(scores, w_gate, w_up, w_down):
 
 def keep_from_ratio(r: float, I: int) -> int:
     return int(lib().oracle_keep_from_ratio(float(r), int(I)))
+
+
+def num_threads() -> int:
+    return int(lib().oracle_num_threads())

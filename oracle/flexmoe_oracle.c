@@ -40,6 +40,7 @@
  * Element type of x and weights: dtype 0 = fp32, 1 = bf16 (raw bits).
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -358,4 +359,10 @@ int oracle_keep_from_ratio(double r, int I)
     if (k > I)
         k = I;
     return (int)k;
+}
+
+/* Threads the OpenMP loops above run with (reported next to CPU timings). */
+int oracle_num_threads(void)
+{
+    return omp_get_max_threads();
 }

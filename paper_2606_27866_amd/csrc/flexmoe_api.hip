@@ -13,6 +13,8 @@
 #include <string.h>
 
 #include <cmath>
+#include <mutex>
+#include <vector>
 
 #include "../../include/flexmoe.h"
 #include "kernels.h"
@@ -107,9 +109,84 @@ long long routed_row_tiles_ub(int T, int E, int k, int bm) {
     return a < b ? a : b;
 }
 
+// ---- optional per-kernel event timing --------------------------------------
+struct TimedLaunch {
+    int kernel;
+    hipEvent_t start, stop;
+};
+std::mutex g_tmu;
+bool g_timing = false;
+std::vector<TimedLaunch> g_pending;
+std::vector<hipEvent_t> g_free_events;
+double g_ms[8];
+int64_t g_launches[8];
+
+hipEvent_t take_event() {
+    if (!g_free_events.empty()) {
+        hipEvent_t e = g_free_events.back();
+        g_free_events.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+// Brackets one kernel launch with an event pair when timing is on.
+struct KernelTimer {
+    int kernel;
+    hipStream_t s;
+    hipEvent_t a = nullptr, b = nullptr;
+    KernelTimer(int k, hipStream_t st) : kernel(k), s(st) {
+        std::lock_guard<std::mutex> g(g_tmu);
+        if (!g_timing) return;
+        a = take_event();
+        b = take_event();
+        if (a && b) hipEventRecord(a, s);
+    }
+    ~KernelTimer() {
+        if (!a || !b) return;
+        hipEventRecord(b, s);
+        std::lock_guard<std::mutex> g(g_tmu);
+        g_pending.push_back({kernel, a, b});
+    }
+};
+
 }  // namespace
 
 extern "C" {
+
+int flexmoe_timing_enable(int on) {
+    std::lock_guard<std::mutex> g(g_tmu);
+    g_timing = on != 0;
+    if (g_timing) {
+        for (int i = 0; i < 8; ++i) g_ms[i] = 0.0, g_launches[i] = 0;
+    }
+    return FLEXMOE_OK;
+}
+
+int flexmoe_timing_read(flexmoe_kernel_times* out) {
+    if (!out) return fail(FLEXMOE_EINVAL, "timing_read: out is NULL");
+    std::lock_guard<std::mutex> g(g_tmu);
+    for (const TimedLaunch& t : g_pending) {
+        hipError_t err = hipEventSynchronize(t.stop);
+        float ms = 0.f;
+        if (err == hipSuccess) err = hipEventElapsedTime(&ms, t.start, t.stop);
+        if (err != hipSuccess) return hip_fail(err, "timing_read");
+        g_ms[t.kernel] += ms;
+        g_launches[t.kernel] += 1;
+        g_free_events.push_back(t.start);
+        g_free_events.push_back(t.stop);
+    }
+    g_pending.clear();
+    for (int i = 0; i < 8; ++i) {
+        out->ms[i] = g_ms[i];
+        out->launches[i] = g_launches[i];
+        g_ms[i] = 0.0;
+        g_launches[i] = 0;
+    }
+    return FLEXMOE_OK;
+}
 
 const char* flexmoe_last_error(void) { return g_err; }
 
@@ -212,14 +289,26 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
     const TileShape ts = bf16 ? TileShape{kBf16BM1, kBf16BN1, kBf16BM2, kBf16BN2}
                               : TileShape{kF32BM, kF32BN, kF32BM, kF32BN};
 
-    route_kernel<<<NB, 256, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, idx, wts, blockcnt, NB);
-    hipError_t err = hipGetLastError();
+    hipError_t err;
+    {
+        KernelTimer kt(FLEXMOE_K_ROUTE, s);
+        route_kernel<<<NB, 256, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, idx, wts, blockcnt, NB);
+        err = hipGetLastError();
+    }
     if (err != hipSuccess) return hip_fail(err, "route launch");
-    dispatch_scan_kernel<<<D.E, 256, 0, s>>>(blockcnt, NB, blockbase, counts);
-    if ((err = hipGetLastError()) != hipSuccess) return hip_fail(err, "dispatch scan launch");
-    dispatch_scatter_kernel<<<NB, 64, 0, s>>>(idx, keep_dev, counts, blockbase, T, D.E, D.top_k, D.I,
-                                              D.I_shared, D.d, NB, ts, perm, pos, offsets, seg, t1, t2);
-    if ((err = hipGetLastError()) != hipSuccess) return hip_fail(err, "dispatch scatter launch");
+    {
+        KernelTimer kt(FLEXMOE_K_DISPATCH_SCAN, s);
+        dispatch_scan_kernel<<<D.E, 256, 0, s>>>(blockcnt, NB, blockbase, counts);
+        err = hipGetLastError();
+    }
+    if (err != hipSuccess) return hip_fail(err, "dispatch scan launch");
+    {
+        KernelTimer kt(FLEXMOE_K_DISPATCH_SCATTER, s);
+        dispatch_scatter_kernel<<<NB, 64, 0, s>>>(idx, keep_dev, counts, blockbase, T, D.E, D.top_k, D.I,
+                                                  D.I_shared, D.d, NB, ts, perm, pos, offsets, seg, t1, t2);
+        err = hipGetLastError();
+    }
+    if (err != hipSuccess) return hip_fail(err, "dispatch scatter launch");
 
     // grid upper bounds from host-known sizes
     const long long rt1 = routed_row_tiles_ub(T, D.E, D.top_k, ts.bm1);
@@ -237,24 +326,43 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
                                (const bf16_t*)ws_gate, (const bf16_t*)ws_up, perm, seg, t1,
                                (bf16_t*)(ws + L.H), (bf16_t*)(ws + L.Hs), D.d, D.I, D.I_shared, D.E,
                                D.top_k, nseg, T};
-        if ((err = launch_gemm1_bf16(p1, (int)g1, s)) != hipSuccess) return hip_fail(err, "gate/up GEMM launch");
+        {
+            KernelTimer kt(FLEXMOE_K_GATE_UP, s);
+            err = launch_gemm1_bf16(p1, (int)g1, s);
+        }
+        if (err != hipSuccess) return hip_fail(err, "gate/up GEMM launch");
         Gemm2Params<bf16_t> p2{(const bf16_t*)(ws + L.H), (const bf16_t*)(ws + L.Hs),
                                (const bf16_t*)w_down_r, (const bf16_t*)ws_down, seg, t2, O, Os, D.d,
                                D.I, D.I_shared, D.E, nseg};
-        if ((err = launch_gemm2_bf16(p2, (int)g2, s)) != hipSuccess) return hip_fail(err, "down GEMM launch");
+        {
+            KernelTimer kt(FLEXMOE_K_DOWN, s);
+            err = launch_gemm2_bf16(p2, (int)g2, s);
+        }
+        if (err != hipSuccess) return hip_fail(err, "down GEMM launch");
     } else {
         Gemm1Params<float> p1{(const float*)x, (const float*)w_gate_r, (const float*)w_up_r,
                               (const float*)ws_gate, (const float*)ws_up, perm, seg, t1,
                               (float*)(ws + L.H), (float*)(ws + L.Hs), D.d, D.I, D.I_shared, D.E,
                               D.top_k, nseg, T};
-        if ((err = launch_gemm1_f32(p1, (int)g1, s)) != hipSuccess) return hip_fail(err, "gate/up GEMM launch");
+        {
+            KernelTimer kt(FLEXMOE_K_GATE_UP, s);
+            err = launch_gemm1_f32(p1, (int)g1, s);
+        }
+        if (err != hipSuccess) return hip_fail(err, "gate/up GEMM launch");
         Gemm2Params<float> p2{(const float*)(ws + L.H), (const float*)(ws + L.Hs),
                               (const float*)w_down_r, (const float*)ws_down, seg, t2, O, Os, D.d, D.I,
                               D.I_shared, D.E, nseg};
-        if ((err = launch_gemm2_f32(p2, (int)g2, s)) != hipSuccess) return hip_fail(err, "down GEMM launch");
+        {
+            KernelTimer kt(FLEXMOE_K_DOWN, s);
+            err = launch_gemm2_f32(p2, (int)g2, s);
+        }
+        if (err != hipSuccess) return hip_fail(err, "down GEMM launch");
     }
-    if ((err = launch_combine(O, Os, pos, wts, T, D.top_k, D.d, has_shared ? 1 : 0, D.dtype, y, s)) != hipSuccess)
-        return hip_fail(err, "combine launch");
+    {
+        KernelTimer kt(FLEXMOE_K_COMBINE, s);
+        err = launch_combine(O, Os, pos, wts, T, D.top_k, D.d, has_shared ? 1 : 0, D.dtype, y, s);
+    }
+    if (err != hipSuccess) return hip_fail(err, "combine launch");
 
     if (dbg) {
         const size_t A = (size_t)T * D.top_k;

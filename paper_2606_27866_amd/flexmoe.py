@@ -29,7 +29,11 @@ ERRORS = {
 }
 
 EXPORTED = ("flexmoe_workspace_bytes", "flexmoe_rank_reorder", "flexmoe_set_budget",
-            "flexmoe_layer_forward", "flexmoe_keep_from_ratio", "flexmoe_last_error")
+            "flexmoe_layer_forward", "flexmoe_keep_from_ratio", "flexmoe_last_error",
+            "flexmoe_timing_enable", "flexmoe_timing_read")
+
+# kernel indices of flexmoe_kernel_times
+KERNELS = ("route", "dispatch_scan", "dispatch_scatter", "gate_up", "down", "combine")
 
 
 class FlexMoEError(RuntimeError):
@@ -41,6 +45,10 @@ class FlexMoEError(RuntimeError):
 class flexmoe_layer_desc(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in
                 ("d", "E", "I", "top_k", "I_shared", "dtype", "norm_topk", "max_tokens")]
+
+
+class flexmoe_kernel_times(ctypes.Structure):
+    _fields_ = [("ms", ctypes.c_double * 8), ("launches", ctypes.c_int64 * 8)]
 
 
 class flexmoe_route_out(ctypes.Structure):
@@ -76,6 +84,10 @@ def lib():
         L.flexmoe_layer_forward.restype = ctypes.c_int
         L.flexmoe_keep_from_ratio.argtypes = [ctypes.c_double, i32]
         L.flexmoe_keep_from_ratio.restype = ctypes.c_int
+        L.flexmoe_timing_enable.argtypes = [ctypes.c_int]
+        L.flexmoe_timing_enable.restype = ctypes.c_int
+        L.flexmoe_timing_read.argtypes = [ctypes.POINTER(flexmoe_kernel_times)]
+        L.flexmoe_timing_read.restype = ctypes.c_int
         L.flexmoe_last_error.argtypes = []
         L.flexmoe_last_error.restype = ctypes.c_char_p
         _lib = L
@@ -109,6 +121,17 @@ def make_desc(d, E, I, top_k, I_shared=0, dtype=FLEXMOE_BF16, norm_topk=1, max_t
 
 def flexmoe_last_error() -> str:
     return lib().flexmoe_last_error().decode()
+
+
+def flexmoe_timing_enable(on: bool):
+    _check(lib().flexmoe_timing_enable(1 if on else 0))
+
+
+def flexmoe_timing_read():
+    """{kernel name: (total ms, launches)} since the last enable/read."""
+    t = flexmoe_kernel_times()
+    _check(lib().flexmoe_timing_read(ctypes.byref(t)))
+    return {n: (t.ms[i], int(t.launches[i])) for i, n in enumerate(KERNELS)}
 
 
 def flexmoe_keep_from_ratio(r: float, I: int) -> int:
