@@ -9,7 +9,7 @@ namespace flexmoe {
 constexpr int kWave = 64;
 constexpr int kMaxExperts = 256;
 constexpr int kMaxTopK = 16;
-constexpr int kRouteTokens = 64;   // tokens per routing block (= dispatch chunk)
+constexpr int kRouteTokens = 16;   // tokens per routing block (= dispatch chunk)
 
 typedef uint16_t bf16_t;           // raw bf16 bits in memory
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));

@@ -292,7 +292,7 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
     hipError_t err;
     {
         KernelTimer kt(FLEXMOE_K_ROUTE, s);
-        route_kernel<<<NB, 256, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, idx, wts, blockcnt, NB);
+        route_kernel<<<NB, 64 * kRouteTokens, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, idx, wts, blockcnt, NB);
         err = hipGetLastError();
     }
     if (err != hipSuccess) return hip_fail(err, "route launch");

@@ -24,27 +24,35 @@ __device__ __forceinline__ bool route_before(float va, int ia, float vb, int ib)
     return ia < ib;
 }
 
-__global__ __launch_bounds__(256) void route_kernel(const float* __restrict__ logits, int T, int E,
-                                                    int k, int norm_topk, int32_t* __restrict__ idx,
-                                                    float* __restrict__ wts,
-                                                    int32_t* __restrict__ blockcnt, int NB) {
+// One chunk of kRouteTokens tokens per workgroup, one wave per token.
+constexpr int kRouteWaves = kRouteTokens;
+constexpr int kTokPerWave = 1;
+
+__global__ __launch_bounds__(64 * kRouteWaves) void route_kernel(
+    const float* __restrict__ logits, int T, int E, int k, int norm_topk,
+    int32_t* __restrict__ idx, float* __restrict__ wts, int32_t* __restrict__ blockcnt, int NB) {
     __shared__ int hist[kMaxExperts];
     for (int e = threadIdx.x; e < E; e += blockDim.x) hist[e] = 0;
-    __syncthreads();
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int t0 = blockIdx.x * kRouteTokens;
-    for (int tt = wave; tt < kRouteTokens; tt += 4) {
-        const int t = t0 + tt;
-        if (t >= T) break;  // uniform across the wave
-        const float* l = logits + (size_t)t * E;
-        float v[4];
-        bool taken[4];
+    const int t0 = blockIdx.x * kRouteTokens + wave;
+    float v[kTokPerWave][4];
+#pragma unroll
+    for (int i = 0; i < kTokPerWave; ++i) {
+        const int t = t0 + i * kRouteWaves;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int e = lane + 64 * q;
-            taken[q] = e >= E;
-            v[q] = e < E ? l[e] : 0.0f;
+            v[i][q] = (t < T && e < E) ? logits[(size_t)t * E + e] : 0.0f;
         }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kTokPerWave; ++i) {
+        const int t = t0 + i * kRouteWaves;
+        if (t >= T) break;  // uniform across the wave
+        bool taken[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) taken[q] = lane + 64 * q >= E;
         int my_id = 0;
         float my_logit = 0.0f, m = 0.0f;
         for (int j = 0; j < k; ++j) {
@@ -53,8 +61,8 @@ __global__ __launch_bounds__(256) void route_kernel(const float* __restrict__ lo
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 const int e = lane + 64 * q;
-                if (!taken[q] && (bi < 0 || route_before(v[q], e, bv, bi))) {
-                    bv = v[q];
+                if (!taken[q] && (bi < 0 || route_before(v[i][q], e, bv, bi))) {
+                    bv = v[i][q];
                     bi = e;
                 }
             }
@@ -81,7 +89,7 @@ __global__ __launch_bounds__(256) void route_kernel(const float* __restrict__ lo
         float z = 0.0f;
 #pragma unroll
         for (int q = 0; q < 4; ++q)
-            if (lane + 64 * q < E) z += expf(v[q] - m);
+            if (lane + 64 * q < E) z += expf(v[i][q] - m);
         z = wave_sum_f(z);
         float w = lane < k ? expf(my_logit - m) / z : 0.0f;
         if (norm_topk) w = w / wave_sum_f(w);
@@ -95,24 +103,40 @@ __global__ __launch_bounds__(256) void route_kernel(const float* __restrict__ lo
     for (int e = threadIdx.x; e < E; e += blockDim.x) blockcnt[(size_t)e * NB + blockIdx.x] = hist[e];
 }
 
+// Per expert: exclusive scan of its chunk counts.  Thread i owns a run of
+// consecutive chunks, so all loads are in flight together.
 __global__ __launch_bounds__(256) void dispatch_scan_kernel(const int32_t* __restrict__ blockcnt,
                                                             int NB, int32_t* __restrict__ blockbase,
                                                             int32_t* __restrict__ counts) {
+    constexpr int kPer = 16;  // chunks per thread per round
     __shared__ int wsum[4];
     __shared__ int carry;
     const int e = blockIdx.x;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int32_t* src = blockcnt + (size_t)e * NB;
+    int32_t* dst = blockbase + (size_t)e * NB;
     if (threadIdx.x == 0) carry = 0;
     __syncthreads();
-    for (int b0 = 0; b0 < NB; b0 += 256) {
-        const int b = b0 + threadIdx.x;
-        const int v = b < NB ? blockcnt[(size_t)e * NB + b] : 0;
-        const int inc = wave_incl_scan(v);
+    for (int b0 = 0; b0 < NB; b0 += 256 * kPer) {
+        const int base = b0 + threadIdx.x * kPer;
+        int v[kPer];
+        int local = 0;
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+            v[i] = base + i < NB ? src[base + i] : 0;
+            local += v[i];
+        }
+        const int inc = wave_incl_scan(local);
         if (lane == 63) wsum[wave] = inc;
         __syncthreads();
         int pre = carry;
         for (int w = 0; w < wave; ++w) pre += wsum[w];
-        if (b < NB) blockbase[(size_t)e * NB + b] = pre + inc - v;
+        int run = pre + inc - local;
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+            if (base + i < NB) dst[base + i] = run;
+            run += v[i];
+        }
         __syncthreads();
         if (threadIdx.x == 255) carry = pre + inc;
         __syncthreads();
