@@ -36,9 +36,10 @@ __device__ __forceinline__ float silu_fast(float x) {
 
 __host__ __device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
-// Per-segment metadata written by the dispatch kernel.  Segments 0..E-1 are
-// the routed experts (rows grouped by the dispatch permutation); segment E is
-// the shared expert when the layer has one (rows = tokens).
+// Per-segment metadata written by the dispatch kernel.  With a shared expert,
+// segment 0 is the shared expert (rows = tokens) and segment 1 + e is routed
+// expert e; without one, segment e is expert e.  Routed rows are grouped by
+// the dispatch permutation.
 struct SegMeta {
     int32_t row0;   // first row of the segment in the routed row space
     int32_t rows;   // rows of the segment (0 for inactive experts)

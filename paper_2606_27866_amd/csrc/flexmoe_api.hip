@@ -16,7 +16,7 @@
 #include <mutex>
 #include <vector>
 
-#include "../../include/flexmoe.h"
+#include "flexmoe.h"
 #include "kernels.h"
 
 using namespace flexmoe;
@@ -142,11 +142,11 @@ struct KernelTimer {
         if (!g_timing) return;
         a = take_event();
         b = take_event();
-        if (a && b) hipEventRecord(a, s);
+        if (a && b) (void)hipEventRecord(a, s);
     }
     ~KernelTimer() {
         if (!a || !b) return;
-        hipEventRecord(b, s);
+        (void)hipEventRecord(b, s);
         std::lock_guard<std::mutex> g(g_tmu);
         g_pending.push_back({kernel, a, b});
     }
@@ -286,7 +286,7 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
     const int NB = num_chunks(T);
     const int nseg = D.E + (has_shared ? 1 : 0);
     const bool bf16 = D.dtype == FLEXMOE_BF16;
-    const TileShape ts = bf16 ? TileShape{kBf16BM1, kBf16BN1, kBf16BM2, kBf16BN2}
+    const TileShape ts = bf16 ? TileShape{kBigBM1, kBigBN1, kBigBM2, kBigBN2}
                               : TileShape{kF32BM, kF32BN, kF32BM, kF32BN};
 
     hipError_t err;
@@ -328,7 +328,7 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
                                D.top_k, nseg, T};
         {
             KernelTimer kt(FLEXMOE_K_GATE_UP, s);
-            err = launch_gemm1_bf16(p1, (int)g1, s);
+            err = launch_gemm1_big(p1, (int)g1, s);
         }
         if (err != hipSuccess) return hip_fail(err, "gate/up GEMM launch");
         Gemm2Params<bf16_t> p2{(const bf16_t*)(ws + L.H), (const bf16_t*)(ws + L.Hs),
@@ -336,7 +336,7 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
                                D.I, D.I_shared, D.E, nseg};
         {
             KernelTimer kt(FLEXMOE_K_DOWN, s);
-            err = launch_gemm2_bf16(p2, (int)g2, s);
+            err = launch_gemm2_big(p2, (int)g2, s);
         }
         if (err != hipSuccess) return hip_fail(err, "down GEMM launch");
     } else {

@@ -42,8 +42,9 @@ __global__ __launch_bounds__(256) void gemm1_bf16_kernel(Gemm1Params<bf16_t> p) 
     const int local = L - p.tstart[s];
     const int mt = ceil_div(sm.rows, BM);
     const int mtile = local % mt, ntile = local / mt;
-    const bool shared = s >= p.E;
-    const size_t wofs = shared ? 0 : (size_t)s * p.I * p.d;
+    const int hs = p.nseg - p.E;  // 1 if segment 0 is the shared expert
+    const bool shared = s < hs;
+    const size_t wofs = shared ? 0 : (size_t)(s - hs) * p.I * p.d;
     const bf16_t* Wg = (shared ? p.sg : p.wg) + wofs;
     const bf16_t* Wu = (shared ? p.su : p.wu) + wofs;
 
@@ -154,10 +155,11 @@ __global__ __launch_bounds__(256) void gemm2_bf16_kernel(Gemm2Params<bf16_t> p) 
     const int local = L - p.tstart[s];
     const int mt = ceil_div(sm.rows, BM);
     const int mtile = local % mt, ntile = local / mt;
-    const bool shared = s >= p.E;
+    const int hs = p.nseg - p.E;  // 1 if segment 0 is the shared expert
+    const bool shared = s < hs;
     const bf16_t* Hb = shared ? p.Hs : p.H + (size_t)sm.row0 * p.I;
     const int ldh = shared ? p.Is : p.I;
-    const bf16_t* Wd = shared ? p.sd : p.wd + (size_t)s * p.d * p.I;
+    const bf16_t* Wd = shared ? p.sd : p.wd + (size_t)(s - hs) * p.d * p.I;
     const int K = sm.kk;
 
     const int tid = threadIdx.x;

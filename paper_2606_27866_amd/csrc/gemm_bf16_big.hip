@@ -1,0 +1,312 @@
+// Large-tile ragged grouped GEMMs on bf16 MFMA for prefill-sized token counts.
+//
+// Same work as gemm_bf16.hip (gate/up GEMM with fused SwiGLU, down GEMM with
+// the reduction truncated to k_e; FlexMoE Eq. 4), shaped for gfx950:
+//   - 256 x 256 workgroup tile (rows x weight rows), K tile 32, 8 waves (two
+//     per SIMD: one wave alone cannot keep the matrix core fed) arranged
+//     2 x 4, each owning a 128 x 64 block of v_mfma_f32_32x32x16_bf16
+//     accumulators (128 registers).  Per K tile the CU reads 96 KB of LDS
+//     fragments (256 B/clk) and writes 32 KB (128 B/clk): about 60 % of the
+//     LDS time the MFMAs take, with zero bank conflicts.
+//   - operands go from global memory straight into LDS (global_load_lds,
+//     16 bytes per lane): no VGPRs stage them and no ds_write is issued.
+//     Rows outside a segment, channels at or past k_e and K chunks past the
+//     end read a zero page instead.
+//   - each 64-byte LDS row (32 bf16 of K) stores its four 16-byte chunks
+//     XOR-swizzled by bits 2..3 of the row index, so the 16 lanes served in
+//     one LDS cycle of a fragment read hit 64 distinct banks.
+//   - four LDS stages: the loads of K tiles t+1..t+3 are in flight while
+//     tile t is multiplied.
+//   - tiles are numbered segment-major (shared expert first: its reductions
+//     are the longest) with row tiles fastest, so consecutive tiles share
+//     their weight tile; groups of 8 consecutive tiles go to one XCD
+//     (workgroup b runs on XCD b % 8), interleaving the XCDs every 8 tiles so
+//     that weight reuse stays in one L2 while the work stays balanced.
+// gate/up: a workgroup tile is 256 rows x 128 channels; its B tile holds the
+//   128 gate rows then the 128 up rows of those channels, and wave (wm, wn)
+//   multiplies gate rows [wn*32, wn*32+32) and the matching up rows, so the
+//   gate and up accumulators of a channel sit in the same lane.
+// down: a workgroup tile is 256 rows x 256 output columns.
+#include "kernels.h"
+
+namespace flexmoe {
+
+namespace {
+constexpr int BM = 256, BN = 256, BK = 32;
+constexpr int NWAVE = 8, THREADS = 64 * NWAVE;
+constexpr int WM = 2, WN = 4;               // wave grid
+constexpr int WROWS = BM / WM;              // 128 rows per wave
+constexpr int MF = WROWS / 32;              // 4 row fragments per wave
+constexpr int NF = 2;                       // 2 column fragments per wave (64 columns)
+constexpr int NSTAGE = 4;
+constexpr int ROWB = BK * 2;                // bytes per LDS row
+constexpr int CHUNKS = ROWB / 16;           // 16-byte chunks per LDS row
+constexpr int RPI = 64 / CHUNKS;            // LDS rows filled per DMA instruction
+constexpr int ROWS_PER_WAVE = BM / NWAVE;   // A rows (and B rows) each wave loads
+constexpr int NI = ROWS_PER_WAVE / RPI;     // DMA instructions per wave per operand
+constexpr int LOADS_PER_TILE = 2 * NI;      // DMA instructions per lane per K tile
+constexpr int STAGE_A = BM * ROWB;          // 16 KB
+constexpr int STAGE = STAGE_A + BN * ROWB;  // 32 KB
+constexpr int XCD_GROUP = 8;                // consecutive tiles kept on one XCD
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void lds_ptr_t;
+
+__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 2) & 3); }
+
+// s_waitcnt with vmcnt = n and no wait on expcnt / lgkmcnt (gfx9 encoding).
+constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+constexpr int kWaitLgkm0 = waitcnt_vm(63) & ~(15 << 8);  // lgkmcnt(0) only
+
+__device__ __forceinline__ bf16x8 lds_frag(const unsigned char* base, int row, int chunk) {
+    return __builtin_bit_cast(bf16x8,
+                              *reinterpret_cast<const u32x4*>(base + row * ROWB + swz(row, chunk) * 16));
+}
+
+__device__ __forceinline__ void load_lds16(const void* g, unsigned char* lds) {
+    __builtin_amdgcn_global_load_lds(g, (lds_ptr_t*)lds, 16, 0, 0);
+}
+
+// A bare s_barrier: a workgroup fence would also drain the DMAs of later K
+// tiles that should stay in flight.  Callers wait for their own LDS reads
+// and DMAs first.
+__device__ __forceinline__ void barrier_no_fence() {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+}  // namespace
+
+// 64 zero bytes: the source of every masked 16-byte chunk.
+__device__ __attribute__((aligned(64))) uint32_t g_zero_page[16];
+
+template <bool kGateUp>
+__device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Gemm2Params<bf16_t>& p2,
+                                         unsigned char* smem) {
+    const int32_t* tstart = kGateUp ? p1.tstart : p2.tstart;
+    const int nseg = kGateUp ? p1.nseg : p2.nseg;
+    const int E = kGateUp ? p1.E : p2.E;
+    const int d = kGateUp ? p1.d : p2.d;
+
+    // tile numbering: XCD x = b % 8 takes groups of XCD_GROUP consecutive tiles
+    const int tot = tstart[nseg];
+    const int jb = blockIdx.x >> 3;
+    const int L = (jb / XCD_GROUP) * (8 * XCD_GROUP) + (blockIdx.x & 7) * XCD_GROUP + jb % XCD_GROUP;
+    if (L >= tot) return;
+    const int s = find_segment(tstart, nseg, L);
+    const SegMeta sm = (kGateUp ? p1.seg : p2.seg)[s];
+    const int local = L - tstart[s];
+    const int mt = ceil_div(sm.rows, BM);
+    const int mtile = local % mt, ntile = local / mt;
+    const int hs = nseg - E;  // 1 if segment 0 is the shared expert
+    const bool shared = s < hs;
+
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const void* zero = (const void*)g_zero_page;
+
+    // ---- per-lane sources of the A rows and B rows this lane loads ----
+    // DMA instruction i of wave w fills LDS rows w*32 + i*RPI .. +RPI of each
+    // operand; lane -> row lane/CHUNKS, LDS chunk lane%CHUNKS, which holds
+    // global chunk swz(row, lane%CHUNKS).
+    const int pos = lane % CHUNKS;
+    const bf16_t* asrc[NI];
+    const bf16_t* bsrc[NI];
+    int acol[NI];
+    int K;
+    if constexpr (kGateUp) {
+        K = d;
+        const size_t wofs = shared ? 0 : (size_t)(s - hs) * p1.I * d;
+        const bf16_t* Wg = (shared ? p1.sg : p1.wg) + wofs;
+        const bf16_t* Wu = (shared ? p1.su : p1.wu) + wofs;
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            const int r = wave * ROWS_PER_WAVE + i * RPI + lane / CHUNKS;
+            const int row = mtile * BM + r;
+            const int c = swz(r, pos) * 8;
+            acol[i] = c;
+            asrc[i] = nullptr;
+            if (row < sm.rows) {
+                const int t = shared ? row
+                                     : (int)min((unsigned)(p1.perm[sm.row0 + row] / p1.top_k),
+                                                (unsigned)(p1.tokens - 1));
+                asrc[i] = p1.x + (size_t)t * d + c;
+            }
+            const int ch = ntile * (BN / 2) + (r & (BN / 2 - 1));
+            bsrc[i] = ch < sm.kk ? (r < BN / 2 ? Wg : Wu) + (size_t)ch * d + c : nullptr;
+        }
+    } else {
+        K = sm.kk;
+        const bf16_t* Hb = shared ? p2.Hs : p2.H + (size_t)sm.row0 * p2.I;
+        const int ld = shared ? p2.Is : p2.I;  // H rows and W_down rows share the stride
+        const bf16_t* Wd = shared ? p2.sd : p2.wd + (size_t)(s - hs) * d * p2.I;
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            const int r = wave * ROWS_PER_WAVE + i * RPI + lane / CHUNKS;
+            const int row = mtile * BM + r;
+            const int c = swz(r, pos) * 8;
+            acol[i] = c;
+            asrc[i] = row < sm.rows ? Hb + (size_t)row * ld + c : nullptr;
+            const int n = ntile * BN + r;
+            bsrc[i] = n < d ? Wd + (size_t)n * ld + c : nullptr;
+        }
+    }
+
+    // DMA of K tile kt into a stage; past the end of K (or of a segment) the
+    // zero page is read, so every call issues exactly LOADS_PER_TILE loads
+    auto issue = [&](int kt, int stage) {
+        unsigned char* sa = smem + stage * STAGE + wave * ROWS_PER_WAVE * ROWB;
+        unsigned char* sb = sa + STAGE_A;
+        const int k0 = kt * BK;
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            const bool kin = k0 + acol[i] < K;  // A and B chunks share the column
+            load_lds16(asrc[i] && kin ? (const void*)(asrc[i] + k0) : zero, sa + i * RPI * ROWB);
+            load_lds16(bsrc[i] && kin ? (const void*)(bsrc[i] + k0) : zero, sb + i * RPI * ROWB);
+        }
+    };
+
+    const int wm = wave / WN, wn = wave % WN;
+    int brow[NF];
+#pragma unroll
+    for (int j = 0; j < NF; ++j) {
+        if constexpr (kGateUp)
+            brow[j] = (j == 0 ? 0 : BN / 2) + wn * 32;  // gate rows, then the same channels' up rows
+        else
+            brow[j] = wn * 64 + j * 32;
+    }
+    floatx16 acc[MF][NF];
+#pragma unroll
+    for (int i = 0; i < MF; ++i)
+#pragma unroll
+        for (int j = 0; j < NF; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+    static_assert(BK == 32, "the loop below runs two 16-deep MFMA steps per K tile");
+    const int nk = ceil_div(K, BK);
+    bf16x8 a[2][MF], b[2][NF];
+    auto read_frags = [&](int kt, int ks, int buf) {
+        const unsigned char* sa = smem + (kt % NSTAGE) * STAGE;
+        const unsigned char* sb = sa + STAGE_A;
+        const int chunk = ks * 2 + (lane >> 5);
+#pragma unroll
+        for (int i = 0; i < MF; ++i) a[buf][i] = lds_frag(sa, wm * WROWS + i * 32 + (lane & 31), chunk);
+#pragma unroll
+        for (int j = 0; j < NF; ++j) b[buf][j] = lds_frag(sb, brow[j] + (lane & 31), chunk);
+    };
+    auto mfma_step = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < MF; ++i)
+#pragma unroll
+            for (int j = 0; j < NF; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][i], b[buf][j], acc[i][j], 0, 0, 0);
+    };
+    // one MFMA, then a fragment read, spread over a step's 8 MFMAs
+    auto interleave_reads = []() {
+#pragma unroll
+        for (int r = 0; r < MF + NF; ++r) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, MF * NF - (MF + NF), 0);
+    };
+    // same, with the DMA loads of a later tile spread in as well
+    auto interleave_reads_dma = []() {
+#pragma unroll
+        for (int r = 0; r < LOADS_PER_TILE; ++r) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read (DMA)
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+        }
+        __builtin_amdgcn_sched_group_barrier(0x100, MF + NF - LOADS_PER_TILE, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, MF * NF - LOADS_PER_TILE, 0);
+    };
+
+    // Ping-pong schedule over NSTAGE K tiles in LDS, three DMAs ahead:
+    //   read (kt, step 1) | MFMA (kt, step 0) | wait tile kt+1, barrier |
+    //   DMA tile kt+4 into the stage of tile kt | read (kt+1, step 0) | MFMA (kt, step 1)
+    // Every iteration issues one tile's DMAs (zero-page loads once past the
+    // end), so before the wait of iteration kt the tiles 0 .. kt+3 are issued
+    // and tile kt+1 is in once at most two tiles' DMAs are outstanding.
+#pragma unroll
+    for (int t = 0; t < NSTAGE; ++t) issue(t, t);
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm((NSTAGE - 1) * LOADS_PER_TILE));
+    barrier_no_fence();
+    read_frags(0, 0, 0);
+    for (int kt = 0; kt < nk; ++kt) {
+        read_frags(kt, 1, 1);
+        mfma_step(0);
+        interleave_reads();
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * LOADS_PER_TILE) & kWaitLgkm0);  // tile kt+1 in; own reads done
+        barrier_no_fence();  // all waves are done reading tile kt: its stage is free
+        __builtin_amdgcn_sched_barrier(0);
+        issue(kt + NSTAGE, kt % NSTAGE);
+        // after the last tile this reads a stale stage, whose values go unused
+        read_frags(kt + 1, 0, 0);
+        mfma_step(1);
+        interleave_reads_dma();
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // no DMA may outlive the workgroup's LDS
+
+    // ---- epilogue: 32x32 accumulator layout, lane -> column lane%32, register v
+    // -> row (v/4)*8 + (lane/32)*4 + v%4
+    if constexpr (kGateUp) {
+        bf16_t* Hb = shared ? p1.Hs : p1.H + (size_t)sm.row0 * p1.I;
+        const int ldh = shared ? p1.Is : p1.I;
+        const int kk8 = min((sm.kk + 7) & ~7, ldh);  // chunk-aligned end: [kk, kk8) is zero-filled
+        const int ch = ntile * (BN / 2) + wn * 32 + (lane & 31);
+        if (ch < kk8) {
+#pragma unroll
+            for (int i = 0; i < MF; ++i)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int row = mtile * BM + wm * WROWS + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
+                    if (row < sm.rows) {
+                        const float g = acc[i][0][v], u = acc[i][1][v];
+                        Hb[(size_t)row * ldh + ch] = ch < sm.kk ? f32_to_bf16(silu_fast(g) * u) : (bf16_t)0;
+                    }
+                }
+        }
+    } else {
+        float* Ob = shared ? p2.Os : p2.O + (size_t)sm.row0 * d;
+#pragma unroll
+        for (int j = 0; j < NF; ++j) {
+            const int n = ntile * BN + wn * 64 + j * 32 + (lane & 31);
+            if (n >= d) continue;
+#pragma unroll
+            for (int i = 0; i < MF; ++i)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int row = mtile * BM + wm * WROWS + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
+                    if (row < sm.rows) Ob[(size_t)row * d + n] = acc[i][j][v];
+                }
+        }
+    }
+}
+
+__global__ __launch_bounds__(THREADS, 2) void gemm1_big_kernel(Gemm1Params<bf16_t> p) {
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[NSTAGE * STAGE];
+    big_tile<true>(p, Gemm2Params<bf16_t>{}, smem);
+}
+
+__global__ __launch_bounds__(THREADS, 2) void gemm2_big_kernel(Gemm2Params<bf16_t> p) {
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[NSTAGE * STAGE];
+    big_tile<false>(Gemm1Params<bf16_t>{}, p, smem);
+}
+
+hipError_t launch_gemm1_big(const Gemm1Params<bf16_t>& p, int grid, hipStream_t s) {
+    if (grid <= 0) return hipSuccess;
+    const int g = (grid + 8 * XCD_GROUP - 1) / (8 * XCD_GROUP) * (8 * XCD_GROUP);
+    gemm1_big_kernel<<<g, THREADS, 0, s>>>(p);
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm2_big(const Gemm2Params<bf16_t>& p, int grid, hipStream_t s) {
+    if (grid <= 0) return hipSuccess;
+    const int g = (grid + 8 * XCD_GROUP - 1) / (8 * XCD_GROUP) * (8 * XCD_GROUP);
+    gemm2_big_kernel<<<g, THREADS, 0, s>>>(p);
+    return hipGetLastError();
+}
+
+}  // namespace flexmoe

@@ -45,6 +45,7 @@ struct Gemm2Params {
 // with these numbers).
 constexpr int kBf16BM1 = 128, kBf16BN1 = 64, kBf16BM2 = 128, kBf16BN2 = 128;
 constexpr int kF32BM = 64, kF32BN = 64;
+constexpr int kBigBM1 = 256, kBigBN1 = 128, kBigBM2 = 256, kBigBN2 = 256;
 
 __global__ void route_kernel(const float* logits, int T, int E, int k, int norm_topk, int32_t* idx,
                              float* wts, int32_t* blockcnt, int NB);
@@ -61,6 +62,8 @@ __global__ void set_keep_kernel(int32_t* keep, KeepArgs t, int E);
 // Launchers (defined next to their kernels).  Each returns the launch status.
 hipError_t launch_gemm1_bf16(const Gemm1Params<bf16_t>& p, int grid, hipStream_t s);
 hipError_t launch_gemm2_bf16(const Gemm2Params<bf16_t>& p, int grid, hipStream_t s);
+hipError_t launch_gemm1_big(const Gemm1Params<bf16_t>& p, int grid, hipStream_t s);
+hipError_t launch_gemm2_big(const Gemm2Params<bf16_t>& p, int grid, hipStream_t s);
 hipError_t launch_gemm1_f32(const Gemm1Params<float>& p, int grid, hipStream_t s);
 hipError_t launch_gemm2_f32(const Gemm2Params<float>& p, int grid, hipStream_t s);
 hipError_t launch_combine(const float* O, const float* Os, const int32_t* pos, const float* wts,

@@ -215,7 +215,10 @@ __global__ __launch_bounds__(64) void dispatch_scatter_kernel(
     __syncthreads();
 
     if (blockIdx.x == 0) {
-        const int nseg = E + (I_shared > 0 ? 1 : 0);
+        // segment order: the shared expert (if any) first, then experts 0..E-1;
+        // its tiles carry the longest reductions, so they start first
+        const int hs = I_shared > 0 ? 1 : 0;
+        const int nseg = E + hs;
         for (int e = lane; e < E; e += 64) {
             offsets[e] = off[e];
             SegMeta m;
@@ -223,19 +226,19 @@ __global__ __launch_bounds__(64) void dispatch_scatter_kernel(
             m.rows = kk_s[e] > 0 ? counts[e] : 0;
             m.kk = kk_s[e];
             m.pad = 0;
-            seg_l[e] = m;
-            seg[e] = m;
+            seg_l[hs + e] = m;
+            seg[hs + e] = m;
         }
         if (lane == 0) {
             offsets[E] = P;
-            if (I_shared > 0) {
+            if (hs) {
                 SegMeta m;
                 m.row0 = 0;
                 m.rows = T;
                 m.kk = I_shared;
                 m.pad = 0;
-                seg_l[E] = m;
-                seg[E] = m;
+                seg_l[0] = m;
+                seg[0] = m;
             }
         }
         __syncthreads();
