@@ -3,6 +3,8 @@
 //   y[t] = sum_{j < top_k, pos[t][j] >= 0} w[t][j] * O[pos[t][j]] + S[t]
 // summed in ascending slot order in fp32, then rounded once to the output
 // type.  Assignments of experts with k_e = 0 have pos = -1 and add nothing.
+// S[t] is the sum of the shared expert's partial rows Os[part][t] (one part
+// unless its down projection was split), added in ascending part order.
 #include "kernels.h"
 
 namespace flexmoe {
@@ -11,10 +13,11 @@ template <typename OutT>
 __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ O,
                                                       const float* __restrict__ Os,
                                                       const int32_t* __restrict__ pos,
-                                                      const float* __restrict__ wts, int k, int d,
-                                                      int has_shared, OutT* __restrict__ y) {
+                                                      const float* __restrict__ wts, int T, int k,
+                                                      int d, int shared_parts, OutT* __restrict__ y) {
     const int t = blockIdx.x;
-    for (int n = threadIdx.x * 4; n < d; n += blockDim.x * 4) {
+    const int n = (blockIdx.y * blockDim.x + threadIdx.x) * 4;  // one float4 column group per thread
+    if (n < d) {
         float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
         for (int j = 0; j < k; ++j) {
             const int p = pos[(size_t)t * k + j];
@@ -26,13 +29,18 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
             acc.z += w * o.z;
             acc.w += w * o.w;
         }
-        if (has_shared) {
-            const float4 sv = *reinterpret_cast<const float4*>(Os + (size_t)t * d + n);
-            acc.x += sv.x;
-            acc.y += sv.y;
-            acc.z += sv.z;
-            acc.w += sv.w;
+        float4 sh = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int q = 0; q < shared_parts; ++q) {
+            const float4 sv = *reinterpret_cast<const float4*>(Os + ((size_t)q * T + t) * d + n);
+            sh.x += sv.x;
+            sh.y += sv.y;
+            sh.z += sv.z;
+            sh.w += sv.w;
         }
+        acc.x += sh.x;
+        acc.y += sh.y;
+        acc.z += sh.z;
+        acc.w += sh.w;
         if constexpr (sizeof(OutT) == 4) {
             *reinterpret_cast<float4*>(y + (size_t)t * d + n) = acc;
         } else {
@@ -44,12 +52,13 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
 }
 
 hipError_t launch_combine(const float* O, const float* Os, const int32_t* pos, const float* wts,
-                          int T, int k, int d, int has_shared, int dtype, void* y, hipStream_t s) {
+                          int T, int k, int d, int shared_parts, int dtype, void* y, hipStream_t s) {
     if (T <= 0) return hipSuccess;
+    const dim3 grid(T, ceil_div(d, 4 * 256));
     if (dtype == 0)
-        combine_kernel<float><<<T, 256, 0, s>>>(O, Os, pos, wts, k, d, has_shared, (float*)y);
+        combine_kernel<float><<<grid, 256, 0, s>>>(O, Os, pos, wts, T, k, d, shared_parts, (float*)y);
     else
-        combine_kernel<bf16_t><<<T, 256, 0, s>>>(O, Os, pos, wts, k, d, has_shared, (bf16_t*)y);
+        combine_kernel<bf16_t><<<grid, 256, 0, s>>>(O, Os, pos, wts, T, k, d, shared_parts, (bf16_t*)y);
     return hipGetLastError();
 }
 

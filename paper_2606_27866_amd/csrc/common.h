@@ -10,6 +10,7 @@ constexpr int kWave = 64;
 constexpr int kMaxExperts = 256;
 constexpr int kMaxTopK = 16;
 constexpr int kRouteTokens = 16;   // tokens per routing block (= dispatch chunk)
+constexpr int kSmallAssign = 256;  // T * top_k at or below which one workgroup dispatches
 
 typedef uint16_t bf16_t;           // raw bf16 bits in memory
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -52,6 +53,8 @@ struct SegMeta {
 struct TileShape {
     int32_t bm1, bn1;   // gate/up GEMM: rows x channels per tile
     int32_t bm2, bn2;   // down GEMM: rows x output columns per tile
+    int32_t ks2;        // > 0: the shared expert's down GEMM is split into
+                        // reductions of ks2 channels (one tile set each)
 };
 
 // Wave-wide inclusive prefix sum of an int (64 lanes).

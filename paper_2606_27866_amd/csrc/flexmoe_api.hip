@@ -12,6 +12,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <cmath>
 #include <mutex>
 #include <vector>
@@ -94,19 +95,25 @@ Layout layout(const flexmoe_layer_desc& D, int T) {
     L.H = take(A * (size_t)D.I * es);
     L.Hs = take((size_t)T * D.I_shared * es);
     L.O = take(A * (size_t)D.d * 4);
-    L.Os = take(D.I_shared > 0 ? (size_t)T * D.d * 4 : 0);
+    // shared-expert rows; at decode sizes its down projection is split into
+    // shared_parts() reductions with one row set each (kept monotone in T)
+    const size_t os_rows = D.I_shared > 0
+        ? std::max((size_t)T, (size_t)std::min(T, kDecodeMaxT) * (size_t)ceil_div(D.I_shared, D.I))
+        : 0;
+    L.Os = take(os_rows * D.d * 4);
     L.total = off;
     return L;
 }
 
 // Upper bound on the number of row tiles of height bm over all routed
-// segments: sum_e ceil(n_e/bm) <= ceil(A/bm) + E - 1, and <= E*ceil(T/bm)
-// because a token routes to an expert at most once.
+// segments: sum_e ceil(n_e/bm) <= ceil(A/bm) + E - 1, <= E*ceil(T/bm)
+// because a token routes to an expert at most once, and <= A because every
+// tile holds at least one row.
 long long routed_row_tiles_ub(int T, int E, int k, int bm) {
     const long long A = (long long)T * k;
     const long long a = (A + bm - 1) / bm + E - 1;
     const long long b = (long long)E * ((T + bm - 1) / bm);
-    return a < b ? a : b;
+    return std::min(std::min(a, b), A);
 }
 
 // ---- optional per-kernel event timing --------------------------------------
@@ -286,29 +293,46 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
     const int NB = num_chunks(T);
     const int nseg = D.E + (has_shared ? 1 : 0);
     const bool bf16 = D.dtype == FLEXMOE_BF16;
-    const TileShape ts = bf16 ? TileShape{kBigBM1, kBigBN1, kBigBM2, kBigBN2}
-                              : TileShape{kF32BM, kF32BN, kF32BM, kF32BN};
+    // kernel family: weight streaming for decode-sized T, large MFMA tiles
+    // otherwise (bf16); LDS-tiled FMA for fp32
+    const bool decode = bf16 && T <= kDecodeMaxT;
+    const int shared_parts = !has_shared ? 0 : decode ? ceil_div(D.I_shared, D.I) : 1;
+    const TileShape ts = !bf16   ? TileShape{kF32BM, kF32BN, kF32BM, kF32BN, 0}
+                         : decode ? TileShape{kDecodeMaxT, kDecBN, kDecodeMaxT, kDecBN, D.I}
+                                  : TileShape{kBigBM1, kBigBN1, kBigBM2, kBigBN2, 0};
 
     hipError_t err;
-    {
+    if ((long long)T * D.top_k <= kSmallAssign) {
+        // one workgroup routes and dispatches everything (timed as routing)
         KernelTimer kt(FLEXMOE_K_ROUTE, s);
-        route_kernel<<<NB, 64 * kRouteTokens, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, idx, wts, blockcnt, NB);
+        dispatch_small_kernel<<<1, 1024, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, keep_dev, D.I,
+                                                  D.I_shared, D.d, ts, idx, wts, counts, perm, pos,
+                                                  offsets, seg, t1, t2);
         err = hipGetLastError();
+        if (err != hipSuccess) return hip_fail(err, "dispatch launch");
+    } else {
+        {
+            KernelTimer kt(FLEXMOE_K_ROUTE, s);
+            route_kernel<<<NB, 64 * kRouteTokens, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, idx, wts,
+                                                          blockcnt, NB);
+            err = hipGetLastError();
+        }
+        if (err != hipSuccess) return hip_fail(err, "route launch");
+        {
+            KernelTimer kt(FLEXMOE_K_DISPATCH_SCAN, s);
+            dispatch_scan_kernel<<<D.E, 256, 0, s>>>(blockcnt, NB, blockbase, counts);
+            err = hipGetLastError();
+        }
+        if (err != hipSuccess) return hip_fail(err, "dispatch scan launch");
+        {
+            KernelTimer kt(FLEXMOE_K_DISPATCH_SCATTER, s);
+            dispatch_scatter_kernel<<<NB, 64, 0, s>>>(idx, keep_dev, counts, blockbase, T, D.E, D.top_k,
+                                                      D.I, D.I_shared, D.d, NB, ts, perm, pos, offsets,
+                                                      seg, t1, t2);
+            err = hipGetLastError();
+        }
+        if (err != hipSuccess) return hip_fail(err, "dispatch scatter launch");
     }
-    if (err != hipSuccess) return hip_fail(err, "route launch");
-    {
-        KernelTimer kt(FLEXMOE_K_DISPATCH_SCAN, s);
-        dispatch_scan_kernel<<<D.E, 256, 0, s>>>(blockcnt, NB, blockbase, counts);
-        err = hipGetLastError();
-    }
-    if (err != hipSuccess) return hip_fail(err, "dispatch scan launch");
-    {
-        KernelTimer kt(FLEXMOE_K_DISPATCH_SCATTER, s);
-        dispatch_scatter_kernel<<<NB, 64, 0, s>>>(idx, keep_dev, counts, blockbase, T, D.E, D.top_k, D.I,
-                                                  D.I_shared, D.d, NB, ts, perm, pos, offsets, seg, t1, t2);
-        err = hipGetLastError();
-    }
-    if (err != hipSuccess) return hip_fail(err, "dispatch scatter launch");
 
     // grid upper bounds from host-known sizes
     const long long rt1 = routed_row_tiles_ub(T, D.E, D.top_k, ts.bm1);
@@ -317,7 +341,7 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
     long long g2 = rt2 * ceil_div(D.d, ts.bn2);
     if (has_shared) {
         g1 += (long long)ceil_div(T, ts.bm1) * ceil_div(D.I_shared, ts.bn1);
-        g2 += (long long)ceil_div(T, ts.bm2) * ceil_div(D.d, ts.bn2);
+        g2 += (long long)ceil_div(T, ts.bm2) * ceil_div(D.d, ts.bn2) * std::max(shared_parts, 1);
     }
     if (g1 > 0x7fffffffLL || g2 > 0x7fffffffLL) return fail(FLEXMOE_ESHAPE, "tile grid too large");
 
@@ -328,15 +352,15 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
                                D.top_k, nseg, T};
         {
             KernelTimer kt(FLEXMOE_K_GATE_UP, s);
-            err = launch_gemm1_big(p1, (int)g1, s);
+            err = decode ? launch_gemm1_decode(p1, (int)g1, s) : launch_gemm1_big(p1, (int)g1, s);
         }
         if (err != hipSuccess) return hip_fail(err, "gate/up GEMM launch");
         Gemm2Params<bf16_t> p2{(const bf16_t*)(ws + L.H), (const bf16_t*)(ws + L.Hs),
                                (const bf16_t*)w_down_r, (const bf16_t*)ws_down, seg, t2, O, Os, D.d,
-                               D.I, D.I_shared, D.E, nseg};
+                               D.I, D.I_shared, D.E, nseg, T};
         {
             KernelTimer kt(FLEXMOE_K_DOWN, s);
-            err = launch_gemm2_big(p2, (int)g2, s);
+            err = decode ? launch_gemm2_decode(p2, (int)g2, s) : launch_gemm2_big(p2, (int)g2, s);
         }
         if (err != hipSuccess) return hip_fail(err, "down GEMM launch");
     } else {
@@ -351,7 +375,7 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
         if (err != hipSuccess) return hip_fail(err, "gate/up GEMM launch");
         Gemm2Params<float> p2{(const float*)(ws + L.H), (const float*)(ws + L.Hs),
                               (const float*)w_down_r, (const float*)ws_down, seg, t2, O, Os, D.d, D.I,
-                              D.I_shared, D.E, nseg};
+                              D.I_shared, D.E, nseg, T};
         {
             KernelTimer kt(FLEXMOE_K_DOWN, s);
             err = launch_gemm2_f32(p2, (int)g2, s);
@@ -360,7 +384,7 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
     }
     {
         KernelTimer kt(FLEXMOE_K_COMBINE, s);
-        err = launch_combine(O, Os, pos, wts, T, D.top_k, D.d, has_shared ? 1 : 0, D.dtype, y, s);
+        err = launch_combine(O, Os, pos, wts, T, D.top_k, D.d, shared_parts, D.dtype, y, s);
     }
     if (err != hipSuccess) return hip_fail(err, "combine launch");
 

@@ -1,0 +1,229 @@
+// Weight-streaming grouped GEMMs for decode-sized token counts (T <= 64).
+//
+// With a few tokens per expert the layer is bound by reading the kept
+// weights (Eq. 4: the first k_e channels of each routed expert, plus the
+// shared expert), so these kernels read every kept weight byte exactly once,
+// straight from HBM into MFMA fragments, with many waves in flight.
+//
+// A workgroup owns one tile: 16 channels (gate/up) or 16 output columns
+// (down) of one segment, for every row (token) of that segment (<= 64 rows =
+// up to four 16-wide MFMA column blocks).  Its four waves split the
+// reduction: wave q takes the 256-wide K batches q, q+4, q+8, ...; the four
+// partial sums are added in wave order through LDS (a fixed order, so the
+// result is deterministic).  Small tiles keep all CUs streaming to the end.
+//
+// The tile's 16 weight rows are the M side of v_mfma_f32_16x16x32_bf16, the
+// tokens the N side.  A 256-wide batch is eight MFMA steps of 32: at step j
+// lane l holds weight row l%16 and the 8 K elements 32*j + 8*(l/16) .. +8,
+// so one load instruction reads 64 contiguous bytes of each of 16 rows and
+// the next one the other half of the same cache lines.  Token fragments are
+// read with the same K mapping, so every product pairs equal K indices.
+//
+// gate/up: SwiGLU is applied to the reduced sums; H is written as bf16.
+// down: the reduction runs over the segment's kept channels; the shared
+//   expert's reduction is split into chunks of I channels (one routed
+//   expert's worth), each chunk writing its own partial rows, which the
+//   combine sums in a fixed order.
+#include "kernels.h"
+
+namespace flexmoe {
+
+namespace {
+constexpr int DCH = 16;    // channels (gate/up) or output columns (down) per tile
+constexpr int DKB = 256;   // K elements per batch
+constexpr int DWAVES = 4;  // waves per workgroup, splitting K
+typedef float floatx4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ bf16x8 as_frag(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+// Sum NACC float4 accumulators per lane over the four waves in wave order;
+// wave 0 ends up with the total.  red holds DWAVES * NACC * 64 float4.
+template <int NACC>
+__device__ __forceinline__ void reduce_waves(floatx4_t (&acc)[NACC], float4* red, int wave, int lane) {
+    if (wave > 0) {
+#pragma unroll
+        for (int i = 0; i < NACC; ++i)
+            red[((wave - 1) * NACC + i) * 64 + lane] = make_float4(acc[i][0], acc[i][1], acc[i][2], acc[i][3]);
+    }
+    __syncthreads();
+    if (wave == 0) {
+#pragma unroll
+        for (int w = 1; w < DWAVES; ++w)
+#pragma unroll
+            for (int i = 0; i < NACC; ++i) {
+                const float4 v = red[((w - 1) * NACC + i) * 64 + lane];
+                acc[i][0] += v.x;
+                acc[i][1] += v.y;
+                acc[i][2] += v.z;
+                acc[i][3] += v.w;
+            }
+    }
+}
+}  // namespace
+
+__global__ __launch_bounds__(64 * DWAVES) void gemm1_decode_kernel(Gemm1Params<bf16_t> p) {
+    __shared__ float4 red[(DWAVES - 1) * 8 * 64];
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int L = blockIdx.x;
+    if (L >= p.tstart[p.nseg]) return;  // workgroup-uniform
+    const int s = find_segment(p.tstart, p.nseg, L);
+    const SegMeta sm = p.seg[s];
+    const int ntile = L - p.tstart[s];  // one row tile per segment (rows <= 64)
+    const int hs = p.nseg - p.E;
+    const bool shared = s < hs;
+    const size_t wofs = shared ? 0 : (size_t)(s - hs) * p.I * p.d;
+    const bf16_t* Wg = (shared ? p.sg : p.wg) + wofs;
+    const bf16_t* Wu = (shared ? p.su : p.wu) + wofs;
+    const int d = p.d;
+    const int g = lane >> 4;  // K group of this lane
+    const int c = ntile * DCH + (lane & 15);
+    const bool cval = c < sm.kk;
+    const int nf = ceil_div(sm.rows, 16);  // 1..4 token blocks
+
+    const bf16_t* xrow[4];
+#pragma unroll
+    for (int f = 0; f < 4; ++f) {
+        const int r = f * 16 + (lane & 15);
+        xrow[f] = nullptr;
+        if (f < nf && r < sm.rows) {
+            const int t = shared ? r
+                                 : (int)min((unsigned)(p.perm[sm.row0 + r] / p.top_k), (unsigned)(p.tokens - 1));
+            xrow[f] = p.x + (size_t)t * d;
+        }
+    }
+    floatx4_t acc[8];  // [0..3] gate, [4..7] up, per token block
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    const bf16_t* wgr = Wg + (size_t)c * d;
+    const bf16_t* wur = Wu + (size_t)c * d;
+    for (int kb = wave * DKB; kb < d; kb += DWAVES * DKB) {
+        const int k0 = kb + g * 8;  // + 32*j at step j
+        u32x4 wgv[8], wuv[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const bool ok = cval && k0 + j * 32 < d;  // d % 8 == 0
+            wgv[j] = ok ? *reinterpret_cast<const u32x4*>(wgr + k0 + j * 32) : zero;
+            wuv[j] = ok ? *reinterpret_cast<const u32x4*>(wur + k0 + j * 32) : zero;
+        }
+#pragma unroll
+        for (int f = 0; f < 4; ++f) {
+            if (f >= nf) break;  // workgroup-uniform
+            u32x4 xv[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                xv[j] = (xrow[f] && k0 + j * 32 < d) ? *reinterpret_cast<const u32x4*>(xrow[f] + k0 + j * 32) : zero;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                acc[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_frag(wgv[j]), as_frag(xv[j]), acc[f], 0, 0, 0);
+                acc[4 + f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_frag(wuv[j]), as_frag(xv[j]), acc[4 + f], 0, 0, 0);
+            }
+        }
+    }
+    reduce_waves(acc, red, wave, lane);
+    if (wave != 0) return;
+    // D[m][n]: lane holds channels m = 4*(lane/16) + i of token n = lane%16
+    bf16_t* Hb = shared ? p.Hs : p.H + (size_t)sm.row0 * p.I;
+    const int ldh = shared ? p.Is : p.I;
+    const int kk8 = min((sm.kk + 7) & ~7, ldh);
+#pragma unroll
+    for (int f = 0; f < 4; ++f) {
+        if (f >= nf) break;
+        const int r = f * 16 + (lane & 15);
+        if (r >= sm.rows) continue;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int ch = ntile * DCH + 4 * g + i;
+            if (ch < kk8)
+                Hb[(size_t)r * ldh + ch] = ch < sm.kk ? f32_to_bf16(silu_fast(acc[f][i]) * acc[4 + f][i]) : (bf16_t)0;
+        }
+    }
+}
+
+__global__ __launch_bounds__(64 * DWAVES) void gemm2_decode_kernel(Gemm2Params<bf16_t> p) {
+    __shared__ float4 red[(DWAVES - 1) * 4 * 64];
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int L = blockIdx.x;
+    if (L >= p.tstart[p.nseg]) return;  // workgroup-uniform
+    const int s = find_segment(p.tstart, p.nseg, L);
+    const SegMeta sm = p.seg[s];
+    const int local = L - p.tstart[s];
+    const int d = p.d;
+    const int nt = ceil_div(d, DCH);
+    const int split = local / nt, ntile = local % nt;  // split > 0 only for the shared expert
+    const int hs = p.nseg - p.E;
+    const bool shared = s < hs;
+    const int ld = shared ? p.Is : p.I;  // H rows and W_down rows share the stride
+    const bf16_t* Hb = shared ? p.Hs : p.H + (size_t)sm.row0 * p.I;
+    const bf16_t* Wd = shared ? p.sd : p.wd + (size_t)(s - hs) * d * p.I;
+    const int kbeg = shared ? split * p.I : 0;
+    const int kend = shared ? min(sm.kk, kbeg + p.I) : sm.kk;
+    const int g = lane >> 4;
+    const int n = ntile * DCH + (lane & 15);
+    const bool nval = n < d;
+    const int nf = ceil_div(sm.rows, 16);
+    const bf16_t* hrow[4];
+#pragma unroll
+    for (int f = 0; f < 4; ++f) {
+        const int r = f * 16 + (lane & 15);
+        hrow[f] = (f < nf && r < sm.rows) ? Hb + (size_t)r * ld : nullptr;
+    }
+    floatx4_t acc[4];
+#pragma unroll
+    for (int f = 0; f < 4; ++f) acc[f] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    const bf16_t* wrow = Wd + (size_t)n * ld;
+    // a chunk is used when it starts before kend; H is zero past k_e within
+    // the chunk-aligned end, and W_down columns there are real (finite)
+    // weights, so their products are exact zeros
+    for (int kb = kbeg + wave * DKB; kb < kend; kb += DWAVES * DKB) {
+        const int k0 = kb + g * 8;  // + 32*j at step j
+        u32x4 wv[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            wv[j] = (nval && k0 + j * 32 < kend) ? *reinterpret_cast<const u32x4*>(wrow + k0 + j * 32) : zero;
+#pragma unroll
+        for (int f = 0; f < 4; ++f) {
+            if (f >= nf) break;
+            u32x4 hv[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                hv[j] = (hrow[f] && k0 + j * 32 < kend) ? *reinterpret_cast<const u32x4*>(hrow[f] + k0 + j * 32) : zero;
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                acc[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_frag(wv[j]), as_frag(hv[j]), acc[f], 0, 0, 0);
+        }
+    }
+    reduce_waves(acc, red, wave, lane);
+    if (wave != 0) return;
+    // D[m][n']: lane holds output columns m = 4*(lane/16) + i of row n' = lane%16
+    float* Ob = shared ? p.Os + (size_t)split * p.tokens * d : p.O + (size_t)sm.row0 * d;
+#pragma unroll
+    for (int f = 0; f < 4; ++f) {
+        if (f >= nf) break;
+        const int r = f * 16 + (lane & 15);
+        if (r >= sm.rows) continue;
+        const int col = ntile * DCH + 4 * g;
+        if (col + 3 < d) {
+            *reinterpret_cast<float4*>(Ob + (size_t)r * d + col) = make_float4(acc[f][0], acc[f][1], acc[f][2], acc[f][3]);
+        } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (col + i < d) Ob[(size_t)r * d + col + i] = acc[f][i];
+        }
+    }
+}
+
+hipError_t launch_gemm1_decode(const Gemm1Params<bf16_t>& p, int tiles, hipStream_t s) {
+    if (tiles <= 0) return hipSuccess;
+    gemm1_decode_kernel<<<tiles, 64 * DWAVES, 0, s>>>(p);
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm2_decode(const Gemm2Params<bf16_t>& p, int tiles, hipStream_t s) {
+    if (tiles <= 0) return hipSuccess;
+    gemm2_decode_kernel<<<tiles, 64 * DWAVES, 0, s>>>(p);
+    return hipGetLastError();
+}
+
+}  // namespace flexmoe

@@ -37,8 +37,8 @@ struct Gemm2Params {
     const SegMeta* seg;
     const int32_t* tstart;
     float* O;                   // routed rows [A][d]
-    float* Os;                  // shared rows [T][d]
-    int d, I, Is, E, nseg;
+    float* Os;                  // shared rows [T][d] (split reductions: [splits][T][d])
+    int d, I, Is, E, nseg, tokens;
 };
 
 // Tile shapes of the kernel families (the dispatch kernel builds tile tables
@@ -46,6 +46,8 @@ struct Gemm2Params {
 constexpr int kBf16BM1 = 128, kBf16BN1 = 64, kBf16BM2 = 128, kBf16BN2 = 128;
 constexpr int kF32BM = 64, kF32BN = 64;
 constexpr int kBigBM1 = 256, kBigBN1 = 128, kBigBM2 = 256, kBigBN2 = 256;
+constexpr int kDecodeMaxT = 64;     // T at or below which the weight-streaming kernels run
+constexpr int kDecBN = 16;          // their channels / output columns per tile
 
 __global__ void route_kernel(const float* logits, int T, int E, int k, int norm_topk, int32_t* idx,
                              float* wts, int32_t* blockcnt, int NB);
@@ -57,6 +59,11 @@ __global__ void dispatch_scatter_kernel(const int32_t* idx, const int32_t* keep,
                                         TileShape ts, int32_t* perm, int32_t* pos,
                                         int32_t* offsets, SegMeta* seg, int32_t* t1start,
                                         int32_t* t2start);
+__global__ void dispatch_small_kernel(const float* logits, int T, int E, int k, int norm_topk,
+                                      const int32_t* keep, int I, int I_shared, int d, TileShape ts,
+                                      int32_t* idx, float* wts, int32_t* counts, int32_t* perm,
+                                      int32_t* pos, int32_t* offsets, SegMeta* seg, int32_t* t1start,
+                                      int32_t* t2start);
 __global__ void set_keep_kernel(int32_t* keep, KeepArgs t, int E);
 
 // Launchers (defined next to their kernels).  Each returns the launch status.
@@ -64,10 +71,12 @@ hipError_t launch_gemm1_bf16(const Gemm1Params<bf16_t>& p, int grid, hipStream_t
 hipError_t launch_gemm2_bf16(const Gemm2Params<bf16_t>& p, int grid, hipStream_t s);
 hipError_t launch_gemm1_big(const Gemm1Params<bf16_t>& p, int grid, hipStream_t s);
 hipError_t launch_gemm2_big(const Gemm2Params<bf16_t>& p, int grid, hipStream_t s);
+hipError_t launch_gemm1_decode(const Gemm1Params<bf16_t>& p, int tiles, hipStream_t s);
+hipError_t launch_gemm2_decode(const Gemm2Params<bf16_t>& p, int tiles, hipStream_t s);
 hipError_t launch_gemm1_f32(const Gemm1Params<float>& p, int grid, hipStream_t s);
 hipError_t launch_gemm2_f32(const Gemm2Params<float>& p, int grid, hipStream_t s);
 hipError_t launch_combine(const float* O, const float* Os, const int32_t* pos, const float* wts,
-                          int T, int k, int d, int has_shared, int dtype, void* y, hipStream_t s);
+                          int T, int k, int d, int shared_parts, int dtype, void* y, hipStream_t s);
 hipError_t launch_rank_reorder(const float* scores, const void* wg, const void* wu,
                                const void* wd, void* wg_r, void* wu_r, void* wd_r,
                                int32_t* perm, int E, int I, int d, int esize, hipStream_t s);

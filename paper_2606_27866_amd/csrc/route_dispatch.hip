@@ -1,17 +1,19 @@
 // Routing and token dispatch (FlexMoE App. C.3: the gather / sort-by-expert
 // step of the kernelized clipped FFN, done on the device without host syncs).
 //
-//   route_kernel           top-k over fp32 logits + softmax weights, and a
-//                          per-chunk expert histogram (chunk = 64 tokens)
-//   dispatch_scan_kernel   per expert, exclusive scan of the chunk histogram
+//   route_kernel           top-k over fp32 logits + softmax weights, one wave
+//                          per token, and the expert histogram of each chunk
+//                          of kRouteTokens tokens
+//   dispatch_scan_kernel   per expert, exclusive scan of the chunk histograms
 //   dispatch_scatter_kernel  stable placement of every assignment into the
 //                          expert-grouped order (ascending assignment id inside
 //                          an expert), inverse map, segment and tile tables
+//   dispatch_small_kernel  all three in one workgroup, for decode-sized T
 //
 // Experts with k_e = 0 are left out of the grouped order (pos = -1) but still
 // counted.  Nothing here uses atomics whose arrival order could change a
-// result: ranks come from wave ballots and per-chunk scans, so the
-// permutation is bit-reproducible.
+// result: ranks come from wave ballots and scans, so the permutation is
+// bit-reproducible, and both dispatch paths produce the same bits.
 #include "kernels.h"
 
 namespace flexmoe {
@@ -24,79 +26,206 @@ __device__ __forceinline__ bool route_before(float va, int ia, float vb, int ib)
     return ia < ib;
 }
 
-// One chunk of kRouteTokens tokens per workgroup, one wave per token.
-constexpr int kRouteWaves = kRouteTokens;
-constexpr int kTokPerWave = 1;
+// One wave routes one token: lane j < k returns the j-th selected expert and
+// its router weight.  Each lane holds up to four logits; k rounds of a
+// butterfly arg-max under the total order above select the experts (every
+// lane ends a round with the same winner).  Softmax over all E experts,
+// shifted by the largest logit; with norm_topk the k weights are divided by
+// their sum.
+__device__ __forceinline__ void route_token(const float* __restrict__ l, int E, int k, int norm_topk,
+                                            int lane, int& my_id, float& my_w) {
+    float v[4];
+    bool taken[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int e = lane + 64 * q;
+        taken[q] = e >= E;
+        v[q] = e < E ? l[e] : 0.0f;
+    }
+    my_id = 0;
+    float my_logit = 0.0f, m = 0.0f;
+    for (int j = 0; j < k; ++j) {
+        float bv = 0.0f;
+        int bi = -1;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int e = lane + 64 * q;
+            if (!taken[q] && (bi < 0 || route_before(v[q], e, bv, bi))) {
+                bv = v[q];
+                bi = e;
+            }
+        }
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) {
+            const float ov = __shfl_xor(bv, o, 64);
+            const int oi = __shfl_xor(bi, o, 64);
+            if (oi >= 0 && (bi < 0 || route_before(ov, oi, bv, bi))) {
+                bv = ov;
+                bi = oi;
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            if (bi == lane + 64 * q) taken[q] = true;
+        if (lane == j) {
+            my_id = bi;
+            my_logit = bv;
+        }
+        if (j == 0) m = bv;
+    }
+    float z = 0.0f;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+        if (lane + 64 * q < E) z += expf(v[q] - m);
+    z = wave_sum_f(z);
+    float w = lane < k ? expf(my_logit - m) / z : 0.0f;
+    if (norm_topk) w = w / wave_sum_f(w);
+    my_w = w;
+}
 
-__global__ __launch_bounds__(64 * kRouteWaves) void route_kernel(
+// One wave: exclusive scan over experts of the active counts (k_e > 0, k_e
+// clamped to [0, I]; device data is never trusted for addressing), four
+// experts per lane.  Fills off[], kk_s[] and zeroes run[]; returns P.
+template <typename CountFn>
+__device__ __forceinline__ int expert_offsets(CountFn count, const int32_t* __restrict__ keep, int E,
+                                              int I, int* off, int* kk_s, int* run) {
+    const int lane = threadIdx.x & 63;
+    int c4[4], k4[4], local = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int e = lane * 4 + q;
+        int kk = 0, c = 0;
+        if (e < E) {
+            kk = min(max(keep[e], 0), I);
+            c = kk > 0 ? count(e) : 0;
+        }
+        c4[q] = c;
+        k4[q] = kk;
+        local += c;
+    }
+    const int inc = wave_incl_scan(local);
+    int base = inc - local;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int e = lane * 4 + q;
+        if (e < E) {
+            off[e] = base;
+            kk_s[e] = k4[q];
+            run[e] = 0;
+        }
+        base += c4[q];
+    }
+    return __shfl(inc, 63, 64);
+}
+
+// One wave: segment table (shared expert first: its tiles carry the longest
+// reductions, so they start first) and the exclusive scans of both GEMMs'
+// tile counts, 64 segments per round.
+template <typename CountFn>
+__device__ void write_tables(CountFn count, const int* off, const int* kk_s, int P, int T, int E,
+                             int I_shared, int d, TileShape ts, int32_t* __restrict__ offsets,
+                             SegMeta* __restrict__ seg, int32_t* __restrict__ t1start,
+                             int32_t* __restrict__ t2start) {
+    const int lane = threadIdx.x & 63;
+    const int hs = I_shared > 0 ? 1 : 0;
+    const int nseg = E + hs;
+    int c1 = 0, c2 = 0;
+    for (int s0 = 0; s0 < nseg; s0 += 64) {
+        const int s = s0 + lane;
+        int n1 = 0, n2 = 0;
+        if (s < nseg) {
+            SegMeta m;
+            if (s < hs) {
+                m.row0 = 0;
+                m.rows = T;
+                m.kk = I_shared;
+            } else {
+                const int e = s - hs;
+                m.row0 = off[e];
+                m.rows = kk_s[e] > 0 ? count(e) : 0;
+                m.kk = kk_s[e];
+                offsets[e] = off[e];
+            }
+            m.pad = 0;
+            seg[s] = m;
+            if (m.rows > 0 && m.kk > 0) {
+                n1 = ceil_div(m.rows, ts.bm1) * ceil_div(m.kk, ts.bn1);
+                n2 = ceil_div(m.rows, ts.bm2) * ceil_div(d, ts.bn2);
+                if (s < hs && ts.ks2 > 0) n2 *= ceil_div(m.kk, ts.ks2);
+            }
+        }
+        const int i1 = wave_incl_scan(n1), i2 = wave_incl_scan(n2);
+        if (s < nseg) {
+            t1start[s] = c1 + i1 - n1;
+            t2start[s] = c2 + i2 - n2;
+        }
+        c1 += __shfl(i1, 63, 64);
+        c2 += __shfl(i2, 63, 64);
+    }
+    if (lane == 0) {
+        offsets[E] = P;
+        t1start[nseg] = c1;
+        t2start[nseg] = c2;
+    }
+}
+
+// One wave: stable placement of assignments [a0, a1) in rounds of 64.  The
+// match mask of equal expert ids comes from 8 ballots; a lane's rank is the
+// number of matching lower lanes; the lowest matching lane advances run[e].
+// base(e) is where this range's first assignment of expert e goes.
+template <typename BaseFn>
+__device__ __forceinline__ void place(const int32_t* __restrict__ idx, int a0, int a1, const int* kk_s,
+                                      int* run, BaseFn base, int32_t* __restrict__ perm,
+                                      int32_t* __restrict__ pos) {
+    const int lane = threadIdx.x & 63;
+    const uint64_t lt = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
+    for (int r0 = a0; r0 < a1; r0 += 64) {
+        const int a = r0 + lane;
+        const bool valid = a < a1;
+        const int e = valid ? idx[a] : 0;
+        uint64_t match = __ballot(valid);
+#pragma unroll
+        for (int bit = 0; bit < 8; ++bit) {
+            const bool b = (e >> bit) & 1;
+            const uint64_t bb = __ballot(valid && b);
+            match &= b ? bb : ~bb;
+        }
+        const int rank = __popcll(match & lt);
+        const int r = valid ? run[e] : 0;
+        __builtin_amdgcn_wave_barrier();
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        if (valid) {
+            if (kk_s[e] > 0) {
+                const int dst = base(e) + r + rank;
+                perm[dst] = a;
+                pos[a] = dst;
+            } else {
+                pos[a] = -1;
+            }
+            if ((match & lt) == 0) run[e] = r + __popcll(match);
+        }
+        __builtin_amdgcn_wave_barrier();
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    }
+}
+
+// One chunk of kRouteTokens tokens per workgroup, one wave per token.
+__global__ __launch_bounds__(64 * kRouteTokens) void route_kernel(
     const float* __restrict__ logits, int T, int E, int k, int norm_topk,
     int32_t* __restrict__ idx, float* __restrict__ wts, int32_t* __restrict__ blockcnt, int NB) {
     __shared__ int hist[kMaxExperts];
     for (int e = threadIdx.x; e < E; e += blockDim.x) hist[e] = 0;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int t0 = blockIdx.x * kRouteTokens + wave;
-    float v[kTokPerWave][4];
-#pragma unroll
-    for (int i = 0; i < kTokPerWave; ++i) {
-        const int t = t0 + i * kRouteWaves;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int e = lane + 64 * q;
-            v[i][q] = (t < T && e < E) ? logits[(size_t)t * E + e] : 0.0f;
-        }
-    }
     __syncthreads();
-#pragma unroll
-    for (int i = 0; i < kTokPerWave; ++i) {
-        const int t = t0 + i * kRouteWaves;
-        if (t >= T) break;  // uniform across the wave
-        bool taken[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) taken[q] = lane + 64 * q >= E;
-        int my_id = 0;
-        float my_logit = 0.0f, m = 0.0f;
-        for (int j = 0; j < k; ++j) {
-            float bv = 0.0f;
-            int bi = -1;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int e = lane + 64 * q;
-                if (!taken[q] && (bi < 0 || route_before(v[i][q], e, bv, bi))) {
-                    bv = v[i][q];
-                    bi = e;
-                }
-            }
-#pragma unroll
-            for (int o = 32; o > 0; o >>= 1) {
-                const float ov = __shfl_xor(bv, o, 64);
-                const int oi = __shfl_xor(bi, o, 64);
-                if (oi >= 0 && (bi < 0 || route_before(ov, oi, bv, bi))) {
-                    bv = ov;
-                    bi = oi;
-                }
-            }
-            // every lane now holds the same winner (a total order makes the
-            // butterfly reduction lane-independent)
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-                if (bi == lane + 64 * q) taken[q] = true;
-            if (lane == j) {
-                my_id = bi;
-                my_logit = bv;
-            }
-            if (j == 0) m = bv;
-        }
-        float z = 0.0f;
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-            if (lane + 64 * q < E) z += expf(v[i][q] - m);
-        z = wave_sum_f(z);
-        float w = lane < k ? expf(my_logit - m) / z : 0.0f;
-        if (norm_topk) w = w / wave_sum_f(w);
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int t = blockIdx.x * kRouteTokens + wave;
+    if (t < T) {  // uniform across the wave
+        int id;
+        float w;
+        route_token(logits + (size_t)t * E, E, k, norm_topk, lane, id, w);
         if (lane < k) {
-            idx[(size_t)t * k + lane] = my_id;
+            idx[(size_t)t * k + lane] = id;
             wts[(size_t)t * k + lane] = w;
-            atomicAdd(&hist[my_id], 1);  // a count: arrival order does not matter
+            atomicAdd(&hist[id], 1);  // a count: arrival order does not matter
         }
     }
     __syncthreads();
@@ -144,35 +273,6 @@ __global__ __launch_bounds__(256) void dispatch_scan_kernel(const int32_t* __res
     if (threadIdx.x == 0) counts[e] = carry;
 }
 
-// Exclusive scan of per-segment tile counts, 64 segments per round.
-__device__ void scan_tiles(const SegMeta* seg_l, int nseg, int d, TileShape ts,
-                           int32_t* t1start, int32_t* t2start) {
-    const int lane = threadIdx.x & 63;
-    int c1 = 0, c2 = 0;
-    for (int s0 = 0; s0 < nseg; s0 += 64) {
-        const int s = s0 + lane;
-        int n1 = 0, n2 = 0;
-        if (s < nseg) {
-            const SegMeta m = seg_l[s];
-            if (m.rows > 0 && m.kk > 0) {
-                n1 = ceil_div(m.rows, ts.bm1) * ceil_div(m.kk, ts.bn1);
-                n2 = ceil_div(m.rows, ts.bm2) * ceil_div(d, ts.bn2);
-            }
-        }
-        const int i1 = wave_incl_scan(n1), i2 = wave_incl_scan(n2);
-        if (s < nseg) {
-            t1start[s] = c1 + i1 - n1;
-            t2start[s] = c2 + i2 - n2;
-        }
-        c1 += __shfl(i1, 63, 64);
-        c2 += __shfl(i2, 63, 64);
-    }
-    if (lane == 0) {
-        t1start[nseg] = c1;
-        t2start[nseg] = c2;
-    }
-}
-
 __global__ __launch_bounds__(64) void dispatch_scatter_kernel(
     const int32_t* __restrict__ idx, const int32_t* __restrict__ keep,
     const int32_t* __restrict__ counts, const int32_t* __restrict__ blockbase, int T, int E, int k,
@@ -182,99 +282,53 @@ __global__ __launch_bounds__(64) void dispatch_scatter_kernel(
     __shared__ int off[kMaxExperts];
     __shared__ int kk_s[kMaxExperts];
     __shared__ int run[kMaxExperts];
-    __shared__ SegMeta seg_l[kMaxExperts + 1];
-    const int lane = threadIdx.x;
-
-    // exclusive scan of the active counts over experts (4 experts per lane)
-    int c4[4], k4[4], local = 0;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const int e = lane * 4 + q;
-        int kk = 0, c = 0;
-        if (e < E) {
-            kk = min(max(keep[e], 0), I);  // device data is clamped, never trusted
-            c = kk > 0 ? counts[e] : 0;
-        }
-        c4[q] = c;
-        k4[q] = kk;
-        local += c;
-    }
-    const int inc = wave_incl_scan(local);
-    int base = inc - local;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const int e = lane * 4 + q;
-        if (e < E) {
-            off[e] = base;
-            kk_s[e] = k4[q];
-            run[e] = 0;
-        }
-        base += c4[q];
-    }
-    const int P = __shfl(inc, 63, 64);
+    auto count = [&](int e) { return counts[e]; };
+    const int P = expert_offsets(count, keep, E, I, off, kk_s, run);
     __syncthreads();
-
-    if (blockIdx.x == 0) {
-        // segment order: the shared expert (if any) first, then experts 0..E-1;
-        // its tiles carry the longest reductions, so they start first
-        const int hs = I_shared > 0 ? 1 : 0;
-        const int nseg = E + hs;
-        for (int e = lane; e < E; e += 64) {
-            offsets[e] = off[e];
-            SegMeta m;
-            m.row0 = off[e];
-            m.rows = kk_s[e] > 0 ? counts[e] : 0;
-            m.kk = kk_s[e];
-            m.pad = 0;
-            seg_l[hs + e] = m;
-            seg[hs + e] = m;
-        }
-        if (lane == 0) {
-            offsets[E] = P;
-            if (hs) {
-                SegMeta m;
-                m.row0 = 0;
-                m.rows = T;
-                m.kk = I_shared;
-                m.pad = 0;
-                seg_l[0] = m;
-                seg[0] = m;
-            }
-        }
-        __syncthreads();
-        scan_tiles(seg_l, nseg, d, ts, t1start, t2start);
-    }
-
-    // stable placement: rounds of 64 consecutive assignments of this chunk
+    if (blockIdx.x == 0) write_tables(count, off, kk_s, P, T, E, I_shared, d, ts, offsets, seg, t1start, t2start);
     const int a0 = blockIdx.x * kRouteTokens * k;
     const int a1 = min((blockIdx.x + 1) * kRouteTokens, T) * k;
-    const uint64_t lt = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
-    for (int r0 = a0; r0 < a1; r0 += 64) {
-        const int a = r0 + lane;
-        const bool valid = a < a1;
-        const int e = valid ? idx[a] : 0;
-        uint64_t match = __ballot(valid);
-#pragma unroll
-        for (int bit = 0; bit < 8; ++bit) {
-            const bool b = (e >> bit) & 1;
-            const uint64_t bb = __ballot(valid && b);
-            match &= b ? bb : ~bb;
+    auto base = [&](int e) { return off[e] + blockbase[(size_t)e * NB + blockIdx.x]; };
+    place(idx, a0, a1, kk_s, run, base, perm, pos);
+}
+
+// Route, count, scan and place in one workgroup (T * k <= kSmallAssign).
+__global__ __launch_bounds__(1024) void dispatch_small_kernel(
+    const float* __restrict__ logits, int T, int E, int k, int norm_topk,
+    const int32_t* __restrict__ keep, int I, int I_shared, int d, TileShape ts,
+    int32_t* __restrict__ idx, float* __restrict__ wts, int32_t* __restrict__ counts,
+    int32_t* __restrict__ perm, int32_t* __restrict__ pos, int32_t* __restrict__ offsets,
+    SegMeta* __restrict__ seg, int32_t* __restrict__ t1start, int32_t* __restrict__ t2start) {
+    __shared__ int hist[kMaxExperts];
+    __shared__ int off[kMaxExperts];
+    __shared__ int kk_s[kMaxExperts];
+    __shared__ int run[kMaxExperts];
+    __shared__ int32_t sidx[kSmallAssign];
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int nwave = blockDim.x >> 6;
+    for (int e = threadIdx.x; e < E; e += blockDim.x) hist[e] = 0;
+    __syncthreads();
+    for (int t = wave; t < T; t += nwave) {
+        int id;
+        float w;
+        route_token(logits + (size_t)t * E, E, k, norm_topk, lane, id, w);
+        if (lane < k) {
+            idx[(size_t)t * k + lane] = id;
+            wts[(size_t)t * k + lane] = w;
+            sidx[t * k + lane] = id;
+            atomicAdd(&hist[id], 1);  // a count: arrival order does not matter
         }
-        const int rank = __popcll(match & lt);
-        const int r = valid ? run[e] : 0;
-        __syncthreads();
-        if (valid) {
-            if (kk_s[e] > 0) {
-                const int dst = off[e] + blockbase[(size_t)e * NB + blockIdx.x] + r + rank;
-                perm[dst] = a;
-                pos[a] = dst;
-            } else {
-                pos[a] = -1;
-            }
-            if ((match & lt) == 0) run[e] = r + __popcll(match);
-        }
-        __syncthreads();
     }
+    __syncthreads();
+    if (wave != 0) return;
+    for (int e = lane; e < E; e += 64) counts[e] = hist[e];
+    auto count = [&](int e) { return hist[e]; };
+    const int P = expert_offsets(count, keep, E, I, off, kk_s, run);
+    __builtin_amdgcn_wave_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    write_tables(count, off, kk_s, P, T, E, I_shared, d, ts, offsets, seg, t1start, t2start);
+    auto base = [&](int e) { return off[e]; };
+    place(sidx, 0, T * k, kk_s, run, base, perm, pos);
 }
 
 __global__ void set_keep_kernel(int32_t* __restrict__ keep, KeepArgs t, int E) {

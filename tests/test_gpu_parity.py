@@ -50,6 +50,17 @@ def test_tiny_fp32_all_tables():
         check_y(y, ref, F32_TOL)
 
 
+def test_fp32_multi_chunk_dispatch():
+    """fp32 layer whose T*top_k exceeds one dispatch workgroup."""
+    cfg, x, lg, w, s = mini_layer("f32_big", 600, 64, 8, 96, 2, 32, dtype=synth.F32, config_id=77)
+    g = gpu_layer_for(cfg, w, s)
+    keep = np.array([96, 0, 17, 64, 65, 1, 96, 33], np.int32)
+    y, r = g.forward(x, lg, keep)
+    ref, rr = oracle_ref(cfg, x, lg, w, s, keep)
+    check_route(r, rr)
+    check_y(y, ref, F32_TOL)
+
+
 def test_tiny_fp32_zero_budget_is_exact_zero():
     cfg = synth.CONFIGS["tiny_fp32"]
     x, lg = synth.make_tokens(cfg)
@@ -71,6 +82,10 @@ MINIS = [
     ("m_top1", 77, 64, 5, 64, 1, 0, 1),
     ("m_256_experts", 100, 64, 256, 64, 8, 64, 0),
     ("m_shared_wide", 150, 192, 6, 72, 2, 520, 1),
+    # T*top_k = 256 is the largest batch dispatched by one workgroup, 258
+    # takes the three-kernel dispatch path
+    ("m_dispatch_256", 128, 64, 8, 64, 2, 0, 1),
+    ("m_dispatch_258", 129, 64, 8, 64, 2, 64, 0),
 ]
 
 
