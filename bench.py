@@ -50,12 +50,15 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-per-budget", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-baseline work")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="after timing, copy this many MiB device-to-device once, so that a "
+                         "counter run sees a plain copy of known size (HBM byte calibration)")
     return ap.parse_args()
 
 
 def kernel_src_hash():
     h = hashlib.sha256()
-    for f in ("gemm_bf16.hip", "common.h", "kernels.h"):
+    for f in ("gemm_bf16_big.hip", "gemm_decode.hip", "common.h", "kernels.h"):
         h.update(open(os.path.join(ROOT, "paper_2606_27866_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
 
@@ -267,6 +270,15 @@ def main():
                                    frac_hbm=a["B"] / sb / 1e9 / PEAK_HBM_GBS))
             log("[bench]   budget %-7s %.4f ms  %.0f tok/s  %.1f TFLOP/s" %
                 (name, sb * 1e3, wl.T / sb, a["F"] / sb / 1e12))
+
+    if args.copy_calibration_mib > 0:
+        n = args.copy_calibration_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     cpu = None
     if not args.no_cpu:
