@@ -27,6 +27,13 @@
 //   multiplies gate rows [wn*32, wn*32+32) and the matching up rows, so the
 //   gate and up accumulators of a channel sit in the same lane.
 // down: a workgroup tile is 256 rows x 256 output columns.
+// A segment's last row tile often holds far fewer than 256 rows (a routed
+// expert gets a few hundred tokens).  A tile with R rows runs the variant in
+// which each wave multiplies ceil(R/64) fragments of 32 rows, so MFMA work
+// follows the rows at a 64-row granularity; the loads stay the same (rows
+// past the segment read the zero page).
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace flexmoe {
@@ -35,8 +42,7 @@ namespace {
 constexpr int BM = 256, BN = 256, BK = 32;
 constexpr int NWAVE = 8, THREADS = 64 * NWAVE;
 constexpr int WM = 2, WN = 4;               // wave grid
-constexpr int WROWS = BM / WM;              // 128 rows per wave
-constexpr int MF = WROWS / 32;              // 4 row fragments per wave
+static_assert(BM == WM * 128, "a full tile gives each M-wave four 32-row fragments");
 constexpr int NF = 2;                       // 2 column fragments per wave (64 columns)
 constexpr int NSTAGE = 4;
 constexpr int ROWB = BK * 2;                // bytes per LDS row
@@ -173,116 +179,122 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
         else
             brow[j] = wn * 64 + j * 32;
     }
-    floatx16 acc[MF][NF];
-#pragma unroll
-    for (int i = 0; i < MF; ++i)
-#pragma unroll
-        for (int j = 0; j < NF; ++j)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
-
     static_assert(BK == 32, "the loop below runs two 16-deep MFMA steps per K tile");
     const int nk = ceil_div(K, BK);
-    bf16x8 a[2][MF], b[2][NF];
-    auto read_frags = [&](int kt, int ks, int buf) {
-        const unsigned char* sa = smem + (kt % NSTAGE) * STAGE;
-        const unsigned char* sb = sa + STAGE_A;
-        const int chunk = ks * 2 + (lane >> 5);
+
+    // The K loop and epilogue for tiles whose waves multiply MFW 32-row
+    // fragments each (the two M-waves then cover 64*MFW rows).
+    auto run = [&](auto mfw_tag) {
+        constexpr int MFW = decltype(mfw_tag)::value;
+        constexpr int WR = 32 * MFW;                    // rows per wave
+        constexpr int NMF = MFW * NF;                   // MFMAs per 16-deep step
+        constexpr int NRD = MFW + NF;                   // fragment reads per step
+        floatx16 acc[MFW][NF];
 #pragma unroll
-        for (int i = 0; i < MF; ++i) a[buf][i] = lds_frag(sa, wm * WROWS + i * 32 + (lane & 31), chunk);
-#pragma unroll
-        for (int j = 0; j < NF; ++j) b[buf][j] = lds_frag(sb, brow[j] + (lane & 31), chunk);
-    };
-    auto mfma_step = [&](int buf) {
-#pragma unroll
-        for (int i = 0; i < MF; ++i)
+        for (int i = 0; i < MFW; ++i)
 #pragma unroll
             for (int j = 0; j < NF; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][i], b[buf][j], acc[i][j], 0, 0, 0);
-    };
-    // one MFMA, then a fragment read, spread over a step's 8 MFMAs
-    auto interleave_reads = []() {
 #pragma unroll
-        for (int r = 0; r < MF + NF; ++r) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
-        }
-        __builtin_amdgcn_sched_group_barrier(0x008, MF * NF - (MF + NF), 0);
-    };
-    // same, with the DMA loads of a later tile spread in as well
-    auto interleave_reads_dma = []() {
+                for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+        bf16x8 a[2][MFW], b[2][NF];
+        auto read_frags = [&](int kt, int ks, int buf) {
+            const unsigned char* sa = smem + (kt % NSTAGE) * STAGE;
+            const unsigned char* sb = sa + STAGE_A;
+            const int chunk = ks * 2 + (lane >> 5);
 #pragma unroll
-        for (int r = 0; r < LOADS_PER_TILE; ++r) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-            __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read (DMA)
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
-        }
-        __builtin_amdgcn_sched_group_barrier(0x100, MF + NF - LOADS_PER_TILE, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, MF * NF - LOADS_PER_TILE, 0);
-    };
+            for (int i = 0; i < MFW; ++i) a[buf][i] = lds_frag(sa, wm * WR + i * 32 + (lane & 31), chunk);
+#pragma unroll
+            for (int j = 0; j < NF; ++j) b[buf][j] = lds_frag(sb, brow[j] + (lane & 31), chunk);
+        };
+        auto mfma_step = [&](int buf) {
+#pragma unroll
+            for (int i = 0; i < MFW; ++i)
+#pragma unroll
+                for (int j = 0; j < NF; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][i], b[buf][j], acc[i][j], 0, 0, 0);
+        };
+        // one MFMA, then a fragment read (then a DMA load), spread over a step
+        auto interleave = [](bool dma) {
+            constexpr int NV = LOADS_PER_TILE;
+            constexpr int R = NMF > NRD ? (NMF > NV ? NMF : NV) : (NRD > NV ? NRD : NV);
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                if (r < NMF) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);      // MFMA
+                if (dma && r < NV) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0); // VMEM read (DMA)
+                if (r < NRD) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);     // DS read
+            }
+        };
 
-    // Ping-pong schedule over NSTAGE K tiles in LDS, three DMAs ahead:
-    //   read (kt, step 1) | MFMA (kt, step 0) | wait tile kt+1, barrier |
-    //   DMA tile kt+4 into the stage of tile kt | read (kt+1, step 0) | MFMA (kt, step 1)
-    // Every iteration issues one tile's DMAs (zero-page loads once past the
-    // end), so before the wait of iteration kt the tiles 0 .. kt+3 are issued
-    // and tile kt+1 is in once at most two tiles' DMAs are outstanding.
+        // Ping-pong schedule over NSTAGE K tiles in LDS, three DMAs ahead:
+        //   read (kt, step 1) | MFMA (kt, step 0) | wait tile kt+1, barrier |
+        //   DMA tile kt+4 into the stage of tile kt | read (kt+1, step 0) | MFMA (kt, step 1)
+        // Every iteration issues one tile's DMAs (zero-page loads once past
+        // the end), so before the wait of iteration kt the tiles 0 .. kt+3 are
+        // issued and tile kt+1 is in once at most two tiles' DMAs are
+        // outstanding.
 #pragma unroll
-    for (int t = 0; t < NSTAGE; ++t) issue(t, t);
-    __builtin_amdgcn_s_waitcnt(waitcnt_vm((NSTAGE - 1) * LOADS_PER_TILE));
-    barrier_no_fence();
-    read_frags(0, 0, 0);
-    for (int kt = 0; kt < nk; ++kt) {
-        read_frags(kt, 1, 1);
-        mfma_step(0);
-        interleave_reads();
-        __builtin_amdgcn_sched_barrier(0);
-        __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * LOADS_PER_TILE) & kWaitLgkm0);  // tile kt+1 in; own reads done
-        barrier_no_fence();  // all waves are done reading tile kt: its stage is free
-        __builtin_amdgcn_sched_barrier(0);
-        issue(kt + NSTAGE, kt % NSTAGE);
-        // after the last tile this reads a stale stage, whose values go unused
-        read_frags(kt + 1, 0, 0);
-        mfma_step(1);
-        interleave_reads_dma();
-        __builtin_amdgcn_sched_barrier(0);
-    }
-    __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // no DMA may outlive the workgroup's LDS
+        for (int t = 0; t < NSTAGE; ++t) issue(t, t);
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm((NSTAGE - 1) * LOADS_PER_TILE));
+        barrier_no_fence();
+        read_frags(0, 0, 0);
+        for (int kt = 0; kt < nk; ++kt) {
+            read_frags(kt, 1, 1);
+            mfma_step(0);
+            interleave(false);
+            __builtin_amdgcn_sched_barrier(0);
+            __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * LOADS_PER_TILE) & kWaitLgkm0);  // tile kt+1 in; own reads done
+            barrier_no_fence();  // all waves are done reading tile kt: its stage is free
+            __builtin_amdgcn_sched_barrier(0);
+            issue(kt + NSTAGE, kt % NSTAGE);
+            // after the last tile this reads a stale stage, whose values go unused
+            read_frags(kt + 1, 0, 0);
+            mfma_step(1);
+            interleave(true);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // no DMA may outlive the workgroup's LDS
 
-    // ---- epilogue: 32x32 accumulator layout, lane -> column lane%32, register v
-    // -> row (v/4)*8 + (lane/32)*4 + v%4
-    if constexpr (kGateUp) {
-        bf16_t* Hb = shared ? p1.Hs : p1.H + (size_t)sm.row0 * p1.I;
-        const int ldh = shared ? p1.Is : p1.I;
-        const int kk8 = min((sm.kk + 7) & ~7, ldh);  // chunk-aligned end: [kk, kk8) is zero-filled
-        const int ch = ntile * (BN / 2) + wn * 32 + (lane & 31);
-        if (ch < kk8) {
+        // ---- epilogue: 32x32 accumulator layout, lane -> column lane%32,
+        // register v -> row (v/4)*8 + (lane/32)*4 + v%4
+        if constexpr (kGateUp) {
+            bf16_t* Hb = shared ? p1.Hs : p1.H + (size_t)sm.row0 * p1.I;
+            const int ldh = shared ? p1.Is : p1.I;
+            const int kk8 = min((sm.kk + 7) & ~7, ldh);  // chunk-aligned end: [kk, kk8) is zero-filled
+            const int ch = ntile * (BN / 2) + wn * 32 + (lane & 31);
+            if (ch < kk8) {
 #pragma unroll
-            for (int i = 0; i < MF; ++i)
+                for (int i = 0; i < MFW; ++i)
 #pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const int row = mtile * BM + wm * WROWS + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
-                    if (row < sm.rows) {
-                        const float g = acc[i][0][v], u = acc[i][1][v];
-                        Hb[(size_t)row * ldh + ch] = ch < sm.kk ? f32_to_bf16(silu_fast(g) * u) : (bf16_t)0;
+                    for (int v = 0; v < 16; ++v) {
+                        const int row = mtile * BM + wm * WR + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
+                        if (row < sm.rows) {
+                            const float g = acc[i][0][v], u = acc[i][1][v];
+                            Hb[(size_t)row * ldh + ch] = ch < sm.kk ? f32_to_bf16(silu_fast(g) * u) : (bf16_t)0;
+                        }
                     }
-                }
+            }
+        } else {
+            float* Ob = shared ? p2.Os : p2.O + (size_t)sm.row0 * d;
+#pragma unroll
+            for (int j = 0; j < NF; ++j) {
+                const int n = ntile * BN + wn * 64 + j * 32 + (lane & 31);
+                if (n >= d) continue;
+#pragma unroll
+                for (int i = 0; i < MFW; ++i)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) {
+                        const int row = mtile * BM + wm * WR + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
+                        if (row < sm.rows) Ob[(size_t)row * d + n] = acc[i][j][v];
+                    }
+            }
         }
-    } else {
-        float* Ob = shared ? p2.Os : p2.O + (size_t)sm.row0 * d;
-#pragma unroll
-        for (int j = 0; j < NF; ++j) {
-            const int n = ntile * BN + wn * 64 + j * 32 + (lane & 31);
-            if (n >= d) continue;
-#pragma unroll
-            for (int i = 0; i < MF; ++i)
-#pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const int row = mtile * BM + wm * WROWS + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
-                    if (row < sm.rows) Ob[(size_t)row * d + n] = acc[i][j][v];
-                }
-        }
-    }
+    };
+
+    const int tile_rows = min(BM, sm.rows - mtile * BM);
+    if (tile_rows > 3 * 64) run(std::integral_constant<int, 4>{});
+    else if (tile_rows > 2 * 64) run(std::integral_constant<int, 3>{});
+    else if (tile_rows > 64) run(std::integral_constant<int, 2>{});
+    else run(std::integral_constant<int, 1>{});
 }
 
 __global__ __launch_bounds__(THREADS, 2) void gemm1_big_kernel(Gemm1Params<bf16_t> p) {
