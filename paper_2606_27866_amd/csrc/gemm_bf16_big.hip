@@ -39,12 +39,16 @@
 namespace flexmoe {
 
 namespace {
-constexpr int BM = 256, BN = 256, BK = 32;
+#ifndef FLEXMOE_BIG_BK
+#define FLEXMOE_BIG_BK 64
+#endif
+constexpr int BM = 256, BN = 256, BK = FLEXMOE_BIG_BK;
 constexpr int NWAVE = 8, THREADS = 64 * NWAVE;
 constexpr int WM = 2, WN = 4;               // wave grid
 static_assert(BM == WM * 128, "a full tile gives each M-wave four 32-row fragments");
 constexpr int NF = 2;                       // 2 column fragments per wave (64 columns)
-constexpr int NSTAGE = 4;
+constexpr int NSTAGE = BK == 32 ? 4 : 2;    // 128 KB of LDS either way
+constexpr int NSTEP = BK / 16;              // 16-deep MFMA steps per K tile
 constexpr int ROWB = BK * 2;                // bytes per LDS row
 constexpr int CHUNKS = ROWB / 16;           // 16-byte chunks per LDS row
 constexpr int RPI = 64 / CHUNKS;            // LDS rows filled per DMA instruction
@@ -57,7 +61,11 @@ constexpr int XCD_GROUP = 8;                // consecutive tiles kept on one XCD
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void lds_ptr_t;
 
-__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 2) & 3); }
+// 16 lanes of a fragment read hit 16 consecutive rows at one logical chunk;
+// XOR-ing the chunk with the row bits above the bank period spreads them
+// over all 64 banks (64-byte rows: bits 2..3; 128-byte rows: bits 1..3).
+constexpr int SWS = BK == 32 ? 2 : 1;
+__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> SWS) & (CHUNKS - 1)); }
 
 // s_waitcnt with vmcnt = n and no wait on expcnt / lgkmcnt (gfx9 encoding).
 constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
@@ -179,7 +187,7 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
         else
             brow[j] = wn * 64 + j * 32;
     }
-    static_assert(BK == 32, "the loop below runs two 16-deep MFMA steps per K tile");
+    static_assert(NSTEP % 2 == 0, "fragment buffers alternate between steps");
     const int nk = ceil_div(K, BK);
 
     // The K loop and epilogue for tiles whose waves multiply MFW 32-row
@@ -225,30 +233,34 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
             }
         };
 
-        // Ping-pong schedule over NSTAGE K tiles in LDS, three DMAs ahead:
-        //   read (kt, step 1) | MFMA (kt, step 0) | wait tile kt+1, barrier |
-        //   DMA tile kt+4 into the stage of tile kt | read (kt+1, step 0) | MFMA (kt, step 1)
+        // Ping-pong schedule over NSTAGE K tiles in LDS, NSTAGE-1 DMAs ahead:
+        //   read (kt, s+1) | MFMA (kt, s)   for the steps s < NSTEP-1
+        //   wait tile kt+1, barrier | DMA tile kt+NSTAGE into the stage of tile kt |
+        //   read (kt+1, 0) | MFMA (kt, NSTEP-1)
         // Every iteration issues one tile's DMAs (zero-page loads once past
-        // the end), so before the wait of iteration kt the tiles 0 .. kt+3 are
-        // issued and tile kt+1 is in once at most two tiles' DMAs are
-        // outstanding.
+        // the end), so before the wait of iteration kt the tiles
+        // 0 .. kt+NSTAGE-1 are issued and tile kt+1 is in once at most
+        // NSTAGE-2 tiles' DMAs are outstanding.
 #pragma unroll
         for (int t = 0; t < NSTAGE; ++t) issue(t, t);
         __builtin_amdgcn_s_waitcnt(waitcnt_vm((NSTAGE - 1) * LOADS_PER_TILE));
         barrier_no_fence();
         read_frags(0, 0, 0);
         for (int kt = 0; kt < nk; ++kt) {
-            read_frags(kt, 1, 1);
-            mfma_step(0);
-            interleave(false);
-            __builtin_amdgcn_sched_barrier(0);
-            __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * LOADS_PER_TILE) & kWaitLgkm0);  // tile kt+1 in; own reads done
+#pragma unroll
+            for (int st = 0; st < NSTEP - 1; ++st) {
+                read_frags(kt, st + 1, (st + 1) & 1);
+                mfma_step(st & 1);
+                interleave(false);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            __builtin_amdgcn_s_waitcnt(waitcnt_vm((NSTAGE - 2) * LOADS_PER_TILE) & kWaitLgkm0);  // tile kt+1 in; own reads done
             barrier_no_fence();  // all waves are done reading tile kt: its stage is free
             __builtin_amdgcn_sched_barrier(0);
             issue(kt + NSTAGE, kt % NSTAGE);
             // after the last tile this reads a stale stage, whose values go unused
             read_frags(kt + 1, 0, 0);
-            mfma_step(1);
+            mfma_step((NSTEP - 1) & 1);
             interleave(true);
             __builtin_amdgcn_sched_barrier(0);
         }
