@@ -5,13 +5,21 @@
 // type.  Assignments of experts with k_e = 0 have pos = -1 and add nothing.
 // S[t] is the sum of the shared expert's partial rows Os[part][t] (one part
 // unless its down projection was split), added in ascending part order.
+// O and Os are fp32 in fp32 mode and bf16 in bf16 mode.
 #include "kernels.h"
 
 namespace flexmoe {
 
+__device__ __forceinline__ float4 load4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+__device__ __forceinline__ float4 load4(const bf16_t* p) {
+    const uint2 v = *reinterpret_cast<const uint2*>(p);
+    return make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u),
+                       __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xffff0000u));
+}
+
 template <typename OutT>
-__global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ O,
-                                                      const float* __restrict__ Os,
+__global__ __launch_bounds__(256) void combine_kernel(const OutT* __restrict__ O,
+                                                      const OutT* __restrict__ Os,
                                                       const int32_t* __restrict__ pos,
                                                       const float* __restrict__ wts, int T, int k,
                                                       int d, int shared_parts, OutT* __restrict__ y) {
@@ -23,7 +31,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
             const int p = pos[(size_t)t * k + j];
             if (p < 0) continue;
             const float w = wts[(size_t)t * k + j];
-            const float4 o = *reinterpret_cast<const float4*>(O + (size_t)p * d + n);
+            const float4 o = load4(O + (size_t)p * d + n);
             acc.x += w * o.x;
             acc.y += w * o.y;
             acc.z += w * o.z;
@@ -31,7 +39,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
         }
         float4 sh = make_float4(0.f, 0.f, 0.f, 0.f);
         for (int q = 0; q < shared_parts; ++q) {
-            const float4 sv = *reinterpret_cast<const float4*>(Os + ((size_t)q * T + t) * d + n);
+            const float4 sv = load4(Os + ((size_t)q * T + t) * d + n);
             sh.x += sv.x;
             sh.y += sv.y;
             sh.z += sv.z;
@@ -51,14 +59,16 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
     }
 }
 
-hipError_t launch_combine(const float* O, const float* Os, const int32_t* pos, const float* wts,
+hipError_t launch_combine(const void* O, const void* Os, const int32_t* pos, const float* wts,
                           int T, int k, int d, int shared_parts, int dtype, void* y, hipStream_t s) {
     if (T <= 0) return hipSuccess;
     const dim3 grid(T, ceil_div(d, 4 * 256));
     if (dtype == 0)
-        combine_kernel<float><<<grid, 256, 0, s>>>(O, Os, pos, wts, T, k, d, shared_parts, (float*)y);
+        combine_kernel<float><<<grid, 256, 0, s>>>((const float*)O, (const float*)Os, pos, wts, T, k, d,
+                                                   shared_parts, (float*)y);
     else
-        combine_kernel<bf16_t><<<grid, 256, 0, s>>>(O, Os, pos, wts, T, k, d, shared_parts, (bf16_t*)y);
+        combine_kernel<bf16_t><<<grid, 256, 0, s>>>((const bf16_t*)O, (const bf16_t*)Os, pos, wts, T, k, d,
+                                                    shared_parts, (bf16_t*)y);
     return hipGetLastError();
 }
 

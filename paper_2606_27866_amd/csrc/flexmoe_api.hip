@@ -94,13 +94,14 @@ Layout layout(const flexmoe_layer_desc& D, int T) {
     L.t2 = take((nseg + 1) * 4);
     L.H = take(A * (size_t)D.I * es);
     L.Hs = take((size_t)T * D.I_shared * es);
-    L.O = take(A * (size_t)D.d * 4);
+    const size_t os_es = D.dtype == FLEXMOE_BF16 ? 2 : 4;  // O / Os element size
+    L.O = take(A * (size_t)D.d * os_es);
     // shared-expert rows; at decode sizes its down projection is split into
     // shared_parts() reductions with one row set each (kept monotone in T)
     const size_t os_rows = D.I_shared > 0
         ? std::max((size_t)T, (size_t)std::min(T, kDecodeMaxT) * (size_t)ceil_div(D.I_shared, D.I))
         : 0;
-    L.Os = take(os_rows * D.d * 4);
+    L.Os = take(os_rows * D.d * os_es);
     L.total = off;
     return L;
 }
@@ -288,8 +289,8 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
     SegMeta* seg = (SegMeta*)(ws + L.seg);
     int32_t* t1 = (int32_t*)(ws + L.t1);
     int32_t* t2 = (int32_t*)(ws + L.t2);
-    float* O = (float*)(ws + L.O);
-    float* Os = (float*)(ws + L.Os);
+    void* O = ws + L.O;
+    void* Os = ws + L.Os;
     const int NB = num_chunks(T);
     const int nseg = D.E + (has_shared ? 1 : 0);
     const bool bf16 = D.dtype == FLEXMOE_BF16;
@@ -356,8 +357,8 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
         }
         if (err != hipSuccess) return hip_fail(err, "gate/up GEMM launch");
         Gemm2Params<bf16_t> p2{(const bf16_t*)(ws + L.H), (const bf16_t*)(ws + L.Hs),
-                               (const bf16_t*)w_down_r, (const bf16_t*)ws_down, seg, t2, O, Os, D.d,
-                               D.I, D.I_shared, D.E, nseg, T};
+                               (const bf16_t*)w_down_r, (const bf16_t*)ws_down, seg, t2, (bf16_t*)O,
+                               (bf16_t*)Os, D.d, D.I, D.I_shared, D.E, nseg, T};
         {
             KernelTimer kt(FLEXMOE_K_DOWN, s);
             err = decode ? launch_gemm2_decode(p2, (int)g2, s) : launch_gemm2_big(p2, (int)g2, s);
@@ -374,8 +375,8 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
         }
         if (err != hipSuccess) return hip_fail(err, "gate/up GEMM launch");
         Gemm2Params<float> p2{(const float*)(ws + L.H), (const float*)(ws + L.Hs),
-                              (const float*)w_down_r, (const float*)ws_down, seg, t2, O, Os, D.d, D.I,
-                              D.I_shared, D.E, nseg, T};
+                              (const float*)w_down_r, (const float*)ws_down, seg, t2, (float*)O,
+                              (float*)Os, D.d, D.I, D.I_shared, D.E, nseg, T};
         {
             KernelTimer kt(FLEXMOE_K_DOWN, s);
             err = launch_gemm2_f32(p2, (int)g2, s);

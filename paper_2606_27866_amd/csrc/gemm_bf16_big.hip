@@ -1,7 +1,7 @@
 // Large-tile ragged grouped GEMMs on bf16 MFMA for prefill-sized token counts.
 //
-// Same work as gemm_bf16.hip (gate/up GEMM with fused SwiGLU, down GEMM with
-// the reduction truncated to k_e; FlexMoE Eq. 4), shaped for gfx950:
+// The gate/up GEMM with fused SwiGLU and the down GEMM with the reduction
+// truncated to k_e (FlexMoE Eq. 4), shaped for gfx950:
 //   - 256 x 256 workgroup tile (rows x weight rows), K tile 32, 8 waves (two
 //     per SIMD: one wave alone cannot keep the matrix core fed) arranged
 //     2 x 4, each owning a 128 x 64 block of v_mfma_f32_32x32x16_bf16
@@ -286,7 +286,7 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
                     }
             }
         } else {
-            float* Ob = shared ? p2.Os : p2.O + (size_t)sm.row0 * d;
+            bf16_t* Ob = shared ? p2.Os : p2.O + (size_t)sm.row0 * d;
 #pragma unroll
             for (int j = 0; j < NF; ++j) {
                 const int n = ntile * BN + wn * 64 + j * 32 + (lane & 31);
@@ -296,7 +296,7 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
 #pragma unroll
                     for (int v = 0; v < 16; ++v) {
                         const int row = mtile * BM + wm * WR + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
-                        if (row < sm.rows) Ob[(size_t)row * d + n] = acc[i][j][v];
+                        if (row < sm.rows) Ob[(size_t)row * d + n] = f32_to_bf16(acc[i][j][v]);
                     }
             }
         }

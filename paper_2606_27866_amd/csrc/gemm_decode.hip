@@ -197,7 +197,7 @@ __global__ __launch_bounds__(64 * DWAVES) void gemm2_decode_kernel(Gemm2Params<b
     reduce_waves(acc, red, wave, lane);
     if (wave != 0) return;
     // D[m][n']: lane holds output columns m = 4*(lane/16) + i of row n' = lane%16
-    float* Ob = shared ? p.Os + (size_t)split * p.tokens * d : p.O + (size_t)sm.row0 * d;
+    bf16_t* Ob = shared ? p.Os + (size_t)split * p.tokens * d : p.O + (size_t)sm.row0 * d;
 #pragma unroll
     for (int f = 0; f < 4; ++f) {
         if (f >= nf) break;
@@ -205,11 +205,13 @@ __global__ __launch_bounds__(64 * DWAVES) void gemm2_decode_kernel(Gemm2Params<b
         if (r >= sm.rows) continue;
         const int col = ntile * DCH + 4 * g;
         if (col + 3 < d) {
-            *reinterpret_cast<float4*>(Ob + (size_t)r * d + col) = make_float4(acc[f][0], acc[f][1], acc[f][2], acc[f][3]);
+            const uint32_t lo = (uint32_t)f32_to_bf16(acc[f][0]) | ((uint32_t)f32_to_bf16(acc[f][1]) << 16);
+            const uint32_t hi = (uint32_t)f32_to_bf16(acc[f][2]) | ((uint32_t)f32_to_bf16(acc[f][3]) << 16);
+            *reinterpret_cast<uint2*>(Ob + (size_t)r * d + col) = make_uint2(lo, hi);
         } else {
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-                if (col + i < d) Ob[(size_t)r * d + col + i] = acc[f][i];
+                if (col + i < d) Ob[(size_t)r * d + col + i] = f32_to_bf16(acc[f][i]);
         }
     }
 }

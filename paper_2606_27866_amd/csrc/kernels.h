@@ -1,6 +1,8 @@
 // Kernel declarations and argument blocks of the FlexMoE HIP library.
 #pragma once
 
+#include <type_traits>
+
 #include "common.h"
 
 namespace flexmoe {
@@ -27,23 +29,25 @@ struct Gemm1Params {
     int d, I, Is, E, top_k, nseg, tokens;
 };
 
-// Down GEMM: O[row][n] = sum_{c < k_s} H[row][c] * W_down[n][c].
+// Down GEMM: O[row][n] = sum_{c < k_s} H[row][c] * W_down[n][c].  O holds one
+// row per routed assignment (and per token for the shared expert); it is fp32
+// in fp32 mode and bf16 (rounded once from the fp32 sum) in bf16 mode.
 template <typename T>
 struct Gemm2Params {
+    typedef typename std::conditional<std::is_same<T, float>::value, float, bf16_t>::type OT;
     const T* H;
     const T* Hs;
     const T* wd;                // routed down [E][d][I]
     const T* sd;                // shared down [d][I_s]
     const SegMeta* seg;
     const int32_t* tstart;
-    float* O;                   // routed rows [A][d]
-    float* Os;                  // shared rows [T][d] (split reductions: [splits][T][d])
+    OT* O;                      // routed rows [A][d]
+    OT* Os;                     // shared rows [T][d] (split reductions: [splits][T][d])
     int d, I, Is, E, nseg, tokens;
 };
 
 // Tile shapes of the kernel families (the dispatch kernel builds tile tables
 // with these numbers).
-constexpr int kBf16BM1 = 128, kBf16BN1 = 64, kBf16BM2 = 128, kBf16BN2 = 128;
 constexpr int kF32BM = 64, kF32BN = 64;
 constexpr int kBigBM1 = 256, kBigBN1 = 128, kBigBM2 = 256, kBigBN2 = 256;
 constexpr int kDecodeMaxT = 64;     // T at or below which the weight-streaming kernels run
@@ -67,15 +71,13 @@ __global__ void dispatch_small_kernel(const float* logits, int T, int E, int k, 
 __global__ void set_keep_kernel(int32_t* keep, KeepArgs t, int E);
 
 // Launchers (defined next to their kernels).  Each returns the launch status.
-hipError_t launch_gemm1_bf16(const Gemm1Params<bf16_t>& p, int grid, hipStream_t s);
-hipError_t launch_gemm2_bf16(const Gemm2Params<bf16_t>& p, int grid, hipStream_t s);
 hipError_t launch_gemm1_big(const Gemm1Params<bf16_t>& p, int grid, hipStream_t s);
 hipError_t launch_gemm2_big(const Gemm2Params<bf16_t>& p, int grid, hipStream_t s);
 hipError_t launch_gemm1_decode(const Gemm1Params<bf16_t>& p, int tiles, hipStream_t s);
 hipError_t launch_gemm2_decode(const Gemm2Params<bf16_t>& p, int tiles, hipStream_t s);
 hipError_t launch_gemm1_f32(const Gemm1Params<float>& p, int grid, hipStream_t s);
 hipError_t launch_gemm2_f32(const Gemm2Params<float>& p, int grid, hipStream_t s);
-hipError_t launch_combine(const float* O, const float* Os, const int32_t* pos, const float* wts,
+hipError_t launch_combine(const void* O, const void* Os, const int32_t* pos, const float* wts,
                           int T, int k, int d, int shared_parts, int dtype, void* y, hipStream_t s);
 hipError_t launch_rank_reorder(const float* scores, const void* wg, const void* wu,
                                const void* wd, void* wg_r, void* wu_r, void* wd_r,
