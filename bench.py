@@ -32,6 +32,7 @@ PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3      # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
 RIDGE = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
+DECODE_MAX_T = 64            # the library runs its weight-streaming GEMMs for T <= 64 (bf16)
 
 
 def log(*a):
@@ -63,14 +64,21 @@ def kernel_src_hash():
     return h.hexdigest()[:16]
 
 
-def load_traffic(workload, table):
+def traffic_file(workload, T):
+    name = workload if workload != "qwen2_57b_a14b_decode" else "%s_T%d" % (workload, T)
+    return os.path.join(ROOT, "profiles", "gate_up_gemm_traffic_%s.json" % name)
+
+
+def load_traffic(workload, T, table):
     """HBM bytes per gate/up-GEMM launch from committed rocprofv3 counter
-    runs, or None if absent or taken on a different kernel source."""
-    path = os.path.join(ROOT, "profiles", "gate_up_gemm_traffic_%s.json" % workload)
+    runs, or None if absent or taken on a different kernel source, token
+    count or keep table."""
+    path = traffic_file(workload, T)
     if not os.path.exists(path):
         return None
     d = json.load(open(path))
-    if d.get("kernel_src_sha") != kernel_src_hash() or d.get("table") != table:
+    if (d.get("kernel_src_sha") != kernel_src_hash() or d.get("table") != table
+            or d.get("T") != T):
         return None
     return d.get("hbm_bytes_per_launch")
 
@@ -182,13 +190,21 @@ def cpu_baseline(wl, keep, target_s):
         oracle.layer_forward(x[:S], lg[:S], *wl.w, keep, cfg.top_k, cfg.norm_topk, *s)
         return time.time() - t0
 
-    S0 = min(8, x.shape[0])
+    T = x.shape[0]
+    S0 = min(64, T)
     t0 = run(S0)
-    S = int(min(x.shape[0], max(S0, S0 * target_s / max(t0, 1e-3))))
+    S = int(min(T, max(S0, S0 * target_s / max(t0, 1e-3))))
     t = run(S) if S != S0 else t0
-    return dict(value=S / t, unit="tokens/s", cores=oracle.num_threads(), kind="oracle",
-                sample="first %d of %d tokens of the workload, same weights and keep table, "
-                       "%.1f s (fp64 accumulation)" % (S, x.shape[0], t))
+    passes = 1
+    # the whole batch may take less than the target: repeat it (at most 4 passes)
+    while S == T and t < 0.6 * target_s and passes < 4:
+        t += run(S)
+        passes += 1
+    what = ("%d pass%s over all %d tokens" % (passes, "es" if passes > 1 else "", T) if S == T
+            else "first %d of %d tokens" % (S, T))
+    return dict(value=S * passes / t, unit="tokens/s", cores=oracle.num_threads(), kind="oracle",
+                sample="%s of the workload, same weights and keep table, %.1f s (fp64 accumulation)"
+                       % (what, t))
 
 
 def main():
@@ -242,8 +258,13 @@ def main():
         roof = dict(bound="hbm", achieved=alg["B1"] / (gu_avg / 1e3) / 1e9, peak=PEAK_HBM_GBS,
                     unit="GB/s")
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = load_traffic(args.workload, wl.table_name) if not wl.decode else None
-    roof["kernel"] = "gate_up GEMM (gemm1_bf16_kernel)" if bf16 else "gate_up GEMM (gemm1_f32_kernel)"
+    roof["traffic"] = load_traffic(args.workload, wl.T, "+".join(keep_names))
+    if not bf16:
+        roof["kernel"] = "gate_up GEMM (gemm1_f32_kernel)"
+    elif wl.T <= DECODE_MAX_T:
+        roof["kernel"] = "gate_up GEMM (gemm1_decode_kernel)"
+    else:
+        roof["kernel"] = "gate_up GEMM (gemm1_big_kernel)"
     roof["avg_launch_ms"] = gu_avg
 
     layer_s = ms_step / 1e3
