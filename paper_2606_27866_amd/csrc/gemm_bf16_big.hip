@@ -2,20 +2,20 @@
 //
 // The gate/up GEMM with fused SwiGLU and the down GEMM with the reduction
 // truncated to k_e (FlexMoE Eq. 4), shaped for gfx950:
-//   - 256 x 256 workgroup tile (rows x weight rows), K tile 32, 8 waves (two
+//   - 256 x 256 workgroup tile (rows x weight rows), K tile 64, 8 waves (two
 //     per SIMD: one wave alone cannot keep the matrix core fed) arranged
 //     2 x 4, each owning a 128 x 64 block of v_mfma_f32_32x32x16_bf16
-//     accumulators (128 registers).  Per K tile the CU reads 96 KB of LDS
-//     fragments (256 B/clk) and writes 32 KB (128 B/clk): about 60 % of the
+//     accumulators (128 registers).  Per K tile the CU reads 192 KB of LDS
+//     fragments (256 B/clk) and writes 64 KB (128 B/clk): about 60 % of the
 //     LDS time the MFMAs take, with zero bank conflicts.
 //   - operands go from global memory straight into LDS (global_load_lds,
 //     16 bytes per lane): no VGPRs stage them and no ds_write is issued.
 //     Rows outside a segment, channels at or past k_e and K chunks past the
 //     end read a zero page instead.
-//   - each 64-byte LDS row (32 bf16 of K) stores its four 16-byte chunks
-//     XOR-swizzled by bits 2..3 of the row index, so the 16 lanes served in
+//   - each 128-byte LDS row (64 bf16 of K) stores its eight 16-byte chunks
+//     XOR-swizzled by bits 1..3 of the row index, so the 16 lanes served in
 //     one LDS cycle of a fragment read hit 64 distinct banks.
-//   - four LDS stages: the loads of K tiles t+1..t+3 are in flight while
+//   - two LDS stages of 64 KB: the loads of K tile t+1 are in flight while
 //     tile t is multiplied.
 //   - tiles are numbered segment-major (shared expert first: its reductions
 //     are the longest) with row tiles fastest, so consecutive tiles share
@@ -219,7 +219,7 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
             for (int i = 0; i < MFW; ++i)
 #pragma unroll
                 for (int j = 0; j < NF; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][i], b[buf][j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[buf][j], a[buf][i], acc[i][j], 0, 0, 0);
         };
         // one MFMA, then a fragment read (then a DMA load), spread over a step
         auto interleave = [](bool dma) {
@@ -266,37 +266,60 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
         }
         __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // no DMA may outlive the workgroup's LDS
 
-        // ---- epilogue: 32x32 accumulator layout, lane -> column lane%32,
-        // register v -> row (v/4)*8 + (lane/32)*4 + v%4
+        // ---- epilogue.  The weight fragment is the MFMA's first operand, so
+        // the accumulator is transposed: lane -> row lane%32 of the fragment,
+        // register v -> weight row (v/4)*8 + (lane/32)*4 + v%4.  Each lane
+        // thus holds four runs of 4 consecutive channels (or output columns)
+        // of one row and stores each run as one 8-byte write.
+        const int row_l = mtile * BM + wm * WR + (lane & 31);
+        const int sub = (lane >> 5) * 4;
         if constexpr (kGateUp) {
             bf16_t* Hb = shared ? p1.Hs : p1.H + (size_t)sm.row0 * p1.I;
             const int ldh = shared ? p1.Is : p1.I;
-            const int kk8 = min((sm.kk + 7) & ~7, ldh);  // chunk-aligned end: [kk, kk8) is zero-filled
-            const int ch = ntile * (BN / 2) + wn * 32 + (lane & 31);
-            if (ch < kk8) {
+            // chunk-aligned end: [kk, kk8) is zero-filled; kk8 and the runs are
+            // multiples of 8 and 4, so a run is wholly inside or outside
+            const int kk8 = min((sm.kk + 7) & ~7, ldh);
+            const int ch0 = ntile * (BN / 2) + wn * 32 + sub;
 #pragma unroll
-                for (int i = 0; i < MFW; ++i)
+            for (int i = 0; i < MFW; ++i) {
+                const int row = row_l + i * 32;
+                if (row >= sm.rows) continue;
+                bf16_t* hr = Hb + (size_t)row * ldh;
 #pragma unroll
-                    for (int v = 0; v < 16; ++v) {
-                        const int row = mtile * BM + wm * WR + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
-                        if (row < sm.rows) {
-                            const float g = acc[i][0][v], u = acc[i][1][v];
-                            Hb[(size_t)row * ldh + ch] = ch < sm.kk ? f32_to_bf16(silu_fast(g) * u) : (bf16_t)0;
-                        }
+                for (int q = 0; q < 4; ++q) {
+                    const int ch = ch0 + q * 8;
+                    if (ch >= kk8) continue;
+                    uint32_t w[2];
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        const int v = q * 4 + h * 2;
+                        const float g0 = acc[i][0][v], u0 = acc[i][1][v];
+                        const float g1 = acc[i][0][v + 1], u1 = acc[i][1][v + 1];
+                        const uint32_t lo = ch + h * 2 < sm.kk ? f32_to_bf16(silu_fast(g0) * u0) : 0u;
+                        const uint32_t hi = ch + h * 2 + 1 < sm.kk ? f32_to_bf16(silu_fast(g1) * u1) : 0u;
+                        w[h] = lo | (hi << 16);
                     }
+                    *reinterpret_cast<uint2*>(hr + ch) = make_uint2(w[0], w[1]);
+                }
             }
         } else {
             bf16_t* Ob = shared ? p2.Os : p2.O + (size_t)sm.row0 * d;
 #pragma unroll
-            for (int j = 0; j < NF; ++j) {
-                const int n = ntile * BN + wn * 64 + j * 32 + (lane & 31);
-                if (n >= d) continue;
+            for (int i = 0; i < MFW; ++i) {
+                const int row = row_l + i * 32;
+                if (row >= sm.rows) continue;
+                bf16_t* orow = Ob + (size_t)row * d;
 #pragma unroll
-                for (int i = 0; i < MFW; ++i)
+                for (int j = 0; j < NF; ++j)
 #pragma unroll
-                    for (int v = 0; v < 16; ++v) {
-                        const int row = mtile * BM + wm * WR + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
-                        if (row < sm.rows) Ob[(size_t)row * d + n] = f32_to_bf16(acc[i][j][v]);
+                    for (int q = 0; q < 4; ++q) {
+                        const int n = ntile * BN + wn * 64 + j * 32 + q * 8 + sub;
+                        if (n >= d) continue;
+                        const uint32_t w0 = (uint32_t)f32_to_bf16(acc[i][j][q * 4]) |
+                                            ((uint32_t)f32_to_bf16(acc[i][j][q * 4 + 1]) << 16);
+                        const uint32_t w1 = (uint32_t)f32_to_bf16(acc[i][j][q * 4 + 2]) |
+                                            ((uint32_t)f32_to_bf16(acc[i][j][q * 4 + 3]) << 16);
+                        *reinterpret_cast<uint2*>(orow + n) = make_uint2(w0, w1);
                     }
             }
         }
