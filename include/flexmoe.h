@@ -28,11 +28,16 @@
  *
  * Element types: dtype FLEXMOE_F32 (x, weights and y in fp32) or FLEXMOE_BF16
  * (x, weights and y in bf16).  Router logits are always fp32.  Accumulation is
- * fp32; in bf16 mode the SwiGLU activations are rounded to bf16 before the
- * down projection and y is rounded once at the end (round to nearest even).
+ * fp32; in bf16 mode the SwiGLU activations and each expert's down-projection
+ * output are rounded to bf16, the weighted combine sums in fp32 and y is
+ * rounded once at the end (round to nearest even throughout).
  *
  * Shape rules (FLEXMOE_ESHAPE otherwise): d, I and I_shared are multiples of
- * 8; 1 <= E <= 256; 1 <= top_k <= min(E, 16); 0 <= T <= max_tokens.
+ * 8; 1 <= E <= 256; 1 <= top_k <= min(E, 16); 0 <= T <= max_tokens;
+ * max_tokens * (top_k + 1) <= 2^30.  In bf16 mode every operand block one
+ * GEMM tile addresses stays below 2^30 elements: max_tokens * d,
+ * max_tokens * I, max_tokens * I_shared, I * d and I_shared * d (the prefill
+ * kernels reach their operands through 32-bit buffer offsets).
  */
 #ifndef FLEXMOE_H
 #define FLEXMOE_H

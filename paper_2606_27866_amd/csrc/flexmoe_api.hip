@@ -59,6 +59,14 @@ int check_desc(const flexmoe_layer_desc* D) {
     const long long A = (long long)D->max_tokens * D->top_k;
     if (A + D->max_tokens > (1LL << 30))
         return fail(FLEXMOE_ESHAPE, "max_tokens * (top_k + 1) exceeds 2^30");
+    if (D->dtype == FLEXMOE_BF16) {
+        // the prefill GEMMs address each operand block with 32-bit byte offsets
+        const long long T = D->max_tokens, wide = std::max(D->I, D->I_shared);
+        if (T * std::max<long long>(D->d, wide) >= (1LL << 30) || wide * D->d >= (1LL << 30))
+            return fail(FLEXMOE_ESHAPE,
+                        "bf16 operand blocks must stay below 2^30 elements (max_tokens * max(d, I, "
+                        "I_shared) and max(I, I_shared) * d)");
+    }
     return FLEXMOE_OK;
 }
 
@@ -69,7 +77,67 @@ struct Layout {
 
 int num_chunks(int T) { return ceil_div(T, kRouteTokens); }
 
-Layout layout(const flexmoe_layer_desc& D, int T) {
+// Upper bound on the number of row tiles of height bm over all routed
+// segments: sum_e ceil(n_e/bm) <= ceil(A/bm) + E - 1, <= E*ceil(T/bm)
+// because a token routes to an expert at most once, and <= A because every
+// tile holds at least one row.
+long long routed_row_tiles_ub(int T, int E, int k, int bm) {
+    const long long A = (long long)T * k;
+    const long long a = (A + bm - 1) / bm + E - 1;
+    const long long b = (long long)E * ((T + bm - 1) / bm);
+    return std::min(std::min(a, b), A);
+}
+
+// The shared expert's down reduction is split into chunks (each writing its
+// own partial rows, added by the combine) when one of its tiles would take
+// longer than a compute unit's average share of the down GEMM, which the host
+// estimates at full budget over MI355X's 256 compute units.  Chunks hold at
+// least kMinSplitK channels.
+constexpr int kComputeUnits = 256;
+constexpr int kMinSplitK = 1024;
+
+// Chunk width of the shared expert's split down reduction for T tokens, 0 for
+// one reduction over I_shared.  Decode-sized batches (weight streaming) use
+// chunks of I channels.
+int shared_ks2(const flexmoe_layer_desc& D, int T) {
+    if (D.I_shared <= 0 || D.dtype != FLEXMOE_BF16) return 0;
+    if (T <= kDecodeMaxT) return D.I;
+    const long long nd = ceil_div(D.d, kBigBN2);
+    const long long sh_tiles = (long long)ceil_div(T, kBigBM2) * nd;
+    if (sh_tiles >= kComputeUnits) return 0;
+    const long long sh_steps = ceil_div(D.I_shared, 64);
+    const long long rt_tiles = routed_row_tiles_ub(T, D.E, D.top_k, kBigBM2) * nd;
+    const long long avg = (sh_tiles * sh_steps + rt_tiles * ceil_div(D.I, 64)) / kComputeUnits;
+    if (sh_steps <= avg) return 0;
+    const long long p = std::min<long long>(ceil_div((int)sh_steps, (int)std::max<long long>(avg, 16)),
+                                            D.I_shared / kMinSplitK);
+    if (p <= 1) return 0;
+    return ceil_div(ceil_div(D.I_shared, (int)p), 64) * 64;
+}
+
+// Row sets of shared-expert output the combine adds (0 without a shared expert).
+int shared_parts(const flexmoe_layer_desc& D, int T) {
+    if (D.I_shared <= 0) return 0;
+    const int ks2 = shared_ks2(D, T);
+    return ks2 > 0 ? ceil_div(D.I_shared, ks2) : 1;
+}
+
+// Rows of the Os buffer a workspace for up to T tokens must hold: the largest
+// shared_parts(T') * T' over T' <= T.  Splits happen only while the shared
+// expert has fewer than kComputeUnits tiles, so the scan stops there.
+size_t os_rows_bound(const flexmoe_layer_desc& D, int T) {
+    if (D.I_shared <= 0 || T <= 0) return 0;
+    size_t best = (size_t)T * shared_parts(D, T);
+    const int t0 = std::min(T, kDecodeMaxT);
+    best = std::max(best, (size_t)t0 * shared_parts(D, t0));
+    const long long nd = ceil_div(D.d, kBigBN2);
+    const long long t_end = std::min<long long>(T, (kComputeUnits + nd - 1) / nd * kBigBM2);
+    for (long long t = kDecodeMaxT + 1; t <= t_end; ++t)
+        best = std::max(best, (size_t)t * shared_parts(D, (int)t));
+    return best;
+}
+
+Layout layout(const flexmoe_layer_desc& D, int T, size_t os_rows) {
     const size_t A = (size_t)T * D.top_k;
     const size_t NB = (size_t)num_chunks(T);
     const size_t nseg = (size_t)D.E + (D.I_shared > 0 ? 1 : 0);
@@ -96,25 +164,11 @@ Layout layout(const flexmoe_layer_desc& D, int T) {
     L.Hs = take((size_t)T * D.I_shared * es);
     const size_t os_es = D.dtype == FLEXMOE_BF16 ? 2 : 4;  // O / Os element size
     L.O = take(A * (size_t)D.d * os_es);
-    // shared-expert rows; at decode sizes its down projection is split into
-    // shared_parts() reductions with one row set each (kept monotone in T)
-    const size_t os_rows = D.I_shared > 0
-        ? std::max((size_t)T, (size_t)std::min(T, kDecodeMaxT) * (size_t)ceil_div(D.I_shared, D.I))
-        : 0;
+    // shared-expert rows, one row set per reduction chunk; last, so that the
+    // offsets above depend on T alone
     L.Os = take(os_rows * D.d * os_es);
     L.total = off;
     return L;
-}
-
-// Upper bound on the number of row tiles of height bm over all routed
-// segments: sum_e ceil(n_e/bm) <= ceil(A/bm) + E - 1, <= E*ceil(T/bm)
-// because a token routes to an expert at most once, and <= A because every
-// tile holds at least one row.
-long long routed_row_tiles_ub(int T, int E, int k, int bm) {
-    const long long A = (long long)T * k;
-    const long long a = (A + bm - 1) / bm + E - 1;
-    const long long b = (long long)E * ((T + bm - 1) / bm);
-    return std::min(std::min(a, b), A);
 }
 
 // ---- optional per-kernel event timing --------------------------------------
@@ -215,7 +269,7 @@ size_t flexmoe_workspace_bytes(const flexmoe_layer_desc* desc, int32_t T) {
         fail(FLEXMOE_ESHAPE, "T = %d outside [0, max_tokens = %d]", T, desc->max_tokens);
         return 0;
     }
-    return layout(*desc, T).total;
+    return layout(*desc, T, os_rows_bound(*desc, T)).total;
 }
 
 int flexmoe_set_budget(const flexmoe_layer_desc* desc, int32_t* keep_dev, const int32_t* keep_host,
@@ -271,7 +325,7 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
     const bool has_shared = D.I_shared > 0;
     if (has_shared != (ws_gate && ws_up && ws_down) || (!has_shared && (ws_gate || ws_up || ws_down)))
         return fail(FLEXMOE_EINVAL, "shared weights must be given iff I_shared > 0");
-    const Layout L = layout(D, T);
+    const Layout L = layout(D, T, (size_t)T * shared_parts(D, T));
     if (!workspace || workspace_bytes < L.total)
         return fail(FLEXMOE_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace_bytes, L.total);
     if (((uintptr_t)workspace) & 255) return fail(FLEXMOE_EWORKSPACE, "workspace is not 256-byte aligned");
@@ -297,10 +351,11 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
     // kernel family: weight streaming for decode-sized T, large MFMA tiles
     // otherwise (bf16); LDS-tiled FMA for fp32
     const bool decode = bf16 && T <= kDecodeMaxT;
-    const int shared_parts = !has_shared ? 0 : decode ? ceil_div(D.I_shared, D.I) : 1;
+    const int ks2 = shared_ks2(D, T);
+    const int parts = shared_parts(D, T);
     const TileShape ts = !bf16   ? TileShape{kF32BM, kF32BN, kF32BM, kF32BN, 0}
-                         : decode ? TileShape{kDecodeMaxT, kDecBN, kDecodeMaxT, kDecBN, D.I}
-                                  : TileShape{kBigBM1, kBigBN1, kBigBM2, kBigBN2, 0};
+                         : decode ? TileShape{kDecodeMaxT, kDecBN, kDecodeMaxT, kDecBN, ks2}
+                                  : TileShape{kBigBM1, kBigBN1, kBigBM2, kBigBN2, ks2};
 
     hipError_t err;
     if ((long long)T * D.top_k <= kSmallAssign) {
@@ -342,7 +397,7 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
     long long g2 = rt2 * ceil_div(D.d, ts.bn2);
     if (has_shared) {
         g1 += (long long)ceil_div(T, ts.bm1) * ceil_div(D.I_shared, ts.bn1);
-        g2 += (long long)ceil_div(T, ts.bm2) * ceil_div(D.d, ts.bn2) * std::max(shared_parts, 1);
+        g2 += (long long)ceil_div(T, ts.bm2) * ceil_div(D.d, ts.bn2) * parts;
     }
     if (g1 > 0x7fffffffLL || g2 > 0x7fffffffLL) return fail(FLEXMOE_ESHAPE, "tile grid too large");
 
@@ -358,7 +413,7 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
         if (err != hipSuccess) return hip_fail(err, "gate/up GEMM launch");
         Gemm2Params<bf16_t> p2{(const bf16_t*)(ws + L.H), (const bf16_t*)(ws + L.Hs),
                                (const bf16_t*)w_down_r, (const bf16_t*)ws_down, seg, t2, (bf16_t*)O,
-                               (bf16_t*)Os, D.d, D.I, D.I_shared, D.E, nseg, T};
+                               (bf16_t*)Os, D.d, D.I, D.I_shared, D.E, nseg, T, ks2};
         {
             KernelTimer kt(FLEXMOE_K_DOWN, s);
             err = decode ? launch_gemm2_decode(p2, (int)g2, s) : launch_gemm2_big(p2, (int)g2, s);
@@ -376,7 +431,7 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
         if (err != hipSuccess) return hip_fail(err, "gate/up GEMM launch");
         Gemm2Params<float> p2{(const float*)(ws + L.H), (const float*)(ws + L.Hs),
                               (const float*)w_down_r, (const float*)ws_down, seg, t2, (float*)O,
-                              (float*)Os, D.d, D.I, D.I_shared, D.E, nseg, T};
+                              (float*)Os, D.d, D.I, D.I_shared, D.E, nseg, T, 0};
         {
             KernelTimer kt(FLEXMOE_K_DOWN, s);
             err = launch_gemm2_f32(p2, (int)g2, s);
@@ -385,7 +440,7 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
     }
     {
         KernelTimer kt(FLEXMOE_K_COMBINE, s);
-        err = launch_combine(O, Os, pos, wts, T, D.top_k, D.d, shared_parts, D.dtype, y, s);
+        err = launch_combine(O, Os, pos, wts, T, D.top_k, D.d, parts, D.dtype, y, s);
     }
     if (err != hipSuccess) return hip_fail(err, "combine launch");
 

@@ -8,10 +8,12 @@
 //     accumulators (128 registers).  Per K tile the CU reads 192 KB of LDS
 //     fragments (256 B/clk) and writes 64 KB (128 B/clk): about 60 % of the
 //     LDS time the MFMAs take, with zero bank conflicts.
-//   - operands go from global memory straight into LDS (global_load_lds,
+//   - operands go from global memory straight into LDS (buffer_load ... lds,
 //     16 bytes per lane): no VGPRs stage them and no ds_write is issued.
-//     Rows outside a segment, channels at or past k_e and K chunks past the
-//     end read a zero page instead.
+//     Each lane's offset into the operand is fixed for the whole reduction;
+//     the K position is a scalar offset.  Rows outside a segment, channels at
+//     or past k_e and K chunks past the end use an offset outside the buffer
+//     descriptor, for which the hardware returns zeros.
 //   - each 128-byte LDS row (64 bf16 of K) stores its eight 16-byte chunks
 //     XOR-swizzled by bits 1..3 of the row index, so the 16 lanes served in
 //     one LDS cycle of a fragment read hit 64 distinct banks.
@@ -26,7 +28,9 @@
 //   128 gate rows then the 128 up rows of those channels, and wave (wm, wn)
 //   multiplies gate rows [wn*32, wn*32+32) and the matching up rows, so the
 //   gate and up accumulators of a channel sit in the same lane.
-// down: a workgroup tile is 256 rows x 256 output columns.
+// down: a workgroup tile is 256 rows x 256 output columns.  When the shared
+//   expert alone has too few tiles to fill the chip, its reduction over I_s
+//   is split into chunks whose partial rows the combine adds in chunk order.
 // A segment's last row tile often holds far fewer than 256 rows (a routed
 // expert gets a few hundred tokens).  A tile with R rows runs the variant in
 // which each wave multiplies ceil(R/64) fragments of 32 rows, so MFMA work
@@ -42,12 +46,25 @@ namespace {
 #ifndef FLEXMOE_BIG_BK
 #define FLEXMOE_BIG_BK 64
 #endif
+#ifndef FLEXMOE_BIG_WAVES
+#define FLEXMOE_BIG_WAVES 8
+#endif
 constexpr int BM = 256, BN = 256, BK = FLEXMOE_BIG_BK;
-constexpr int NWAVE = 8, THREADS = 64 * NWAVE;
-constexpr int WM = 2, WN = 4;               // wave grid
+constexpr int NWAVE = FLEXMOE_BIG_WAVES, THREADS = 64 * NWAVE;
+constexpr int WAVES_PER_SIMD = NWAVE / 4;
+constexpr int WM = 2, WN = NWAVE / WM;      // wave grid
 static_assert(BM == WM * 128, "a full tile gives each M-wave four 32-row fragments");
-constexpr int NF = 2;                       // 2 column fragments per wave (64 columns)
-constexpr int NSTAGE = BK == 32 ? 4 : 2;    // 128 KB of LDS either way
+constexpr int NF = BN / (WN * 32);          // 32-column fragments per wave
+constexpr int WCOL = BN / WN;               // weight rows per wave
+#ifndef FLEXMOE_BIG_NSTAGE
+#define FLEXMOE_BIG_NSTAGE (BK == 32 ? 4 : 2)
+#endif
+constexpr int NSTAGE = FLEXMOE_BIG_NSTAGE;  // LDS stages of BK-deep operand tiles
+#ifndef FLEXMOE_BIG_SPREAD
+#define FLEXMOE_BIG_SPREAD 0
+#endif
+constexpr bool SPREAD = FLEXMOE_BIG_SPREAD;  // spread each tile's DMAs over a step
+static_assert(!SPREAD || NSTAGE >= 3, "spread DMAs write the stage freed one step earlier");
 constexpr int NSTEP = BK / 16;              // 16-deep MFMA steps per K tile
 constexpr int ROWB = BK * 2;                // bytes per LDS row
 constexpr int CHUNKS = ROWB / 16;           // 16-byte chunks per LDS row
@@ -76,8 +93,21 @@ __device__ __forceinline__ bf16x8 lds_frag(const unsigned char* base, int row, i
                               *reinterpret_cast<const u32x4*>(base + row * ROWB + swz(row, chunk) * 16));
 }
 
-__device__ __forceinline__ void load_lds16(const void* g, unsigned char* lds) {
-    __builtin_amdgcn_global_load_lds(g, (lds_ptr_t*)lds, 16, 0, 0);
+// Raw buffer descriptor over `elems` bf16 elements (the extent must stay
+// below 2^31 bytes: the host checks the layer shape).  The fourth dword is
+// the gfx9 raw-buffer format word.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const bf16_t* base, size_t elems) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(base), (short)0, (int)(elems * 2),
+                                             0x00020000);
+}
+// A byte offset past every descriptor's extent: the load returns zeros (the
+// scalar offset added to it stays below 2^31, so it cannot wrap into range).
+constexpr uint32_t kOOB = 0x80000000u;
+
+// 16 bytes per lane from base + voff + soff straight into LDS (M0 = lds).
+__device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff,
+                                           unsigned char* lds) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t*)lds, 16, voff, soff, 0, 0);
 }
 
 // A bare s_barrier: a workgroup fence would also drain the DMAs of later K
@@ -89,9 +119,6 @@ __device__ __forceinline__ void barrier_no_fence() {
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 }  // namespace
-
-// 64 zero bytes: the source of every masked 16-byte chunk.
-__device__ __attribute__((aligned(64))) uint32_t g_zero_page[16];
 
 template <bool kGateUp>
 __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Gemm2Params<bf16_t>& p2,
@@ -110,82 +137,103 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
     const SegMeta sm = (kGateUp ? p1.seg : p2.seg)[s];
     const int local = L - tstart[s];
     const int mt = ceil_div(sm.rows, BM);
-    const int mtile = local % mt, ntile = local / mt;
+    const int mtile = local % mt;
+    // down GEMM of the shared expert: tiles of reduction chunk `split` follow
+    // those of chunk split-1 (routed segments and gate/up: split 0)
+    const int nt = kGateUp ? 0x7fffffff : ceil_div(d, BN);
+    const int ntile = (local / mt) % nt, split = (local / mt) / nt;
     const int hs = nseg - E;  // 1 if segment 0 is the shared expert
     const bool shared = s < hs;
 
-    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-    const void* zero = (const void*)g_zero_page;
+    // the wave index is uniform: keeping it in a scalar register makes every
+    // LDS destination address (M0) scalar arithmetic
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
 
-    // ---- per-lane sources of the A rows and B rows this lane loads ----
-    // DMA instruction i of wave w fills LDS rows w*32 + i*RPI .. +RPI of each
-    // operand; lane -> row lane/CHUNKS, LDS chunk lane%CHUNKS, which holds
-    // global chunk swz(row, lane%CHUNKS).
+    // ---- buffer descriptors and per-lane byte offsets of the A rows and B
+    // rows this lane loads.  DMA instruction i of a wave fills LDS rows
+    // wave*ROWS_PER_WAVE + i*RPI .. +RPI of each operand; lane -> row
+    // lane/CHUNKS, LDS chunk lane%CHUNKS, which holds global chunk
+    // swz(row, lane%CHUNKS).  Masked rows (outside the segment, channels at or
+    // past k_e, columns past d) get an offset past the descriptor's extent,
+    // for which the load returns zeros.
     const int pos = lane % CHUNKS;
-    const bf16_t* asrc[NI];
-    const bf16_t* bsrc[NI];
+    uint32_t aoff[NI], boff[NI];
     int acol[NI];
     int K;
+    __amdgpu_buffer_rsrc_t ra, rb;
     if constexpr (kGateUp) {
         K = d;
+        const int nI = shared ? p1.Is : p1.I;
         const size_t wofs = shared ? 0 : (size_t)(s - hs) * p1.I * d;
-        const bf16_t* Wg = (shared ? p1.sg : p1.wg) + wofs;
-        const bf16_t* Wu = (shared ? p1.su : p1.wu) + wofs;
+        // this wave's B rows are all gate rows or all up rows
+        const bf16_t* W = (wave * ROWS_PER_WAVE < BN / 2 ? (shared ? p1.sg : p1.wg) : (shared ? p1.su : p1.wu)) + wofs;
+        ra = make_rsrc(p1.x, (size_t)p1.tokens * d);
+        rb = make_rsrc(W, (size_t)nI * d);
 #pragma unroll
         for (int i = 0; i < NI; ++i) {
             const int r = wave * ROWS_PER_WAVE + i * RPI + lane / CHUNKS;
             const int row = mtile * BM + r;
             const int c = swz(r, pos) * 8;
             acol[i] = c;
-            asrc[i] = nullptr;
+            aoff[i] = kOOB;
             if (row < sm.rows) {
                 const int t = shared ? row
                                      : (int)min((unsigned)(p1.perm[sm.row0 + row] / p1.top_k),
                                                 (unsigned)(p1.tokens - 1));
-                asrc[i] = p1.x + (size_t)t * d + c;
+                aoff[i] = (uint32_t)(((size_t)t * d + c) * 2);
             }
             const int ch = ntile * (BN / 2) + (r & (BN / 2 - 1));
-            bsrc[i] = ch < sm.kk ? (r < BN / 2 ? Wg : Wu) + (size_t)ch * d + c : nullptr;
+            boff[i] = ch < sm.kk ? (uint32_t)(((size_t)ch * d + c) * 2) : kOOB;
         }
     } else {
-        K = sm.kk;
-        const bf16_t* Hb = shared ? p2.Hs : p2.H + (size_t)sm.row0 * p2.I;
+        const int kbeg = shared && p2.ks2 > 0 ? split * p2.ks2 : 0;
+        K = shared && p2.ks2 > 0 ? min(sm.kk - kbeg, p2.ks2) : sm.kk;
         const int ld = shared ? p2.Is : p2.I;  // H rows and W_down rows share the stride
-        const bf16_t* Wd = shared ? p2.sd : p2.wd + (size_t)(s - hs) * d * p2.I;
+        const int hrows = shared ? p2.tokens : sm.rows;
+        const bf16_t* Hb = (shared ? p2.Hs : p2.H + (size_t)sm.row0 * p2.I) + kbeg;
+        const bf16_t* Wd = (shared ? p2.sd : p2.wd + (size_t)(s - hs) * d * p2.I) + kbeg;
+        ra = make_rsrc(Hb, (size_t)hrows * ld - kbeg);
+        rb = make_rsrc(Wd, (size_t)d * ld - kbeg);
 #pragma unroll
         for (int i = 0; i < NI; ++i) {
             const int r = wave * ROWS_PER_WAVE + i * RPI + lane / CHUNKS;
             const int row = mtile * BM + r;
             const int c = swz(r, pos) * 8;
             acol[i] = c;
-            asrc[i] = row < sm.rows ? Hb + (size_t)row * ld + c : nullptr;
+            aoff[i] = row < sm.rows ? (uint32_t)(((size_t)row * ld + c) * 2) : kOOB;
             const int n = ntile * BN + r;
-            bsrc[i] = n < d ? Wd + (size_t)n * ld + c : nullptr;
+            boff[i] = n < d ? (uint32_t)(((size_t)n * ld + c) * 2) : kOOB;
         }
     }
 
-    // DMA of K tile kt into a stage; past the end of K (or of a segment) the
-    // zero page is read, so every call issues exactly LOADS_PER_TILE loads
-    auto issue = [&](int kt, int stage) {
+    // DMA of K tile kt into a stage (instructions i0 <= i < i1 of each
+    // operand).  Chunks at or past K are masked as well, and tiles past the
+    // end load nothing useful (their stage is never read), so every tile
+    // issues exactly LOADS_PER_TILE loads.
+    auto issue_rows = [&](int kt, int stage, int i0, int i1) {
         unsigned char* sa = smem + stage * STAGE + wave * ROWS_PER_WAVE * ROWB;
         unsigned char* sb = sa + STAGE_A;
         const int k0 = kt * BK;
+        const int lim = K - k0;
+        const uint32_t soff = (uint32_t)k0 * 2u;
 #pragma unroll
         for (int i = 0; i < NI; ++i) {
-            const bool kin = k0 + acol[i] < K;  // A and B chunks share the column
-            load_lds16(asrc[i] && kin ? (const void*)(asrc[i] + k0) : zero, sa + i * RPI * ROWB);
-            load_lds16(bsrc[i] && kin ? (const void*)(bsrc[i] + k0) : zero, sb + i * RPI * ROWB);
+            if (i < i0 || i >= i1) continue;
+            const bool kin = acol[i] < lim;  // A and B chunks share the column
+            load_lds16(ra, kin ? aoff[i] : kOOB, soff, sa + i * RPI * ROWB);
+            load_lds16(rb, kin ? boff[i] : kOOB, soff, sb + i * RPI * ROWB);
         }
     };
+    auto issue = [&](int kt, int stage) { issue_rows(kt, stage, 0, NI); };
 
     const int wm = wave / WN, wn = wave % WN;
     int brow[NF];
 #pragma unroll
     for (int j = 0; j < NF; ++j) {
-        if constexpr (kGateUp)
-            brow[j] = (j == 0 ? 0 : BN / 2) + wn * 32;  // gate rows, then the same channels' up rows
+        if constexpr (kGateUp)  // gate rows, then the same channels' up rows
+            brow[j] = (j < NF / 2 ? 0 : BN / 2) + wn * (WCOL / 2) + (j % (NF / 2)) * 32;
         else
-            brow[j] = wn * 64 + j * 32;
+            brow[j] = wn * WCOL + j * 32;
     }
     static_assert(NSTEP % 2 == 0, "fragment buffers alternate between steps");
     const int nk = ceil_div(K, BK);
@@ -222,8 +270,9 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[buf][j], a[buf][i], acc[i][j], 0, 0, 0);
         };
         // one MFMA, then a fragment read (then a DMA load), spread over a step
+        constexpr int NV_STEP = SPREAD ? LOADS_PER_TILE / NSTEP : LOADS_PER_TILE;
         auto interleave = [](bool dma) {
-            constexpr int NV = LOADS_PER_TILE;
+            constexpr int NV = NV_STEP;
             constexpr int R = NMF > NRD ? (NMF > NV ? NMF : NV) : (NRD > NV ? NRD : NV);
 #pragma unroll
             for (int r = 0; r < R; ++r) {
@@ -241,6 +290,41 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
         // the end), so before the wait of iteration kt the tiles
         // 0 .. kt+NSTAGE-1 are issued and tile kt+1 is in once at most
         // NSTAGE-2 tiles' DMAs are outstanding.
+        if constexpr (SPREAD) {
+            // Tile kt+NSTAGE-1 goes into the stage tile kt-1 used (free since
+            // the barrier that ended step kt-1), a part of its loads with each
+            // 16-deep step: read (kt, s+1) | MFMA (kt, s) | DMA part s, then
+            // wait tile kt+1, barrier | read (kt+1, 0) | MFMA (kt, last) |
+            // DMA last part.  At the wait, the loads issued after tile kt+1's
+            // are NSTAGE-3 whole tiles and NSTEP-1 parts of the next.
+            constexpr int PART = NI / NSTEP;
+            constexpr int WAIT = SPREAD ? (NSTAGE - 3) * LOADS_PER_TILE + (NSTEP - 1) * 2 * PART : 0;
+#pragma unroll
+            for (int t = 0; t < NSTAGE - 1; ++t) issue(t, t);
+            __builtin_amdgcn_s_waitcnt(waitcnt_vm((NSTAGE - 2) * LOADS_PER_TILE));
+            barrier_no_fence();
+            read_frags(0, 0, 0);
+            for (int kt = 0; kt < nk; ++kt) {
+                const int tn = kt + NSTAGE - 1, sn = tn % NSTAGE;
+#pragma unroll
+                for (int st = 0; st < NSTEP - 1; ++st) {
+                    issue_rows(tn, sn, st * PART, st * PART + PART);
+                    read_frags(kt, st + 1, (st + 1) & 1);
+                    mfma_step(st & 1);
+                    interleave(true);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+                __builtin_amdgcn_s_waitcnt(waitcnt_vm(WAIT) & kWaitLgkm0);  // tile kt+1 in; own reads done
+                barrier_no_fence();  // all waves are done reading tile kt
+                __builtin_amdgcn_sched_barrier(0);
+                issue_rows(tn, sn, (NSTEP - 1) * PART, NI);
+                read_frags(kt + 1, 0, 0);
+                mfma_step((NSTEP - 1) & 1);
+                interleave(true);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // no DMA may outlive the workgroup's LDS
+        } else {
 #pragma unroll
         for (int t = 0; t < NSTAGE; ++t) issue(t, t);
         __builtin_amdgcn_s_waitcnt(waitcnt_vm((NSTAGE - 1) * LOADS_PER_TILE));
@@ -265,6 +349,7 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
             __builtin_amdgcn_sched_barrier(0);
         }
         __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // no DMA may outlive the workgroup's LDS
+        }
 
         // ---- epilogue.  The weight fragment is the MFMA's first operand, so
         // the accumulator is transposed: lane -> row lane%32 of the fragment,
@@ -279,22 +364,23 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
             // chunk-aligned end: [kk, kk8) is zero-filled; kk8 and the runs are
             // multiples of 8 and 4, so a run is wholly inside or outside
             const int kk8 = min((sm.kk + 7) & ~7, ldh);
-            const int ch0 = ntile * (BN / 2) + wn * 32 + sub;
 #pragma unroll
             for (int i = 0; i < MFW; ++i) {
                 const int row = row_l + i * 32;
                 if (row >= sm.rows) continue;
                 bf16_t* hr = Hb + (size_t)row * ldh;
 #pragma unroll
+                for (int jj = 0; jj < NF / 2; ++jj)
+#pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const int ch = ch0 + q * 8;
+                    const int ch = ntile * (BN / 2) + wn * (WCOL / 2) + jj * 32 + q * 8 + sub;
                     if (ch >= kk8) continue;
                     uint32_t w[2];
 #pragma unroll
                     for (int h = 0; h < 2; ++h) {
                         const int v = q * 4 + h * 2;
-                        const float g0 = acc[i][0][v], u0 = acc[i][1][v];
-                        const float g1 = acc[i][0][v + 1], u1 = acc[i][1][v + 1];
+                        const float g0 = acc[i][jj][v], u0 = acc[i][jj + NF / 2][v];
+                        const float g1 = acc[i][jj][v + 1], u1 = acc[i][jj + NF / 2][v + 1];
                         const uint32_t lo = ch + h * 2 < sm.kk ? f32_to_bf16(silu_fast(g0) * u0) : 0u;
                         const uint32_t hi = ch + h * 2 + 1 < sm.kk ? f32_to_bf16(silu_fast(g1) * u1) : 0u;
                         w[h] = lo | (hi << 16);
@@ -303,7 +389,7 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
                 }
             }
         } else {
-            bf16_t* Ob = shared ? p2.Os : p2.O + (size_t)sm.row0 * d;
+            bf16_t* Ob = shared ? p2.Os + (size_t)split * p2.tokens * d : p2.O + (size_t)sm.row0 * d;
 #pragma unroll
             for (int i = 0; i < MFW; ++i) {
                 const int row = row_l + i * 32;
@@ -313,7 +399,7 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
                 for (int j = 0; j < NF; ++j)
 #pragma unroll
                     for (int q = 0; q < 4; ++q) {
-                        const int n = ntile * BN + wn * 64 + j * 32 + q * 8 + sub;
+                        const int n = ntile * BN + wn * WCOL + j * 32 + q * 8 + sub;
                         if (n >= d) continue;
                         const uint32_t w0 = (uint32_t)f32_to_bf16(acc[i][j][q * 4]) |
                                             ((uint32_t)f32_to_bf16(acc[i][j][q * 4 + 1]) << 16);
@@ -332,12 +418,12 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
     else run(std::integral_constant<int, 1>{});
 }
 
-__global__ __launch_bounds__(THREADS, 2) void gemm1_big_kernel(Gemm1Params<bf16_t> p) {
+__global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void gemm1_big_kernel(Gemm1Params<bf16_t> p) {
     __shared__ __attribute__((aligned(1024))) unsigned char smem[NSTAGE * STAGE];
     big_tile<true>(p, Gemm2Params<bf16_t>{}, smem);
 }
 
-__global__ __launch_bounds__(THREADS, 2) void gemm2_big_kernel(Gemm2Params<bf16_t> p) {
+__global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void gemm2_big_kernel(Gemm2Params<bf16_t> p) {
     __shared__ __attribute__((aligned(1024))) unsigned char smem[NSTAGE * STAGE];
     big_tile<false>(Gemm1Params<bf16_t>{}, p, smem);
 }

@@ -156,8 +156,8 @@ __global__ __launch_bounds__(64 * DWAVES) void gemm2_decode_kernel(Gemm2Params<b
     const int ld = shared ? p.Is : p.I;  // H rows and W_down rows share the stride
     const bf16_t* Hb = shared ? p.Hs : p.H + (size_t)sm.row0 * p.I;
     const bf16_t* Wd = shared ? p.sd : p.wd + (size_t)(s - hs) * d * p.I;
-    const int kbeg = shared ? split * p.I : 0;
-    const int kend = shared ? min(sm.kk, kbeg + p.I) : sm.kk;
+    const int kbeg = shared ? split * p.ks2 : 0;
+    const int kend = shared ? min(sm.kk, kbeg + p.ks2) : sm.kk;
     const int g = lane >> 4;
     const int n = ntile * DCH + (lane & 15);
     const bool nval = n < d;

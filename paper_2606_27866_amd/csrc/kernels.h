@@ -44,6 +44,7 @@ struct Gemm2Params {
     OT* O;                      // routed rows [A][d]
     OT* Os;                     // shared rows [T][d] (split reductions: [splits][T][d])
     int d, I, Is, E, nseg, tokens;
+    int ks2;                    // > 0: the shared reduction is split into chunks of ks2 channels
 };
 
 // Tile shapes of the kernel families (the dispatch kernel builds tile tables

@@ -43,6 +43,9 @@ def good_desc(**kw):
     (dict(I_shared=-8), -2), (dict(E=0), -2), (dict(E=257), -2), (dict(top_k=0), -2),
     (dict(top_k=9), -2), (dict(E=32, top_k=17), -2), (dict(max_tokens=-1), -2),
     (dict(norm_topk=2), -1), (dict(max_tokens=1 << 29), -2),
+    # bf16 operand blocks of 2^30 elements or more
+    (dict(d=1 << 14, max_tokens=1 << 16), -2), (dict(I=1 << 15, d=1 << 15), -2),
+    (dict(I_shared=1 << 13, max_tokens=1 << 17), -2),
 ])
 def test_bad_descriptor(kw, code):
     desc = good_desc(**kw)
@@ -53,6 +56,11 @@ def test_bad_descriptor(kw, code):
     assert ei.value.code == code
 
 
+def test_fp32_has_no_operand_block_limit():
+    desc = good_desc(d=1 << 14, max_tokens=1 << 16, dtype=fm.FLEXMOE_F32)
+    assert fm.lib().flexmoe_workspace_bytes(ctypes.byref(desc), 1) > 0
+
+
 def test_workspace_monotone_in_T():
     desc = good_desc(I_shared=64)
     sizes = [fm.flexmoe_workspace_bytes(desc, T) for T in (0, 1, 2, 63, 64, 65, 100)]
@@ -60,6 +68,22 @@ def test_workspace_monotone_in_T():
     assert all(s % 256 == 0 for s in sizes)
     with pytest.raises(fm.FlexMoEError):
         fm.flexmoe_workspace_bytes(desc, 101)
+
+
+@pytest.mark.parametrize("shape", [
+    dict(d=2048, E=60, I=1408, top_k=4, I_shared=5632),   # split at T < 8193
+    dict(d=256, E=8, I=128, top_k=2, I_shared=3080),      # split 3 ways, ragged chunk
+    dict(d=4096, E=8, I=14336, top_k=2, I_shared=0),
+    dict(d=256, E=8, I=128, top_k=2, I_shared=3080, dtype=fm.FLEXMOE_F32),
+])
+def test_workspace_monotone_across_shared_splits(shape):
+    """The shared expert's down reduction is split into more chunks (each
+    with its own rows) at smaller T; a workspace sized for max_tokens must
+    still serve every smaller T."""
+    desc = good_desc(max_tokens=20000, **shape)
+    Ts = list(range(0, 700)) + list(range(700, 20001, 37)) + [20000]
+    sizes = [fm.flexmoe_workspace_bytes(desc, T) for T in Ts]
+    assert all(a <= b for a, b in zip(sizes, sizes[1:]))
 
 
 def test_forward_argument_errors():

@@ -86,6 +86,10 @@ MINIS = [
     # takes the three-kernel dispatch path
     ("m_dispatch_256", 128, 64, 8, 64, 2, 0, 1),
     ("m_dispatch_258", 129, 64, 8, 64, 2, 64, 0),
+    # few down tiles and a wide shared expert: its reduction is split into
+    # chunks (2 of 1024 channels; 3 of 1088, 1088 and 904)
+    ("m_shared_split2", 300, 256, 8, 128, 2, 2048, 1),
+    ("m_shared_split3", 200, 128, 4, 64, 2, 3080, 0),
 ]
 
 
