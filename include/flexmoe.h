@@ -13,10 +13,19 @@
  *   - All pointers except the descriptor, the host keep table of
  *     flexmoe_set_budget and the debug-output struct are DEVICE pointers of the
  *     current HIP device.  The caller owns and allocates every buffer,
- *     including the forward workspace; the library allocates nothing and keeps
- *     no device state between calls.
+ *     including the forward workspace; the library allocates no device memory
+ *     and keeps no device data between calls.
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
- *     work is enqueued on it; no call synchronises the host.
+ *     work is ordered after the work already queued on it, and later work
+ *     queued on it is ordered after the call's work; no call synchronises the
+ *     host.  A forward of a layer with a shared expert may run that expert's
+ *     two GEMMs on a second stream of the same device (forked from `stream` by
+ *     an event before routing, joined by an event before the combine): it does
+ *     so for T <= 64 and while the shared expert's gate/up GEMM has fewer than
+ *     1024 tiles.  The library creates that stream on first use per device
+ *     (default priority) and keeps it for the life of the process; forwards
+ *     on one device share it, so concurrent forwards on one device also
+ *     serialise their shared-expert GEMMs.
  *   - Return value 0 = success, otherwise one of the negative FLEXMOE_E* codes;
  *     flexmoe_last_error() then returns a message (thread-local).  Argument
  *     checks happen on the host before any device work: a call that returns
@@ -171,7 +180,9 @@ enum {
     FLEXMOE_K_GATE_UP = 3,        /* gate/up GEMM with fused SwiGLU            */
     FLEXMOE_K_DOWN = 4,           /* down GEMM                                 */
     FLEXMOE_K_COMBINE = 5,        /* weighted combine + shared add             */
-    FLEXMOE_K_COUNT = 6
+    FLEXMOE_K_GATE_UP_SHARED = 6, /* gate/up GEMM of the shared expert         */
+    FLEXMOE_K_DOWN_SHARED = 7,    /* down GEMM of the shared expert            */
+    FLEXMOE_K_COUNT = 8
 };
 typedef struct flexmoe_kernel_times {
     double ms[8];

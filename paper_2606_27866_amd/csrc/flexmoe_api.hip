@@ -4,10 +4,11 @@
 //   route -> dispatch scan -> dispatch scatter -> gate/up GEMM -> down GEMM
 //   -> combine
 //
-// All launches go to the caller's stream.  The host never reads routing
-// results back: tile counts live on the device and the GEMM grids are sized
-// by an upper bound computed from (T, E, I, I_shared); surplus workgroups
-// exit at once.
+// Launches go to the caller's stream, except the shared expert's two GEMMs,
+// which run on a side stream forked before routing and joined before the
+// combine.  The host never reads routing results back: tile counts live on
+// the device and the routed GEMM grids are sized by an upper bound computed
+// from (T, E, I); surplus workgroups exit at once.
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -95,6 +96,9 @@ long long routed_row_tiles_ub(int T, int E, int k, int bm) {
 // least kMinSplitK channels.
 constexpr int kComputeUnits = 256;
 constexpr int kMinSplitK = 1024;
+// Waves of shared-expert gate/up tiles below which the shared expert runs on
+// the side stream during prefill.
+constexpr int kSideWaves = 4;
 
 // Chunk width of the shared expert's split down reduction for T tokens, 0 for
 // one reduction over I_shared.  Decode-sized batches (weight streaming) use
@@ -213,6 +217,49 @@ struct KernelTimer {
         g_pending.push_back({kernel, a, b});
     }
 };
+
+// ---- the side stream of the shared expert -------------------------------
+// The shared expert's GEMMs need no routing, so they run on a second stream
+// of the same device, forked from the caller's stream before routing starts
+// and joined before the combine.  Its tiles then fill the compute units the
+// routed GEMMs leave idle (their tails, the routing kernels).  One stream
+// and two events per device are created on first use (default priority,
+// non-blocking) and kept for the life of the process; the mutex keeps the
+// fork/join of concurrent callers on one device apart.
+struct SideStream {
+    hipStream_t stream = nullptr;
+    hipEvent_t fork = nullptr, join = nullptr;
+    std::mutex mu;
+};
+constexpr int kMaxDevices = 64;
+SideStream g_side[kMaxDevices];
+std::mutex g_side_init;
+
+int side_stream(SideStream** out) {
+    int dev = 0;
+    hipError_t err = hipGetDevice(&dev);
+    if (err != hipSuccess) return hip_fail(err, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) return fail(FLEXMOE_EHIP, "device %d beyond %d", dev, kMaxDevices);
+    SideStream& ss = g_side[dev];
+    std::lock_guard<std::mutex> g(g_side_init);
+    if (!ss.stream) {
+        hipStream_t st = nullptr;
+        hipEvent_t a = nullptr, b = nullptr;
+        if ((err = hipStreamCreateWithFlags(&st, hipStreamNonBlocking)) != hipSuccess)
+            return hip_fail(err, "side stream create");
+        if ((err = hipEventCreateWithFlags(&a, hipEventDisableTiming)) != hipSuccess ||
+            (err = hipEventCreateWithFlags(&b, hipEventDisableTiming)) != hipSuccess) {
+            (void)hipStreamDestroy(st);
+            if (a) (void)hipEventDestroy(a);
+            return hip_fail(err, "side stream event create");
+        }
+        ss.fork = a;
+        ss.join = b;
+        ss.stream = st;
+    }
+    *out = &ss;
+    return FLEXMOE_OK;
+}
 
 }  // namespace
 
@@ -358,6 +405,84 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
                                   : TileShape{kBigBM1, kBigBN1, kBigBM2, kBigBN2, ks2};
 
     hipError_t err;
+    // grid upper bounds from host-known sizes: the routed part's from the
+    // row-tile bound, the shared part's exactly
+    const long long rt1 = routed_row_tiles_ub(T, D.E, D.top_k, ts.bm1);
+    const long long rt2 = routed_row_tiles_ub(T, D.E, D.top_k, ts.bm2);
+    const long long g1r = rt1 * ceil_div(D.I, ts.bn1);
+    const long long g2r = rt2 * ceil_div(D.d, ts.bn2);
+    const long long g1s = has_shared ? (long long)ceil_div(T, ts.bm1) * ceil_div(D.I_shared, ts.bn1) : 0;
+    const long long g2s = has_shared ? (long long)ceil_div(T, ts.bm2) * ceil_div(D.d, ts.bn2) * parts : 0;
+    if (g1r + g1s > 0x7fffffffLL || g2r + g2s > 0x7fffffffLL) return fail(FLEXMOE_ESHAPE, "tile grid too large");
+
+    // The two GEMMs over one part of the tile list, on one stream.
+    auto gemms = [&](int part, hipStream_t st) -> int {
+        const bool sh = part == kPartShared;
+        const int n1 = (int)(sh ? g1s : part == kPartRouted ? g1r : g1r + g1s);
+        const int n2 = (int)(sh ? g2s : part == kPartRouted ? g2r : g2r + g2s);
+        const int k1 = sh ? FLEXMOE_K_GATE_UP_SHARED : FLEXMOE_K_GATE_UP;
+        const int k2 = sh ? FLEXMOE_K_DOWN_SHARED : FLEXMOE_K_DOWN;
+        hipError_t e;
+        if (bf16) {
+            Gemm1Params<bf16_t> p1{(const bf16_t*)x, (const bf16_t*)w_gate_r, (const bf16_t*)w_up_r,
+                                   (const bf16_t*)ws_gate, (const bf16_t*)ws_up, perm, seg, t1,
+                                   (bf16_t*)(ws + L.H), (bf16_t*)(ws + L.Hs), D.d, D.I, D.I_shared, D.E,
+                                   D.top_k, nseg, T, part, (int)g1s};
+            {
+                KernelTimer kt(k1, st);
+                e = decode ? launch_gemm1_decode(p1, n1, st) : launch_gemm1_big(p1, n1, st);
+            }
+            if (e != hipSuccess) return hip_fail(e, "gate/up GEMM launch");
+            Gemm2Params<bf16_t> p2{(const bf16_t*)(ws + L.H), (const bf16_t*)(ws + L.Hs),
+                                   (const bf16_t*)w_down_r, (const bf16_t*)ws_down, seg, t2, (bf16_t*)O,
+                                   (bf16_t*)Os, D.d, D.I, D.I_shared, D.E, nseg, T, ks2, part, (int)g2s};
+            {
+                KernelTimer kt(k2, st);
+                e = decode ? launch_gemm2_decode(p2, n2, st) : launch_gemm2_big(p2, n2, st);
+            }
+            if (e != hipSuccess) return hip_fail(e, "down GEMM launch");
+        } else {
+            Gemm1Params<float> p1{(const float*)x, (const float*)w_gate_r, (const float*)w_up_r,
+                                  (const float*)ws_gate, (const float*)ws_up, perm, seg, t1,
+                                  (float*)(ws + L.H), (float*)(ws + L.Hs), D.d, D.I, D.I_shared, D.E,
+                                  D.top_k, nseg, T, part, (int)g1s};
+            {
+                KernelTimer kt(k1, st);
+                e = launch_gemm1_f32(p1, n1, st);
+            }
+            if (e != hipSuccess) return hip_fail(e, "gate/up GEMM launch");
+            Gemm2Params<float> p2{(const float*)(ws + L.H), (const float*)(ws + L.Hs),
+                                  (const float*)w_down_r, (const float*)ws_down, seg, t2, (float*)O,
+                                  (float*)Os, D.d, D.I, D.I_shared, D.E, nseg, T, 0, part, (int)g2s};
+            {
+                KernelTimer kt(k2, st);
+                e = launch_gemm2_f32(p2, n2, st);
+            }
+            if (e != hipSuccess) return hip_fail(e, "down GEMM launch");
+        }
+        return FLEXMOE_OK;
+    };
+
+    // The shared expert's chain goes first, on the side stream (it needs no
+    // routing); the routed chain follows the routing on the caller's stream;
+    // the combine waits for both.  This pays where the tails of the GEMMs and
+    // the routing kernels leave compute units idle: decode-sized batches and
+    // shared experts whose gate/up GEMM alone fills fewer than kSideWaves
+    // waves of tiles.  Past that, one launch over all segments keeps each
+    // XCD's L2 serving one GEMM at a time.
+    const bool use_side = has_shared && (decode || g1s < (long long)kSideWaves * kComputeUnits);
+    SideStream* side = nullptr;
+    std::unique_lock<std::mutex> side_lock;
+    if (use_side) {
+        if ((rc = side_stream(&side)) != FLEXMOE_OK) return rc;
+        side_lock = std::unique_lock<std::mutex>(side->mu);
+        if ((err = hipEventRecord(side->fork, s)) != hipSuccess) return hip_fail(err, "fork record");
+        if ((err = hipStreamWaitEvent(side->stream, side->fork, 0)) != hipSuccess)
+            return hip_fail(err, "fork wait");
+        if ((rc = gemms(kPartShared, side->stream)) != FLEXMOE_OK) return rc;
+        if ((err = hipEventRecord(side->join, side->stream)) != hipSuccess) return hip_fail(err, "join record");
+    }
+
     if ((long long)T * D.top_k <= kSmallAssign) {
         // one workgroup routes and dispatches everything (timed as routing)
         KernelTimer kt(FLEXMOE_K_ROUTE, s);
@@ -390,53 +515,10 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
         if (err != hipSuccess) return hip_fail(err, "dispatch scatter launch");
     }
 
-    // grid upper bounds from host-known sizes
-    const long long rt1 = routed_row_tiles_ub(T, D.E, D.top_k, ts.bm1);
-    const long long rt2 = routed_row_tiles_ub(T, D.E, D.top_k, ts.bm2);
-    long long g1 = rt1 * ceil_div(D.I, ts.bn1);
-    long long g2 = rt2 * ceil_div(D.d, ts.bn2);
-    if (has_shared) {
-        g1 += (long long)ceil_div(T, ts.bm1) * ceil_div(D.I_shared, ts.bn1);
-        g2 += (long long)ceil_div(T, ts.bm2) * ceil_div(D.d, ts.bn2) * parts;
-    }
-    if (g1 > 0x7fffffffLL || g2 > 0x7fffffffLL) return fail(FLEXMOE_ESHAPE, "tile grid too large");
-
-    if (bf16) {
-        Gemm1Params<bf16_t> p1{(const bf16_t*)x, (const bf16_t*)w_gate_r, (const bf16_t*)w_up_r,
-                               (const bf16_t*)ws_gate, (const bf16_t*)ws_up, perm, seg, t1,
-                               (bf16_t*)(ws + L.H), (bf16_t*)(ws + L.Hs), D.d, D.I, D.I_shared, D.E,
-                               D.top_k, nseg, T};
-        {
-            KernelTimer kt(FLEXMOE_K_GATE_UP, s);
-            err = decode ? launch_gemm1_decode(p1, (int)g1, s) : launch_gemm1_big(p1, (int)g1, s);
-        }
-        if (err != hipSuccess) return hip_fail(err, "gate/up GEMM launch");
-        Gemm2Params<bf16_t> p2{(const bf16_t*)(ws + L.H), (const bf16_t*)(ws + L.Hs),
-                               (const bf16_t*)w_down_r, (const bf16_t*)ws_down, seg, t2, (bf16_t*)O,
-                               (bf16_t*)Os, D.d, D.I, D.I_shared, D.E, nseg, T, ks2};
-        {
-            KernelTimer kt(FLEXMOE_K_DOWN, s);
-            err = decode ? launch_gemm2_decode(p2, (int)g2, s) : launch_gemm2_big(p2, (int)g2, s);
-        }
-        if (err != hipSuccess) return hip_fail(err, "down GEMM launch");
-    } else {
-        Gemm1Params<float> p1{(const float*)x, (const float*)w_gate_r, (const float*)w_up_r,
-                              (const float*)ws_gate, (const float*)ws_up, perm, seg, t1,
-                              (float*)(ws + L.H), (float*)(ws + L.Hs), D.d, D.I, D.I_shared, D.E,
-                              D.top_k, nseg, T};
-        {
-            KernelTimer kt(FLEXMOE_K_GATE_UP, s);
-            err = launch_gemm1_f32(p1, (int)g1, s);
-        }
-        if (err != hipSuccess) return hip_fail(err, "gate/up GEMM launch");
-        Gemm2Params<float> p2{(const float*)(ws + L.H), (const float*)(ws + L.Hs),
-                              (const float*)w_down_r, (const float*)ws_down, seg, t2, (float*)O,
-                              (float*)Os, D.d, D.I, D.I_shared, D.E, nseg, T, 0};
-        {
-            KernelTimer kt(FLEXMOE_K_DOWN, s);
-            err = launch_gemm2_f32(p2, (int)g2, s);
-        }
-        if (err != hipSuccess) return hip_fail(err, "down GEMM launch");
+    if ((rc = gemms(use_side ? kPartRouted : kPartAll, s)) != FLEXMOE_OK) return rc;
+    if (use_side) {
+        if ((err = hipStreamWaitEvent(s, side->join, 0)) != hipSuccess) return hip_fail(err, "join wait");
+        side_lock.unlock();
     }
     {
         KernelTimer kt(FLEXMOE_K_COMBINE, s);

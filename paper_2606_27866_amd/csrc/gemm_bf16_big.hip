@@ -18,7 +18,10 @@
 //     XOR-swizzled by bits 1..3 of the row index, so the 16 lanes served in
 //     one LDS cycle of a fragment read hit 64 distinct banks.
 //   - two LDS stages of 64 KB: the loads of K tile t+1 are in flight while
-//     tile t is multiplied.
+//     tile t is multiplied.  MFMA operand fragments are read from LDS two
+//     16-deep steps ahead of their use (one register buffer per step), and
+//     the workgroup barrier that hands a stage back to the DMA sits in the
+//     middle of a K tile, so no step waits on a fragment read just issued.
 //   - tiles are numbered segment-major (shared expert first: its reductions
 //     are the longest) with row tiles fastest, so consecutive tiles share
 //     their weight tile; groups of 8 consecutive tiles go to one XCD
@@ -43,46 +46,31 @@
 namespace flexmoe {
 
 namespace {
-#ifndef FLEXMOE_BIG_BK
-#define FLEXMOE_BIG_BK 64
-#endif
-#ifndef FLEXMOE_BIG_WAVES
-#define FLEXMOE_BIG_WAVES 8
-#endif
-constexpr int BM = 256, BN = 256, BK = FLEXMOE_BIG_BK;
-constexpr int NWAVE = FLEXMOE_BIG_WAVES, THREADS = 64 * NWAVE;
+constexpr int BM = 256, BN = 256, BK = 64;
+constexpr int NWAVE = 8, THREADS = 64 * NWAVE;
 constexpr int WAVES_PER_SIMD = NWAVE / 4;
 constexpr int WM = 2, WN = NWAVE / WM;      // wave grid
 static_assert(BM == WM * 128, "a full tile gives each M-wave four 32-row fragments");
 constexpr int NF = BN / (WN * 32);          // 32-column fragments per wave
 constexpr int WCOL = BN / WN;               // weight rows per wave
-#ifndef FLEXMOE_BIG_NSTAGE
-#define FLEXMOE_BIG_NSTAGE (BK == 32 ? 4 : 2)
-#endif
-constexpr int NSTAGE = FLEXMOE_BIG_NSTAGE;  // LDS stages of BK-deep operand tiles
-#ifndef FLEXMOE_BIG_SPREAD
-#define FLEXMOE_BIG_SPREAD 0
-#endif
-constexpr bool SPREAD = FLEXMOE_BIG_SPREAD;  // spread each tile's DMAs over a step
-static_assert(!SPREAD || NSTAGE >= 3, "spread DMAs write the stage freed one step earlier");
+constexpr int NSTAGE = 2;                   // LDS stages of BK-deep operand tiles
 constexpr int NSTEP = BK / 16;              // 16-deep MFMA steps per K tile
+static_assert(NSTEP == 4, "the K-loop schedule is laid out for four steps per K tile");
 constexpr int ROWB = BK * 2;                // bytes per LDS row
 constexpr int CHUNKS = ROWB / 16;           // 16-byte chunks per LDS row
 constexpr int RPI = 64 / CHUNKS;            // LDS rows filled per DMA instruction
 constexpr int ROWS_PER_WAVE = BM / NWAVE;   // A rows (and B rows) each wave loads
 constexpr int NI = ROWS_PER_WAVE / RPI;     // DMA instructions per wave per operand
 constexpr int LOADS_PER_TILE = 2 * NI;      // DMA instructions per lane per K tile
-constexpr int STAGE_A = BM * ROWB;          // 16 KB
-constexpr int STAGE = STAGE_A + BN * ROWB;  // 32 KB
+constexpr int STAGE_A = BM * ROWB;          // 32 KB
+constexpr int STAGE = STAGE_A + BN * ROWB;  // 64 KB
 constexpr int XCD_GROUP = 8;                // consecutive tiles kept on one XCD
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void lds_ptr_t;
 
 // 16 lanes of a fragment read hit 16 consecutive rows at one logical chunk;
-// XOR-ing the chunk with the row bits above the bank period spreads them
-// over all 64 banks (64-byte rows: bits 2..3; 128-byte rows: bits 1..3).
-constexpr int SWS = BK == 32 ? 2 : 1;
-__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> SWS) & (CHUNKS - 1)); }
+// XOR-ing the chunk with row bits 1..3 spreads them over all 64 banks.
+__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & (CHUNKS - 1)); }
 
 // s_waitcnt with vmcnt = n and no wait on expcnt / lgkmcnt (gfx9 encoding).
 constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
@@ -118,24 +106,34 @@ __device__ __forceinline__ void barrier_no_fence() {
     __builtin_amdgcn_s_barrier();
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
+
+// Scheduling template for one 16-deep step: NMF MFMAs, NV vector memory
+// reads (DMA) and NRD LDS reads, issued round-robin.
+template <int NMF, int NV, int NRD>
+__device__ __forceinline__ void sched_interleave() {
+    constexpr int R = NMF > NRD ? (NMF > NV ? NMF : NV) : (NRD > NV ? NRD : NV);
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        if (r < NMF) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        if (r < NV) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM read (DMA)
+        if (r < NRD) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+    }
+}
 }  // namespace
 
 template <bool kGateUp>
 __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Gemm2Params<bf16_t>& p2,
                                          unsigned char* smem) {
-    const int32_t* tstart = kGateUp ? p1.tstart : p2.tstart;
-    const int nseg = kGateUp ? p1.nseg : p2.nseg;
     const int E = kGateUp ? p1.E : p2.E;
+    const int nseg = kGateUp ? p1.nseg : p2.nseg;
     const int d = kGateUp ? p1.d : p2.d;
 
     // tile numbering: XCD x = b % 8 takes groups of XCD_GROUP consecutive tiles
-    const int tot = tstart[nseg];
     const int jb = blockIdx.x >> 3;
     const int L = (jb / XCD_GROUP) * (8 * XCD_GROUP) + (blockIdx.x & 7) * XCD_GROUP + jb % XCD_GROUP;
-    if (L >= tot) return;
-    const int s = find_segment(tstart, nseg, L);
-    const SegMeta sm = (kGateUp ? p1.seg : p2.seg)[s];
-    const int local = L - tstart[s];
+    int s, local;
+    SegMeta sm;
+    if (!(kGateUp ? tile_of(p1, L, s, sm, local) : tile_of(p2, L, s, sm, local))) return;
     const int mt = ceil_div(sm.rows, BM);
     const int mtile = local % mt;
     // down GEMM of the shared expert: tiles of reduction chunk `split` follow
@@ -206,11 +204,10 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
         }
     }
 
-    // DMA of K tile kt into a stage (instructions i0 <= i < i1 of each
-    // operand).  Chunks at or past K are masked as well, and tiles past the
-    // end load nothing useful (their stage is never read), so every tile
-    // issues exactly LOADS_PER_TILE loads.
-    auto issue_rows = [&](int kt, int stage, int i0, int i1) {
+    // DMA of K tile kt into a stage.  Chunks at or past K are masked as well,
+    // and tiles past the end load nothing useful (their stage is never read),
+    // so every tile issues exactly LOADS_PER_TILE loads.
+    auto issue = [&](int kt, int stage) {
         unsigned char* sa = smem + stage * STAGE + wave * ROWS_PER_WAVE * ROWB;
         unsigned char* sb = sa + STAGE_A;
         const int k0 = kt * BK;
@@ -218,13 +215,11 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
         const uint32_t soff = (uint32_t)k0 * 2u;
 #pragma unroll
         for (int i = 0; i < NI; ++i) {
-            if (i < i0 || i >= i1) continue;
             const bool kin = acol[i] < lim;  // A and B chunks share the column
             load_lds16(ra, kin ? aoff[i] : kOOB, soff, sa + i * RPI * ROWB);
             load_lds16(rb, kin ? boff[i] : kOOB, soff, sb + i * RPI * ROWB);
         }
     };
-    auto issue = [&](int kt, int stage) { issue_rows(kt, stage, 0, NI); };
 
     const int wm = wave / WN, wn = wave % WN;
     int brow[NF];
@@ -235,7 +230,6 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
         else
             brow[j] = wn * WCOL + j * 32;
     }
-    static_assert(NSTEP % 2 == 0, "fragment buffers alternate between steps");
     const int nk = ceil_div(K, BK);
 
     // The K loop and epilogue for tiles whose waves multiply MFW 32-row
@@ -252,104 +246,65 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
             for (int j = 0; j < NF; ++j)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
-        bf16x8 a[2][MFW], b[2][NF];
-        auto read_frags = [&](int kt, int ks, int buf) {
+        bf16x8 a[NSTEP][MFW], b[NSTEP][NF];  // one fragment buffer per step of a K tile
+        auto read_frags = [&](int kt, int ks) {
             const unsigned char* sa = smem + (kt % NSTAGE) * STAGE;
             const unsigned char* sb = sa + STAGE_A;
             const int chunk = ks * 2 + (lane >> 5);
 #pragma unroll
-            for (int i = 0; i < MFW; ++i) a[buf][i] = lds_frag(sa, wm * WR + i * 32 + (lane & 31), chunk);
+            for (int i = 0; i < MFW; ++i) a[ks][i] = lds_frag(sa, wm * WR + i * 32 + (lane & 31), chunk);
 #pragma unroll
-            for (int j = 0; j < NF; ++j) b[buf][j] = lds_frag(sb, brow[j] + (lane & 31), chunk);
+            for (int j = 0; j < NF; ++j) b[ks][j] = lds_frag(sb, brow[j] + (lane & 31), chunk);
         };
-        auto mfma_step = [&](int buf) {
+        auto mfma_step = [&](int ks) {
 #pragma unroll
             for (int i = 0; i < MFW; ++i)
 #pragma unroll
                 for (int j = 0; j < NF; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[buf][j], a[buf][i], acc[i][j], 0, 0, 0);
-        };
-        // one MFMA, then a fragment read (then a DMA load), spread over a step
-        constexpr int NV_STEP = SPREAD ? LOADS_PER_TILE / NSTEP : LOADS_PER_TILE;
-        auto interleave = [](bool dma) {
-            constexpr int NV = NV_STEP;
-            constexpr int R = NMF > NRD ? (NMF > NV ? NMF : NV) : (NRD > NV ? NRD : NV);
-#pragma unroll
-            for (int r = 0; r < R; ++r) {
-                if (r < NMF) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);      // MFMA
-                if (dma && r < NV) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0); // VMEM read (DMA)
-                if (r < NRD) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);     // DS read
-            }
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[ks][j], a[ks][i], acc[i][j], 0, 0, 0);
         };
 
-        // Ping-pong schedule over NSTAGE K tiles in LDS, NSTAGE-1 DMAs ahead:
-        //   read (kt, s+1) | MFMA (kt, s)   for the steps s < NSTEP-1
-        //   wait tile kt+1, barrier | DMA tile kt+NSTAGE into the stage of tile kt |
-        //   read (kt+1, 0) | MFMA (kt, NSTEP-1)
-        // Every iteration issues one tile's DMAs (zero-page loads once past
-        // the end), so before the wait of iteration kt the tiles
-        // 0 .. kt+NSTAGE-1 are issued and tile kt+1 is in once at most
-        // NSTAGE-2 tiles' DMAs are outstanding.
-        if constexpr (SPREAD) {
-            // Tile kt+NSTAGE-1 goes into the stage tile kt-1 used (free since
-            // the barrier that ended step kt-1), a part of its loads with each
-            // 16-deep step: read (kt, s+1) | MFMA (kt, s) | DMA part s, then
-            // wait tile kt+1, barrier | read (kt+1, 0) | MFMA (kt, last) |
-            // DMA last part.  At the wait, the loads issued after tile kt+1's
-            // are NSTAGE-3 whole tiles and NSTEP-1 parts of the next.
-            constexpr int PART = NI / NSTEP;
-            constexpr int WAIT = SPREAD ? (NSTAGE - 3) * LOADS_PER_TILE + (NSTEP - 1) * 2 * PART : 0;
-#pragma unroll
-            for (int t = 0; t < NSTAGE - 1; ++t) issue(t, t);
-            __builtin_amdgcn_s_waitcnt(waitcnt_vm((NSTAGE - 2) * LOADS_PER_TILE));
-            barrier_no_fence();
-            read_frags(0, 0, 0);
-            for (int kt = 0; kt < nk; ++kt) {
-                const int tn = kt + NSTAGE - 1, sn = tn % NSTAGE;
-#pragma unroll
-                for (int st = 0; st < NSTEP - 1; ++st) {
-                    issue_rows(tn, sn, st * PART, st * PART + PART);
-                    read_frags(kt, st + 1, (st + 1) & 1);
-                    mfma_step(st & 1);
-                    interleave(true);
-                    __builtin_amdgcn_sched_barrier(0);
-                }
-                __builtin_amdgcn_s_waitcnt(waitcnt_vm(WAIT) & kWaitLgkm0);  // tile kt+1 in; own reads done
-                barrier_no_fence();  // all waves are done reading tile kt
-                __builtin_amdgcn_sched_barrier(0);
-                issue_rows(tn, sn, (NSTEP - 1) * PART, NI);
-                read_frags(kt + 1, 0, 0);
-                mfma_step((NSTEP - 1) & 1);
-                interleave(true);
-                __builtin_amdgcn_sched_barrier(0);
-            }
-            __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // no DMA may outlive the workgroup's LDS
-        } else {
-#pragma unroll
-        for (int t = 0; t < NSTAGE; ++t) issue(t, t);
-        __builtin_amdgcn_s_waitcnt(waitcnt_vm((NSTAGE - 1) * LOADS_PER_TILE));
+        // Two LDS stages, fragments two steps ahead, barrier mid-tile:
+        //   step 0: MFMA (kt, 0) | read (kt, 2)
+        //   step 1: MFMA (kt, 1) | read (kt, 3)
+        //   wait for tile kt+1 and this wave's reads, barrier
+        //   step 2: DMA tile kt+2 into the stage of tile kt | MFMA (kt, 2) | read (kt+1, 0)
+        //   step 3: MFMA (kt, 3) | read (kt+1, 1)
+        // At the barrier every wave has finished reading tile kt (its last
+        // fragments are in registers), so its stage can be refilled, and tile
+        // kt+1 has landed, so its fragments can be read.  Every iteration
+        // issues one tile's DMAs (zero-page loads once past the end), so at
+        // the wait no later tile's loads are outstanding (two stages).
+        issue(0, 0);
+        issue(1, 1);
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm(LOADS_PER_TILE));  // tile 0 in
         barrier_no_fence();
-        read_frags(0, 0, 0);
+        read_frags(0, 0);
+        read_frags(0, 1);
         for (int kt = 0; kt < nk; ++kt) {
-#pragma unroll
-            for (int st = 0; st < NSTEP - 1; ++st) {
-                read_frags(kt, st + 1, (st + 1) & 1);
-                mfma_step(st & 1);
-                interleave(false);
-                __builtin_amdgcn_sched_barrier(0);
-            }
-            __builtin_amdgcn_s_waitcnt(waitcnt_vm((NSTAGE - 2) * LOADS_PER_TILE) & kWaitLgkm0);  // tile kt+1 in; own reads done
+            read_frags(kt, 2);
+            mfma_step(0);
+            sched_interleave<NMF, 0, NRD>();
+            __builtin_amdgcn_sched_barrier(0);
+            read_frags(kt, 3);
+            mfma_step(1);
+            sched_interleave<NMF, 0, NRD>();
+            __builtin_amdgcn_sched_barrier(0);
+            __builtin_amdgcn_s_waitcnt(waitcnt_vm(0) & kWaitLgkm0);  // tile kt+1 in; own reads done
             barrier_no_fence();  // all waves are done reading tile kt: its stage is free
             __builtin_amdgcn_sched_barrier(0);
             issue(kt + NSTAGE, kt % NSTAGE);
-            // after the last tile this reads a stale stage, whose values go unused
-            read_frags(kt + 1, 0, 0);
-            mfma_step((NSTEP - 1) & 1);
-            interleave(true);
+            // after the last tile these read a stale stage, whose values go unused
+            read_frags(kt + 1, 0);
+            mfma_step(2);
+            sched_interleave<NMF, LOADS_PER_TILE, NRD>();
+            __builtin_amdgcn_sched_barrier(0);
+            read_frags(kt + 1, 1);
+            mfma_step(3);
+            sched_interleave<NMF, 0, NRD>();
             __builtin_amdgcn_sched_barrier(0);
         }
         __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // no DMA may outlive the workgroup's LDS
-        }
 
         // ---- epilogue.  The weight fragment is the MFMA's first operand, so
         // the accumulator is transposed: lane -> row lane%32 of the fragment,

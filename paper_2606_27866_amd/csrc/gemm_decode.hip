@@ -64,11 +64,9 @@ __device__ __forceinline__ void reduce_waves(floatx4_t (&acc)[NACC], float4* red
 __global__ __launch_bounds__(64 * DWAVES) void gemm1_decode_kernel(Gemm1Params<bf16_t> p) {
     __shared__ float4 red[(DWAVES - 1) * 8 * 64];
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int L = blockIdx.x;
-    if (L >= p.tstart[p.nseg]) return;  // workgroup-uniform
-    const int s = find_segment(p.tstart, p.nseg, L);
-    const SegMeta sm = p.seg[s];
-    const int ntile = L - p.tstart[s];  // one row tile per segment (rows <= 64)
+    int s, ntile;  // one row tile per segment (rows <= 64): the local tile is the channel tile
+    SegMeta sm;
+    if (!tile_of(p, blockIdx.x, s, sm, ntile)) return;  // workgroup-uniform
     const int hs = p.nseg - p.E;
     const bool shared = s < hs;
     const size_t wofs = shared ? 0 : (size_t)(s - hs) * p.I * p.d;
@@ -143,11 +141,9 @@ __global__ __launch_bounds__(64 * DWAVES) void gemm1_decode_kernel(Gemm1Params<b
 __global__ __launch_bounds__(64 * DWAVES) void gemm2_decode_kernel(Gemm2Params<bf16_t> p) {
     __shared__ float4 red[(DWAVES - 1) * 4 * 64];
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int L = blockIdx.x;
-    if (L >= p.tstart[p.nseg]) return;  // workgroup-uniform
-    const int s = find_segment(p.tstart, p.nseg, L);
-    const SegMeta sm = p.seg[s];
-    const int local = L - p.tstart[s];
+    int s, local;
+    SegMeta sm;
+    if (!tile_of(p, blockIdx.x, s, sm, local)) return;  // workgroup-uniform
     const int d = p.d;
     const int nt = ceil_div(d, DCH);
     const int split = local / nt, ntile = local % nt;  // split > 0 only for the shared expert

@@ -14,11 +14,9 @@ __global__ __launch_bounds__(256) void gemm1_f32_kernel(Gemm1Params<float> p) {
     __shared__ float As[BK][BM + 4];
     __shared__ float Bg[BK][BN + 4];
     __shared__ float Bu[BK][BN + 4];
-    const int L = blockIdx.x;
-    if (L >= p.tstart[p.nseg]) return;
-    const int s = find_segment(p.tstart, p.nseg, L);
-    const SegMeta sm = p.seg[s];
-    const int local = L - p.tstart[s];
+    int s, local;
+    SegMeta sm;
+    if (!tile_of(p, blockIdx.x, s, sm, local)) return;
     const int mt = ceil_div(sm.rows, BM);
     const int mtile = local % mt, ntile = local / mt;
     const int hs = p.nseg - p.E;  // 1 if segment 0 is the shared expert
@@ -89,11 +87,9 @@ __global__ __launch_bounds__(256) void gemm1_f32_kernel(Gemm1Params<float> p) {
 __global__ __launch_bounds__(256) void gemm2_f32_kernel(Gemm2Params<float> p) {
     __shared__ float As[BK][BM + 4];
     __shared__ float Bs[BK][BN + 4];
-    const int L = blockIdx.x;
-    if (L >= p.tstart[p.nseg]) return;
-    const int s = find_segment(p.tstart, p.nseg, L);
-    const SegMeta sm = p.seg[s];
-    const int local = L - p.tstart[s];
+    int s, local;
+    SegMeta sm;
+    if (!tile_of(p, blockIdx.x, s, sm, local)) return;
     const int mt = ceil_div(sm.rows, BM);
     const int mtile = local % mt, ntile = local / mt;
     const int hs = p.nseg - p.E;  // 1 if segment 0 is the shared expert

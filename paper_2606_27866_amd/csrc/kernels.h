@@ -11,6 +11,15 @@ struct KeepArgs {
     int32_t v[kMaxExperts];
 };
 
+// Which segments one GEMM launch covers.  The shared expert needs no routing,
+// so its GEMMs can run on a second stream while the routed experts are being
+// dispatched; each launch then covers one part of the tile list.
+enum GemmPart : int32_t {
+    kPartAll = 0,     // every segment (tiles 0 .. tstart[nseg])
+    kPartShared = 1,  // the shared expert alone; its tile count comes from the host
+    kPartRouted = 2   // the routed experts (tiles tstart[hs] .. tstart[nseg])
+};
+
 // Gate/up GEMM with fused SwiGLU:
 //   H[row][c] = silu(<W_gate[c], x_t>) * <W_up[c], x_t>,  c < k_s
 // over every segment s (routed experts, then the shared expert).
@@ -27,6 +36,8 @@ struct Gemm1Params {
     T* H;                       // routed activations [A][I]
     T* Hs;                      // shared activations [T][I_s]
     int d, I, Is, E, top_k, nseg, tokens;
+    int part;                   // GemmPart
+    int shared_tiles;           // tiles of the shared segment (kPartShared)
 };
 
 // Down GEMM: O[row][n] = sum_{c < k_s} H[row][c] * W_down[n][c].  O holds one
@@ -45,7 +56,30 @@ struct Gemm2Params {
     OT* Os;                     // shared rows [T][d] (split reductions: [splits][T][d])
     int d, I, Is, E, nseg, tokens;
     int ks2;                    // > 0: the shared reduction is split into chunks of ks2 channels
+    int part;                   // GemmPart
+    int shared_tiles;           // tiles of the shared segment (kPartShared)
 };
+
+// Tile L of a launch -> segment s, its metadata and the tile's index inside
+// the segment.  False when L is past the launch's last tile (the caller's
+// workgroup then has nothing to do).  The shared segment's metadata is known
+// without the dispatch tables: rows = tokens, channels = I_s.
+template <typename P>
+__device__ __forceinline__ bool tile_of(const P& p, int L, int& s, SegMeta& sm, int& local) {
+    if (p.part == kPartShared) {
+        if (L >= p.shared_tiles) return false;
+        s = 0;
+        sm = SegMeta{0, p.tokens, p.Is, 0};
+        local = L;
+        return true;
+    }
+    if (p.part == kPartRouted) L += p.tstart[p.nseg - p.E];
+    if (L >= p.tstart[p.nseg]) return false;
+    s = find_segment(p.tstart, p.nseg, L);
+    sm = p.seg[s];
+    local = L - p.tstart[s];
+    return true;
+}
 
 // Tile shapes of the kernel families (the dispatch kernel builds tile tables
 // with these numbers).

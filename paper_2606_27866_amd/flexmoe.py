@@ -33,7 +33,8 @@ EXPORTED = ("flexmoe_workspace_bytes", "flexmoe_rank_reorder", "flexmoe_set_budg
             "flexmoe_timing_enable", "flexmoe_timing_read")
 
 # kernel indices of flexmoe_kernel_times
-KERNELS = ("route", "dispatch_scan", "dispatch_scatter", "gate_up", "down", "combine")
+KERNELS = ("route", "dispatch_scan", "dispatch_scatter", "gate_up", "down", "combine",
+           "gate_up_shared", "down_shared")
 
 
 class FlexMoEError(RuntimeError):
