@@ -12,7 +12,8 @@ device copies so that no step finds them in the 256 MB last-level cache.
 Prints ONE JSON line on stdout.  `value` is tokens/s of the whole layer;
 `roofline` describes the dominant kernel (the gate/up GEMM) with its
 algorithmic flops or bytes per launch over its average launch time, measured
-with HIP events around that kernel inside the timed region; `cpu_baseline` is
+with HIP events around each launch in a second pass of the same K steps (the
+first, uninstrumented pass gives the step time); `cpu_baseline` is
 the CPU oracle timed on a bounded sample of the same workload.  Per-budget
 results (the nested 100/80/60/40/20 % tables) go into `per_budget`.
 """
@@ -239,10 +240,17 @@ def main():
         keep_names = [wl.table_name]
 
     wl.run(args.warmup, keep_names)
-    ms, kt = wl.run(args.steps, keep_names, with_kernel_times=True)
+    # The timed region: exactly K steps, no instrumentation inside.
+    ms, _ = wl.run(args.steps, keep_names)
+    # Per-kernel durations for the roofline: the same K steps again, each
+    # kernel bracketed by a HIP event pair on the stream it runs on (the
+    # events add a few microseconds per kernel, so this pass is not the one
+    # whose step time is reported).
+    ms_inst, kt = wl.run(args.steps, keep_names, with_kernel_times=True)
     ms_step = ms / args.steps
     value = wl.T * args.steps / (ms / 1e3)
-    log("[bench] %s: %.4f ms/step, %.0f tokens/s" % (args.workload, ms_step, value))
+    log("[bench] %s: %.4f ms/step, %.0f tokens/s (%.4f ms/step with per-kernel events)"
+        % (args.workload, ms_step, value, ms_inst / args.steps))
     for kname, (kms, cnt) in kt.items():
         if cnt:
             log("[bench]   %-17s %8.4f ms avg over %d launches" % (kname, kms / cnt, cnt))
@@ -275,6 +283,7 @@ def main():
         roof["kernel"] = "gate_up GEMM (gemm1_big_kernel)"
     roof["avg_launch_ms"] = gu_avg
     roof["launches_per_step"] = gu_per_step
+    roof["timing"] = "HIP events around each launch, on its stream, over a second pass of the K steps"
 
     layer_s = ms_step / 1e3
     layer = dict(tflops=alg["F"] / layer_s / 1e12, frac_mfma=alg["F"] / layer_s / 1e12 / peak_flops,

@@ -10,7 +10,9 @@ constexpr int kWave = 64;
 constexpr int kMaxExperts = 256;
 constexpr int kMaxTopK = 16;
 constexpr int kRouteTokens = 16;   // tokens per routing block (= dispatch chunk)
-constexpr int kSmallAssign = 256;  // T * top_k at or below which one workgroup dispatches
+constexpr int kSmallAssign = 1024; // T * top_k at or below which one workgroup dispatches
+                                   // (every decode-sized batch: T <= 64, top_k <= 16)
+constexpr int kSmallWaves = 16;    // waves of that workgroup
 
 typedef uint16_t bf16_t;           // raw bf16 bits in memory
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));

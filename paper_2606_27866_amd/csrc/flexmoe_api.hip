@@ -486,7 +486,7 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
     if ((long long)T * D.top_k <= kSmallAssign) {
         // one workgroup routes and dispatches everything (timed as routing)
         KernelTimer kt(FLEXMOE_K_ROUTE, s);
-        dispatch_small_kernel<<<1, 1024, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, keep_dev, D.I,
+        dispatch_small_kernel<<<1, 64 * kSmallWaves, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, keep_dev, D.I,
                                                   D.I_shared, D.d, ts, idx, wts, counts, perm, pos,
                                                   offsets, seg, t1, t2);
         err = hipGetLastError();

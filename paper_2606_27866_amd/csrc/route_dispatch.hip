@@ -26,53 +26,75 @@ __device__ __forceinline__ bool route_before(float va, int ia, float vb, int ib)
     return ia < ib;
 }
 
-// One wave routes one token: lane j < k returns the j-th selected expert and
-// its router weight.  Each lane holds up to four logits; k rounds of a
-// butterfly arg-max under the total order above select the experts (every
-// lane ends a round with the same winner).  Softmax over all E experts,
-// shifted by the largest logit; with norm_topk the k weights are divided by
-// their sum.
-__device__ __forceinline__ void route_token(const float* __restrict__ l, int E, int k, int norm_topk,
-                                            int lane, int& my_id, float& my_w) {
-    float v[4];
-    bool taken[4];
+// Per-wave LDS scratch of route_token: the token's logits and the k slots.
+struct RouteScratch {
+    float v[kMaxExperts];
+    float slot_v[kMaxTopK];
+    int slot_id[kMaxTopK];
+};
+
+// The logits of one token, experts lane + 64*q (q < 4), as four independent
+// loads (addresses clamped into the row; entries past E are replaced by 0).
+__device__ __forceinline__ void load_logits(const float* __restrict__ l, int E, int lane, float (&v)[4]) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
         const int e = lane + 64 * q;
-        taken[q] = e >= E;
-        v[q] = e < E ? l[e] : 0.0f;
+        const float t = l[min(e, E - 1)];
+        v[q] = e < E ? t : 0.0f;
     }
-    my_id = 0;
-    float my_logit = 0.0f, m = 0.0f;
-    for (int j = 0; j < k; ++j) {
-        float bv = 0.0f;
-        int bi = -1;
+}
+
+// One wave routes one token whose logits are in v (load_logits): lane j < k
+// returns the j-th selected expert and its router weight.  Each lane ranks
+// its (up to four) experts by counting the experts ordered before them under
+// the total order above, reading the token's logits back from LDS (all lanes
+// read the same address: a broadcast).  Ranks are a permutation of 0..E-1,
+// so the expert of rank j < k fills slot j -- the top-k in order, with no
+// chain of cross-lane steps.  The LDS row is padded to a multiple of 8 with
+// NaN: a NaN whose id is at or past E is ordered after every expert, so the
+// padding never counts.  Softmax over all E experts, shifted by the largest
+// logit; with norm_topk the k weights are divided by their sum.
+__device__ __forceinline__ void route_token(const float (&v)[4], int E, int k, int norm_topk, int lane,
+                                            RouteScratch& rs, int& my_id, float& my_w) {
+    const int nq = ceil_div(E, 64);         // wave-uniform
+    const int E8 = ceil_div(E, 8) * 8;      // <= kMaxExperts
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int e = lane + 64 * q;
+        if (e < E) rs.v[e] = v[q];
+        else if (e < E8) rs.v[e] = __builtin_nanf("");
+    }
+    __builtin_amdgcn_wave_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    int rank[4] = {0, 0, 0, 0};
+    for (int j0 = 0; j0 < E8; j0 += 8) {
+        const float4 o0 = *reinterpret_cast<const float4*>(&rs.v[j0]);
+        const float4 o1 = *reinterpret_cast<const float4*>(&rs.v[j0 + 4]);
+        const float o[8] = {o0.x, o0.y, o0.z, o0.w, o1.x, o1.y, o1.z, o1.w};
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            const int e = lane + 64 * q;
-            if (!taken[q] && (bi < 0 || route_before(v[q], e, bv, bi))) {
-                bv = v[q];
-                bi = e;
-            }
-        }
+            if (q >= nq) break;
+            int c = 0;
 #pragma unroll
-        for (int o = 32; o > 0; o >>= 1) {
-            const float ov = __shfl_xor(bv, o, 64);
-            const int oi = __shfl_xor(bi, o, 64);
-            if (oi >= 0 && (bi < 0 || route_before(ov, oi, bv, bi))) {
-                bv = ov;
-                bi = oi;
-            }
+            for (int i = 0; i < 8; ++i) c += route_before(o[i], j0 + i, v[q], lane + 64 * q) ? 1 : 0;
+            rank[q] += c;
         }
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-            if (bi == lane + 64 * q) taken[q] = true;
-        if (lane == j) {
-            my_id = bi;
-            my_logit = bv;
-        }
-        if (j == 0) m = bv;
     }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int e = lane + 64 * q;
+        if (e < E && rank[q] < k) {
+            rs.slot_id[rank[q]] = e;
+            rs.slot_v[rank[q]] = v[q];
+        }
+    }
+    __builtin_amdgcn_wave_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    const float m = rs.slot_v[0];
+    my_id = lane < k ? rs.slot_id[lane] : 0;
+    const float my_logit = lane < k ? rs.slot_v[lane] : 0.0f;
+    __builtin_amdgcn_wave_barrier();  // the scratch is reused by the wave's next token
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
     float z = 0.0f;
 #pragma unroll
     for (int q = 0; q < 4; ++q)
@@ -214,14 +236,16 @@ __global__ __launch_bounds__(64 * kRouteTokens) void route_kernel(
     const float* __restrict__ logits, int T, int E, int k, int norm_topk,
     int32_t* __restrict__ idx, float* __restrict__ wts, int32_t* __restrict__ blockcnt, int NB) {
     __shared__ int hist[kMaxExperts];
+    __shared__ RouteScratch rs[kRouteTokens];
     for (int e = threadIdx.x; e < E; e += blockDim.x) hist[e] = 0;
     __syncthreads();
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int t = blockIdx.x * kRouteTokens + wave;
     if (t < T) {  // uniform across the wave
         int id;
-        float w;
-        route_token(logits + (size_t)t * E, E, k, norm_topk, lane, id, w);
+        float w, v[4];
+        load_logits(logits + (size_t)t * E, E, lane, v);
+        route_token(v, E, k, norm_topk, lane, rs[wave], id, w);
         if (lane < k) {
             idx[(size_t)t * k + lane] = id;
             wts[(size_t)t * k + lane] = w;
@@ -293,42 +317,69 @@ __global__ __launch_bounds__(64) void dispatch_scatter_kernel(
 }
 
 // Route, count, scan and place in one workgroup (T * k <= kSmallAssign).
-__global__ __launch_bounds__(1024) void dispatch_small_kernel(
+// Wave w routes the contiguous tokens [w*per, (w+1)*per) and counts its own
+// expert histogram; a scan over the waves gives each wave its base inside
+// every expert's segment, so the 16 waves place their assignments at once,
+// in the same order as one pass over the tokens would.
+__global__ __launch_bounds__(64 * kSmallWaves) void dispatch_small_kernel(
     const float* __restrict__ logits, int T, int E, int k, int norm_topk,
     const int32_t* __restrict__ keep, int I, int I_shared, int d, TileShape ts,
     int32_t* __restrict__ idx, float* __restrict__ wts, int32_t* __restrict__ counts,
     int32_t* __restrict__ perm, int32_t* __restrict__ pos, int32_t* __restrict__ offsets,
     SegMeta* __restrict__ seg, int32_t* __restrict__ t1start, int32_t* __restrict__ t2start) {
-    __shared__ int hist[kMaxExperts];
+    __shared__ int hist[kSmallWaves][kMaxExperts];  // per-wave counts, then per-wave bases
+    __shared__ int cnt[kMaxExperts];
     __shared__ int off[kMaxExperts];
     __shared__ int kk_s[kMaxExperts];
     __shared__ int run[kMaxExperts];
     __shared__ int32_t sidx[kSmallAssign];
+    __shared__ RouteScratch rs[kSmallWaves];
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int nwave = blockDim.x >> 6;
-    for (int e = threadIdx.x; e < E; e += blockDim.x) hist[e] = 0;
-    __syncthreads();
-    for (int t = wave; t < T; t += nwave) {
+    for (int e = lane; e < E; e += 64) hist[wave][e] = 0;
+    __builtin_amdgcn_wave_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    const int per = ceil_div(T, kSmallWaves);
+    const int t0 = min(T, wave * per), t1 = min(T, t0 + per);
+    // the next token's logits are loaded while this one is ranked
+    float vn[4];
+    if (t0 < t1) load_logits(logits + (size_t)t0 * E, E, lane, vn);
+    for (int t = t0; t < t1; ++t) {
         int id;
-        float w;
-        route_token(logits + (size_t)t * E, E, k, norm_topk, lane, id, w);
+        float w, v[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[q] = vn[q];
+        if (t + 1 < t1) load_logits(logits + (size_t)(t + 1) * E, E, lane, vn);
+        route_token(v, E, k, norm_topk, lane, rs[wave], id, w);
         if (lane < k) {
             idx[(size_t)t * k + lane] = id;
             wts[(size_t)t * k + lane] = w;
             sidx[t * k + lane] = id;
-            atomicAdd(&hist[id], 1);  // a count: arrival order does not matter
+            atomicAdd(&hist[wave][id], 1);  // a count: arrival order does not matter
         }
     }
     __syncthreads();
-    if (wave != 0) return;
-    for (int e = lane; e < E; e += 64) counts[e] = hist[e];
-    auto count = [&](int e) { return hist[e]; };
-    const int P = expert_offsets(count, keep, E, I, off, kk_s, run);
-    __builtin_amdgcn_wave_barrier();
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    write_tables(count, off, kk_s, P, T, E, I_shared, d, ts, offsets, seg, t1start, t2start);
+    for (int e = threadIdx.x; e < E; e += blockDim.x) {
+        int c = 0;
+        for (int w = 0; w < kSmallWaves; ++w) {
+            const int h = hist[w][e];
+            hist[w][e] = c;
+            c += h;
+        }
+        cnt[e] = c;
+        counts[e] = c;
+    }
+    __syncthreads();
+    if (wave == 0) {
+        auto count = [&](int e) { return cnt[e]; };
+        const int P = expert_offsets(count, keep, E, I, off, kk_s, run);
+        __builtin_amdgcn_wave_barrier();
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        write_tables(count, off, kk_s, P, T, E, I_shared, d, ts, offsets, seg, t1start, t2start);
+    }
+    __syncthreads();
+    // this wave's running position inside each expert starts at its base
     auto base = [&](int e) { return off[e]; };
-    place(sidx, 0, T * k, kk_s, run, base, perm, pos);
+    place(sidx, t0 * k, t1 * k, kk_s, hist[wave], base, perm, pos);
 }
 
 __global__ void set_keep_kernel(int32_t* __restrict__ keep, KeepArgs t, int E) {

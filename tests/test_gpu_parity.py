@@ -82,10 +82,12 @@ MINIS = [
     ("m_top1", 77, 64, 5, 64, 1, 0, 1),
     ("m_256_experts", 100, 64, 256, 64, 8, 64, 0),
     ("m_shared_wide", 150, 192, 6, 72, 2, 520, 1),
-    # T*top_k = 256 is the largest batch dispatched by one workgroup, 258
+    # T*top_k = 1024 is the largest batch dispatched by one workgroup, 1026
     # takes the three-kernel dispatch path
-    ("m_dispatch_256", 128, 64, 8, 64, 2, 0, 1),
-    ("m_dispatch_258", 129, 64, 8, 64, 2, 64, 0),
+    ("m_dispatch_1024", 512, 64, 8, 64, 2, 0, 1),
+    ("m_dispatch_1026", 513, 64, 8, 64, 2, 64, 0),
+    # a decode-sized batch with 16 experts per token (T*top_k = 1024)
+    ("m_decode_top16", 64, 128, 24, 72, 16, 64, 0),
     # few down tiles and a wide shared expert: its reduction is split into
     # chunks (2 of 1024 channels; 3 of 1088, 1088 and 904)
     ("m_shared_split2", 300, 256, 8, 128, 2, 2048, 1),
