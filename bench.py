@@ -15,7 +15,9 @@ algorithmic flops or bytes per launch over its average launch time, measured
 with HIP events around each launch in a second pass of the same K steps (the
 first, uninstrumented pass gives the step time); `cpu_baseline` is
 the CPU oracle timed on a bounded sample of the same workload.  Per-budget
-results (the nested 100/80/60/40/20 % tables) go into `per_budget`.
+results (the nested 100/80/60/40/20 % tables) go into `per_budget`, each with
+the same budget run offline (exported as compact weights: the paper's static
+checkpoint mode) and the online/offline throughput ratio.
 """
 import argparse
 import hashlib
@@ -178,6 +180,31 @@ class Workload:
             fm.flexmoe_timing_enable(False)
         return ms, kt
 
+    def export_clipped(self, table_name):
+        """Offline clipping: each weight copy packed for one budget."""
+        cws = []
+        for c in range(len(self.copies)):
+            self.use_copy(c)
+            cws.append(self.layer.export_clipped(self.tables[table_name]))
+        self.torch.cuda.synchronize()
+        return cws
+
+    def run_clipped(self, steps, cws):
+        """Time `steps` forwards of the offline-clipped subnetwork (packed
+        weights rotated like the ranked ones)."""
+        torch = self.torch
+        torch.cuda.synchronize()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        ev0.record()
+        for i in range(steps):
+            self.use_copy(i)  # shared expert of this copy
+            x, lg = self.xd[i % len(self.xd)]
+            self.layer.forward(x, lg, y=self.y, clipped=cws[i % len(cws)])
+        ev1.record()
+        torch.cuda.synchronize()
+        return ev0.elapsed_time(ev1)
+
 
 def cpu_baseline(wl, keep, target_s):
     """The oracle, untouched, on the first S tokens of the workload."""
@@ -302,13 +329,20 @@ def main():
             wl.run(2, [name])
             msb, _ = wl.run(steps_b, [name])
             sb = msb / steps_b / 1e3
+            # the same budget exported offline (compact weights, Table 2 mode)
+            cws = wl.export_clipped(name)
+            wl.run_clipped(2, cws)
+            so = wl.run_clipped(steps_b, cws) / steps_b / 1e3
+            del cws
             per_budget.append(dict(table=name, kept=synth.keep_fraction(wl.tables[name], cfg.I),
                                    ms=sb * 1e3, tokens_per_s=wl.T / sb,
                                    tflops=a["F"] / sb / 1e12,
                                    frac_mfma=a["F"] / sb / 1e12 / peak_flops,
-                                   frac_hbm=a["B"] / sb / 1e9 / PEAK_HBM_GBS))
-            log("[bench]   budget %-7s %.4f ms  %.0f tok/s  %.1f TFLOP/s" %
-                (name, sb * 1e3, wl.T / sb, a["F"] / sb / 1e12))
+                                   frac_hbm=a["B"] / sb / 1e9 / PEAK_HBM_GBS,
+                                   offline_ms=so * 1e3, offline_tokens_per_s=wl.T / so,
+                                   online_over_offline=so / sb))
+            log("[bench]   budget %-7s %.4f ms  %.0f tok/s  %.1f TFLOP/s | offline %.4f ms, online/offline %.3f" %
+                (name, sb * 1e3, wl.T / sb, a["F"] / sb / 1e12, so * 1e3, so / sb))
 
     if args.copy_calibration_mib > 0:
         n = args.copy_calibration_mib << 20

@@ -42,8 +42,8 @@
  * rounded once at the end (round to nearest even throughout).
  *
  * Shape rules (FLEXMOE_ESHAPE otherwise): d, I and I_shared are multiples of
- * 8; 1 <= E <= 256; 1 <= top_k <= min(E, 16); 0 <= T <= max_tokens;
- * max_tokens * (top_k + 1) <= 2^30.  In bf16 mode every operand block one
+ * 8; 1 <= E <= 256; 1 <= top_k <= min(E, 16); E * I < 2^31; 0 <= T <=
+ * max_tokens; max_tokens * (top_k + 1) <= 2^30.  In bf16 mode every operand block one
  * GEMM tile addresses stays below 2^30 elements: max_tokens * d,
  * max_tokens * I, max_tokens * I_shared, I * d and I_shared * d (the prefill
  * kernels reach their operands through 32-bit buffer offsets).
@@ -159,6 +159,48 @@ int flexmoe_layer_forward(const flexmoe_layer_desc *desc, int32_t T, const void 
                           const void *w_down_r, const int32_t *keep_dev, const void *ws_gate,
                           const void *ws_up, const void *ws_down, void *y, void *workspace,
                           size_t workspace_bytes, const flexmoe_route_out *dbg, void *stream);
+
+/* ---- Offline clipping (Sec. 4.4, Table 2): one budget exported as a
+ * standalone compact subnetwork, run by the same kernels.
+ *
+ * Clipped layout of a budget k[E]: expert e keeps kp_e = ceil8(k_e) channels
+ * (k_e rounded up to a multiple of 8, so every packed row is 16-byte
+ * aligned), and the experts' blocks follow one another in expert order:
+ *   w_gate_c, w_up_c  expert e's block [kp_e][d]: row c < k_e = ranked row c,
+ *                     rows k_e .. kp_e-1 are zero
+ *   w_down_c          expert e's block [d][kp_e]: column c < k_e = ranked
+ *                     column c, the other columns are zero
+ * Expert e's blocks start at element ch0_e * d of each buffer, ch0_e =
+ * sum_{e' < e} kp_e'.  Each buffer holds P * d elements of dtype, P =
+ * flexmoe_clipped_channels(desc, k).  Experts with k_e = 0 hold nothing.
+ *
+ * flexmoe_clipped_channels: P for the keep table keep_host [E] (host array);
+ *   FLEXMOE_EKEEP if some k_e is outside [0, I], another negative code for
+ *   a bad descriptor or NULL table.
+ * flexmoe_export_clipped: packs the ranked weights (layouts of
+ *   flexmoe_layer_forward) into caller-allocated buffers of P * d elements
+ *   each, on `stream`.  keep_host is validated on the host and may be reused
+ *   when the call returns.  The ranked buffers are only read.
+ * flexmoe_layer_forward_clipped: flexmoe_layer_forward over the packed
+ *   weights.  keep_dev must hold the exported budget; packed_channels = P.
+ *   Results equal those of flexmoe_layer_forward on the ranked weights with
+ *   the same keep counts, bit for bit.  Device keep counts are not trusted
+ *   for addressing: an expert whose packed block would end past
+ *   packed_channels is skipped (as if k_e = 0), so a wrong table yields a
+ *   wrong result but never an access outside the buffers.
+ *   FLEXMOE_EINVAL if packed_channels is outside [0, E * ceil8(I)]; every
+ *   other rule and error of flexmoe_layer_forward applies. */
+int64_t flexmoe_clipped_channels(const flexmoe_layer_desc *desc, const int32_t *keep_host);
+int flexmoe_export_clipped(const flexmoe_layer_desc *desc, const int32_t *keep_host,
+                           const void *w_gate_r, const void *w_up_r, const void *w_down_r,
+                           void *w_gate_c, void *w_up_c, void *w_down_c, void *stream);
+int flexmoe_layer_forward_clipped(const flexmoe_layer_desc *desc, int32_t T, const void *x,
+                                  const float *logits, const void *w_gate_c, const void *w_up_c,
+                                  const void *w_down_c, const int32_t *keep_dev,
+                                  int64_t packed_channels, const void *ws_gate, const void *ws_up,
+                                  const void *ws_down, void *y, void *workspace,
+                                  size_t workspace_bytes, const flexmoe_route_out *dbg,
+                                  void *stream);
 
 /* k = ceil(r * I) for a retention ratio r in [0, 1] (Sec. 3.1).  A slack of
  * 1e-9 absorbs the binary representation error of decimal ratios (0.7 * 1000

@@ -172,6 +172,40 @@ def rank_reorder(scores, w_gate, w_up, w_down):
     return wg_r, wu_r, wd_r, perm
 
 
+def packed_width(k: int) -> int:
+    """Channels an expert occupies in the clipped layout: k rounded up to 8."""
+    return (int(k) + 7) // 8 * 8
+
+
+def export_clipped(keep, w_gate_r, w_up_r, w_down_r):
+    """Offline clipping (Sec. 4.4, Table 2): the subnetwork of budget `keep`
+    as standalone compact weights, by the definition of the clipped layout.
+
+    Expert e keeps its first k_e ranked channels, padded with zeros to
+    kp_e = ceil8(k_e): a gate/up block [kp_e][d] (rows = channels) and a down
+    block [d][kp_e] (columns = channels), the experts' blocks in expert
+    order.  Returns the three packed buffers as flat arrays of P*d elements
+    (P = sum_e kp_e) -- a pure rearrangement of the ranked weights, no
+    arithmetic.
+    """
+    keep = np.asarray(keep, dtype=np.int64)
+    E, I, d = w_gate_r.shape
+    g_blocks, u_blocks, d_blocks = [], [], []
+    for e in range(E):
+        k, kp = int(keep[e]), packed_width(keep[e])
+        g = np.zeros((kp, d), dtype=w_gate_r.dtype)
+        u = np.zeros((kp, d), dtype=w_up_r.dtype)
+        dn = np.zeros((d, kp), dtype=w_down_r.dtype)
+        g[:k] = w_gate_r[e, :k]
+        u[:k] = w_up_r[e, :k]
+        dn[:, :k] = w_down_r[e, :, :k]
+        g_blocks.append(g.reshape(-1))
+        u_blocks.append(u.reshape(-1))
+        d_blocks.append(dn.reshape(-1))
+    cat = lambda bl, dt: np.concatenate(bl) if bl else np.zeros(0, dtype=dt)
+    return (cat(g_blocks, w_gate_r.dtype), cat(u_blocks, w_up_r.dtype), cat(d_blocks, w_down_r.dtype))
+
+
 def keep_from_ratio(r: float, I: int) -> int:
     return int(lib().oracle_keep_from_ratio(float(r), int(I)))
 

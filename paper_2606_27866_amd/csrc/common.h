@@ -47,8 +47,12 @@ struct SegMeta {
     int32_t row0;   // first row of the segment in the routed row space
     int32_t rows;   // rows of the segment (0 for inactive experts)
     int32_t kk;     // channels of the segment (k_e, or I_shared)
-    int32_t pad;
+    int32_t ch0;    // clipped weight layout: the expert's first packed channel
 };
+
+// Channels an expert occupies in the clipped (offline) weight layout: k_e
+// rounded up to 8, so every packed row starts on a 16-byte boundary.
+__host__ __device__ __forceinline__ int packed_width(int k) { return (k + 7) & ~7; }
 
 // Tile shapes of one GEMM-kernel family; the dispatch kernel builds the tile
 // tables with the same numbers the GEMM kernels use.

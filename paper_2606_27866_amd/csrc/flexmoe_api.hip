@@ -56,6 +56,8 @@ int check_desc(const flexmoe_layer_desc* D) {
     if (D->top_k < 1 || D->top_k > D->E || D->top_k > kMaxTopK)
         return fail(FLEXMOE_ESHAPE, "top_k = %d outside [1, min(E, %d)]", D->top_k, kMaxTopK);
     if (D->max_tokens < 0) return fail(FLEXMOE_ESHAPE, "max_tokens = %d is negative", D->max_tokens);
+    if ((long long)D->E * packed_width(D->I) >= (1LL << 31))
+        return fail(FLEXMOE_ESHAPE, "E * I must stay below 2^31 channels");
     // every row index and tile count below stays inside int32
     const long long A = (long long)D->max_tokens * D->top_k;
     if (A + D->max_tokens > (1LL << 30))
@@ -352,11 +354,18 @@ int flexmoe_rank_reorder(const flexmoe_layer_desc* desc, const float* scores, co
     return FLEXMOE_OK;
 }
 
-int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void* x,
-                          const float* logits, const void* w_gate_r, const void* w_up_r,
-                          const void* w_down_r, const int32_t* keep_dev, const void* ws_gate,
-                          const void* ws_up, const void* ws_down, void* y, void* workspace,
-                          size_t workspace_bytes, const flexmoe_route_out* dbg, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// The forward of both weight layouts.  clipped = 0: ranked weights (online
+// clipping, any keep table); clipped = 1: the packed weights of one exported
+// budget, holding packed_limit channels per matrix.
+int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const float* logits,
+                 const void* w_gate_r, const void* w_up_r, const void* w_down_r, const int32_t* keep_dev,
+                 int clipped, int packed_limit, const void* ws_gate, const void* ws_up,
+                 const void* ws_down, void* y, void* workspace, size_t workspace_bytes,
+                 const flexmoe_route_out* dbg, void* stream) {
     int rc = check_desc(desc);
     if (rc) return rc;
     const flexmoe_layer_desc& D = *desc;
@@ -427,7 +436,7 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
             Gemm1Params<bf16_t> p1{(const bf16_t*)x, (const bf16_t*)w_gate_r, (const bf16_t*)w_up_r,
                                    (const bf16_t*)ws_gate, (const bf16_t*)ws_up, perm, seg, t1,
                                    (bf16_t*)(ws + L.H), (bf16_t*)(ws + L.Hs), D.d, D.I, D.I_shared, D.E,
-                                   D.top_k, nseg, T, part, (int)g1s};
+                                   D.top_k, nseg, T, part, (int)g1s, clipped};
             {
                 KernelTimer kt(k1, st);
                 e = decode ? launch_gemm1_decode(p1, n1, st) : launch_gemm1_big(p1, n1, st);
@@ -435,7 +444,8 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
             if (e != hipSuccess) return hip_fail(e, "gate/up GEMM launch");
             Gemm2Params<bf16_t> p2{(const bf16_t*)(ws + L.H), (const bf16_t*)(ws + L.Hs),
                                    (const bf16_t*)w_down_r, (const bf16_t*)ws_down, seg, t2, (bf16_t*)O,
-                                   (bf16_t*)Os, D.d, D.I, D.I_shared, D.E, nseg, T, ks2, part, (int)g2s};
+                                   (bf16_t*)Os, D.d, D.I, D.I_shared, D.E, nseg, T, ks2, part, (int)g2s,
+                                   clipped};
             {
                 KernelTimer kt(k2, st);
                 e = decode ? launch_gemm2_decode(p2, n2, st) : launch_gemm2_big(p2, n2, st);
@@ -445,7 +455,7 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
             Gemm1Params<float> p1{(const float*)x, (const float*)w_gate_r, (const float*)w_up_r,
                                   (const float*)ws_gate, (const float*)ws_up, perm, seg, t1,
                                   (float*)(ws + L.H), (float*)(ws + L.Hs), D.d, D.I, D.I_shared, D.E,
-                                  D.top_k, nseg, T, part, (int)g1s};
+                                  D.top_k, nseg, T, part, (int)g1s, clipped};
             {
                 KernelTimer kt(k1, st);
                 e = launch_gemm1_f32(p1, n1, st);
@@ -453,7 +463,8 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
             if (e != hipSuccess) return hip_fail(e, "gate/up GEMM launch");
             Gemm2Params<float> p2{(const float*)(ws + L.H), (const float*)(ws + L.Hs),
                                   (const float*)w_down_r, (const float*)ws_down, seg, t2, (float*)O,
-                                  (float*)Os, D.d, D.I, D.I_shared, D.E, nseg, T, 0, part, (int)g2s};
+                                  (float*)Os, D.d, D.I, D.I_shared, D.E, nseg, T, 0, part, (int)g2s,
+                                  clipped};
             {
                 KernelTimer kt(k2, st);
                 e = launch_gemm2_f32(p2, n2, st);
@@ -486,9 +497,9 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
     if ((long long)T * D.top_k <= kSmallAssign) {
         // one workgroup routes and dispatches everything (timed as routing)
         KernelTimer kt(FLEXMOE_K_ROUTE, s);
-        dispatch_small_kernel<<<1, 64 * kSmallWaves, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, keep_dev, D.I,
-                                                  D.I_shared, D.d, ts, idx, wts, counts, perm, pos,
-                                                  offsets, seg, t1, t2);
+        dispatch_small_kernel<<<1, 64 * kSmallWaves, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, keep_dev,
+                                                             D.I, D.I_shared, D.d, ts, packed_limit, idx,
+                                                             wts, counts, perm, pos, offsets, seg, t1, t2);
         err = hipGetLastError();
         if (err != hipSuccess) return hip_fail(err, "dispatch launch");
     } else {
@@ -508,8 +519,8 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
         {
             KernelTimer kt(FLEXMOE_K_DISPATCH_SCATTER, s);
             dispatch_scatter_kernel<<<NB, 64, 0, s>>>(idx, keep_dev, counts, blockbase, T, D.E, D.top_k,
-                                                      D.I, D.I_shared, D.d, NB, ts, perm, pos, offsets,
-                                                      seg, t1, t2);
+                                                      D.I, D.I_shared, D.d, NB, ts, packed_limit, perm,
+                                                      pos, offsets, seg, t1, t2);
             err = hipGetLastError();
         }
         if (err != hipSuccess) return hip_fail(err, "dispatch scatter launch");
@@ -542,6 +553,71 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
         }
     }
     return FLEXMOE_OK;
+}
+
+// Packed channels of the clipped layout of keep_host, or a negative error.
+long long clipped_channels(const flexmoe_layer_desc* desc, const int32_t* keep_host) {
+    int rc = check_desc(desc);
+    if (rc) return rc;
+    if (!keep_host) return fail(FLEXMOE_EINVAL, "keep_host is NULL");
+    long long c = 0;
+    for (int e = 0; e < desc->E; ++e) {
+        if (keep_host[e] < 0 || keep_host[e] > desc->I)
+            return fail(FLEXMOE_EKEEP, "keep[%d] = %d outside [0, I = %d]", e, keep_host[e], desc->I);
+        c += packed_width(keep_host[e]);
+    }
+    return c;
+}
+
+}  // namespace
+
+extern "C" {
+
+int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void* x,
+                          const float* logits, const void* w_gate_r, const void* w_up_r,
+                          const void* w_down_r, const int32_t* keep_dev, const void* ws_gate,
+                          const void* ws_up, const void* ws_down, void* y, void* workspace,
+                          size_t workspace_bytes, const flexmoe_route_out* dbg, void* stream) {
+    return forward_impl(desc, T, x, logits, w_gate_r, w_up_r, w_down_r, keep_dev, 0, 0x7fffffff, ws_gate,
+                        ws_up, ws_down, y, workspace, workspace_bytes, dbg, stream);
+}
+
+int64_t flexmoe_clipped_channels(const flexmoe_layer_desc* desc, const int32_t* keep_host) {
+    return clipped_channels(desc, keep_host);
+}
+
+int flexmoe_export_clipped(const flexmoe_layer_desc* desc, const int32_t* keep_host, const void* w_gate_r,
+                           const void* w_up_r, const void* w_down_r, void* w_gate_c, void* w_up_c,
+                           void* w_down_c, void* stream) {
+    const long long c = clipped_channels(desc, keep_host);
+    if (c < 0) return (int)c;
+    if (!w_gate_r || !w_up_r || !w_down_r || !w_gate_c || !w_up_c || !w_down_c)
+        return fail(FLEXMOE_EINVAL, "export_clipped: a weight pointer is NULL");
+    for (const void* ptr : {w_gate_r, w_up_r, w_down_r, (const void*)w_gate_c, (const void*)w_up_c,
+                            (const void*)w_down_c})
+        if (((uintptr_t)ptr) & 15) return fail(FLEXMOE_EINVAL, "weights must be 16-byte aligned");
+    if (c == 0) return FLEXMOE_OK;
+    KeepArgs k;
+    for (int e = 0; e < kMaxExperts; ++e) k.v[e] = e < desc->E ? keep_host[e] : 0;
+    const hipError_t err = launch_export_clipped(k, w_gate_r, w_up_r, w_down_r, w_gate_c, w_up_c, w_down_c,
+                                                 desc->E, desc->I, desc->d,
+                                                 desc->dtype == FLEXMOE_BF16 ? 2 : 4, (hipStream_t)stream);
+    if (err != hipSuccess) return hip_fail(err, "export_clipped launch");
+    return FLEXMOE_OK;
+}
+
+int flexmoe_layer_forward_clipped(const flexmoe_layer_desc* desc, int32_t T, const void* x,
+                                  const float* logits, const void* w_gate_c, const void* w_up_c,
+                                  const void* w_down_c, const int32_t* keep_dev, int64_t packed_channels,
+                                  const void* ws_gate, const void* ws_up, const void* ws_down, void* y,
+                                  void* workspace, size_t workspace_bytes, const flexmoe_route_out* dbg,
+                                  void* stream) {
+    int rc = check_desc(desc);
+    if (rc) return rc;
+    if (packed_channels < 0 || packed_channels > (long long)desc->E * packed_width(desc->I))
+        return fail(FLEXMOE_EINVAL, "packed_channels = %lld outside [0, E * ceil8(I)]", (long long)packed_channels);
+    return forward_impl(desc, T, x, logits, w_gate_c, w_up_c, w_down_c, keep_dev, 1, (int)packed_channels,
+                        ws_gate, ws_up, ws_down, y, workspace, workspace_bytes, dbg, stream);
 }
 
 }  // extern "C"

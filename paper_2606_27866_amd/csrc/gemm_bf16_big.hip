@@ -161,12 +161,11 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
     __amdgpu_buffer_rsrc_t ra, rb;
     if constexpr (kGateUp) {
         K = d;
-        const int nI = shared ? p1.Is : p1.I;
-        const size_t wofs = shared ? 0 : (size_t)(s - hs) * p1.I * d;
+        const RoutedWeights rw = shared ? RoutedWeights{0, p1.Is, 0} : routed_weights(p1, s - hs, sm);
         // this wave's B rows are all gate rows or all up rows
-        const bf16_t* W = (wave * ROWS_PER_WAVE < BN / 2 ? (shared ? p1.sg : p1.wg) : (shared ? p1.su : p1.wu)) + wofs;
+        const bf16_t* W = (wave * ROWS_PER_WAVE < BN / 2 ? (shared ? p1.sg : p1.wg) : (shared ? p1.su : p1.wu)) + rw.base;
         ra = make_rsrc(p1.x, (size_t)p1.tokens * d);
-        rb = make_rsrc(W, (size_t)nI * d);
+        rb = make_rsrc(W, (size_t)rw.rows * d);
 #pragma unroll
         for (int i = 0; i < NI; ++i) {
             const int r = wave * ROWS_PER_WAVE + i * RPI + lane / CHUNKS;
@@ -186,21 +185,23 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
     } else {
         const int kbeg = shared && p2.ks2 > 0 ? split * p2.ks2 : 0;
         K = shared && p2.ks2 > 0 ? min(sm.kk - kbeg, p2.ks2) : sm.kk;
-        const int ld = shared ? p2.Is : p2.I;  // H rows and W_down rows share the stride
+        const RoutedWeights rw = shared ? RoutedWeights{0, 0, p2.Is} : routed_weights(p2, s - hs, sm);
+        const int ldh = shared ? p2.Is : p2.I;  // H row stride
+        const int ldw = rw.ldd;                 // W_down row stride
         const int hrows = shared ? p2.tokens : sm.rows;
         const bf16_t* Hb = (shared ? p2.Hs : p2.H + (size_t)sm.row0 * p2.I) + kbeg;
-        const bf16_t* Wd = (shared ? p2.sd : p2.wd + (size_t)(s - hs) * d * p2.I) + kbeg;
-        ra = make_rsrc(Hb, (size_t)hrows * ld - kbeg);
-        rb = make_rsrc(Wd, (size_t)d * ld - kbeg);
+        const bf16_t* Wd = (shared ? p2.sd : p2.wd + rw.base) + kbeg;
+        ra = make_rsrc(Hb, (size_t)hrows * ldh - kbeg);
+        rb = make_rsrc(Wd, (size_t)d * ldw - kbeg);
 #pragma unroll
         for (int i = 0; i < NI; ++i) {
             const int r = wave * ROWS_PER_WAVE + i * RPI + lane / CHUNKS;
             const int row = mtile * BM + r;
             const int c = swz(r, pos) * 8;
             acol[i] = c;
-            aoff[i] = row < sm.rows ? (uint32_t)(((size_t)row * ld + c) * 2) : kOOB;
+            aoff[i] = row < sm.rows ? (uint32_t)(((size_t)row * ldh + c) * 2) : kOOB;
             const int n = ntile * BN + r;
-            boff[i] = n < d ? (uint32_t)(((size_t)n * ld + c) * 2) : kOOB;
+            boff[i] = n < d ? (uint32_t)(((size_t)n * ldw + c) * 2) : kOOB;
         }
     }
 

@@ -69,7 +69,7 @@ __global__ __launch_bounds__(64 * DWAVES) void gemm1_decode_kernel(Gemm1Params<b
     if (!tile_of(p, blockIdx.x, s, sm, ntile)) return;  // workgroup-uniform
     const int hs = p.nseg - p.E;
     const bool shared = s < hs;
-    const size_t wofs = shared ? 0 : (size_t)(s - hs) * p.I * p.d;
+    const size_t wofs = shared ? 0 : routed_weights(p, s - hs, sm).base;
     const bf16_t* Wg = (shared ? p.sg : p.wg) + wofs;
     const bf16_t* Wu = (shared ? p.su : p.wu) + wofs;
     const int d = p.d;
@@ -149,9 +149,10 @@ __global__ __launch_bounds__(64 * DWAVES) void gemm2_decode_kernel(Gemm2Params<b
     const int split = local / nt, ntile = local % nt;  // split > 0 only for the shared expert
     const int hs = p.nseg - p.E;
     const bool shared = s < hs;
-    const int ld = shared ? p.Is : p.I;  // H rows and W_down rows share the stride
+    const RoutedWeights rw = shared ? RoutedWeights{0, 0, p.Is} : routed_weights(p, s - hs, sm);
+    const int ldh = shared ? p.Is : p.I;  // H row stride
     const bf16_t* Hb = shared ? p.Hs : p.H + (size_t)sm.row0 * p.I;
-    const bf16_t* Wd = shared ? p.sd : p.wd + (size_t)(s - hs) * d * p.I;
+    const bf16_t* Wd = shared ? p.sd : p.wd + rw.base;
     const int kbeg = shared ? split * p.ks2 : 0;
     const int kend = shared ? min(sm.kk, kbeg + p.ks2) : sm.kk;
     const int g = lane >> 4;
@@ -162,13 +163,13 @@ __global__ __launch_bounds__(64 * DWAVES) void gemm2_decode_kernel(Gemm2Params<b
 #pragma unroll
     for (int f = 0; f < 4; ++f) {
         const int r = f * 16 + (lane & 15);
-        hrow[f] = (f < nf && r < sm.rows) ? Hb + (size_t)r * ld : nullptr;
+        hrow[f] = (f < nf && r < sm.rows) ? Hb + (size_t)r * ldh : nullptr;
     }
     floatx4_t acc[4];
 #pragma unroll
     for (int f = 0; f < 4; ++f) acc[f] = floatx4_t{0.f, 0.f, 0.f, 0.f};
     const u32x4 zero = {0u, 0u, 0u, 0u};
-    const bf16_t* wrow = Wd + (size_t)n * ld;
+    const bf16_t* wrow = Wd + (size_t)n * rw.ldd;
     // a chunk is used when it starts before kend; H is zero past k_e within
     // the chunk-aligned end, and W_down columns there are real (finite)
     // weights, so their products are exact zeros

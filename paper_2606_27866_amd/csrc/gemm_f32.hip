@@ -21,7 +21,7 @@ __global__ __launch_bounds__(256) void gemm1_f32_kernel(Gemm1Params<float> p) {
     const int mtile = local % mt, ntile = local / mt;
     const int hs = p.nseg - p.E;  // 1 if segment 0 is the shared expert
     const bool shared = s < hs;
-    const size_t wofs = shared ? 0 : (size_t)(s - hs) * p.I * p.d;
+    const size_t wofs = shared ? 0 : routed_weights(p, s - hs, sm).base;
     const float* Wg = (shared ? p.sg : p.wg) + wofs;
     const float* Wu = (shared ? p.su : p.wu) + wofs;
 
@@ -95,16 +95,17 @@ __global__ __launch_bounds__(256) void gemm2_f32_kernel(Gemm2Params<float> p) {
     const int hs = p.nseg - p.E;  // 1 if segment 0 is the shared expert
     const bool shared = s < hs;
     const float* Hb = shared ? p.Hs : p.H + (size_t)sm.row0 * p.I;
-    const int ld = shared ? p.Is : p.I;  // H rows and W_down rows share the stride
-    const float* Wd = shared ? p.sd : p.wd + (size_t)(s - hs) * p.d * p.I;
+    const RoutedWeights rw = shared ? RoutedWeights{0, 0, p.Is} : routed_weights(p, s - hs, sm);
+    const int ldh = shared ? p.Is : p.I;  // H row stride
+    const float* Wd = shared ? p.sd : p.wd + rw.base;
     const int K = sm.kk;
 
     const int tid = threadIdx.x;
     const int lr = tid >> 2, lk = (tid & 3) * 4;
     const int row = mtile * BM + lr;
-    const float* asrc = row < sm.rows ? Hb + (size_t)row * ld : nullptr;
+    const float* asrc = row < sm.rows ? Hb + (size_t)row * ldh : nullptr;
     const int n = ntile * BN + lr;
-    const float* bsrc = n < p.d ? Wd + (size_t)n * ld : nullptr;
+    const float* bsrc = n < p.d ? Wd + (size_t)n * rw.ldd : nullptr;
 
     const int ty = tid >> 4, tx = tid & 15;
     float acc[4][4] = {};

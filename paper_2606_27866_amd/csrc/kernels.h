@@ -38,6 +38,7 @@ struct Gemm1Params {
     int d, I, Is, E, top_k, nseg, tokens;
     int part;                   // GemmPart
     int shared_tiles;           // tiles of the shared segment (kPartShared)
+    int clipped;                // routed weights in the clipped layout (see RoutedWeights)
 };
 
 // Down GEMM: O[row][n] = sum_{c < k_s} H[row][c] * W_down[n][c].  O holds one
@@ -58,7 +59,26 @@ struct Gemm2Params {
     int ks2;                    // > 0: the shared reduction is split into chunks of ks2 channels
     int part;                   // GemmPart
     int shared_tiles;           // tiles of the shared segment (kPartShared)
+    int clipped;                // routed weights in the clipped layout (see RoutedWeights)
 };
+
+// Where routed expert e's weights live.  Ranked layout (online clipping):
+// gate/up [E][I][d], down [E][d][I]; expert e's blocks start at e*I*d and a
+// down row holds I channels.  Clipped layout (one budget exported offline):
+// the experts' blocks are packed back to back, expert e holding
+// packed_width(k_e) channels -- gate/up [kp_e][d], down [d][kp_e] -- from
+// packed channel ch0; both blocks start at ch0*d and a down row holds kp_e
+// channels.
+struct RoutedWeights {
+    size_t base;   // element offset of the expert's gate/up block and of its down block
+    int rows;      // gate/up rows the block holds
+    int ldd;       // elements per down row
+};
+template <typename P>
+__device__ __forceinline__ RoutedWeights routed_weights(const P& p, int e, const SegMeta& sm) {
+    if (p.clipped) return RoutedWeights{(size_t)sm.ch0 * p.d, packed_width(sm.kk), packed_width(sm.kk)};
+    return RoutedWeights{(size_t)e * p.I * p.d, p.I, p.I};
+}
 
 // Tile L of a launch -> segment s, its metadata and the tile's index inside
 // the segment.  False when L is past the launch's last tile (the caller's
@@ -92,17 +112,20 @@ __global__ void route_kernel(const float* logits, int T, int E, int k, int norm_
                              float* wts, int32_t* blockcnt, int NB);
 __global__ void dispatch_scan_kernel(const int32_t* blockcnt, int NB, int32_t* blockbase,
                                      int32_t* counts);
+// `packed_limit`: in the clipped layout, the packed channels the weight
+// buffers hold; an expert whose block would reach past it is treated as
+// k_e = 0 (the ranked layout passes INT32_MAX).
 __global__ void dispatch_scatter_kernel(const int32_t* idx, const int32_t* keep,
                                         const int32_t* counts, const int32_t* blockbase, int T,
                                         int E, int k, int I, int I_shared, int d, int NB,
-                                        TileShape ts, int32_t* perm, int32_t* pos,
+                                        TileShape ts, int packed_limit, int32_t* perm, int32_t* pos,
                                         int32_t* offsets, SegMeta* seg, int32_t* t1start,
                                         int32_t* t2start);
 __global__ void dispatch_small_kernel(const float* logits, int T, int E, int k, int norm_topk,
                                       const int32_t* keep, int I, int I_shared, int d, TileShape ts,
-                                      int32_t* idx, float* wts, int32_t* counts, int32_t* perm,
-                                      int32_t* pos, int32_t* offsets, SegMeta* seg, int32_t* t1start,
-                                      int32_t* t2start);
+                                      int packed_limit, int32_t* idx, float* wts, int32_t* counts,
+                                      int32_t* perm, int32_t* pos, int32_t* offsets, SegMeta* seg,
+                                      int32_t* t1start, int32_t* t2start);
 __global__ void set_keep_kernel(int32_t* keep, KeepArgs t, int E);
 
 // Launchers (defined next to their kernels).  Each returns the launch status.
@@ -117,5 +140,10 @@ hipError_t launch_combine(const void* O, const void* Os, const int32_t* pos, con
 hipError_t launch_rank_reorder(const float* scores, const void* wg, const void* wu,
                                const void* wd, void* wg_r, void* wu_r, void* wd_r,
                                int32_t* perm, int E, int I, int d, int esize, hipStream_t s);
+// Packs one budget's ranked weights into the clipped layout (RoutedWeights);
+// keep holds the budget, already validated on the host.
+hipError_t launch_export_clipped(const KeepArgs& keep, const void* wg_r, const void* wu_r,
+                                 const void* wd_r, void* wg_c, void* wu_c, void* wd_c, int E, int I,
+                                 int d, int esize, hipStream_t s);
 
 }  // namespace flexmoe

@@ -107,23 +107,34 @@ __device__ __forceinline__ void route_token(const float (&v)[4], int E, int k, i
 
 // One wave: exclusive scan over experts of the active counts (k_e > 0, k_e
 // clamped to [0, I]; device data is never trusted for addressing), four
-// experts per lane.  Fills off[], kk_s[] and zeroes run[]; returns P.
+// experts per lane.  Also scans the packed widths of the clipped weight
+// layout: an expert whose block would end past packed_limit is treated as
+// k_e = 0.  Fills off[], kk_s[], ch0[] and zeroes run[]; returns P.
 template <typename CountFn>
 __device__ __forceinline__ int expert_offsets(CountFn count, const int32_t* __restrict__ keep, int E,
-                                              int I, int* off, int* kk_s, int* run) {
+                                              int I, int packed_limit, int* off, int* kk_s, int* ch0,
+                                              int* run) {
     const int lane = threadIdx.x & 63;
-    int c4[4], k4[4], local = 0;
+    int k4[4], w4 = 0;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
         const int e = lane * 4 + q;
-        int kk = 0, c = 0;
-        if (e < E) {
-            kk = min(max(keep[e], 0), I);
-            c = kk > 0 ? count(e) : 0;
-        }
-        c4[q] = c;
-        k4[q] = kk;
-        local += c;
+        k4[q] = e < E ? min(max(keep[e], 0), I) : 0;
+        w4 += packed_width(k4[q]);
+    }
+    // packed channel offsets (a prefix of at most 256 * 2^20 fits in int)
+    const int winc = wave_incl_scan(w4);
+    int wbase = winc - w4;
+    int c4[4], local = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int e = lane * 4 + q;
+        const int w = packed_width(k4[q]);
+        if (e < E) ch0[e] = wbase;
+        if (wbase + w > packed_limit) k4[q] = 0;
+        wbase += w;
+        c4[q] = (e < E && k4[q] > 0) ? count(e) : 0;
+        local += c4[q];
     }
     const int inc = wave_incl_scan(local);
     int base = inc - local;
@@ -144,8 +155,8 @@ __device__ __forceinline__ int expert_offsets(CountFn count, const int32_t* __re
 // reductions, so they start first) and the exclusive scans of both GEMMs'
 // tile counts, 64 segments per round.
 template <typename CountFn>
-__device__ void write_tables(CountFn count, const int* off, const int* kk_s, int P, int T, int E,
-                             int I_shared, int d, TileShape ts, int32_t* __restrict__ offsets,
+__device__ void write_tables(CountFn count, const int* off, const int* kk_s, const int* ch0, int P,
+                             int T, int E, int I_shared, int d, TileShape ts, int32_t* __restrict__ offsets,
                              SegMeta* __restrict__ seg, int32_t* __restrict__ t1start,
                              int32_t* __restrict__ t2start) {
     const int lane = threadIdx.x & 63;
@@ -161,14 +172,15 @@ __device__ void write_tables(CountFn count, const int* off, const int* kk_s, int
                 m.row0 = 0;
                 m.rows = T;
                 m.kk = I_shared;
+                m.ch0 = 0;
             } else {
                 const int e = s - hs;
                 m.row0 = off[e];
                 m.rows = kk_s[e] > 0 ? count(e) : 0;
                 m.kk = kk_s[e];
+                m.ch0 = ch0[e];
                 offsets[e] = off[e];
             }
-            m.pad = 0;
             seg[s] = m;
             if (m.rows > 0 && m.kk > 0) {
                 n1 = ceil_div(m.rows, ts.bm1) * ceil_div(m.kk, ts.bn1);
@@ -300,16 +312,18 @@ __global__ __launch_bounds__(256) void dispatch_scan_kernel(const int32_t* __res
 __global__ __launch_bounds__(64) void dispatch_scatter_kernel(
     const int32_t* __restrict__ idx, const int32_t* __restrict__ keep,
     const int32_t* __restrict__ counts, const int32_t* __restrict__ blockbase, int T, int E, int k,
-    int I, int I_shared, int d, int NB, TileShape ts, int32_t* __restrict__ perm,
+    int I, int I_shared, int d, int NB, TileShape ts, int packed_limit, int32_t* __restrict__ perm,
     int32_t* __restrict__ pos, int32_t* __restrict__ offsets, SegMeta* __restrict__ seg,
     int32_t* __restrict__ t1start, int32_t* __restrict__ t2start) {
     __shared__ int off[kMaxExperts];
     __shared__ int kk_s[kMaxExperts];
+    __shared__ int ch0[kMaxExperts];
     __shared__ int run[kMaxExperts];
     auto count = [&](int e) { return counts[e]; };
-    const int P = expert_offsets(count, keep, E, I, off, kk_s, run);
+    const int P = expert_offsets(count, keep, E, I, packed_limit, off, kk_s, ch0, run);
     __syncthreads();
-    if (blockIdx.x == 0) write_tables(count, off, kk_s, P, T, E, I_shared, d, ts, offsets, seg, t1start, t2start);
+    if (blockIdx.x == 0)
+        write_tables(count, off, kk_s, ch0, P, T, E, I_shared, d, ts, offsets, seg, t1start, t2start);
     const int a0 = blockIdx.x * kRouteTokens * k;
     const int a1 = min((blockIdx.x + 1) * kRouteTokens, T) * k;
     auto base = [&](int e) { return off[e] + blockbase[(size_t)e * NB + blockIdx.x]; };
@@ -323,7 +337,7 @@ __global__ __launch_bounds__(64) void dispatch_scatter_kernel(
 // in the same order as one pass over the tokens would.
 __global__ __launch_bounds__(64 * kSmallWaves) void dispatch_small_kernel(
     const float* __restrict__ logits, int T, int E, int k, int norm_topk,
-    const int32_t* __restrict__ keep, int I, int I_shared, int d, TileShape ts,
+    const int32_t* __restrict__ keep, int I, int I_shared, int d, TileShape ts, int packed_limit,
     int32_t* __restrict__ idx, float* __restrict__ wts, int32_t* __restrict__ counts,
     int32_t* __restrict__ perm, int32_t* __restrict__ pos, int32_t* __restrict__ offsets,
     SegMeta* __restrict__ seg, int32_t* __restrict__ t1start, int32_t* __restrict__ t2start) {
@@ -331,6 +345,7 @@ __global__ __launch_bounds__(64 * kSmallWaves) void dispatch_small_kernel(
     __shared__ int cnt[kMaxExperts];
     __shared__ int off[kMaxExperts];
     __shared__ int kk_s[kMaxExperts];
+    __shared__ int ch0[kMaxExperts];
     __shared__ int run[kMaxExperts];
     __shared__ int32_t sidx[kSmallAssign];
     __shared__ RouteScratch rs[kSmallWaves];
@@ -371,10 +386,10 @@ __global__ __launch_bounds__(64 * kSmallWaves) void dispatch_small_kernel(
     __syncthreads();
     if (wave == 0) {
         auto count = [&](int e) { return cnt[e]; };
-        const int P = expert_offsets(count, keep, E, I, off, kk_s, run);
+        const int P = expert_offsets(count, keep, E, I, packed_limit, off, kk_s, ch0, run);
         __builtin_amdgcn_wave_barrier();
         __atomic_signal_fence(__ATOMIC_SEQ_CST);
-        write_tables(count, off, kk_s, P, T, E, I_shared, d, ts, offsets, seg, t1start, t2start);
+        write_tables(count, off, kk_s, ch0, P, T, E, I_shared, d, ts, offsets, seg, t1start, t2start);
     }
     __syncthreads();
     // this wave's running position inside each expert starts at its base

@@ -30,7 +30,8 @@ ERRORS = {
 
 EXPORTED = ("flexmoe_workspace_bytes", "flexmoe_rank_reorder", "flexmoe_set_budget",
             "flexmoe_layer_forward", "flexmoe_keep_from_ratio", "flexmoe_last_error",
-            "flexmoe_timing_enable", "flexmoe_timing_read")
+            "flexmoe_timing_enable", "flexmoe_timing_read", "flexmoe_clipped_channels",
+            "flexmoe_export_clipped", "flexmoe_layer_forward_clipped")
 
 # kernel indices of flexmoe_kernel_times
 KERNELS = ("route", "dispatch_scan", "dispatch_scatter", "gate_up", "down", "combine",
@@ -83,6 +84,13 @@ def lib():
         L.flexmoe_set_budget.restype = ctypes.c_int
         L.flexmoe_layer_forward.argtypes = [D, i32] + [vp] * 11 + [sz, ctypes.POINTER(flexmoe_route_out), vp]
         L.flexmoe_layer_forward.restype = ctypes.c_int
+        L.flexmoe_clipped_channels.argtypes = [D, vp]
+        L.flexmoe_clipped_channels.restype = ctypes.c_int64
+        L.flexmoe_export_clipped.argtypes = [D] + [vp] * 8
+        L.flexmoe_export_clipped.restype = ctypes.c_int
+        L.flexmoe_layer_forward_clipped.argtypes = ([D, i32] + [vp] * 6 + [ctypes.c_int64] + [vp] * 5
+                                                    + [sz, ctypes.POINTER(flexmoe_route_out), vp])
+        L.flexmoe_layer_forward_clipped.restype = ctypes.c_int
         L.flexmoe_keep_from_ratio.argtypes = [ctypes.c_double, i32]
         L.flexmoe_keep_from_ratio.restype = ctypes.c_int
         L.flexmoe_timing_enable.argtypes = [ctypes.c_int]
@@ -174,6 +182,48 @@ def flexmoe_layer_forward(desc, T, x, logits, w_gate_r, w_up_r, w_down_r, keep_d
         int(workspace_bytes), ctypes.byref(ro) if ro is not None else None, _stream(stream)))
 
 
+def flexmoe_clipped_channels(desc, keep_host: Sequence[int]) -> int:
+    kh = np.ascontiguousarray(np.asarray(keep_host, dtype=np.int32))
+    n = int(lib().flexmoe_clipped_channels(ctypes.byref(desc), kh.ctypes.data_as(ctypes.c_void_p)))
+    if n < 0:
+        raise FlexMoEError(n, flexmoe_last_error())
+    return n
+
+
+def flexmoe_export_clipped(desc, keep_host, w_gate_r, w_up_r, w_down_r, w_gate_c, w_up_c, w_down_c,
+                           stream=None):
+    kh = np.ascontiguousarray(np.asarray(keep_host, dtype=np.int32))
+    _check(lib().flexmoe_export_clipped(ctypes.byref(desc), kh.ctypes.data_as(ctypes.c_void_p),
+                                        _p(w_gate_r), _p(w_up_r), _p(w_down_r), _p(w_gate_c),
+                                        _p(w_up_c), _p(w_down_c), _stream(stream)))
+
+
+def flexmoe_layer_forward_clipped(desc, T, x, logits, w_gate_c, w_up_c, w_down_c, keep_dev,
+                                  packed_channels, ws_gate, ws_up, ws_down, y, workspace,
+                                  workspace_bytes=None, dbg=None, stream=None):
+    if workspace_bytes is None:
+        workspace_bytes = workspace.numel() * workspace.element_size()
+    ro = None
+    if dbg:
+        ro = flexmoe_route_out(*[_p(dbg.get(n)) for n, _ in flexmoe_route_out._fields_])
+    _check(lib().flexmoe_layer_forward_clipped(
+        ctypes.byref(desc), int(T), _p(x), _p(logits), _p(w_gate_c), _p(w_up_c), _p(w_down_c),
+        _p(keep_dev), int(packed_channels), _p(ws_gate), _p(ws_up), _p(ws_down), _p(y),
+        _p(workspace), int(workspace_bytes), ctypes.byref(ro) if ro is not None else None,
+        _stream(stream)))
+
+
+class ClippedWeights:
+    """The packed weights of one exported budget (offline clipping) and its
+    device keep table."""
+
+    def __init__(self, keep_host, w_gate_c, w_up_c, w_down_c, packed_channels, keep_dev):
+        self.keep_host = np.asarray(keep_host, dtype=np.int32).copy()
+        self.w_gate_c, self.w_up_c, self.w_down_c = w_gate_c, w_up_c, w_down_c
+        self.packed_channels = packed_channels
+        self.keep_dev = keep_dev
+
+
 class Layer:
     """Device-resident masked MoE layer: weights, keep table, workspace.
 
@@ -200,11 +250,29 @@ class Layer:
     def set_budget(self, keep_host, stream=None):
         flexmoe_set_budget(self.desc, self.keep, keep_host, stream)
 
-    def forward(self, x, logits, y=None, keep=None, dbg=None, stream=None):
+    def export_clipped(self, keep_host, stream=None) -> ClippedWeights:
+        """Pack the current ranked weights for the budget keep_host."""
+        import torch
+        P = flexmoe_clipped_channels(self.desc, keep_host)
+        bufs = [torch.empty((max(P, 1) * self.desc.d,), dtype=self.tdtype, device=self.device)
+                for _ in range(3)]
+        flexmoe_export_clipped(self.desc, keep_host, self.w_gate, self.w_up, self.w_down, *bufs,
+                               stream=stream)
+        keep_dev = torch.from_numpy(np.asarray(keep_host, dtype=np.int32).copy()).to(self.device)
+        return ClippedWeights(keep_host, *bufs, P, keep_dev)
+
+    def forward(self, x, logits, y=None, keep=None, dbg=None, stream=None, clipped=None):
+        """clipped: a ClippedWeights of this layer -> the offline-clipped path."""
         import torch
         T = x.shape[0]
         if y is None:
             y = torch.empty((T, self.desc.d), dtype=self.tdtype, device=self.device)
+        if clipped is not None:
+            flexmoe_layer_forward_clipped(self.desc, T, x, logits, clipped.w_gate_c, clipped.w_up_c,
+                                          clipped.w_down_c, clipped.keep_dev if keep is None else keep,
+                                          clipped.packed_channels, self.ws_gate, self.ws_up,
+                                          self.ws_down, y, self.workspace, dbg=dbg, stream=stream)
+            return y
         flexmoe_layer_forward(self.desc, T, x, logits, self.w_gate, self.w_up, self.w_down,
                               self.keep if keep is None else keep, self.ws_gate, self.ws_up,
                               self.ws_down, y, self.workspace, dbg=dbg, stream=stream)
