@@ -17,7 +17,8 @@ first, uninstrumented pass gives the step time); `cpu_baseline` is
 the CPU oracle timed on a bounded sample of the same workload.  Per-budget
 results (the nested 100/80/60/40/20 % tables) go into `per_budget`, each with
 the same budget run offline (exported as compact weights: the paper's static
-checkpoint mode) and the online/offline throughput ratio.
+checkpoint mode) and the online/offline throughput ratio, and with the
+paper's bucketed kernel design (width groups, aligned widths) as an ablation.
 """
 import argparse
 import hashlib
@@ -54,6 +55,8 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-per-budget", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-baseline work")
+    ap.add_argument("--bucket-align", type=int, default=128,
+                    help="k_align of the bucketed ablation in the per-budget results")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after timing, copy this many MiB device-to-device once, so that a "
                          "counter run sees a plain copy of known size (HBM byte calibration)")
@@ -179,6 +182,23 @@ class Workload:
             kt = fm.flexmoe_timing_read()
             fm.flexmoe_timing_enable(False)
         return ms, kt
+
+    def run_bucketed(self, steps, table_name, k_align):
+        """Time `steps` forwards of the bucketed ablation (width groups, one
+        launch pair each, widths aligned up to k_align)."""
+        torch = self.torch
+        keep = self.tables[table_name]
+        torch.cuda.synchronize()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        ev0.record()
+        for i in range(steps):
+            self.use_copy(i)
+            x, lg = self.xd[i % len(self.xd)]
+            self.layer.forward(x, lg, y=self.y, bucketed=(keep, k_align))
+        ev1.record()
+        torch.cuda.synchronize()
+        return ev0.elapsed_time(ev1)
 
     def export_clipped(self, table_name):
         """Offline clipping: each weight copy packed for one budget."""
@@ -334,15 +354,46 @@ def main():
             wl.run_clipped(2, cws)
             so = wl.run_clipped(steps_b, cws) / steps_b / 1e3
             del cws
+            # the paper's bucketed design (Alg. 2) as an ablation
+            wl.run_bucketed(2, name, args.bucket_align)
+            sk = wl.run_bucketed(steps_b, name, args.bucket_align) / steps_b / 1e3
             per_budget.append(dict(table=name, kept=synth.keep_fraction(wl.tables[name], cfg.I),
                                    ms=sb * 1e3, tokens_per_s=wl.T / sb,
                                    tflops=a["F"] / sb / 1e12,
                                    frac_mfma=a["F"] / sb / 1e12 / peak_flops,
                                    frac_hbm=a["B"] / sb / 1e9 / PEAK_HBM_GBS,
                                    offline_ms=so * 1e3, offline_tokens_per_s=wl.T / so,
-                                   online_over_offline=so / sb))
-            log("[bench]   budget %-7s %.4f ms  %.0f tok/s  %.1f TFLOP/s | offline %.4f ms, online/offline %.3f" %
-                (name, sb * 1e3, wl.T / sb, a["F"] / sb / 1e12, so * 1e3, so / sb))
+                                   online_over_offline=so / sb,
+                                   bucketed_ms=sk * 1e3, bucketed_k_align=args.bucket_align,
+                                   ragged_over_bucketed=sk / sb))
+            log("[bench]   budget %-7s %.4f ms  %.0f tok/s  %.1f TFLOP/s | offline %.4f ms, online/offline %.3f"
+                " | bucketed(%d) %.4f ms, ragged/bucketed %.3f" %
+                (name, sb * 1e3, wl.T / sb, a["F"] / sb / 1e12, so * 1e3, so / sb, args.bucket_align,
+                 sk * 1e3, sk / sb))
+
+    # The bucketed ablation on keep tables drawn from the paper's action set
+    # {0.1, 0.4, 0.7, 1.0} (at most four width groups, as in its deployments).
+    action_ablation = None
+    if not args.no_per_budget and not wl.decode:
+        action_ablation = []
+        levels = [fm.flexmoe_keep_from_ratio(r, cfg.I) for r in synth.ACTION_RATIOS]
+        steps_b = max(5, args.steps // 2)
+        for f in (0.75, 0.5, 0.25):
+            name = "action%d" % int(round(f * 100))
+            wl.tables[name] = synth.action_keep_table(cfg.E, levels, 1000 * cfg.config_id + synth._TID_ACTION,
+                                                      f)
+            wl.keep_dev[name] = fm.to_device(wl.tables[name])
+            wl.run(2, [name])
+            sb = wl.run(steps_b, [name])[0] / steps_b / 1e3
+            wl.run_bucketed(2, name, args.bucket_align)
+            sk = wl.run_bucketed(steps_b, name, args.bucket_align) / steps_b / 1e3
+            widths = sorted(set(int(v) for v in wl.tables[name] if v > 0))
+            action_ablation.append(dict(table=name, kept=synth.keep_fraction(wl.tables[name], cfg.I),
+                                        widths=widths, ragged_ms=sb * 1e3, bucketed_ms=sk * 1e3,
+                                        bucketed_k_align=args.bucket_align, ragged_over_bucketed=sk / sb))
+            log("[bench]   action-set table %-9s kept %.3f widths %s: ragged %.4f ms, bucketed(%d) %.4f ms, "
+                "ragged/bucketed %.3f" % (name, synth.keep_fraction(wl.tables[name], cfg.I), widths, sb * 1e3,
+                                          args.bucket_align, sk * 1e3, sk / sb))
 
     if args.copy_calibration_mib > 0:
         n = args.copy_calibration_mib << 20
@@ -379,6 +430,7 @@ def main():
         "roofline": roof,
         "layer": layer,
         "per_budget": per_budget,
+        "action_set_ablation": action_ablation,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

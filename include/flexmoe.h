@@ -202,6 +202,25 @@ int flexmoe_layer_forward_clipped(const flexmoe_layer_desc *desc, int32_t T, con
                                   size_t workspace_bytes, const flexmoe_route_out *dbg,
                                   void *stream);
 
+/* Bucketed forward (App. C.3, Alg. 2), kept as an ablation of the ragged
+ * design of flexmoe_layer_forward: the routed experts are grouped by retained
+ * width k_e (widest group first), and each group's gate/up and down GEMMs run
+ * as their own launch pair over AlignUp(k_e, k_align) channels (capped at I):
+ * the extra channels are computed with the ranked weights and their
+ * activations zeroed before the down projection, as the paper does.  The
+ * widths are read from keep_host [E] (a host array, validated on the host:
+ * FLEXMOE_EKEEP outside [0, I]); k_align >= 1 (FLEXMOE_EINVAL otherwise).
+ * The workspace of flexmoe_workspace_bytes serves this call too.  Results
+ * equal those of flexmoe_layer_forward with keep_dev = keep_host (the padded
+ * channels contribute exact zeros); every other argument, rule and error is
+ * that of flexmoe_layer_forward. */
+int flexmoe_layer_forward_bucketed(const flexmoe_layer_desc *desc, int32_t T, const void *x,
+                                   const float *logits, const void *w_gate_r, const void *w_up_r,
+                                   const void *w_down_r, const int32_t *keep_host, int32_t k_align,
+                                   const void *ws_gate, const void *ws_up, const void *ws_down,
+                                   void *y, void *workspace, size_t workspace_bytes,
+                                   const flexmoe_route_out *dbg, void *stream);
+
 /* k = ceil(r * I) for a retention ratio r in [0, 1] (Sec. 3.1).  A slack of
  * 1e-9 absorbs the binary representation error of decimal ratios (0.7 * 1000
  * gives 700).  Returns -1 for r outside [0, 1], NaN, or I < 1. */

@@ -48,6 +48,10 @@ struct SegMeta {
     int32_t rows;   // rows of the segment (0 for inactive experts)
     int32_t kk;     // channels of the segment (k_e, or I_shared)
     int32_t ch0;    // clipped weight layout: the expert's first packed channel
+    int32_t kg;     // channels the GEMMs compute: kk, or kk aligned up in the
+                    // bucketed forward (the extra channels' activations are 0)
+    int32_t e;      // routed expert id (-1: the shared expert)
+    int32_t pad[2];
 };
 
 // Channels an expert occupies in the clipped (offline) weight layout: k_e

@@ -74,7 +74,7 @@ int check_desc(const flexmoe_layer_desc* D) {
 }
 
 struct Layout {
-    size_t idx, wts, blockcnt, blockbase, counts, offsets, perm, pos, seg, t1, t2, H, Hs, O, Os;
+    size_t idx, wts, blockcnt, blockbase, counts, offsets, perm, pos, seg, t1, t2, keep, plan, H, Hs, O, Os;
     size_t total;
 };
 
@@ -166,6 +166,8 @@ Layout layout(const flexmoe_layer_desc& D, int T, size_t os_rows) {
     L.seg = take(nseg * sizeof(SegMeta));
     L.t1 = take((nseg + 1) * 4);
     L.t2 = take((nseg + 1) * 4);
+    L.keep = take((size_t)D.E * 4);      // bucketed forward: the uploaded keep table
+    L.plan = take((size_t)D.E * 2 * 4);  // bucketed forward: segment order, GEMM widths
     L.H = take(A * (size_t)D.I * es);
     L.Hs = take((size_t)T * D.I_shared * es);
     const size_t os_es = D.dtype == FLEXMOE_BF16 ? 2 : 4;  // O / Os element size
@@ -361,22 +363,62 @@ namespace {
 // The forward of both weight layouts.  clipped = 0: ranked weights (online
 // clipping, any keep table); clipped = 1: the packed weights of one exported
 // budget, holding packed_limit channels per matrix.
+// The bucketed forward (the paper's Alg. 2 as an ablation of the ragged
+// design): routed experts are grouped by retained width k_e, each group's
+// GEMMs run as their own launch pair and compute AlignUp(k_e, k_align)
+// channels (capped at I), whose extra activations are zeroed.
+struct BucketPlan {
+    std::vector<int> order;   // expert ids, grouped by width (widest first), id ascending inside
+    std::vector<int> kg;      // GEMM width of each expert
+    std::vector<int> start;   // first position in `order` of each group, plus the end
+    std::vector<int> width;   // the group's aligned width
+};
+
+BucketPlan make_plan(const int32_t* keep, int E, int I, int k_align) {
+    BucketPlan b;
+    std::vector<int> ids(E);
+    for (int e = 0; e < E; ++e) ids[e] = e;
+    std::stable_sort(ids.begin(), ids.end(), [&](int a, int c) { return keep[a] > keep[c]; });
+    b.kg.assign(E, 0);
+    for (int i = 0; i < E; ++i) {
+        const int e = ids[i], k = keep[e];
+        b.order.push_back(e);
+        if (k <= 0) continue;  // inactive experts come last and form no group
+        b.kg[e] = std::min(I, (k + k_align - 1) / k_align * k_align);
+        if (i == 0 || keep[ids[i - 1]] != k) {
+            b.start.push_back(i);
+            b.width.push_back(b.kg[e]);
+        }
+    }
+    int end = 0;
+    while (end < E && keep[b.order[end]] > 0) ++end;
+    b.start.push_back(end);
+    return b;
+}
+
 int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const float* logits,
                  const void* w_gate_r, const void* w_up_r, const void* w_down_r, const int32_t* keep_dev,
-                 int clipped, int packed_limit, const void* ws_gate, const void* ws_up,
-                 const void* ws_down, void* y, void* workspace, size_t workspace_bytes,
-                 const flexmoe_route_out* dbg, void* stream) {
+                 int clipped, int packed_limit, const int32_t* bucket_keep, int k_align,
+                 const void* ws_gate, const void* ws_up, const void* ws_down, void* y, void* workspace,
+                 size_t workspace_bytes, const flexmoe_route_out* dbg, void* stream) {
     int rc = check_desc(desc);
     if (rc) return rc;
     const flexmoe_layer_desc& D = *desc;
+    const bool bucketed = bucket_keep != nullptr;
+    if (bucketed) {
+        if (k_align < 1) return fail(FLEXMOE_EINVAL, "k_align = %d must be positive", k_align);
+        for (int e = 0; e < D.E; ++e)
+            if (bucket_keep[e] < 0 || bucket_keep[e] > D.I)
+                return fail(FLEXMOE_EKEEP, "keep[%d] = %d outside [0, I = %d]", e, bucket_keep[e], D.I);
+    }
     if (T < 0) return fail(FLEXMOE_EINVAL, "T = %d is negative", T);
     if (T > D.max_tokens) return fail(FLEXMOE_ESHAPE, "T = %d exceeds max_tokens = %d", T, D.max_tokens);
     if (T == 0) return FLEXMOE_OK;
-    if (!x || !logits || !w_gate_r || !w_up_r || !w_down_r || !keep_dev || !y)
+    if (!x || !logits || !w_gate_r || !w_up_r || !w_down_r || (!keep_dev && !bucketed) || !y)
         return fail(FLEXMOE_EINVAL, "forward: an input/output pointer is NULL");
     for (const void* ptr : {x, w_gate_r, w_up_r, w_down_r, ws_gate, ws_up, ws_down, (const void*)y})
         if (((uintptr_t)ptr) & 15) return fail(FLEXMOE_EINVAL, "x, weights and y must be 16-byte aligned");
-    if (((uintptr_t)logits) & 3 || ((uintptr_t)keep_dev) & 3)
+    if (((uintptr_t)logits) & 3 || (!bucketed && ((uintptr_t)keep_dev) & 3))
         return fail(FLEXMOE_EINVAL, "logits and keep_dev must be 4-byte aligned");
     const bool has_shared = D.I_shared > 0;
     if (has_shared != (ws_gate && ws_up && ws_down) || (!has_shared && (ws_gate || ws_up || ws_down)))
@@ -401,6 +443,23 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
     int32_t* t2 = (int32_t*)(ws + L.t2);
     void* O = ws + L.O;
     void* Os = ws + L.Os;
+    int32_t* plan = nullptr;
+    BucketPlan bp;
+    if (bucketed) {
+        bp = make_plan(bucket_keep, D.E, D.I, k_align);
+        KeepArgs ka, oa, ga;
+        for (int e = 0; e < kMaxExperts; ++e) {
+            ka.v[e] = e < D.E ? bucket_keep[e] : 0;
+            oa.v[e] = e < D.E ? bp.order[e] : 0;
+            ga.v[e] = e < D.E ? bp.kg[e] : 0;
+        }
+        keep_dev = (const int32_t*)(ws + L.keep);
+        plan = (int32_t*)(ws + L.plan);
+        set_plan_kernel<<<1, kMaxExperts, 0, (hipStream_t)stream>>>((int32_t*)(ws + L.keep), plan, ka, oa, ga,
+                                                                     D.E);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return hip_fail(e, "plan upload");
+    }
     const int NB = num_chunks(T);
     const int nseg = D.E + (has_shared ? 1 : 0);
     const bool bf16 = D.dtype == FLEXMOE_BF16;
@@ -424,11 +483,10 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
     const long long g2s = has_shared ? (long long)ceil_div(T, ts.bm2) * ceil_div(D.d, ts.bn2) * parts : 0;
     if (g1r + g1s > 0x7fffffffLL || g2r + g2s > 0x7fffffffLL) return fail(FLEXMOE_ESHAPE, "tile grid too large");
 
-    // The two GEMMs over one part of the tile list, on one stream.
-    auto gemms = [&](int part, hipStream_t st) -> int {
+    // The two GEMMs over one part of the tile list (n1, n2 workgroups), on
+    // one stream.
+    auto gemms = [&](int part, int seg_lo, int seg_hi, long long n1, long long n2, hipStream_t st) -> int {
         const bool sh = part == kPartShared;
-        const int n1 = (int)(sh ? g1s : part == kPartRouted ? g1r : g1r + g1s);
-        const int n2 = (int)(sh ? g2s : part == kPartRouted ? g2r : g2r + g2s);
         const int k1 = sh ? FLEXMOE_K_GATE_UP_SHARED : FLEXMOE_K_GATE_UP;
         const int k2 = sh ? FLEXMOE_K_DOWN_SHARED : FLEXMOE_K_DOWN;
         hipError_t e;
@@ -436,38 +494,38 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
             Gemm1Params<bf16_t> p1{(const bf16_t*)x, (const bf16_t*)w_gate_r, (const bf16_t*)w_up_r,
                                    (const bf16_t*)ws_gate, (const bf16_t*)ws_up, perm, seg, t1,
                                    (bf16_t*)(ws + L.H), (bf16_t*)(ws + L.Hs), D.d, D.I, D.I_shared, D.E,
-                                   D.top_k, nseg, T, part, (int)g1s, clipped};
+                                   D.top_k, nseg, T, part, seg_lo, seg_hi, (int)g1s, clipped};
             {
                 KernelTimer kt(k1, st);
-                e = decode ? launch_gemm1_decode(p1, n1, st) : launch_gemm1_big(p1, n1, st);
+                e = decode ? launch_gemm1_decode(p1, (int)n1, st) : launch_gemm1_big(p1, (int)n1, st);
             }
             if (e != hipSuccess) return hip_fail(e, "gate/up GEMM launch");
             Gemm2Params<bf16_t> p2{(const bf16_t*)(ws + L.H), (const bf16_t*)(ws + L.Hs),
                                    (const bf16_t*)w_down_r, (const bf16_t*)ws_down, seg, t2, (bf16_t*)O,
-                                   (bf16_t*)Os, D.d, D.I, D.I_shared, D.E, nseg, T, ks2, part, (int)g2s,
-                                   clipped};
+                                   (bf16_t*)Os, D.d, D.I, D.I_shared, D.E, nseg, T, ks2, part, seg_lo,
+                                   seg_hi, (int)g2s, clipped};
             {
                 KernelTimer kt(k2, st);
-                e = decode ? launch_gemm2_decode(p2, n2, st) : launch_gemm2_big(p2, n2, st);
+                e = decode ? launch_gemm2_decode(p2, (int)n2, st) : launch_gemm2_big(p2, (int)n2, st);
             }
             if (e != hipSuccess) return hip_fail(e, "down GEMM launch");
         } else {
             Gemm1Params<float> p1{(const float*)x, (const float*)w_gate_r, (const float*)w_up_r,
                                   (const float*)ws_gate, (const float*)ws_up, perm, seg, t1,
                                   (float*)(ws + L.H), (float*)(ws + L.Hs), D.d, D.I, D.I_shared, D.E,
-                                  D.top_k, nseg, T, part, (int)g1s, clipped};
+                                  D.top_k, nseg, T, part, seg_lo, seg_hi, (int)g1s, clipped};
             {
                 KernelTimer kt(k1, st);
-                e = launch_gemm1_f32(p1, n1, st);
+                e = launch_gemm1_f32(p1, (int)n1, st);
             }
             if (e != hipSuccess) return hip_fail(e, "gate/up GEMM launch");
             Gemm2Params<float> p2{(const float*)(ws + L.H), (const float*)(ws + L.Hs),
                                   (const float*)w_down_r, (const float*)ws_down, seg, t2, (float*)O,
-                                  (float*)Os, D.d, D.I, D.I_shared, D.E, nseg, T, 0, part, (int)g2s,
-                                  clipped};
+                                  (float*)Os, D.d, D.I, D.I_shared, D.E, nseg, T, 0, part, seg_lo, seg_hi,
+                                  (int)g2s, clipped};
             {
                 KernelTimer kt(k2, st);
-                e = launch_gemm2_f32(p2, n2, st);
+                e = launch_gemm2_f32(p2, (int)n2, st);
             }
             if (e != hipSuccess) return hip_fail(e, "down GEMM launch");
         }
@@ -490,7 +548,7 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
         if ((err = hipEventRecord(side->fork, s)) != hipSuccess) return hip_fail(err, "fork record");
         if ((err = hipStreamWaitEvent(side->stream, side->fork, 0)) != hipSuccess)
             return hip_fail(err, "fork wait");
-        if ((rc = gemms(kPartShared, side->stream)) != FLEXMOE_OK) return rc;
+        if ((rc = gemms(kPartShared, 0, 0, g1s, g2s, side->stream)) != FLEXMOE_OK) return rc;
         if ((err = hipEventRecord(side->join, side->stream)) != hipSuccess) return hip_fail(err, "join record");
     }
 
@@ -498,8 +556,9 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
         // one workgroup routes and dispatches everything (timed as routing)
         KernelTimer kt(FLEXMOE_K_ROUTE, s);
         dispatch_small_kernel<<<1, 64 * kSmallWaves, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, keep_dev,
-                                                             D.I, D.I_shared, D.d, ts, packed_limit, idx,
-                                                             wts, counts, perm, pos, offsets, seg, t1, t2);
+                                                             D.I, D.I_shared, D.d, ts, packed_limit, plan,
+                                                             idx, wts, counts, perm, pos, offsets, seg, t1,
+                                                             t2);
         err = hipGetLastError();
         if (err != hipSuccess) return hip_fail(err, "dispatch launch");
     } else {
@@ -519,14 +578,30 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
         {
             KernelTimer kt(FLEXMOE_K_DISPATCH_SCATTER, s);
             dispatch_scatter_kernel<<<NB, 64, 0, s>>>(idx, keep_dev, counts, blockbase, T, D.E, D.top_k,
-                                                      D.I, D.I_shared, D.d, NB, ts, packed_limit, perm,
-                                                      pos, offsets, seg, t1, t2);
+                                                      D.I, D.I_shared, D.d, NB, ts, packed_limit, plan,
+                                                      perm, pos, offsets, seg, t1, t2);
             err = hipGetLastError();
         }
         if (err != hipSuccess) return hip_fail(err, "dispatch scatter launch");
     }
 
-    if ((rc = gemms(use_side ? kPartRouted : kPartAll, s)) != FLEXMOE_OK) return rc;
+    const int hs = has_shared ? 1 : 0;
+    if (!bucketed) {
+        if (use_side) rc = gemms(kPartRange, hs, nseg, g1r, g2r, s);
+        else rc = gemms(kPartRange, 0, nseg, g1r + g1s, g2r + g2s, s);
+        if (rc != FLEXMOE_OK) return rc;
+    } else {
+        if (!use_side && has_shared && (rc = gemms(kPartRange, 0, 1, g1s, g2s, s)) != FLEXMOE_OK) return rc;
+        // one launch pair per width group, grids bounded by the group's size
+        for (size_t b = 0; b + 1 < bp.start.size(); ++b) {
+            const int nb = bp.start[b + 1] - bp.start[b];
+            const long long r1 = std::min(routed_row_tiles_ub(T, D.E, D.top_k, ts.bm1), (long long)nb * ceil_div(T, ts.bm1));
+            const long long r2 = std::min(routed_row_tiles_ub(T, D.E, D.top_k, ts.bm2), (long long)nb * ceil_div(T, ts.bm2));
+            rc = gemms(kPartRange, hs + bp.start[b], hs + bp.start[b + 1], r1 * ceil_div(bp.width[b], ts.bn1),
+                       r2 * ceil_div(D.d, ts.bn2), s);
+            if (rc != FLEXMOE_OK) return rc;
+        }
+    }
     if (use_side) {
         if ((err = hipStreamWaitEvent(s, side->join, 0)) != hipSuccess) return hip_fail(err, "join wait");
         side_lock.unlock();
@@ -578,8 +653,8 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
                           const void* w_down_r, const int32_t* keep_dev, const void* ws_gate,
                           const void* ws_up, const void* ws_down, void* y, void* workspace,
                           size_t workspace_bytes, const flexmoe_route_out* dbg, void* stream) {
-    return forward_impl(desc, T, x, logits, w_gate_r, w_up_r, w_down_r, keep_dev, 0, 0x7fffffff, ws_gate,
-                        ws_up, ws_down, y, workspace, workspace_bytes, dbg, stream);
+    return forward_impl(desc, T, x, logits, w_gate_r, w_up_r, w_down_r, keep_dev, 0, 0x7fffffff, nullptr, 0,
+                        ws_gate, ws_up, ws_down, y, workspace, workspace_bytes, dbg, stream);
 }
 
 int64_t flexmoe_clipped_channels(const flexmoe_layer_desc* desc, const int32_t* keep_host) {
@@ -617,7 +692,18 @@ int flexmoe_layer_forward_clipped(const flexmoe_layer_desc* desc, int32_t T, con
     if (packed_channels < 0 || packed_channels > (long long)desc->E * packed_width(desc->I))
         return fail(FLEXMOE_EINVAL, "packed_channels = %lld outside [0, E * ceil8(I)]", (long long)packed_channels);
     return forward_impl(desc, T, x, logits, w_gate_c, w_up_c, w_down_c, keep_dev, 1, (int)packed_channels,
-                        ws_gate, ws_up, ws_down, y, workspace, workspace_bytes, dbg, stream);
+                        nullptr, 0, ws_gate, ws_up, ws_down, y, workspace, workspace_bytes, dbg, stream);
+}
+
+int flexmoe_layer_forward_bucketed(const flexmoe_layer_desc* desc, int32_t T, const void* x,
+                                   const float* logits, const void* w_gate_r, const void* w_up_r,
+                                   const void* w_down_r, const int32_t* keep_host, int32_t k_align,
+                                   const void* ws_gate, const void* ws_up, const void* ws_down, void* y,
+                                   void* workspace, size_t workspace_bytes, const flexmoe_route_out* dbg,
+                                   void* stream) {
+    if (!keep_host) return fail(FLEXMOE_EINVAL, "keep_host is NULL");
+    return forward_impl(desc, T, x, logits, w_gate_r, w_up_r, w_down_r, nullptr, 0, 0x7fffffff, keep_host,
+                        k_align, ws_gate, ws_up, ws_down, y, workspace, workspace_bytes, dbg, stream);
 }
 
 }  // extern "C"

@@ -124,8 +124,6 @@ __device__ __forceinline__ void sched_interleave() {
 template <bool kGateUp>
 __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Gemm2Params<bf16_t>& p2,
                                          unsigned char* smem) {
-    const int E = kGateUp ? p1.E : p2.E;
-    const int nseg = kGateUp ? p1.nseg : p2.nseg;
     const int d = kGateUp ? p1.d : p2.d;
 
     // tile numbering: XCD x = b % 8 takes groups of XCD_GROUP consecutive tiles
@@ -140,8 +138,7 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
     // those of chunk split-1 (routed segments and gate/up: split 0)
     const int nt = kGateUp ? 0x7fffffff : ceil_div(d, BN);
     const int ntile = (local / mt) % nt, split = (local / mt) / nt;
-    const int hs = nseg - E;  // 1 if segment 0 is the shared expert
-    const bool shared = s < hs;
+    const bool shared = sm.e < 0;
 
     // the wave index is uniform: keeping it in a scalar register makes every
     // LDS destination address (M0) scalar arithmetic
@@ -161,7 +158,7 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
     __amdgpu_buffer_rsrc_t ra, rb;
     if constexpr (kGateUp) {
         K = d;
-        const RoutedWeights rw = shared ? RoutedWeights{0, p1.Is, 0} : routed_weights(p1, s - hs, sm);
+        const RoutedWeights rw = shared ? RoutedWeights{0, p1.Is, 0} : routed_weights(p1, sm);
         // this wave's B rows are all gate rows or all up rows
         const bf16_t* W = (wave * ROWS_PER_WAVE < BN / 2 ? (shared ? p1.sg : p1.wg) : (shared ? p1.su : p1.wu)) + rw.base;
         ra = make_rsrc(p1.x, (size_t)p1.tokens * d);
@@ -180,12 +177,12 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
                 aoff[i] = (uint32_t)(((size_t)t * d + c) * 2);
             }
             const int ch = ntile * (BN / 2) + (r & (BN / 2 - 1));
-            boff[i] = ch < sm.kk ? (uint32_t)(((size_t)ch * d + c) * 2) : kOOB;
+            boff[i] = ch < sm.kg ? (uint32_t)(((size_t)ch * d + c) * 2) : kOOB;
         }
     } else {
         const int kbeg = shared && p2.ks2 > 0 ? split * p2.ks2 : 0;
-        K = shared && p2.ks2 > 0 ? min(sm.kk - kbeg, p2.ks2) : sm.kk;
-        const RoutedWeights rw = shared ? RoutedWeights{0, 0, p2.Is} : routed_weights(p2, s - hs, sm);
+        K = shared && p2.ks2 > 0 ? min(sm.kg - kbeg, p2.ks2) : sm.kg;
+        const RoutedWeights rw = shared ? RoutedWeights{0, 0, p2.Is} : routed_weights(p2, sm);
         const int ldh = shared ? p2.Is : p2.I;  // H row stride
         const int ldw = rw.ldd;                 // W_down row stride
         const int hrows = shared ? p2.tokens : sm.rows;
@@ -317,9 +314,11 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
         if constexpr (kGateUp) {
             bf16_t* Hb = shared ? p1.Hs : p1.H + (size_t)sm.row0 * p1.I;
             const int ldh = shared ? p1.Is : p1.I;
-            // chunk-aligned end: [kk, kk8) is zero-filled; kk8 and the runs are
-            // multiples of 8 and 4, so a run is wholly inside or outside
-            const int kk8 = min((sm.kk + 7) & ~7, ldh);
+            // channels [kk, kk8) are written as zeros, kk8 = the GEMM width
+            // rounded up to 8 (the down GEMM reads whole 16-byte chunks); kk8
+            // and the runs are multiples of 8 and 4, so a run is wholly inside
+            // or outside
+            const int kk8 = min((sm.kg + 7) & ~7, ldh);
 #pragma unroll
             for (int i = 0; i < MFW; ++i) {
                 const int row = row_l + i * 32;

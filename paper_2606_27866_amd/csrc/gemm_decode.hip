@@ -67,15 +67,14 @@ __global__ __launch_bounds__(64 * DWAVES) void gemm1_decode_kernel(Gemm1Params<b
     int s, ntile;  // one row tile per segment (rows <= 64): the local tile is the channel tile
     SegMeta sm;
     if (!tile_of(p, blockIdx.x, s, sm, ntile)) return;  // workgroup-uniform
-    const int hs = p.nseg - p.E;
-    const bool shared = s < hs;
-    const size_t wofs = shared ? 0 : routed_weights(p, s - hs, sm).base;
+    const bool shared = sm.e < 0;
+    const size_t wofs = shared ? 0 : routed_weights(p, sm).base;
     const bf16_t* Wg = (shared ? p.sg : p.wg) + wofs;
     const bf16_t* Wu = (shared ? p.su : p.wu) + wofs;
     const int d = p.d;
     const int g = lane >> 4;  // K group of this lane
     const int c = ntile * DCH + (lane & 15);
-    const bool cval = c < sm.kk;
+    const bool cval = c < sm.kg;  // channels the GEMM computes
     const int nf = ceil_div(sm.rows, 16);  // 1..4 token blocks
 
     const bf16_t* xrow[4];
@@ -123,7 +122,7 @@ __global__ __launch_bounds__(64 * DWAVES) void gemm1_decode_kernel(Gemm1Params<b
     // D[m][n]: lane holds channels m = 4*(lane/16) + i of token n = lane%16
     bf16_t* Hb = shared ? p.Hs : p.H + (size_t)sm.row0 * p.I;
     const int ldh = shared ? p.Is : p.I;
-    const int kk8 = min((sm.kk + 7) & ~7, ldh);
+    const int kk8 = min((sm.kg + 7) & ~7, ldh);  // [kk, kk8) written as zeros
 #pragma unroll
     for (int f = 0; f < 4; ++f) {
         if (f >= nf) break;
@@ -147,14 +146,13 @@ __global__ __launch_bounds__(64 * DWAVES) void gemm2_decode_kernel(Gemm2Params<b
     const int d = p.d;
     const int nt = ceil_div(d, DCH);
     const int split = local / nt, ntile = local % nt;  // split > 0 only for the shared expert
-    const int hs = p.nseg - p.E;
-    const bool shared = s < hs;
-    const RoutedWeights rw = shared ? RoutedWeights{0, 0, p.Is} : routed_weights(p, s - hs, sm);
+    const bool shared = sm.e < 0;
+    const RoutedWeights rw = shared ? RoutedWeights{0, 0, p.Is} : routed_weights(p, sm);
     const int ldh = shared ? p.Is : p.I;  // H row stride
     const bf16_t* Hb = shared ? p.Hs : p.H + (size_t)sm.row0 * p.I;
     const bf16_t* Wd = shared ? p.sd : p.wd + rw.base;
     const int kbeg = shared ? split * p.ks2 : 0;
-    const int kend = shared ? min(sm.kk, kbeg + p.ks2) : sm.kk;
+    const int kend = shared ? min(sm.kg, kbeg + p.ks2) : sm.kg;
     const int g = lane >> 4;
     const int n = ntile * DCH + (lane & 15);
     const bool nval = n < d;

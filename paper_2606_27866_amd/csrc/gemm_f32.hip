@@ -19,9 +19,8 @@ __global__ __launch_bounds__(256) void gemm1_f32_kernel(Gemm1Params<float> p) {
     if (!tile_of(p, blockIdx.x, s, sm, local)) return;
     const int mt = ceil_div(sm.rows, BM);
     const int mtile = local % mt, ntile = local / mt;
-    const int hs = p.nseg - p.E;  // 1 if segment 0 is the shared expert
-    const bool shared = s < hs;
-    const size_t wofs = shared ? 0 : routed_weights(p, s - hs, sm).base;
+    const bool shared = sm.e < 0;
+    const size_t wofs = shared ? 0 : routed_weights(p, sm).base;
     const float* Wg = (shared ? p.sg : p.wg) + wofs;
     const float* Wu = (shared ? p.su : p.wu) + wofs;
 
@@ -34,8 +33,8 @@ __global__ __launch_bounds__(256) void gemm1_f32_kernel(Gemm1Params<float> p) {
         asrc = p.x + (size_t)t * p.d;
     }
     const int ch = ntile * BN + lr;
-    const float* gsrc = ch < sm.kk ? Wg + (size_t)ch * p.d : nullptr;
-    const float* usrc = ch < sm.kk ? Wu + (size_t)ch * p.d : nullptr;
+    const float* gsrc = ch < sm.kg ? Wg + (size_t)ch * p.d : nullptr;  // channels the GEMM computes
+    const float* usrc = ch < sm.kg ? Wu + (size_t)ch * p.d : nullptr;
 
     const int ty = tid >> 4, tx = tid & 15;
     float ag[4][4] = {}, au[4][4] = {};
@@ -77,9 +76,9 @@ __global__ __launch_bounds__(256) void gemm1_f32_kernel(Gemm1Params<float> p) {
         for (int j = 0; j < 4; ++j) {
             const int r = mtile * BM + ty * 4 + i;
             const int c = ntile * BN + tx * 4 + j;
-            if (r < sm.rows && c < sm.kk) {
+            if (r < sm.rows && c < sm.kg) {  // channels [kk, kg) are written as zeros
                 const float g = ag[i][j];
-                Hb[(size_t)r * ldh + c] = g / (1.0f + expf(-g)) * au[i][j];
+                Hb[(size_t)r * ldh + c] = c < sm.kk ? g / (1.0f + expf(-g)) * au[i][j] : 0.0f;
             }
         }
 }
@@ -92,13 +91,12 @@ __global__ __launch_bounds__(256) void gemm2_f32_kernel(Gemm2Params<float> p) {
     if (!tile_of(p, blockIdx.x, s, sm, local)) return;
     const int mt = ceil_div(sm.rows, BM);
     const int mtile = local % mt, ntile = local / mt;
-    const int hs = p.nseg - p.E;  // 1 if segment 0 is the shared expert
-    const bool shared = s < hs;
+    const bool shared = sm.e < 0;
     const float* Hb = shared ? p.Hs : p.H + (size_t)sm.row0 * p.I;
-    const RoutedWeights rw = shared ? RoutedWeights{0, 0, p.Is} : routed_weights(p, s - hs, sm);
+    const RoutedWeights rw = shared ? RoutedWeights{0, 0, p.Is} : routed_weights(p, sm);
     const int ldh = shared ? p.Is : p.I;  // H row stride
     const float* Wd = shared ? p.sd : p.wd + rw.base;
-    const int K = sm.kk;
+    const int K = sm.kg;
 
     const int tid = threadIdx.x;
     const int lr = tid >> 2, lk = (tid & 3) * 4;

@@ -15,9 +15,8 @@ struct KeepArgs {
 // so its GEMMs can run on a second stream while the routed experts are being
 // dispatched; each launch then covers one part of the tile list.
 enum GemmPart : int32_t {
-    kPartAll = 0,     // every segment (tiles 0 .. tstart[nseg])
-    kPartShared = 1,  // the shared expert alone; its tile count comes from the host
-    kPartRouted = 2   // the routed experts (tiles tstart[hs] .. tstart[nseg])
+    kPartRange = 0,   // segments [seg_lo, seg_hi) (tiles tstart[seg_lo] .. tstart[seg_hi])
+    kPartShared = 1   // the shared expert alone; its tile count comes from the host
 };
 
 // Gate/up GEMM with fused SwiGLU:
@@ -37,6 +36,7 @@ struct Gemm1Params {
     T* Hs;                      // shared activations [T][I_s]
     int d, I, Is, E, top_k, nseg, tokens;
     int part;                   // GemmPart
+    int seg_lo, seg_hi;         // kPartRange: the segments covered
     int shared_tiles;           // tiles of the shared segment (kPartShared)
     int clipped;                // routed weights in the clipped layout (see RoutedWeights)
 };
@@ -58,6 +58,7 @@ struct Gemm2Params {
     int d, I, Is, E, nseg, tokens;
     int ks2;                    // > 0: the shared reduction is split into chunks of ks2 channels
     int part;                   // GemmPart
+    int seg_lo, seg_hi;         // kPartRange: the segments covered
     int shared_tiles;           // tiles of the shared segment (kPartShared)
     int clipped;                // routed weights in the clipped layout (see RoutedWeights)
 };
@@ -75,26 +76,27 @@ struct RoutedWeights {
     int ldd;       // elements per down row
 };
 template <typename P>
-__device__ __forceinline__ RoutedWeights routed_weights(const P& p, int e, const SegMeta& sm) {
+__device__ __forceinline__ RoutedWeights routed_weights(const P& p, const SegMeta& sm) {
     if (p.clipped) return RoutedWeights{(size_t)sm.ch0 * p.d, packed_width(sm.kk), packed_width(sm.kk)};
-    return RoutedWeights{(size_t)e * p.I * p.d, p.I, p.I};
+    return RoutedWeights{(size_t)sm.e * p.I * p.d, p.I, p.I};
 }
 
 // Tile L of a launch -> segment s, its metadata and the tile's index inside
 // the segment.  False when L is past the launch's last tile (the caller's
 // workgroup then has nothing to do).  The shared segment's metadata is known
-// without the dispatch tables: rows = tokens, channels = I_s.
+// without the dispatch tables: rows = tokens, channels = I_s.  The shared
+// expert, when present, is always segment 0.
 template <typename P>
 __device__ __forceinline__ bool tile_of(const P& p, int L, int& s, SegMeta& sm, int& local) {
     if (p.part == kPartShared) {
         if (L >= p.shared_tiles) return false;
         s = 0;
-        sm = SegMeta{0, p.tokens, p.Is, 0};
+        sm = SegMeta{0, p.tokens, p.Is, 0, p.Is, -1, {0, 0}};
         local = L;
         return true;
     }
-    if (p.part == kPartRouted) L += p.tstart[p.nseg - p.E];
-    if (L >= p.tstart[p.nseg]) return false;
+    L += p.tstart[p.seg_lo];
+    if (L >= p.tstart[p.seg_hi]) return false;
     s = find_segment(p.tstart, p.nseg, L);
     sm = p.seg[s];
     local = L - p.tstart[s];
@@ -114,16 +116,21 @@ __global__ void dispatch_scan_kernel(const int32_t* blockcnt, int NB, int32_t* b
                                      int32_t* counts);
 // `packed_limit`: in the clipped layout, the packed channels the weight
 // buffers hold; an expert whose block would reach past it is treated as
-// k_e = 0 (the ranked layout passes INT32_MAX).
+// k_e = 0 (the ranked layout passes INT32_MAX).  `plan` (NULL: experts in id
+// order, GEMM width = k_e): the bucketed forward's segment order plan[0..E)
+// (expert ids) and GEMM widths plan[E..2E).
+__global__ void set_plan_kernel(int32_t* keep, int32_t* plan, KeepArgs k, KeepArgs order, KeepArgs kg, int E);
 __global__ void dispatch_scatter_kernel(const int32_t* idx, const int32_t* keep,
                                         const int32_t* counts, const int32_t* blockbase, int T,
                                         int E, int k, int I, int I_shared, int d, int NB,
-                                        TileShape ts, int packed_limit, int32_t* perm, int32_t* pos,
+                                        TileShape ts, int packed_limit, const int32_t* plan,
+                                        int32_t* perm, int32_t* pos,
                                         int32_t* offsets, SegMeta* seg, int32_t* t1start,
                                         int32_t* t2start);
 __global__ void dispatch_small_kernel(const float* logits, int T, int E, int k, int norm_topk,
                                       const int32_t* keep, int I, int I_shared, int d, TileShape ts,
-                                      int packed_limit, int32_t* idx, float* wts, int32_t* counts,
+                                      int packed_limit, const int32_t* plan, int32_t* idx, float* wts,
+                                      int32_t* counts,
                                       int32_t* perm, int32_t* pos, int32_t* offsets, SegMeta* seg,
                                       int32_t* t1start, int32_t* t2start);
 __global__ void set_keep_kernel(int32_t* keep, KeepArgs t, int E);

@@ -155,8 +155,9 @@ __device__ __forceinline__ int expert_offsets(CountFn count, const int32_t* __re
 // reductions, so they start first) and the exclusive scans of both GEMMs'
 // tile counts, 64 segments per round.
 template <typename CountFn>
-__device__ void write_tables(CountFn count, const int* off, const int* kk_s, const int* ch0, int P,
-                             int T, int E, int I_shared, int d, TileShape ts, int32_t* __restrict__ offsets,
+__device__ void write_tables(CountFn count, const int* off, const int* kk_s, const int* ch0,
+                             const int32_t* __restrict__ plan, int P, int T, int E, int I,
+                             int I_shared, int d, TileShape ts, int32_t* __restrict__ offsets,
                              SegMeta* __restrict__ seg, int32_t* __restrict__ t1start,
                              int32_t* __restrict__ t2start) {
     const int lane = threadIdx.x & 63;
@@ -168,26 +169,32 @@ __device__ void write_tables(CountFn count, const int* off, const int* kk_s, con
         int n1 = 0, n2 = 0;
         if (s < nseg) {
             SegMeta m;
+            m.pad[0] = m.pad[1] = 0;
             if (s < hs) {
                 m.row0 = 0;
                 m.rows = T;
                 m.kk = I_shared;
                 m.ch0 = 0;
+                m.kg = I_shared;
+                m.e = -1;
             } else {
-                const int e = s - hs;
+                // plan entries are device data: clamped so that addressing stays in range
+                const int e = plan ? min(max(plan[s - hs], 0), E - 1) : s - hs;
                 m.row0 = off[e];
                 m.rows = kk_s[e] > 0 ? count(e) : 0;
                 m.kk = kk_s[e];
                 m.ch0 = ch0[e];
-                offsets[e] = off[e];
+                m.kg = plan && m.kk > 0 ? min(max(plan[E + e], m.kk), I) : m.kk;
+                m.e = e;
             }
             seg[s] = m;
             if (m.rows > 0 && m.kk > 0) {
-                n1 = ceil_div(m.rows, ts.bm1) * ceil_div(m.kk, ts.bn1);
+                n1 = ceil_div(m.rows, ts.bm1) * ceil_div(m.kg, ts.bn1);
                 n2 = ceil_div(m.rows, ts.bm2) * ceil_div(d, ts.bn2);
                 if (s < hs && ts.ks2 > 0) n2 *= ceil_div(m.kk, ts.ks2);
             }
         }
+        if (s >= hs && s < nseg) offsets[s - hs] = off[s - hs];
         const int i1 = wave_incl_scan(n1), i2 = wave_incl_scan(n2);
         if (s < nseg) {
             t1start[s] = c1 + i1 - n1;
@@ -312,7 +319,8 @@ __global__ __launch_bounds__(256) void dispatch_scan_kernel(const int32_t* __res
 __global__ __launch_bounds__(64) void dispatch_scatter_kernel(
     const int32_t* __restrict__ idx, const int32_t* __restrict__ keep,
     const int32_t* __restrict__ counts, const int32_t* __restrict__ blockbase, int T, int E, int k,
-    int I, int I_shared, int d, int NB, TileShape ts, int packed_limit, int32_t* __restrict__ perm,
+    int I, int I_shared, int d, int NB, TileShape ts, int packed_limit, const int32_t* __restrict__ plan,
+    int32_t* __restrict__ perm,
     int32_t* __restrict__ pos, int32_t* __restrict__ offsets, SegMeta* __restrict__ seg,
     int32_t* __restrict__ t1start, int32_t* __restrict__ t2start) {
     __shared__ int off[kMaxExperts];
@@ -323,7 +331,7 @@ __global__ __launch_bounds__(64) void dispatch_scatter_kernel(
     const int P = expert_offsets(count, keep, E, I, packed_limit, off, kk_s, ch0, run);
     __syncthreads();
     if (blockIdx.x == 0)
-        write_tables(count, off, kk_s, ch0, P, T, E, I_shared, d, ts, offsets, seg, t1start, t2start);
+        write_tables(count, off, kk_s, ch0, plan, P, T, E, I, I_shared, d, ts, offsets, seg, t1start, t2start);
     const int a0 = blockIdx.x * kRouteTokens * k;
     const int a1 = min((blockIdx.x + 1) * kRouteTokens, T) * k;
     auto base = [&](int e) { return off[e] + blockbase[(size_t)e * NB + blockIdx.x]; };
@@ -338,7 +346,8 @@ __global__ __launch_bounds__(64) void dispatch_scatter_kernel(
 __global__ __launch_bounds__(64 * kSmallWaves) void dispatch_small_kernel(
     const float* __restrict__ logits, int T, int E, int k, int norm_topk,
     const int32_t* __restrict__ keep, int I, int I_shared, int d, TileShape ts, int packed_limit,
-    int32_t* __restrict__ idx, float* __restrict__ wts, int32_t* __restrict__ counts,
+    const int32_t* __restrict__ plan, int32_t* __restrict__ idx, float* __restrict__ wts,
+    int32_t* __restrict__ counts,
     int32_t* __restrict__ perm, int32_t* __restrict__ pos, int32_t* __restrict__ offsets,
     SegMeta* __restrict__ seg, int32_t* __restrict__ t1start, int32_t* __restrict__ t2start) {
     __shared__ int hist[kSmallWaves][kMaxExperts];  // per-wave counts, then per-wave bases
@@ -389,7 +398,7 @@ __global__ __launch_bounds__(64 * kSmallWaves) void dispatch_small_kernel(
         const int P = expert_offsets(count, keep, E, I, packed_limit, off, kk_s, ch0, run);
         __builtin_amdgcn_wave_barrier();
         __atomic_signal_fence(__ATOMIC_SEQ_CST);
-        write_tables(count, off, kk_s, ch0, P, T, E, I_shared, d, ts, offsets, seg, t1start, t2start);
+        write_tables(count, off, kk_s, ch0, plan, P, T, E, I, I_shared, d, ts, offsets, seg, t1start, t2start);
     }
     __syncthreads();
     // this wave's running position inside each expert starts at its base
@@ -400,6 +409,16 @@ __global__ __launch_bounds__(64 * kSmallWaves) void dispatch_small_kernel(
 __global__ void set_keep_kernel(int32_t* __restrict__ keep, KeepArgs t, int E) {
     const int e = threadIdx.x;
     if (e < E) keep[e] = t.v[e];
+}
+
+__global__ void set_plan_kernel(int32_t* __restrict__ keep, int32_t* __restrict__ plan, KeepArgs k,
+                                KeepArgs order, KeepArgs kg, int E) {
+    const int e = threadIdx.x;
+    if (e < E) {
+        keep[e] = k.v[e];
+        plan[e] = order.v[e];
+        plan[E + e] = kg.v[e];
+    }
 }
 
 }  // namespace flexmoe

@@ -31,7 +31,8 @@ ERRORS = {
 EXPORTED = ("flexmoe_workspace_bytes", "flexmoe_rank_reorder", "flexmoe_set_budget",
             "flexmoe_layer_forward", "flexmoe_keep_from_ratio", "flexmoe_last_error",
             "flexmoe_timing_enable", "flexmoe_timing_read", "flexmoe_clipped_channels",
-            "flexmoe_export_clipped", "flexmoe_layer_forward_clipped")
+            "flexmoe_export_clipped", "flexmoe_layer_forward_clipped",
+            "flexmoe_layer_forward_bucketed")
 
 # kernel indices of flexmoe_kernel_times
 KERNELS = ("route", "dispatch_scan", "dispatch_scatter", "gate_up", "down", "combine",
@@ -91,6 +92,9 @@ def lib():
         L.flexmoe_layer_forward_clipped.argtypes = ([D, i32] + [vp] * 6 + [ctypes.c_int64] + [vp] * 5
                                                     + [sz, ctypes.POINTER(flexmoe_route_out), vp])
         L.flexmoe_layer_forward_clipped.restype = ctypes.c_int
+        L.flexmoe_layer_forward_bucketed.argtypes = ([D, i32] + [vp] * 6 + [i32] + [vp] * 5
+                                                     + [sz, ctypes.POINTER(flexmoe_route_out), vp])
+        L.flexmoe_layer_forward_bucketed.restype = ctypes.c_int
         L.flexmoe_keep_from_ratio.argtypes = [ctypes.c_double, i32]
         L.flexmoe_keep_from_ratio.restype = ctypes.c_int
         L.flexmoe_timing_enable.argtypes = [ctypes.c_int]
@@ -213,6 +217,22 @@ def flexmoe_layer_forward_clipped(desc, T, x, logits, w_gate_c, w_up_c, w_down_c
         _stream(stream)))
 
 
+def flexmoe_layer_forward_bucketed(desc, T, x, logits, w_gate_r, w_up_r, w_down_r, keep_host, k_align,
+                                   ws_gate, ws_up, ws_down, y, workspace, workspace_bytes=None,
+                                   dbg=None, stream=None):
+    if workspace_bytes is None:
+        workspace_bytes = workspace.numel() * workspace.element_size()
+    kh = np.ascontiguousarray(np.asarray(keep_host, dtype=np.int32))
+    ro = None
+    if dbg:
+        ro = flexmoe_route_out(*[_p(dbg.get(n)) for n, _ in flexmoe_route_out._fields_])
+    _check(lib().flexmoe_layer_forward_bucketed(
+        ctypes.byref(desc), int(T), _p(x), _p(logits), _p(w_gate_r), _p(w_up_r), _p(w_down_r),
+        kh.ctypes.data_as(ctypes.c_void_p), int(k_align), _p(ws_gate), _p(ws_up), _p(ws_down), _p(y),
+        _p(workspace), int(workspace_bytes), ctypes.byref(ro) if ro is not None else None,
+        _stream(stream)))
+
+
 class ClippedWeights:
     """The packed weights of one exported budget (offline clipping) and its
     device keep table."""
@@ -261,12 +281,19 @@ class Layer:
         keep_dev = torch.from_numpy(np.asarray(keep_host, dtype=np.int32).copy()).to(self.device)
         return ClippedWeights(keep_host, *bufs, P, keep_dev)
 
-    def forward(self, x, logits, y=None, keep=None, dbg=None, stream=None, clipped=None):
-        """clipped: a ClippedWeights of this layer -> the offline-clipped path."""
+    def forward(self, x, logits, y=None, keep=None, dbg=None, stream=None, clipped=None,
+                bucketed=None):
+        """clipped: a ClippedWeights of this layer -> the offline-clipped path;
+        bucketed: (keep_host, k_align) -> the bucketed ablation."""
         import torch
         T = x.shape[0]
         if y is None:
             y = torch.empty((T, self.desc.d), dtype=self.tdtype, device=self.device)
+        if bucketed is not None:
+            flexmoe_layer_forward_bucketed(self.desc, T, x, logits, self.w_gate, self.w_up, self.w_down,
+                                           bucketed[0], bucketed[1], self.ws_gate, self.ws_up,
+                                           self.ws_down, y, self.workspace, dbg=dbg, stream=stream)
+            return y
         if clipped is not None:
             flexmoe_layer_forward_clipped(self.desc, T, x, logits, clipped.w_gate_c, clipped.w_up_c,
                                           clipped.w_down_c, clipped.keep_dev if keep is None else keep,

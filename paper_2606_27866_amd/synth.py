@@ -304,6 +304,34 @@ def quarter_keep_table(E: int, I: int, seed: int, mean_quarters: int = 2) -> np.
     return (q * (I // 4)).astype(np.int32)
 
 
+# The paper's discrete action set of retention ratios (Sec. 4.1).
+ACTION_RATIOS = (0.1, 0.4, 0.7, 1.0)
+_TID_ACTION = 15
+
+
+def action_keep_table(E: int, levels, seed: int, kept_fraction: float) -> np.ndarray:
+    """Keep table whose widths come from a discrete action set.
+
+    `levels` are the channel counts of the actions, ascending (the caller
+    maps the ratios to widths).  Every expert starts at the widest action;
+    seeded-uniform experts above the narrowest action step down one action
+    at a time until the kept fraction sum(k) / (E * max(levels)) is at most
+    `kept_fraction` (or every expert is at the narrowest action).
+    """
+    levels = [int(v) for v in levels]
+    g = np.random.Generator(np.random.PCG64(seed))
+    a = np.full(E, len(levels) - 1, dtype=np.int64)
+    full = E * levels[-1]
+
+    def kept():
+        return sum(levels[i] for i in a) / full
+
+    while kept() > kept_fraction and (a > 0).any():
+        live = np.nonzero(a > 0)[0]
+        a[live[g.integers(0, live.size)]] -= 1
+    return np.array([levels[i] for i in a], dtype=np.int32)
+
+
 def tiny_keep_table(E: int, I: int, seed: int) -> np.ndarray:
     """Arbitrary integers in [0, I] that include 0, I and non-tile multiples."""
     g = np.random.Generator(np.random.PCG64(seed))

@@ -1,0 +1,69 @@
+"""The bucketed forward (App. C.3, Alg. 2) kept as an ablation of the ragged
+design: width groups, one launch pair per group, aligned-up widths whose
+extra activations are zeroed.  Its results must be those of the masked layer
+(the padded channels contribute exact zeros), so on the GPU it is checked
+against the ragged forward (same bits) and the oracle.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_27866_amd import flexmoe as fm
+from paper_2606_27866_amd import synth
+from tests.gpu_util import BF16_TOL, F32_TOL, check_y, mini_layer, say
+
+
+def test_bucketed_rejects_bad_arguments_on_host():
+    desc = fm.make_desc(24, 8, 40, 2, 0, fm.FLEXMOE_BF16, 1, 16)
+    for keep, align, code in (([41] + [0] * 7, 64, -3), ([-1] + [0] * 7, 64, -3), ([8] * 8, 0, -1)):
+        with pytest.raises(fm.FlexMoEError) as ei:
+            fm.flexmoe_layer_forward_bucketed(desc, 1, 0x1000, 0x1000, 0x1000, 0x1000, 0x1000, keep, align,
+                                              None, None, None, 0x1000, 0x1000, workspace_bytes=1 << 30,
+                                              stream=0)
+        assert ei.value.code == code
+
+
+CASES = [
+    # name, T, d, E, I, k, I_s, dtype, norm
+    ("b_f32", 60, 64, 8, 96, 2, 32, synth.F32, 1),
+    ("b_prefill", 300, 256, 8, 320, 2, 0, synth.BF16, 1),
+    ("b_prefill_shared", 200, 512, 16, 192, 4, 256, synth.BF16, 0),
+    ("b_decode", 8, 256, 16, 200, 4, 128, synth.BF16, 0),
+]
+
+
+def case_keeps(E, I, seed):
+    rng = np.random.default_rng(seed)
+    # few distinct widths (a discrete action set) and some arbitrary ones
+    grid = np.array([0, I // 4, I // 2, I], np.int32)
+    return [grid[rng.integers(0, 4, size=E)], rng.integers(0, I + 1, size=E).astype(np.int32),
+            np.full(E, I, np.int32)]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("align", [1, 64, 128, 256])
+@pytest.mark.parametrize("spec", CASES, ids=[c[0] for c in CASES])
+def test_gpu_bucketed_equals_ragged_and_oracle(spec, align):
+    import torch
+    name, T, d, E, I, k, I_s, dtype, norm = spec
+    cfg, x, lg, w, s = mini_layer(name, T, d, E, I, k, I_s, dtype=dtype, norm=norm,
+                                  config_id=150 + CASES.index(spec))
+    layer = fm.Layer(d, E, I, k, I_s, dtype, norm, max_tokens=T)
+    layer.set_weights(*[fm.to_device(a) if a is not None else None for a in (*w, *s)])
+    xd, ld = fm.to_device(x), fm.to_device(lg)
+    for keep in case_keeps(E, I, 3 + CASES.index(spec)):
+        say(name, "align", align, "keep", keep.tolist())
+        layer.set_budget(keep)
+        y_r = layer.forward(xd, ld)
+        y_b = layer.forward(xd, ld, bucketed=(keep, align))
+        torch.cuda.synchronize()
+        hr, hb = fm.to_host(y_r), fm.to_host(y_b)
+        # exact zeros added to the reductions: the same values (up to the sign of a zero)
+        if hr.dtype == np.uint16:
+            canon = lambda v: np.where((v & 0x7FFF) == 0, 0, v)
+        else:
+            canon = lambda v: np.where(v == 0, 0.0, v)
+        assert np.array_equal(canon(hr), canon(hb))
+        ref = oracle.layer_forward(x, lg, *w, keep, k, norm, *s)
+        yb = synth.bf16_bits_to_f32(hb).astype(np.float64) if dtype == synth.BF16 else hb.astype(np.float64)
+        check_y(yb, ref, BF16_TOL if dtype == synth.BF16 else F32_TOL)

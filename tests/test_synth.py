@@ -65,3 +65,15 @@ def test_zipf_bias_gives_zipf_load():
     share = np.bincount(top2.reshape(-1), minlength=cfg.E) / top2.size
     want = np.sort(synth.zipf_shares(cfg.E, 1.2))[::-1]
     np.testing.assert_allclose(np.sort(share)[::-1], want, atol=0.01)
+
+
+def test_action_keep_table_uses_only_action_widths():
+    levels = [141, 564, 986, 1408]
+    for f in (0.9, 0.75, 0.5, 0.25, 0.05):
+        t = synth.action_keep_table(60, levels, 7, f)
+        assert set(t.tolist()) <= set(levels)
+        kept = t.sum() / (60 * 1408)
+        # at most the target, unless every expert already sits at the narrowest action
+        assert kept <= f + 1e-12 or (t == levels[0]).all()
+        # one step wider on any expert would exceed the target (the walk stops at the first fit)
+        assert kept > f - (levels[-1] - levels[0]) / (60 * 1408) - 1e-12 or (t == levels[0]).all()
