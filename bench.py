@@ -331,6 +331,10 @@ def main():
     roof["avg_launch_ms"] = gu_avg
     roof["launches_per_step"] = gu_per_step
     roof["timing"] = "HIP events around each launch, on its stream, over a second pass of the K steps"
+    if kt["gate_up_shared"][1]:
+        roof["note"] = ("the shared expert's gate/up launch runs on a side stream concurrently with the "
+                        "routed one; each launch's duration includes the time the two share the chip, so "
+                        "this per-launch figure is below the layer's own (layer.tflops)")
 
     layer_s = ms_step / 1e3
     layer = dict(tflops=alg["F"] / layer_s / 1e12, frac_mfma=alg["F"] / layer_s / 1e12 / peak_flops,

@@ -532,9 +532,10 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
         return FLEXMOE_OK;
     };
 
-    // The shared expert's chain goes first, on the side stream (it needs no
-    // routing); the routed chain follows the routing on the caller's stream;
-    // the combine waits for both.  This pays where the tails of the GEMMs and
+    // The shared expert's chain runs on the side stream, forked before the
+    // routing (it needs none); the routed chain follows the routing on the
+    // caller's stream; the combine waits for both.  This pays where the tails
+    // of the GEMMs and
     // the routing kernels leave compute units idle: decode-sized batches and
     // shared experts whose gate/up GEMM alone fills fewer than kSideWaves
     // waves of tiles.  Past that, one launch over all segments keeps each
@@ -546,13 +547,13 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
         if ((rc = side_stream(&side)) != FLEXMOE_OK) return rc;
         side_lock = std::unique_lock<std::mutex>(side->mu);
         if ((err = hipEventRecord(side->fork, s)) != hipSuccess) return hip_fail(err, "fork record");
-        if ((err = hipStreamWaitEvent(side->stream, side->fork, 0)) != hipSuccess)
-            return hip_fail(err, "fork wait");
-        if ((rc = gemms(kPartShared, 0, 0, g1s, g2s, side->stream)) != FLEXMOE_OK) return rc;
-        if ((err = hipEventRecord(side->join, side->stream)) != hipSuccess) return hip_fail(err, "join record");
     }
 
-    if ((long long)T * D.top_k <= kSmallAssign) {
+    // Routing and dispatch on the caller's stream.  The first routing kernel
+    // is submitted before the shared expert's GEMMs (it then reaches the
+    // compute units first); the rest follow them.
+    const bool small = (long long)T * D.top_k <= kSmallAssign;
+    if (small) {
         // one workgroup routes and dispatches everything (timed as routing)
         KernelTimer kt(FLEXMOE_K_ROUTE, s);
         dispatch_small_kernel<<<1, 64 * kSmallWaves, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, keep_dev,
@@ -562,13 +563,21 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
         err = hipGetLastError();
         if (err != hipSuccess) return hip_fail(err, "dispatch launch");
     } else {
-        {
-            KernelTimer kt(FLEXMOE_K_ROUTE, s);
-            route_kernel<<<NB, 64 * kRouteTokens, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, idx, wts,
-                                                          blockcnt, NB);
-            err = hipGetLastError();
-        }
+        KernelTimer kt(FLEXMOE_K_ROUTE, s);
+        route_kernel<<<NB, 64 * kRouteTokens, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, idx, wts,
+                                                      blockcnt, NB);
+        err = hipGetLastError();
         if (err != hipSuccess) return hip_fail(err, "route launch");
+    }
+
+    if (use_side) {
+        if ((err = hipStreamWaitEvent(side->stream, side->fork, 0)) != hipSuccess)
+            return hip_fail(err, "fork wait");
+        if ((rc = gemms(kPartShared, 0, 0, g1s, g2s, side->stream)) != FLEXMOE_OK) return rc;
+        if ((err = hipEventRecord(side->join, side->stream)) != hipSuccess) return hip_fail(err, "join record");
+    }
+
+    if (!small) {
         {
             KernelTimer kt(FLEXMOE_K_DISPATCH_SCAN, s);
             dispatch_scan_kernel<<<D.E, 256, 0, s>>>(blockcnt, NB, blockbase, counts);

@@ -18,10 +18,12 @@
 //     XOR-swizzled by bits 1..3 of the row index, so the 16 lanes served in
 //     one LDS cycle of a fragment read hit 64 distinct banks.
 //   - two LDS stages of 64 KB: the loads of K tile t+1 are in flight while
-//     tile t is multiplied.  MFMA operand fragments are read from LDS two
-//     16-deep steps ahead of their use (one register buffer per step), and
-//     the workgroup barrier that hands a stage back to the DMA sits in the
-//     middle of a K tile, so no step waits on a fragment read just issued.
+//     tile t is multiplied.  MFMA operand fragments are read from LDS one
+//     16-deep step ahead of their use.  This keeps the kernel near 200 VGPRs:
+//     its two waves per SIMD then leave room on every compute unit for the
+//     small routing kernels of a concurrently dispatched batch, which a
+//     deeper fragment pipeline (about 240 VGPRs) would lock out until a tile
+//     finished.
 //   - tiles are numbered segment-major (shared expert first: its reductions
 //     are the longest) with row tiles fastest, so consecutive tiles share
 //     their weight tile; groups of 8 consecutive tiles go to one XCD
@@ -244,30 +246,28 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
             for (int j = 0; j < NF; ++j)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
-        bf16x8 a[NSTEP][MFW], b[NSTEP][NF];  // one fragment buffer per step of a K tile
-        auto read_frags = [&](int kt, int ks) {
+        bf16x8 a[2][MFW], b[2][NF];  // fragment buffers of alternate steps
+        auto read_frags = [&](int kt, int ks, int buf) {
             const unsigned char* sa = smem + (kt % NSTAGE) * STAGE;
             const unsigned char* sb = sa + STAGE_A;
             const int chunk = ks * 2 + (lane >> 5);
 #pragma unroll
-            for (int i = 0; i < MFW; ++i) a[ks][i] = lds_frag(sa, wm * WR + i * 32 + (lane & 31), chunk);
+            for (int i = 0; i < MFW; ++i) a[buf][i] = lds_frag(sa, wm * WR + i * 32 + (lane & 31), chunk);
 #pragma unroll
-            for (int j = 0; j < NF; ++j) b[ks][j] = lds_frag(sb, brow[j] + (lane & 31), chunk);
+            for (int j = 0; j < NF; ++j) b[buf][j] = lds_frag(sb, brow[j] + (lane & 31), chunk);
         };
-        auto mfma_step = [&](int ks) {
+        auto mfma_step = [&](int buf) {
 #pragma unroll
             for (int i = 0; i < MFW; ++i)
 #pragma unroll
                 for (int j = 0; j < NF; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[ks][j], a[ks][i], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[buf][j], a[buf][i], acc[i][j], 0, 0, 0);
         };
 
-        // Two LDS stages, fragments two steps ahead, barrier mid-tile:
-        //   step 0: MFMA (kt, 0) | read (kt, 2)
-        //   step 1: MFMA (kt, 1) | read (kt, 3)
+        // Two LDS stages, fragments one step ahead:
+        //   steps s < 3: read (kt, s+1) | MFMA (kt, s)
         //   wait for tile kt+1 and this wave's reads, barrier
-        //   step 2: DMA tile kt+2 into the stage of tile kt | MFMA (kt, 2) | read (kt+1, 0)
-        //   step 3: MFMA (kt, 3) | read (kt+1, 1)
+        //   DMA tile kt+2 into the stage of tile kt | read (kt+1, 0) | MFMA (kt, 3)
         // At the barrier every wave has finished reading tile kt (its last
         // fragments are in registers), so its stage can be refilled, and tile
         // kt+1 has landed, so its fragments can be read.  Every iteration
@@ -277,29 +277,23 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
         issue(1, 1);
         __builtin_amdgcn_s_waitcnt(waitcnt_vm(LOADS_PER_TILE));  // tile 0 in
         barrier_no_fence();
-        read_frags(0, 0);
-        read_frags(0, 1);
+        read_frags(0, 0, 0);
         for (int kt = 0; kt < nk; ++kt) {
-            read_frags(kt, 2);
-            mfma_step(0);
-            sched_interleave<NMF, 0, NRD>();
-            __builtin_amdgcn_sched_barrier(0);
-            read_frags(kt, 3);
-            mfma_step(1);
-            sched_interleave<NMF, 0, NRD>();
-            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int st = 0; st < NSTEP - 1; ++st) {
+                read_frags(kt, st + 1, (st + 1) & 1);
+                mfma_step(st & 1);
+                sched_interleave<NMF, 0, NRD>();
+                __builtin_amdgcn_sched_barrier(0);
+            }
             __builtin_amdgcn_s_waitcnt(waitcnt_vm(0) & kWaitLgkm0);  // tile kt+1 in; own reads done
             barrier_no_fence();  // all waves are done reading tile kt: its stage is free
             __builtin_amdgcn_sched_barrier(0);
             issue(kt + NSTAGE, kt % NSTAGE);
-            // after the last tile these read a stale stage, whose values go unused
-            read_frags(kt + 1, 0);
-            mfma_step(2);
+            // after the last tile this reads a stale stage, whose values go unused
+            read_frags(kt + 1, 0, 0);
+            mfma_step((NSTEP - 1) & 1);
             sched_interleave<NMF, LOADS_PER_TILE, NRD>();
-            __builtin_amdgcn_sched_barrier(0);
-            read_frags(kt + 1, 1);
-            mfma_step(3);
-            sched_interleave<NMF, 0, NRD>();
             __builtin_amdgcn_sched_barrier(0);
         }
         __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // no DMA may outlive the workgroup's LDS
