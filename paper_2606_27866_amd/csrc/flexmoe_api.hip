@@ -553,11 +553,12 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
     // is submitted before the shared expert's GEMMs (it then reaches the
     // compute units first); the rest follow them.
     const bool small = (long long)T * D.top_k <= kSmallAssign;
-    if (small) {
+    const bool pre_routed = small && T > kSmallRouteT;
+    if (small && !pre_routed) {
         // one workgroup routes and dispatches everything (timed as routing)
         KernelTimer kt(FLEXMOE_K_ROUTE, s);
         dispatch_small_kernel<<<1, 64 * kSmallWaves, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, keep_dev,
-                                                             D.I, D.I_shared, D.d, ts, packed_limit, plan,
+                                                             D.I, D.I_shared, D.d, ts, packed_limit, plan, 0,
                                                              idx, wts, counts, perm, pos, offsets, seg, t1,
                                                              t2);
         err = hipGetLastError();
@@ -577,7 +578,16 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
         if ((err = hipEventRecord(side->join, side->stream)) != hipSuccess) return hip_fail(err, "join record");
     }
 
-    if (!small) {
+    if (pre_routed) {
+        // the tokens are routed; one workgroup dispatches them
+        KernelTimer kt(FLEXMOE_K_DISPATCH_SCATTER, s);
+        dispatch_small_kernel<<<1, 64 * kSmallWaves, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, keep_dev,
+                                                             D.I, D.I_shared, D.d, ts, packed_limit, plan, 1,
+                                                             idx, wts, counts, perm, pos, offsets, seg, t1,
+                                                             t2);
+        err = hipGetLastError();
+        if (err != hipSuccess) return hip_fail(err, "dispatch launch");
+    } else if (!small) {
         {
             KernelTimer kt(FLEXMOE_K_DISPATCH_SCAN, s);
             dispatch_scan_kernel<<<D.E, 256, 0, s>>>(blockcnt, NB, blockbase, counts);

@@ -129,8 +129,8 @@ __global__ void dispatch_scatter_kernel(const int32_t* idx, const int32_t* keep,
                                         int32_t* t2start);
 __global__ void dispatch_small_kernel(const float* logits, int T, int E, int k, int norm_topk,
                                       const int32_t* keep, int I, int I_shared, int d, TileShape ts,
-                                      int packed_limit, const int32_t* plan, int32_t* idx, float* wts,
-                                      int32_t* counts,
+                                      int packed_limit, const int32_t* plan, int pre_routed, int32_t* idx,
+                                      float* wts, int32_t* counts,
                                       int32_t* perm, int32_t* pos, int32_t* offsets, SegMeta* seg,
                                       int32_t* t1start, int32_t* t2start);
 __global__ void set_keep_kernel(int32_t* keep, KeepArgs t, int E);

@@ -342,11 +342,13 @@ __global__ __launch_bounds__(64) void dispatch_scatter_kernel(
 // Wave w routes the contiguous tokens [w*per, (w+1)*per) and counts its own
 // expert histogram; a scan over the waves gives each wave its base inside
 // every expert's segment, so the 16 waves place their assignments at once,
-// in the same order as one pass over the tokens would.
+// in the same order as one pass over the tokens would.  With pre_routed the
+// tokens were routed by route_kernel (spread over several compute units):
+// the waves read their tokens' expert ids instead.
 __global__ __launch_bounds__(64 * kSmallWaves) void dispatch_small_kernel(
     const float* __restrict__ logits, int T, int E, int k, int norm_topk,
     const int32_t* __restrict__ keep, int I, int I_shared, int d, TileShape ts, int packed_limit,
-    const int32_t* __restrict__ plan, int32_t* __restrict__ idx, float* __restrict__ wts,
+    const int32_t* __restrict__ plan, int pre_routed, int32_t* __restrict__ idx, float* __restrict__ wts,
     int32_t* __restrict__ counts,
     int32_t* __restrict__ perm, int32_t* __restrict__ pos, int32_t* __restrict__ offsets,
     SegMeta* __restrict__ seg, int32_t* __restrict__ t1start, int32_t* __restrict__ t2start) {
@@ -364,10 +366,17 @@ __global__ __launch_bounds__(64 * kSmallWaves) void dispatch_small_kernel(
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
     const int per = ceil_div(T, kSmallWaves);
     const int t0 = min(T, wave * per), t1 = min(T, t0 + per);
+    if (pre_routed) {
+        for (int a = t0 * k + lane; a < t1 * k; a += 64) {
+            const int id = min(max(idx[a], 0), E - 1);
+            sidx[a] = id;
+            atomicAdd(&hist[wave][id], 1);  // a count: arrival order does not matter
+        }
+    }
     // the next token's logits are loaded while this one is ranked
     float vn[4];
-    if (t0 < t1) load_logits(logits + (size_t)t0 * E, E, lane, vn);
-    for (int t = t0; t < t1; ++t) {
+    if (!pre_routed && t0 < t1) load_logits(logits + (size_t)t0 * E, E, lane, vn);
+    for (int t = pre_routed ? t1 : t0; t < t1; ++t) {
         int id;
         float w, v[4];
 #pragma unroll
