@@ -57,8 +57,11 @@ def lib():
         L.oracle_rank_reorder.argtypes = [i, i, i, i] + [p] * 8
         L.oracle_keep_from_ratio.argtypes = [ctypes.c_double, i]
         L.oracle_num_threads.argtypes = []
+        L.oracle_layer_grads.argtypes = [i] * 8 + [p] * 14
+        L.oracle_channel_saliency.argtypes = [i] * 4 + [p] * 7
         for f in (L.oracle_route, L.oracle_dispatch, L.oracle_layer_forward,
-                  L.oracle_rank_reorder, L.oracle_keep_from_ratio, L.oracle_num_threads):
+                  L.oracle_rank_reorder, L.oracle_keep_from_ratio, L.oracle_num_threads,
+                  L.oracle_layer_grads, L.oracle_channel_saliency):
             f.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -160,9 +163,9 @@ def rank_reorder(scores, w_gate, w_up, w_down):
     E, I = scores.shape
     dtype = _dtype_of(w_gate)
     d = w_gate.shape[2]
-    wg_r = np.empty_like(w_gate)
-    wu_r = np.empty_like(w_up)
-    wd_r = np.empty_like(w_down)
+    wg_r = np.empty(w_gate.shape, dtype=w_gate.dtype)
+    wu_r = np.empty(w_up.shape, dtype=w_up.dtype)
+    wd_r = np.empty(w_down.shape, dtype=w_down.dtype)
     perm = np.empty((E, I), dtype=np.int32)
     rc = lib().oracle_rank_reorder(E, I, d, dtype, _ptr(scores), _ptr(np.ascontiguousarray(w_gate)),
                                    _ptr(np.ascontiguousarray(w_up)), _ptr(np.ascontiguousarray(w_down)),
@@ -170,6 +173,72 @@ def rank_reorder(scores, w_gate, w_up, w_down):
     if rc != 0:
         raise ValueError("oracle_rank_reorder failed (%d)" % rc)
     return wg_r, wu_r, wd_r, perm
+
+
+def layer_grads(x, logits, w_gate, w_up, w_down, keep, top_k, norm_topk, y_target,
+                ws_gate=None, ws_up=None, ws_down=None):
+    """Gradients of L = 1/2 sum_t ||y_t - y_target_t||^2 of the masked layer
+    with respect to the routed expert weights (the g of Eq. 2).
+
+    Returns (L, g_gate [E][I][d], g_up [E][I][d], g_down [E][d][I]), fp64.
+    Same argument conventions as layer_forward; y_target [T][d] fp32.
+    """
+    x = np.ascontiguousarray(x)
+    dtype = _dtype_of(x)
+    logits = np.ascontiguousarray(logits, dtype=np.float32)
+    T, d = x.shape
+    E, I, _ = w_gate.shape
+    I_s = 0 if ws_gate is None else ws_gate.shape[0]
+    y_target = np.ascontiguousarray(y_target, dtype=np.float32)
+    assert y_target.shape == (T, d)
+    keep = np.ascontiguousarray(keep, dtype=np.int32)
+    gg = np.empty((E, I, d), dtype=np.float64)
+    gu = np.empty((E, I, d), dtype=np.float64)
+    gd = np.empty((E, d, I), dtype=np.float64)
+    loss = np.zeros(1, dtype=np.float64)
+    rc = lib().oracle_layer_grads(
+        T, d, E, I, top_k, I_s, dtype, int(norm_topk), _ptr(x), _ptr(logits),
+        _ptr(np.ascontiguousarray(w_gate)), _ptr(np.ascontiguousarray(w_up)),
+        _ptr(np.ascontiguousarray(w_down)), _ptr(keep),
+        _ptr(None if ws_gate is None else np.ascontiguousarray(ws_gate)),
+        _ptr(None if ws_up is None else np.ascontiguousarray(ws_up)),
+        _ptr(None if ws_down is None else np.ascontiguousarray(ws_down)),
+        _ptr(y_target), _ptr(loss), _ptr(gg), _ptr(gu), _ptr(gd))
+    if rc != 0:
+        raise ValueError("oracle_layer_grads failed (%d)" % rc)
+    return float(loss[0]), gg, gu, gd
+
+
+def channel_saliency_from_grads(w_gate, w_up, w_down, g_gate, g_up, g_down):
+    """Eq. 2 for one batch: s[e][j] = sum over channel j's group of (theta * g)^2."""
+    dtype = _dtype_of(w_gate)
+    E, I, d = w_gate.shape
+    s = np.empty((E, I), dtype=np.float64)
+    rc = lib().oracle_channel_saliency(
+        d, E, I, dtype, _ptr(np.ascontiguousarray(w_gate)), _ptr(np.ascontiguousarray(w_up)),
+        _ptr(np.ascontiguousarray(w_down)), _ptr(np.ascontiguousarray(g_gate, dtype=np.float64)),
+        _ptr(np.ascontiguousarray(g_up, dtype=np.float64)),
+        _ptr(np.ascontiguousarray(g_down, dtype=np.float64)), _ptr(s))
+    if rc != 0:
+        raise ValueError("oracle_channel_saliency failed (%d)" % rc)
+    return s
+
+
+def channel_saliency(batches, w_gate, w_up, w_down, top_k, norm_topk,
+                     ws_gate=None, ws_up=None, ws_down=None):
+    """Eq. 2 over a ranking set: the mean over batches of the per-batch
+    saliency of the unpruned layer (every k_e = I).
+
+    batches: sequence of (x, logits, y_target).  Returns s [E][I] fp64.
+    """
+    E, I, _ = w_gate.shape
+    keep = np.full(E, I, dtype=np.int32)
+    total = np.zeros((E, I), dtype=np.float64)
+    for x, logits, y_target in batches:
+        _, gg, gu, gd = layer_grads(x, logits, w_gate, w_up, w_down, keep, top_k, norm_topk,
+                                    y_target, ws_gate, ws_up, ws_down)
+        total += channel_saliency_from_grads(w_gate, w_up, w_down, gg, gu, gd)
+    return total / max(len(batches), 1)
 
 
 def packed_width(k: int) -> int:

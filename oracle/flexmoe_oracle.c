@@ -17,7 +17,14 @@
  *   - the channel reorder of Eq. 3 (Sec. 3.1): a descending sort of the
  *     saliency scores gives pi; gate/up rows and down columns are permuted
  *     consistently;
- *   - k = ceil(r * d_ff) for a retention ratio r (Sec. 3.1, after Eq. 3).
+ *   - k = ceil(r * d_ff) for a retention ratio r (Sec. 3.1, after Eq. 3);
+ *   - the first-order Taylor channel saliency of Eq. 2 (Sec. 3.1): the
+ *     gradient of a loss with respect to every routed expert weight, then
+ *     per hidden channel j the sum over its group (gate row j, up row j,
+ *     down column j) of (theta * dL/dtheta)^2.  The paper's loss is the
+ *     language-model loss; here it is the layer-level
+ *     L = 1/2 sum_t ||y_t - y_target_t||^2, with the gradients written out
+ *     by the chain rule (router weights and logits are inputs, not trained).
  *
  * Readings where the paper is silent (each listed with its reason in the
  * design notes):
@@ -295,6 +302,151 @@ done:
     free(pos);
     free(O);
     return rc;
+}
+
+/* Gradients of L = 1/2 sum_t sum_n (y[t][n] - y_target[t][n])^2 for the
+ * masked layer above, with respect to the routed experts' weights (Sec. 3.1,
+ * the g of Eq. 2).  With dY_t = y_t - y_target_t, for every active
+ * assignment a = (t, j) of expert e with router weight w_a and every kept
+ * channel c < k_e:
+ *   g_c = <W_gate[c], x_t>, u_c = <W_up[c], x_t>, h_c = silu(g_c) u_c
+ *   dO_a[n]  = w_a dY_t[n]                      (y_t = sum_a w_a O_a + S_t)
+ *   dL/dW_down[n][c] += dO_a[n] h_c             (O_a[n] = sum_c W_down[n][c] h_c)
+ *   dh_c     = sum_n W_down[n][c] dO_a[n]
+ *   dg_c     = dh_c u_c silu'(g_c),  du_c = dh_c silu(g_c)
+ *   dL/dW_gate[c][i] += dg_c x_t[i],  dL/dW_up[c][i] += du_c x_t[i]
+ * with silu'(g) = s (1 + g (1 - s)), s = 1 / (1 + e^-g).  Channels c >= k_e
+ * and experts with k_e = 0 take no part in the layer and get zero gradient.
+ * The shared expert enters through y only.
+ * g_gate, g_up [E][I][d], g_down [E][d][I] (fp64, overwritten); *loss = L.
+ * Returns 0, or the error of oracle_layer_forward. */
+int oracle_layer_grads(int T, int d, int E, int I, int k, int I_s, int dtype, int norm_topk,
+                       const void *x, const float *logits, const void *w_gate, const void *w_up,
+                       const void *w_down, const int32_t *keep, const void *ws_gate,
+                       const void *ws_up, const void *ws_down, const float *y_target,
+                       double *loss, double *g_gate, double *g_up, double *g_down)
+{
+    if (T < 0 || d < 1 || E < 1 || I < 1 || k < 1 || k > E || !y_target || !loss || !g_gate ||
+        !g_up || !g_down)
+        return -1;
+    size_t nw = (size_t)E * I * d;
+    memset(g_gate, 0, nw * sizeof(double));
+    memset(g_up, 0, nw * sizeof(double));
+    memset(g_down, 0, nw * sizeof(double));
+    *loss = 0.0;
+    if (T == 0)
+        return 0;
+    size_t A = (size_t)T * k;
+    double *y = (double *)malloc((size_t)T * d * sizeof(double));
+    double *w = (double *)malloc(A * sizeof(double));
+    int32_t *idx = (int32_t *)malloc(A * sizeof(int32_t));
+    int32_t *counts = (int32_t *)malloc((size_t)E * sizeof(int32_t));
+    int32_t *offsets = (int32_t *)malloc((size_t)(E + 1) * sizeof(int32_t));
+    int32_t *perm = (int32_t *)malloc(A * sizeof(int32_t));
+    int32_t *pos = (int32_t *)malloc(A * sizeof(int32_t));
+    int rc = -1;
+    if (!y || !w || !idx || !counts || !offsets || !perm || !pos)
+        goto done;
+    rc = oracle_layer_forward(T, d, E, I, k, I_s, dtype, norm_topk, x, logits, w_gate, w_up,
+                              w_down, keep, ws_gate, ws_up, ws_down, y, idx, w, counts, offsets,
+                              perm, pos);
+    if (rc != 0)
+        goto done;
+
+    /* dY = y - y_target (overwrites y) and the loss */
+    double L = 0.0;
+    for (size_t i = 0; i < (size_t)T * d; ++i) {
+        y[i] -= (double)y_target[i];
+        L += 0.5 * y[i] * y[i];
+    }
+    *loss = L;
+
+    /* experts are independent: one thread per expert, its assignments in
+     * dispatch order */
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int e = 0; e < E; ++e) {
+        int kk = keep[e];
+        if (kk == 0 || offsets[e + 1] == offsets[e])
+            continue;
+        double *g = (double *)malloc((size_t)kk * sizeof(double));
+        double *u = (double *)malloc((size_t)kk * sizeof(double));
+        double *dO = (double *)malloc((size_t)d * sizeof(double));
+        const size_t wb = (size_t)e * I * d; /* gate/up block [I][d], down block [d][I] */
+        for (int p = offsets[e]; p < offsets[e + 1]; ++p) {
+            int a = perm[p], t = a / k;
+            const size_t xo = (size_t)t * d;
+            for (int c = 0; c < kk; ++c) {
+                double gc = 0.0, uc = 0.0;
+                for (int i = 0; i < d; ++i) {
+                    double xi = elem(x, dtype, xo + i);
+                    gc += elem(w_gate, dtype, wb + (size_t)c * d + i) * xi;
+                    uc += elem(w_up, dtype, wb + (size_t)c * d + i) * xi;
+                }
+                g[c] = gc;
+                u[c] = uc;
+            }
+            for (int n = 0; n < d; ++n)
+                dO[n] = w[a] * y[xo + n];
+            for (int c = 0; c < kk; ++c) {
+                double sg = 1.0 / (1.0 + exp(-g[c]));
+                double silu = g[c] * sg, dsilu = sg * (1.0 + g[c] * (1.0 - sg));
+                double h = silu * u[c], dh = 0.0;
+                for (int n = 0; n < d; ++n) {
+                    g_down[wb + (size_t)n * I + c] += dO[n] * h;
+                    dh += elem(w_down, dtype, wb + (size_t)n * I + c) * dO[n];
+                }
+                double dg = dh * u[c] * dsilu, du = dh * silu;
+                for (int i = 0; i < d; ++i) {
+                    double xi = elem(x, dtype, xo + i);
+                    g_gate[wb + (size_t)c * d + i] += dg * xi;
+                    g_up[wb + (size_t)c * d + i] += du * xi;
+                }
+            }
+        }
+        free(g);
+        free(u);
+        free(dO);
+    }
+    rc = 0;
+done:
+    free(y);
+    free(w);
+    free(idx);
+    free(counts);
+    free(offsets);
+    free(perm);
+    free(pos);
+    return rc;
+}
+
+/* Eq. 2 for one batch: the saliency of hidden channel j of expert e is the
+ * sum over its parameter group -- gate row j, up row j, down column j -- of
+ * (theta * dL/dtheta)^2 (a sum of squares, not the square of a sum).
+ * s [E][I] fp64 (overwritten). */
+int oracle_channel_saliency(int d, int E, int I, int dtype, const void *w_gate, const void *w_up,
+                            const void *w_down, const double *g_gate, const double *g_up,
+                            const double *g_down, double *s)
+{
+    if (d < 1 || E < 1 || I < 1 || !w_gate || !w_up || !w_down || !g_gate || !g_up || !g_down || !s)
+        return -1;
+#pragma omp parallel for schedule(static)
+    for (int e = 0; e < E; ++e) {
+        const size_t wb = (size_t)e * I * d;
+        for (int j = 0; j < I; ++j) {
+            double acc = 0.0;
+            for (int i = 0; i < d; ++i) {
+                double tg = elem(w_gate, dtype, wb + (size_t)j * d + i) * g_gate[wb + (size_t)j * d + i];
+                double tu = elem(w_up, dtype, wb + (size_t)j * d + i) * g_up[wb + (size_t)j * d + i];
+                acc += tg * tg + tu * tu;
+            }
+            for (int n = 0; n < d; ++n) {
+                double td = elem(w_down, dtype, wb + (size_t)n * I + j) * g_down[wb + (size_t)n * I + j];
+                acc += td * td;
+            }
+            s[(size_t)e * I + j] = acc;
+        }
+    }
+    return 0;
 }
 
 /* Eq. 3: sort scores in descending order to get pi, then

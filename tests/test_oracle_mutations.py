@@ -30,6 +30,14 @@ MUTANTS = {
     "ratio_floor": ("double k = ceil(r * (double)I - 1e-9);", "double k = floor(r * (double)I + 1e-9);"),
     "shared_half_weight": ("yt[n] += s[n];", "yt[n] += 0.5 * s[n];"),
     "router_weight_dropped": ("yt[n] += wt * O[(size_t)p * d + n];", "yt[n] += O[(size_t)p * d + n];"),
+    "grad_dsilu_term_dropped": ("dsilu = sg * (1.0 + g[c] * (1.0 - sg));", "dsilu = sg;"),
+    "grad_router_weight_dropped": ("dO[n] = w[a] * y[xo + n];", "dO[n] = y[xo + n];"),
+    "grad_down_uses_preactivation": ("g_down[wb + (size_t)n * I + c] += dO[n] * h;",
+                                     "g_down[wb + (size_t)n * I + c] += dO[n] * silu;"),
+    "grad_up_gets_gate_term": ("g_up[wb + (size_t)c * d + i] += du * xi;",
+                               "g_up[wb + (size_t)c * d + i] += dg * xi;"),
+    "saliency_down_not_squared": ("acc += td * td;", "acc += fabs(td);"),
+    "saliency_gate_term_dropped": ("acc += tg * tg + tu * tu;", "acc += tu * tu;"),
     "prefix_short_by_one": ("    for (int c = 0; c < kk; ++c) {\n        double g = 0.0, u = 0.0;",
                             "    for (int c = 0; c < kk; ++c) {\n        if (c == kk - 1 && kk > 1) { h[c] = 0; continue; }\n        double g = 0.0, u = 0.0;"),
 }
@@ -38,7 +46,8 @@ MUTANTS = {
 def _run_pins(lib_path):
     env = dict(os.environ, FLEXMOE_ORACLE_LIB=lib_path)
     return subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
-                           os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                           os.path.join(ROOT, "tests", "test_oracle_pins.py"),
+                           os.path.join(ROOT, "tests", "test_saliency_pins.py")],
                           cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
 
 
