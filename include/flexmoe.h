@@ -126,6 +126,37 @@ int flexmoe_rank_reorder(const flexmoe_layer_desc *desc, const float *scores,
                          void *w_gate_r, void *w_up_r, void *w_down_r, int32_t *perm,
                          void *stream);
 
+/* ---- Channel saliency on the device (Sec. 3.1, Eq. 2) --------------------
+ * The first-order Taylor saliency of every hidden channel of every routed
+ * expert, for one calibration batch, added into a running score table:
+ *   scores[e][j] += scale * sum over theta in {W_gate[e][j][:], W_up[e][j][:],
+ *                                              W_down[e][:][j]} of (theta * dL/dtheta)^2
+ * The loss is the layer-level L = 1/2 sum_t ||Y_t - y_target_t||^2 of the
+ * UNPRUNED layer (every k_e = I) on this batch; the paper's language-model
+ * loss needs a whole model and is out of this library's scope.  Router
+ * weights come from the logits (not trained); the shared expert contributes
+ * to Y but is not scored.  With scale = 1/|B_rank| over the calibration
+ * batches, scores ends as Eq. 2's mean; flexmoe_rank_reorder then sorts it.
+ *   x [T][d], weights (original order) as for flexmoe_rank_reorder, shared
+ *   weights as for the forward (or NULL iff I_shared == 0), logits [T][E] fp32,
+ *   y_target [T][d] fp32 (16-byte aligned), scores [E][I] fp32 (4-byte
+ *   aligned; read and written, on `stream`).
+ * bf16 layers only (FLEXMOE_EDTYPE otherwise).  Arithmetic: fp32 accumulation
+ * in every GEMM; g, u, h, dO = w*dY, dG and dU are rounded to bf16 as MFMA
+ * operands; Y and dY stay fp32; the squares and their sums are fp32, summed in
+ * a fixed order (repeated calls give identical bits).
+ * Workspace: flexmoe_saliency_workspace_bytes(desc, T), 256-byte aligned; it
+ * holds a transposed copy of W_down (E*I*d bf16) besides per-token buffers.
+ * Shapes: the bf16 rules of the forward, and
+ * max(d, I) * (T*top_k + 7*E rounded up to 8) < 2^30 (FLEXMOE_ESHAPE). */
+size_t flexmoe_saliency_workspace_bytes(const flexmoe_layer_desc *desc, int32_t T);
+int flexmoe_channel_saliency(const flexmoe_layer_desc *desc, int32_t T, const void *x,
+                             const float *logits, const void *w_gate, const void *w_up,
+                             const void *w_down, const void *ws_gate, const void *ws_up,
+                             const void *ws_down, const float *y_target, float scale,
+                             float *scores, void *workspace, size_t workspace_bytes,
+                             void *stream);
+
 /* Budget switch: validates 0 <= keep_host[e] <= I for every e on the host, then
  * writes the E counts into keep_dev [E] on `stream` (one small kernel whose
  * arguments carry the table, so keep_host may be reused as soon as the call
@@ -243,11 +274,16 @@ enum {
     FLEXMOE_K_COMBINE = 5,        /* weighted combine + shared add             */
     FLEXMOE_K_GATE_UP_SHARED = 6, /* gate/up GEMM of the shared expert         */
     FLEXMOE_K_DOWN_SHARED = 7,    /* down GEMM of the shared expert            */
-    FLEXMOE_K_COUNT = 8
+    FLEXMOE_K_SAL_TRANSPOSE = 8,  /* saliency: transposed down-weight copy     */
+    FLEXMOE_K_SAL_PREP = 9,       /* saliency: transposed x and dO copies      */
+    FLEXMOE_K_SAL_DGRAD = 10,     /* saliency: dgrad GEMM + SwiGLU backward    */
+    FLEXMOE_K_SAL_WGRAD = 11,     /* saliency: wgrad GEMMs + Eq. 2 reduction   */
+    FLEXMOE_K_SAL_REDUCE = 12,    /* saliency: sum of the partial scores       */
+    FLEXMOE_K_COUNT = 13
 };
 typedef struct flexmoe_kernel_times {
-    double ms[8];
-    int64_t launches[8];
+    double ms[FLEXMOE_K_COUNT];
+    int64_t launches[FLEXMOE_K_COUNT];
 } flexmoe_kernel_times;
 int flexmoe_timing_enable(int on);
 int flexmoe_timing_read(flexmoe_kernel_times *out);

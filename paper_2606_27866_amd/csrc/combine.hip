@@ -6,7 +6,7 @@
 // S[t] is the sum of the shared expert's partial rows Os[part][t] (one part
 // unless its down projection was split), added in ascending part order.
 // O and Os are fp32 in fp32 mode and bf16 in bf16 mode.
-#include "kernels.h"
+#include "saliency.h"
 
 namespace flexmoe {
 
@@ -15,6 +15,37 @@ __device__ __forceinline__ float4 load4(const bf16_t* p) {
     const uint2 v = *reinterpret_cast<const uint2*>(p);
     return make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u),
                        __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xffff0000u));
+}
+
+// Columns n .. n+3 of token t's combined output, in fp32.
+template <typename OutT>
+__device__ __forceinline__ float4 combine_cols(const OutT* __restrict__ O, const OutT* __restrict__ Os,
+                                               const int32_t* __restrict__ pos, const float* __restrict__ wts,
+                                               int T, int k, int d, int shared_parts, int t, int n) {
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int j = 0; j < k; ++j) {
+        const int p = pos[(size_t)t * k + j];
+        if (p < 0) continue;
+        const float w = wts[(size_t)t * k + j];
+        const float4 o = load4(O + (size_t)p * d + n);
+        acc.x += w * o.x;
+        acc.y += w * o.y;
+        acc.z += w * o.z;
+        acc.w += w * o.w;
+    }
+    float4 sh = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int q = 0; q < shared_parts; ++q) {
+        const float4 sv = load4(Os + ((size_t)q * T + t) * d + n);
+        sh.x += sv.x;
+        sh.y += sv.y;
+        sh.z += sv.z;
+        sh.w += sv.w;
+    }
+    acc.x += sh.x;
+    acc.y += sh.y;
+    acc.z += sh.z;
+    acc.w += sh.w;
+    return acc;
 }
 
 template <typename OutT>
@@ -26,29 +57,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const OutT* __restrict__ O
     const int t = blockIdx.x;
     const int n = (blockIdx.y * blockDim.x + threadIdx.x) * 4;  // one float4 column group per thread
     if (n < d) {
-        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-        for (int j = 0; j < k; ++j) {
-            const int p = pos[(size_t)t * k + j];
-            if (p < 0) continue;
-            const float w = wts[(size_t)t * k + j];
-            const float4 o = load4(O + (size_t)p * d + n);
-            acc.x += w * o.x;
-            acc.y += w * o.y;
-            acc.z += w * o.z;
-            acc.w += w * o.w;
-        }
-        float4 sh = make_float4(0.f, 0.f, 0.f, 0.f);
-        for (int q = 0; q < shared_parts; ++q) {
-            const float4 sv = load4(Os + ((size_t)q * T + t) * d + n);
-            sh.x += sv.x;
-            sh.y += sv.y;
-            sh.z += sv.z;
-            sh.w += sv.w;
-        }
-        acc.x += sh.x;
-        acc.y += sh.y;
-        acc.z += sh.z;
-        acc.w += sh.w;
+        const float4 acc = combine_cols(O, Os, pos, wts, T, k, d, shared_parts, t, n);
         if constexpr (sizeof(OutT) == 4) {
             *reinterpret_cast<float4*>(y + (size_t)t * d + n) = acc;
         } else {
@@ -57,6 +66,33 @@ __global__ __launch_bounds__(256) void combine_kernel(const OutT* __restrict__ O
             *reinterpret_cast<uint2*>(y + (size_t)t * d + n) = make_uint2(lo, hi);
         }
     }
+}
+
+// The residual of the saliency's loss: dY = y - target, y unrounded.
+__global__ __launch_bounds__(256) void combine_residual_kernel(const bf16_t* __restrict__ O,
+                                                               const bf16_t* __restrict__ Os,
+                                                               const int32_t* __restrict__ pos,
+                                                               const float* __restrict__ wts, int T, int k,
+                                                               int d, int shared_parts,
+                                                               const float* __restrict__ target,
+                                                               float* __restrict__ dy) {
+    const int t = blockIdx.x;
+    const int n = (blockIdx.y * blockDim.x + threadIdx.x) * 4;
+    if (n < d) {
+        const float4 acc = combine_cols(O, Os, pos, wts, T, k, d, shared_parts, t, n);
+        const float4 tg = *reinterpret_cast<const float4*>(target + (size_t)t * d + n);
+        *reinterpret_cast<float4*>(dy + (size_t)t * d + n) =
+            make_float4(acc.x - tg.x, acc.y - tg.y, acc.z - tg.z, acc.w - tg.w);
+    }
+}
+
+hipError_t launch_combine_residual(const bf16_t* O, const bf16_t* Os, const int32_t* pos, const float* wts,
+                                   int T, int k, int d, int shared_parts, const float* target, float* dy,
+                                   hipStream_t s) {
+    if (T <= 0) return hipSuccess;
+    const dim3 grid(T, ceil_div(d, 4 * 256));
+    combine_residual_kernel<<<grid, 256, 0, s>>>(O, Os, pos, wts, T, k, d, shared_parts, target, dy);
+    return hipGetLastError();
 }
 
 hipError_t launch_combine(const void* O, const void* Os, const int32_t* pos, const float* wts,

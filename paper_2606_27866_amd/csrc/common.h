@@ -54,7 +54,11 @@ struct SegMeta {
     int32_t kg;     // channels the GEMMs compute: kk, or kk aligned up in the
                     // bucketed forward (the extra channels' activations are 0)
     int32_t e;      // routed expert id (-1: the shared expert)
-    int32_t pad[2];
+    int32_t prow0;  // routed segments: first row in the padded row space, where
+                    // every segment takes packed_width(rows) rows (the column
+                    // offset of the segment in transposed activation copies)
+    int32_t rt0;    // routed segments: row tiles (of the gate/up tile height) of
+                    // the routed segments before this one
 };
 
 // Channels an expert occupies in the clipped (offline) weight layout: k_e

@@ -20,6 +20,7 @@
 
 #include "flexmoe.h"
 #include "kernels.h"
+#include "saliency.h"
 
 using namespace flexmoe;
 
@@ -188,8 +189,8 @@ std::mutex g_tmu;
 bool g_timing = false;
 std::vector<TimedLaunch> g_pending;
 std::vector<hipEvent_t> g_free_events;
-double g_ms[8];
-int64_t g_launches[8];
+double g_ms[FLEXMOE_K_COUNT];
+int64_t g_launches[FLEXMOE_K_COUNT];
 
 hipEvent_t take_event() {
     if (!g_free_events.empty()) {
@@ -273,7 +274,7 @@ int flexmoe_timing_enable(int on) {
     std::lock_guard<std::mutex> g(g_tmu);
     g_timing = on != 0;
     if (g_timing) {
-        for (int i = 0; i < 8; ++i) g_ms[i] = 0.0, g_launches[i] = 0;
+        for (int i = 0; i < FLEXMOE_K_COUNT; ++i) g_ms[i] = 0.0, g_launches[i] = 0;
     }
     return FLEXMOE_OK;
 }
@@ -292,7 +293,7 @@ int flexmoe_timing_read(flexmoe_kernel_times* out) {
         g_free_events.push_back(t.stop);
     }
     g_pending.clear();
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < FLEXMOE_K_COUNT; ++i) {
         out->ms[i] = g_ms[i];
         out->launches[i] = g_launches[i];
         g_ms[i] = 0.0;
@@ -723,6 +724,238 @@ int flexmoe_layer_forward_bucketed(const flexmoe_layer_desc* desc, int32_t T, co
     if (!keep_host) return fail(FLEXMOE_EINVAL, "keep_host is NULL");
     return forward_impl(desc, T, x, logits, w_gate_r, w_up_r, w_down_r, nullptr, 0, 0x7fffffff, keep_host,
                         k_align, ws_gate, ws_up, ws_down, y, workspace, workspace_bytes, dbg, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+// ---- channel saliency -------------------------------------------------------
+struct SalLayout {
+    Layout f;  // the forward's regions (shared expert unsplit)
+    size_t dy, dO, xt, dot, gt, ut, ht, dgt, dut, wdt, partial, total;
+    int ldt, nI, nM;
+};
+
+// Row stride of the transposed activation copies: every routed segment takes
+// packed_width(rows) <= rows + 7 rows, so A + 7E bounds the padded total.
+long long sal_ldt(const flexmoe_layer_desc& D, int T) {
+    return ((long long)T * D.top_k + 7LL * D.E + 7) & ~7LL;
+}
+
+SalLayout sal_layout(const flexmoe_layer_desc& D, int T) {
+    SalLayout S{};
+    S.f = layout(D, T, (size_t)T);
+    S.ldt = (int)sal_ldt(D, T);
+    S.nI = ceil_div(D.I, kSalTile);
+    S.nM = ceil_div(D.d, kSalTile);
+    const size_t A = (size_t)T * D.top_k, d = D.d, I = D.I, ldt = S.ldt;
+    size_t off = S.f.total;
+    auto take = [&](size_t bytes) {
+        const size_t o = off;
+        off += align256(bytes);
+        return o;
+    };
+    S.dy = take((size_t)T * d * 4);
+    S.dO = take(A * d * 2);
+    S.xt = take(d * ldt * 2);
+    S.dot = take(d * ldt * 2);
+    S.gt = take(I * ldt * 2);
+    S.ut = take(I * ldt * 2);
+    S.ht = take(I * ldt * 2);
+    S.dgt = take(I * ldt * 2);
+    S.dut = take(I * ldt * 2);
+    S.wdt = take((size_t)D.E * I * d * 2);
+    S.partial = take(3 * (size_t)D.E * I * S.nM * kSalWaveM * 4);
+    S.total = off;
+    return S;
+}
+
+int check_saliency_shape(const flexmoe_layer_desc& D, int T) {
+    if (D.dtype != FLEXMOE_BF16) return fail(FLEXMOE_EDTYPE, "channel saliency runs on bf16 layers only");
+    if (T < 0) return fail(FLEXMOE_EINVAL, "T = %d is negative", T);
+    if (T > D.max_tokens) return fail(FLEXMOE_ESHAPE, "T = %d exceeds max_tokens = %d", T, D.max_tokens);
+    if ((long long)std::max(D.d, D.I) * sal_ldt(D, T) >= (1LL << 30))
+        return fail(FLEXMOE_ESHAPE, "max(d, I) * (T * top_k + 7 * E) must stay below 2^30");
+    return FLEXMOE_OK;
+}
+
+int saliency_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const float* logits,
+                  const void* w_gate, const void* w_up, const void* w_down, const void* ws_gate,
+                  const void* ws_up, const void* ws_down, const float* y_target, float scale, float* scores,
+                  void* workspace, size_t workspace_bytes, void* stream) {
+    int rc = check_desc(desc);
+    if (rc) return rc;
+    const flexmoe_layer_desc& D = *desc;
+    if ((rc = check_saliency_shape(D, T)) != FLEXMOE_OK) return rc;
+    if (T == 0) return FLEXMOE_OK;
+    if (!x || !logits || !w_gate || !w_up || !w_down || !y_target || !scores)
+        return fail(FLEXMOE_EINVAL, "saliency: an input/output pointer is NULL");
+    for (const void* ptr : {x, w_gate, w_up, w_down, ws_gate, ws_up, ws_down, (const void*)y_target})
+        if (((uintptr_t)ptr) & 15) return fail(FLEXMOE_EINVAL, "x, weights and y_target must be 16-byte aligned");
+    if (((uintptr_t)logits) & 3 || ((uintptr_t)scores) & 3)
+        return fail(FLEXMOE_EINVAL, "logits and scores must be 4-byte aligned");
+    const bool has_shared = D.I_shared > 0;
+    if (has_shared != (ws_gate && ws_up && ws_down) || (!has_shared && (ws_gate || ws_up || ws_down)))
+        return fail(FLEXMOE_EINVAL, "shared weights must be given iff I_shared > 0");
+    const SalLayout S = sal_layout(D, T);
+    if (!workspace || workspace_bytes < S.total)
+        return fail(FLEXMOE_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace_bytes, S.total);
+    if (((uintptr_t)workspace) & 255) return fail(FLEXMOE_EWORKSPACE, "workspace is not 256-byte aligned");
+
+    hipStream_t s = (hipStream_t)stream;
+    char* ws = (char*)workspace;
+    const Layout& L = S.f;
+    int32_t* idx = (int32_t*)(ws + L.idx);
+    float* wts = (float*)(ws + L.wts);
+    int32_t* blockcnt = (int32_t*)(ws + L.blockcnt);
+    int32_t* blockbase = (int32_t*)(ws + L.blockbase);
+    int32_t* counts = (int32_t*)(ws + L.counts);
+    int32_t* offsets = (int32_t*)(ws + L.offsets);
+    int32_t* perm = (int32_t*)(ws + L.perm);
+    int32_t* pos = (int32_t*)(ws + L.pos);
+    SegMeta* seg = (SegMeta*)(ws + L.seg);
+    int32_t* t1 = (int32_t*)(ws + L.t1);
+    int32_t* t2 = (int32_t*)(ws + L.t2);
+    int32_t* keep = (int32_t*)(ws + L.keep);
+    bf16_t* H = (bf16_t*)(ws + L.H);
+    bf16_t* Hs = (bf16_t*)(ws + L.Hs);
+    bf16_t* O = (bf16_t*)(ws + L.O);
+    bf16_t* Os = (bf16_t*)(ws + L.Os);
+    float* dy = (float*)(ws + S.dy);
+    bf16_t* dO = (bf16_t*)(ws + S.dO);
+    bf16_t* xt = (bf16_t*)(ws + S.xt);
+    bf16_t* dot = (bf16_t*)(ws + S.dot);
+    bf16_t* gt = (bf16_t*)(ws + S.gt);
+    bf16_t* ut = (bf16_t*)(ws + S.ut);
+    bf16_t* ht = (bf16_t*)(ws + S.ht);
+    bf16_t* dgt = (bf16_t*)(ws + S.dgt);
+    bf16_t* dut = (bf16_t*)(ws + S.dut);
+    bf16_t* wdt = (bf16_t*)(ws + S.wdt);
+    float* partial = (float*)(ws + S.partial);
+    const int hs = has_shared ? 1 : 0, nseg = D.E + hs;
+    hipError_t err;
+
+    // 1. the transposed down weights (no dependence on the batch's routing)
+    {
+        KernelTimer kt(FLEXMOE_K_SAL_TRANSPOSE, s);
+        err = launch_transpose_down((const bf16_t*)w_down, wdt, D.E, D.d, D.I, s);
+    }
+    if (err != hipSuccess) return hip_fail(err, "down-weight transpose launch");
+
+    // 2. routing and dispatch of the unpruned layer (every k_e = I), with the
+    //    prefill tile shapes and the shared expert's down GEMM unsplit
+    KeepArgs ka;
+    for (int e = 0; e < kMaxExperts; ++e) ka.v[e] = e < D.E ? D.I : 0;
+    set_keep_kernel<<<1, kMaxExperts, 0, s>>>(keep, ka, D.E);
+    if ((err = hipGetLastError()) != hipSuccess) return hip_fail(err, "keep upload");
+    const TileShape ts{kBigBM1, kBigBN1, kBigBM2, kBigBN2, 0};
+    static_assert(kBigBM1 == kSalTile, "segment row tiles (rt0) are counted in saliency tile rows");
+    const int NB = num_chunks(T);
+    if ((long long)T * D.top_k <= kSmallAssign) {
+        KernelTimer kt(FLEXMOE_K_ROUTE, s);
+        dispatch_small_kernel<<<1, 64 * kSmallWaves, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, keep, D.I,
+                                                             D.I_shared, D.d, ts, 0x7fffffff, nullptr, 0, idx,
+                                                             wts, counts, perm, pos, offsets, seg, t1, t2);
+        if ((err = hipGetLastError()) != hipSuccess) return hip_fail(err, "dispatch launch");
+    } else {
+        {
+            KernelTimer kt(FLEXMOE_K_ROUTE, s);
+            route_kernel<<<NB, 64 * kRouteTokens, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, idx, wts,
+                                                          blockcnt, NB);
+            err = hipGetLastError();
+        }
+        if (err != hipSuccess) return hip_fail(err, "route launch");
+        {
+            KernelTimer kt(FLEXMOE_K_DISPATCH_SCAN, s);
+            dispatch_scan_kernel<<<D.E, 256, 0, s>>>(blockcnt, NB, blockbase, counts);
+            err = hipGetLastError();
+        }
+        if (err != hipSuccess) return hip_fail(err, "dispatch scan launch");
+        {
+            KernelTimer kt(FLEXMOE_K_DISPATCH_SCATTER, s);
+            dispatch_scatter_kernel<<<NB, 64, 0, s>>>(idx, keep, counts, blockbase, T, D.E, D.top_k, D.I,
+                                                      D.I_shared, D.d, NB, ts, 0x7fffffff, nullptr, perm, pos,
+                                                      offsets, seg, t1, t2);
+            err = hipGetLastError();
+        }
+        if (err != hipSuccess) return hip_fail(err, "dispatch scatter launch");
+    }
+
+    // 3. the forward, keeping transposed g, u, h of the routed rows
+    const long long g1 = routed_row_tiles_ub(T, D.E, D.top_k, ts.bm1) * ceil_div(D.I, ts.bn1) +
+                         (has_shared ? (long long)ceil_div(T, ts.bm1) * ceil_div(D.I_shared, ts.bn1) : 0);
+    const long long g2s = has_shared ? (long long)ceil_div(T, ts.bm2) * ceil_div(D.d, ts.bn2) : 0;
+    const long long g2 = routed_row_tiles_ub(T, D.E, D.top_k, ts.bm2) * ceil_div(D.d, ts.bn2) + g2s;
+    const long long gd = routed_row_tiles_ub(T, D.E, D.top_k, kSalTile) * S.nI;
+    if (g1 > 0x7fffffffLL || g2 > 0x7fffffffLL || gd > 0x7fffffffLL ||
+        3LL * D.E * S.nI * S.nM > 0x7fffffffLL)
+        return fail(FLEXMOE_ESHAPE, "tile grid too large");
+    {
+        Gemm1Params<bf16_t> p1{(const bf16_t*)x, (const bf16_t*)w_gate, (const bf16_t*)w_up,
+                               (const bf16_t*)ws_gate, (const bf16_t*)ws_up, perm, seg, t1, H, Hs, D.d, D.I,
+                               D.I_shared, D.E, D.top_k, nseg, T, kPartRange, 0, nseg, 0, 0, gt, ut, ht, S.ldt};
+        KernelTimer kt(FLEXMOE_K_GATE_UP, s);
+        err = launch_gemm1_big_train(p1, (int)g1, s);
+    }
+    if (err != hipSuccess) return hip_fail(err, "training gate/up GEMM launch");
+    {
+        Gemm2Params<bf16_t> p2{H, Hs, (const bf16_t*)w_down, (const bf16_t*)ws_down, seg, t2, O, Os, D.d, D.I,
+                               D.I_shared, D.E, nseg, T, 0, kPartRange, 0, nseg, (int)g2s, 0};
+        KernelTimer kt(FLEXMOE_K_DOWN, s);
+        err = launch_gemm2_big(p2, (int)g2, s);
+    }
+    if (err != hipSuccess) return hip_fail(err, "down GEMM launch");
+    {
+        KernelTimer kt(FLEXMOE_K_COMBINE, s);
+        err = launch_combine_residual(O, Os, pos, wts, T, D.top_k, D.d, has_shared ? 1 : 0, y_target, dy, s);
+    }
+    if (err != hipSuccess) return hip_fail(err, "residual launch");
+
+    // 4. backward: transposed x and dO, dgrad + SwiGLU backward, wgrad + Eq. 2
+    {
+        SalPrepParams pp{(const bf16_t*)x, dy, perm, wts, seg, xt, dot, dO, D.d, D.top_k, hs, nseg, S.ldt};
+        KernelTimer kt(FLEXMOE_K_SAL_PREP, s);
+        err = launch_sal_prep(pp, s);
+    }
+    if (err != hipSuccess) return hip_fail(err, "saliency prep launch");
+    {
+        SalDgradParams pd{dO, wdt, seg, gt, ut, dgt, dut, hs, nseg, D.d, D.I, S.ldt, S.nI};
+        KernelTimer kt(FLEXMOE_K_SAL_DGRAD, s);
+        err = launch_sal_dgrad(pd, gd, s);
+    }
+    if (err != hipSuccess) return hip_fail(err, "dgrad launch");
+    {
+        SalWgradParams pw{{xt, xt, dot}, {dgt, dut, ht}, {(const bf16_t*)w_gate, (const bf16_t*)w_up, wdt},
+                          seg, partial, hs, D.d, D.I, D.E, S.ldt, S.nI, S.nM};
+        KernelTimer kt(FLEXMOE_K_SAL_WGRAD, s);
+        err = launch_sal_wgrad(pw, s);
+    }
+    if (err != hipSuccess) return hip_fail(err, "wgrad launch");
+    {
+        KernelTimer kt(FLEXMOE_K_SAL_REDUCE, s);
+        err = launch_sal_reduce(partial, D.E, D.I, S.nM * kSalWaveM, scale, scores, s);
+    }
+    if (err != hipSuccess) return hip_fail(err, "saliency reduce launch");
+    return FLEXMOE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t flexmoe_saliency_workspace_bytes(const flexmoe_layer_desc* desc, int32_t T) {
+    if (check_desc(desc) != FLEXMOE_OK) return 0;
+    if (check_saliency_shape(*desc, T) != FLEXMOE_OK) return 0;
+    return sal_layout(*desc, T).total;
+}
+
+int flexmoe_channel_saliency(const flexmoe_layer_desc* desc, int32_t T, const void* x, const float* logits,
+                             const void* w_gate, const void* w_up, const void* w_down, const void* ws_gate,
+                             const void* ws_up, const void* ws_down, const float* y_target, float scale,
+                             float* scores, void* workspace, size_t workspace_bytes, void* stream) {
+    return saliency_impl(desc, T, x, logits, w_gate, w_up, w_down, ws_gate, ws_up, ws_down, y_target, scale,
+                         scores, workspace, workspace_bytes, stream);
 }
 
 }  // extern "C"

@@ -43,12 +43,13 @@
 // past the segment read the zero page).
 #include <type_traits>
 
-#include "kernels.h"
+#include "mfma_tile.h"
 
 namespace flexmoe {
 
 namespace {
-constexpr int BM = 256, BN = 256, BK = 64;
+using namespace mfma;
+constexpr int BM = 256, BN = 256;
 constexpr int NWAVE = 8, THREADS = 64 * NWAVE;
 constexpr int WAVES_PER_SIMD = NWAVE / 4;
 constexpr int WM = 2, WN = NWAVE / WM;      // wave grid
@@ -58,8 +59,6 @@ constexpr int WCOL = BN / WN;               // weight rows per wave
 constexpr int NSTAGE = 2;                   // LDS stages of BK-deep operand tiles
 constexpr int NSTEP = BK / 16;              // 16-deep MFMA steps per K tile
 static_assert(NSTEP == 4, "the K-loop schedule is laid out for four steps per K tile");
-constexpr int ROWB = BK * 2;                // bytes per LDS row
-constexpr int CHUNKS = ROWB / 16;           // 16-byte chunks per LDS row
 constexpr int RPI = 64 / CHUNKS;            // LDS rows filled per DMA instruction
 constexpr int ROWS_PER_WAVE = BM / NWAVE;   // A rows (and B rows) each wave loads
 constexpr int NI = ROWS_PER_WAVE / RPI;     // DMA instructions per wave per operand
@@ -67,63 +66,9 @@ constexpr int LOADS_PER_TILE = 2 * NI;      // DMA instructions per lane per K t
 constexpr int STAGE_A = BM * ROWB;          // 32 KB
 constexpr int STAGE = STAGE_A + BN * ROWB;  // 64 KB
 constexpr int XCD_GROUP = 8;                // consecutive tiles kept on one XCD
-typedef float floatx16 __attribute__((ext_vector_type(16)));
-typedef __attribute__((address_space(3))) void lds_ptr_t;
-
-// 16 lanes of a fragment read hit 16 consecutive rows at one logical chunk;
-// XOR-ing the chunk with row bits 1..3 spreads them over all 64 banks.
-__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & (CHUNKS - 1)); }
-
-// s_waitcnt with vmcnt = n and no wait on expcnt / lgkmcnt (gfx9 encoding).
-constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
-constexpr int kWaitLgkm0 = waitcnt_vm(63) & ~(15 << 8);  // lgkmcnt(0) only
-
-__device__ __forceinline__ bf16x8 lds_frag(const unsigned char* base, int row, int chunk) {
-    return __builtin_bit_cast(bf16x8,
-                              *reinterpret_cast<const u32x4*>(base + row * ROWB + swz(row, chunk) * 16));
-}
-
-// Raw buffer descriptor over `elems` bf16 elements (the extent must stay
-// below 2^31 bytes: the host checks the layer shape).  The fourth dword is
-// the gfx9 raw-buffer format word.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const bf16_t* base, size_t elems) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(base), (short)0, (int)(elems * 2),
-                                             0x00020000);
-}
-// A byte offset past every descriptor's extent: the load returns zeros (the
-// scalar offset added to it stays below 2^31, so it cannot wrap into range).
-constexpr uint32_t kOOB = 0x80000000u;
-
-// 16 bytes per lane from base + voff + soff straight into LDS (M0 = lds).
-__device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff,
-                                           unsigned char* lds) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t*)lds, 16, voff, soff, 0, 0);
-}
-
-// A bare s_barrier: a workgroup fence would also drain the DMAs of later K
-// tiles that should stay in flight.  Callers wait for their own LDS reads
-// and DMAs first.
-__device__ __forceinline__ void barrier_no_fence() {
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    __builtin_amdgcn_s_barrier();
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-}
-
-// Scheduling template for one 16-deep step: NMF MFMAs, NV vector memory
-// reads (DMA) and NRD LDS reads, issued round-robin.
-template <int NMF, int NV, int NRD>
-__device__ __forceinline__ void sched_interleave() {
-    constexpr int R = NMF > NRD ? (NMF > NV ? NMF : NV) : (NRD > NV ? NRD : NV);
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-        if (r < NMF) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-        if (r < NV) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM read (DMA)
-        if (r < NRD) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
-    }
-}
 }  // namespace
 
-template <bool kGateUp>
+template <bool kGateUp, bool kTrain = false>
 __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Gemm2Params<bf16_t>& p2,
                                          unsigned char* smem) {
     const int d = kGateUp ? p1.d : p2.d;
@@ -337,6 +282,36 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
                     *reinterpret_cast<uint2*>(hr + ch) = make_uint2(w[0], w[1]);
                 }
             }
+            if constexpr (kTrain) {
+                // transposed copies of g, u and h for the backward GEMMs:
+                // element [c][prow0 + row]; the rows up to the segment's
+                // padded height are written as zeros
+                if (!shared) {
+                    const int prow = packed_width(sm.rows);
+#pragma unroll
+                    for (int i = 0; i < MFW; ++i) {
+                        const int row = row_l + i * 32;
+                        if (row >= prow) continue;
+                        const bool real = row < sm.rows;
+                        const size_t col = (size_t)sm.prow0 + row;
+#pragma unroll
+                        for (int jj = 0; jj < NF / 2; ++jj)
+#pragma unroll
+                            for (int q = 0; q < 4; ++q) {
+                                const int ch = ntile * (BN / 2) + wn * (WCOL / 2) + jj * 32 + q * 8 + sub;
+                                if (ch >= sm.kg) continue;
+#pragma unroll
+                                for (int r = 0; r < 4; ++r) {
+                                    const float g = acc[i][jj][q * 4 + r], u = acc[i][jj + NF / 2][q * 4 + r];
+                                    const size_t o = (size_t)(ch + r) * p1.ldt + col;
+                                    p1.gt[o] = real ? f32_to_bf16(g) : (bf16_t)0;
+                                    p1.ut[o] = real ? f32_to_bf16(u) : (bf16_t)0;
+                                    p1.ht[o] = real ? f32_to_bf16(silu_fast(g) * u) : (bf16_t)0;
+                                }
+                            }
+                    }
+                }
+            }
         } else {
             bf16_t* Ob = shared ? p2.Os + (size_t)split * p2.tokens * d : p2.O + (size_t)sm.row0 * d;
 #pragma unroll
@@ -372,6 +347,13 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void gemm1_big_kernel(Gemm
     big_tile<true>(p, Gemm2Params<bf16_t>{}, smem);
 }
 
+// The gate/up GEMM of the training forward: the same tiles, plus the
+// transposed g, u and h copies of the routed segments (Gemm1Params).
+__global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void gemm1_big_train_kernel(Gemm1Params<bf16_t> p) {
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[NSTAGE * STAGE];
+    big_tile<true, true>(p, Gemm2Params<bf16_t>{}, smem);
+}
+
 __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void gemm2_big_kernel(Gemm2Params<bf16_t> p) {
     __shared__ __attribute__((aligned(1024))) unsigned char smem[NSTAGE * STAGE];
     big_tile<false>(Gemm1Params<bf16_t>{}, p, smem);
@@ -381,6 +363,13 @@ hipError_t launch_gemm1_big(const Gemm1Params<bf16_t>& p, int grid, hipStream_t 
     if (grid <= 0) return hipSuccess;
     const int g = (grid + 8 * XCD_GROUP - 1) / (8 * XCD_GROUP) * (8 * XCD_GROUP);
     gemm1_big_kernel<<<g, THREADS, 0, s>>>(p);
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm1_big_train(const Gemm1Params<bf16_t>& p, int grid, hipStream_t s) {
+    if (grid <= 0) return hipSuccess;
+    const int g = (grid + 8 * XCD_GROUP - 1) / (8 * XCD_GROUP) * (8 * XCD_GROUP);
+    gemm1_big_train_kernel<<<g, THREADS, 0, s>>>(p);
     return hipGetLastError();
 }
 

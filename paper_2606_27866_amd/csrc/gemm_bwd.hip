@@ -1,0 +1,334 @@
+// Backward GEMMs of the channel saliency (FlexMoE Sec. 3.1, Eq. 2) on bf16
+// MFMA.  For the loss L = 1/2 sum_t ||Y_t - Y_target_t||^2 and routed expert
+// e with dO_a = w_a dY_t (one row per routed assignment):
+//   dgrad:  dH[a][c] = sum_n dO_a[n] W_down[n][c]; fused epilogue
+//           dG = dH u silu'(g), dU = dH silu(g)           (SwiGLU backward)
+//   wgrad:  dW_gate[c][i] = sum_a dG[a][c] x_a[i], dW_up likewise with dU,
+//           dW_down[n][c] = sum_a dO_a[n] h_a[c]; fused epilogue
+//           s[e][c] += sum over the tile of (theta * dW)^2  (Eq. 2)
+// so the weight gradients are never written: each wgrad tile reduces its
+// 256 x 256 block of (theta * g)^2 to one partial sum per channel.
+//
+// Both kernels are "NT" GEMMs: A rows and B rows are contiguous in K, staged
+// by the same LDS pipeline as the forward's big tiles (mfma_tile.h: 256 x 256
+// x 64 tiles, 8 waves as 2 x 4, direct-to-LDS DMA, two stages, fragments one
+// step ahead).  The MFMA takes the A fragment first, so a lane's accumulator
+// holds one B row (a channel) and runs of 4 consecutive A rows: the
+// transposed stores of the dgrad epilogue and the weight reads of the wgrad
+// epilogue are 8-byte accesses.
+//   dgrad: A = dO [A][d] (a segment's rows), B = W_down^T [E][I][d] (a
+//          transposed copy of the down weights), K = d.
+//   wgrad: A = x^T or dO^T [d][ldt], B = dG^T, dU^T or h^T [I][ldt], with a
+//          segment's rows as K (columns prow0 .. prow0 + rows of the
+//          transposed copies, zero-padded to a multiple of 8).
+#include "mfma_tile.h"
+#include "saliency.h"
+
+namespace flexmoe {
+
+namespace {
+using namespace mfma;
+constexpr int BM = 256, BN = 256;
+constexpr int NWAVE = 8, THREADS = 64 * NWAVE;
+constexpr int WAVES_PER_SIMD = NWAVE / 4;
+constexpr int WM = 2, WN = NWAVE / WM;      // wave grid
+constexpr int NF = BN / (WN * 32);          // 32-row B fragments per wave
+constexpr int WCOL = BN / WN;               // B rows per wave
+constexpr int NSTAGE = 2;
+constexpr int NSTEP = BK / 16;
+static_assert(NSTEP == 4, "the K-loop schedule is laid out for four steps per K tile");
+constexpr int RPI = 64 / CHUNKS;            // LDS rows filled per DMA instruction
+constexpr int ROWS_PER_WAVE = BM / NWAVE;   // A rows (and B rows) each wave loads
+constexpr int NI = ROWS_PER_WAVE / RPI;     // DMA instructions per wave per operand
+constexpr int LOADS_PER_TILE = 2 * NI;
+constexpr int STAGE_A = BM * ROWB;
+constexpr int STAGE = STAGE_A + BN * ROWB;
+constexpr int XCD_GROUP = 8;
+static_assert(BM == kSalTile && BN == kSalTile, "host tile counts use kSalTile");
+
+// The operands of one tile: per-lane byte offsets of the A and B rows this
+// lane loads (kOOB for rows outside the operand), the chunk column of each,
+// and the reduction length.
+struct NTOperands {
+    __amdgpu_buffer_rsrc_t ra, rb;
+    uint32_t aoff[NI], boff[NI];
+    int acol[NI];
+    int K;
+};
+
+// DMA instruction i of a wave fills LDS rows wave*ROWS_PER_WAVE + i*RPI ..
+// +RPI; lane -> row lane/CHUNKS, LDS chunk lane%CHUNKS, which holds global
+// chunk swz(row, lane%CHUNKS).  Rows at or past `valid` (counted from the
+// operand's base) read zeros.
+__device__ __forceinline__ void nt_rows(int wave, int lane, int row_base, int valid, int ld, uint32_t* off,
+                                        int* acol) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+        const int r = wave * ROWS_PER_WAVE + i * RPI + lane / CHUNKS;
+        const int c = swz(r, lane % CHUNKS) * 8;
+        const int row = row_base + r;
+        acol[i] = c;
+        off[i] = row < valid ? (uint32_t)(((size_t)row * ld + c) * 2) : kOOB;
+    }
+}
+
+// The K loop of one tile whose waves multiply MFW 32-row A fragments each:
+// acc[i][j] = A rows wm*32*MFW + i*32 .. x B rows wn*WCOL + j*32 ...  The
+// schedule is the forward's (two LDS stages, fragments one step ahead).
+template <int MFW>
+__device__ __forceinline__ void nt_mainloop(unsigned char* smem, const NTOperands& op, int wave, int lane,
+                                            floatx16 (&acc)[MFW][NF]) {
+    constexpr int WR = 32 * MFW;
+    constexpr int NMF = MFW * NF;
+    constexpr int NRD = MFW + NF;
+    const int wm = wave / WN, wn = wave % WN;
+#pragma unroll
+    for (int i = 0; i < MFW; ++i)
+#pragma unroll
+        for (int j = 0; j < NF; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+    auto issue = [&](int kt, int stage) {
+        unsigned char* sa = smem + stage * STAGE + wave * ROWS_PER_WAVE * ROWB;
+        unsigned char* sb = sa + STAGE_A;
+        const int k0 = kt * BK;
+        const int lim = op.K - k0;
+        const uint32_t soff = (uint32_t)k0 * 2u;
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            const bool kin = op.acol[i] < lim;
+            load_lds16(op.ra, kin ? op.aoff[i] : kOOB, soff, sa + i * RPI * ROWB);
+            load_lds16(op.rb, kin ? op.boff[i] : kOOB, soff, sb + i * RPI * ROWB);
+        }
+    };
+    bf16x8 a[2][MFW], b[2][NF];
+    auto read_frags = [&](int kt, int ks, int buf) {
+        const unsigned char* sa = smem + (kt % NSTAGE) * STAGE;
+        const unsigned char* sb = sa + STAGE_A;
+        const int chunk = ks * 2 + (lane >> 5);
+#pragma unroll
+        for (int i = 0; i < MFW; ++i) a[buf][i] = lds_frag(sa, wm * WR + i * 32 + (lane & 31), chunk);
+#pragma unroll
+        for (int j = 0; j < NF; ++j) b[buf][j] = lds_frag(sb, wn * WCOL + j * 32 + (lane & 31), chunk);
+    };
+    auto mfma_step = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < MFW; ++i)
+#pragma unroll
+            for (int j = 0; j < NF; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][i], b[buf][j], acc[i][j], 0, 0, 0);
+    };
+    const int nk = ceil_div(op.K, BK);
+    issue(0, 0);
+    issue(1, 1);
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(LOADS_PER_TILE));
+    barrier_no_fence();
+    read_frags(0, 0, 0);
+    for (int kt = 0; kt < nk; ++kt) {
+#pragma unroll
+        for (int st = 0; st < NSTEP - 1; ++st) {
+            read_frags(kt, st + 1, (st + 1) & 1);
+            mfma_step(st & 1);
+            sched_interleave<NMF, 0, NRD>();
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm(0) & kWaitLgkm0);
+        barrier_no_fence();
+        __builtin_amdgcn_sched_barrier(0);
+        issue(kt + NSTAGE, kt % NSTAGE);
+        read_frags(kt + 1, 0, 0);
+        mfma_step((NSTEP - 1) & 1);
+        sched_interleave<NMF, LOADS_PER_TILE, NRD>();
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // no DMA may outlive the workgroup's LDS
+}
+
+// Runs `body` with the fragment count for a tile of `rows` A rows (the two
+// M-waves cover 64*MFW rows).
+template <typename F>
+__device__ __forceinline__ void by_rows(int rows, F&& body) {
+    if (rows > 3 * 64) body(std::integral_constant<int, 4>{});
+    else if (rows > 2 * 64) body(std::integral_constant<int, 3>{});
+    else if (rows > 64) body(std::integral_constant<int, 2>{});
+    else body(std::integral_constant<int, 1>{});
+}
+
+__device__ __forceinline__ int xcd_tile() {
+    const int jb = blockIdx.x >> 3;
+    return (jb / XCD_GROUP) * (8 * XCD_GROUP) + (blockIdx.x & 7) * XCD_GROUP + jb % XCD_GROUP;
+}
+
+__device__ __forceinline__ float lo_bf16(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float hi_bf16(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+}  // namespace
+
+// ---- dgrad: one tile = 256 rows of a routed segment x 256 channels --------
+__global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void sal_dgrad_kernel(SalDgradParams p) {
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[NSTAGE * STAGE];
+    const int L = xcd_tile();
+    // routed segment: the last one whose first tile is at or before L
+    int lo = p.hs, hi = p.nseg - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (p.seg[mid].rt0 * p.nI <= L) lo = mid;
+        else hi = mid - 1;
+    }
+    const SegMeta sm = p.seg[lo];
+    const int mt = ceil_div(sm.rows, BM);
+    const int local = L - sm.rt0 * p.nI;
+    if (local >= mt * p.nI) return;  // past the last tile (or an empty segment)
+    const int ntile = local / mt, mtile = local % mt;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+
+    NTOperands op;
+    op.K = p.d;
+    op.ra = make_rsrc(p.dO + (size_t)sm.row0 * p.d, (size_t)sm.rows * p.d);
+    op.rb = make_rsrc(p.wdt + (size_t)sm.e * p.I * p.d, (size_t)p.I * p.d);
+    int bcol[NI];
+    nt_rows(wave, lane, mtile * BM, sm.rows, p.d, op.aoff, op.acol);
+    nt_rows(wave, lane, ntile * BN, p.I, p.d, op.boff, bcol);  // same chunk columns as A
+
+    const int wm = wave / WN, wn = wave % WN;
+    by_rows(sm.rows - mtile * BM, [&](auto tag) {
+        constexpr int MFW = decltype(tag)::value;
+        floatx16 acc[MFW][NF];
+        nt_mainloop<MFW>(smem, op, wave, lane, acc);
+        // epilogue: lane -> channel c, register v -> row 8(v/4) + 4(lane/32) + v%4
+        const int prow = packed_width(sm.rows);
+#pragma unroll
+        for (int j = 0; j < NF; ++j) {
+            const int c = ntile * BN + wn * WCOL + j * 32 + (lane & 31);
+            if (c >= p.I) continue;
+            const size_t base = (size_t)c * p.ldt + sm.prow0;
+#pragma unroll
+            for (int i = 0; i < MFW; ++i)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int r0 = mtile * BM + wm * 32 * MFW + i * 32 + q * 8 + (lane >> 5) * 4;
+                    if (r0 >= prow) continue;
+                    const uint2 gv = *reinterpret_cast<const uint2*>(p.gt + base + r0);
+                    const uint2 uv = *reinterpret_cast<const uint2*>(p.ut + base + r0);
+                    const float g[4] = {lo_bf16(gv.x), hi_bf16(gv.x), lo_bf16(gv.y), hi_bf16(gv.y)};
+                    const float u[4] = {lo_bf16(uv.x), hi_bf16(uv.x), lo_bf16(uv.y), hi_bf16(uv.y)};
+                    uint32_t dg[2], du[2];
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        uint32_t pg = 0, pu = 0;
+#pragma unroll
+                        for (int r = 0; r < 2; ++r) {
+                            const int rr = h * 2 + r;
+                            float vg = 0.f, vu = 0.f;
+                            if (r0 + rr < sm.rows) {
+                                const float x = g[rr];
+                                const float sg = 1.0f / (1.0f + __builtin_amdgcn_exp2f(-x * 1.4426950408889634f));
+                                const float dh = acc[i][j][q * 4 + rr];
+                                vg = dh * u[rr] * (sg * (1.0f + x * (1.0f - sg)));
+                                vu = dh * (x * sg);
+                            }
+                            pg |= (uint32_t)f32_to_bf16(vg) << (16 * r);
+                            pu |= (uint32_t)f32_to_bf16(vu) << (16 * r);
+                        }
+                        dg[h] = pg;
+                        du[h] = pu;
+                    }
+                    *reinterpret_cast<uint2*>(p.dgt + base + r0) = make_uint2(dg[0], dg[1]);
+                    *reinterpret_cast<uint2*>(p.dut + base + r0) = make_uint2(du[0], du[1]);
+                }
+        }
+    });
+}
+
+// ---- wgrad + saliency: one tile = 256 hidden units x 256 channels of one
+// (matrix, expert) ----------------------------------------------------------
+__global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void sal_wgrad_kernel(SalWgradParams p) {
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[NSTAGE * STAGE];
+    const int L = xcd_tile();
+    if (L >= 3 * p.E * p.nI * p.nM) return;
+    const int mtile = L % p.nM;
+    int rest = L / p.nM;
+    const int ntile = rest % p.nI;
+    rest /= p.nI;
+    const int e = rest % p.E, mat = rest / p.E;
+    const SegMeta sm = p.seg[p.hs + e];
+    const int MP = p.nM * WM;  // partial sums per channel
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+    const int wm = wave / WN, wn = wave % WN;
+    float* part_out = p.partial + ((size_t)mat * p.E + e) * p.I * MP;
+
+    if (sm.rows == 0) {  // no token reached the expert: its gradient is zero
+        if (lane < 32)
+#pragma unroll
+            for (int j = 0; j < NF; ++j) {
+                const int c = ntile * BN + wn * WCOL + j * 32 + lane;
+                if (c < p.I) part_out[(size_t)c * MP + mtile * WM + wm] = 0.f;
+            }
+        return;
+    }
+
+    const bf16_t* A = p.a[mat] + sm.prow0;
+    const bf16_t* B = p.b[mat] + sm.prow0;
+    NTOperands op;
+    op.K = sm.rows;
+    op.ra = make_rsrc(A, (size_t)p.d * p.ldt - sm.prow0);
+    op.rb = make_rsrc(B, (size_t)p.I * p.ldt - sm.prow0);
+    int bcol[NI];
+    nt_rows(wave, lane, mtile * BM, p.d, p.ldt, op.aoff, op.acol);
+    nt_rows(wave, lane, ntile * BN, p.I, p.ldt, op.boff, bcol);
+
+    const bf16_t* W = p.w[mat] + (size_t)e * p.I * p.d;
+    by_rows(p.d - mtile * BM, [&](auto tag) {
+        constexpr int MFW = decltype(tag)::value;
+        floatx16 acc[MFW][NF];
+        nt_mainloop<MFW>(smem, op, wave, lane, acc);
+        // epilogue: theta is W[c][m] (gate, up, or the transposed down
+        // weight), read as runs of 4 hidden units m matching the accumulator
+        float part[NF];
+#pragma unroll
+        for (int j = 0; j < NF; ++j) {
+            part[j] = 0.f;
+            const int c = ntile * BN + wn * WCOL + j * 32 + (lane & 31);
+            if (c >= p.I) continue;
+            const bf16_t* wr = W + (size_t)c * p.d;
+#pragma unroll
+            for (int i = 0; i < MFW; ++i)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int m0 = mtile * BM + wm * 32 * MFW + i * 32 + q * 8 + (lane >> 5) * 4;
+                    if (m0 >= p.d) continue;
+                    const uint2 th = *reinterpret_cast<const uint2*>(wr + m0);
+                    const float t0 = lo_bf16(th.x) * acc[i][j][q * 4 + 0];
+                    const float t1 = hi_bf16(th.x) * acc[i][j][q * 4 + 1];
+                    const float t2 = lo_bf16(th.y) * acc[i][j][q * 4 + 2];
+                    const float t3 = hi_bf16(th.y) * acc[i][j][q * 4 + 3];
+                    part[j] += (t0 * t0 + t1 * t1) + (t2 * t2 + t3 * t3);
+                }
+        }
+#pragma unroll
+        for (int j = 0; j < NF; ++j) part[j] += __shfl_xor(part[j], 32, 64);
+        if (lane < 32)
+#pragma unroll
+            for (int j = 0; j < NF; ++j) {
+                const int c = ntile * BN + wn * WCOL + j * 32 + lane;
+                if (c < p.I) part_out[(size_t)c * MP + mtile * WM + wm] = part[j];
+            }
+    });
+}
+
+hipError_t launch_sal_dgrad(const SalDgradParams& p, long long tiles, hipStream_t s) {
+    if (tiles <= 0) return hipSuccess;
+    const long long g = (tiles + 8 * XCD_GROUP - 1) / (8 * XCD_GROUP) * (8 * XCD_GROUP);
+    sal_dgrad_kernel<<<(int)g, THREADS, 0, s>>>(p);
+    return hipGetLastError();
+}
+
+hipError_t launch_sal_wgrad(const SalWgradParams& p, hipStream_t s) {
+    const long long tiles = 3LL * p.E * p.nI * p.nM;
+    if (tiles <= 0) return hipSuccess;
+    const long long g = (tiles + 8 * XCD_GROUP - 1) / (8 * XCD_GROUP) * (8 * XCD_GROUP);
+    sal_wgrad_kernel<<<(int)g, THREADS, 0, s>>>(p);
+    return hipGetLastError();
+}
+
+}  // namespace flexmoe

@@ -39,6 +39,14 @@ struct Gemm1Params {
     int seg_lo, seg_hi;         // kPartRange: the segments covered
     int shared_tiles;           // tiles of the shared segment (kPartShared)
     int clipped;                // routed weights in the clipped layout (see RoutedWeights)
+    // Training forward only (launch_gemm1_big_train): the routed segments'
+    // pre-activations g, u and activations h, transposed -- element
+    // [c][prow0 + r] for row r of a segment -- with zeros in the rows
+    // [rows, packed_width(rows)) of each segment.  Row stride ldt.
+    T* gt;
+    T* ut;
+    T* ht;
+    int ldt;
 };
 
 // Down GEMM: O[row][n] = sum_{c < k_s} H[row][c] * W_down[n][c].  O holds one
@@ -91,7 +99,7 @@ __device__ __forceinline__ bool tile_of(const P& p, int L, int& s, SegMeta& sm, 
     if (p.part == kPartShared) {
         if (L >= p.shared_tiles) return false;
         s = 0;
-        sm = SegMeta{0, p.tokens, p.Is, 0, p.Is, -1, {0, 0}};
+        sm = SegMeta{0, p.tokens, p.Is, 0, p.Is, -1, 0, 0};
         local = L;
         return true;
     }

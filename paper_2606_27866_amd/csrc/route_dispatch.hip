@@ -163,13 +163,12 @@ __device__ void write_tables(CountFn count, const int* off, const int* kk_s, con
     const int lane = threadIdx.x & 63;
     const int hs = I_shared > 0 ? 1 : 0;
     const int nseg = E + hs;
-    int c1 = 0, c2 = 0;
+    int c1 = 0, c2 = 0, c3 = 0, c4 = 0;
     for (int s0 = 0; s0 < nseg; s0 += 64) {
         const int s = s0 + lane;
-        int n1 = 0, n2 = 0;
+        int n1 = 0, n2 = 0, n3 = 0, n4 = 0;
+        SegMeta m{};
         if (s < nseg) {
-            SegMeta m;
-            m.pad[0] = m.pad[1] = 0;
             if (s < hs) {
                 m.row0 = 0;
                 m.rows = T;
@@ -186,8 +185,9 @@ __device__ void write_tables(CountFn count, const int* off, const int* kk_s, con
                 m.ch0 = ch0[e];
                 m.kg = plan && m.kk > 0 ? min(max(plan[E + e], m.kk), I) : m.kk;
                 m.e = e;
+                n3 = packed_width(m.rows);
+                n4 = ceil_div(m.rows, ts.bm1);
             }
-            seg[s] = m;
             if (m.rows > 0 && m.kk > 0) {
                 n1 = ceil_div(m.rows, ts.bm1) * ceil_div(m.kg, ts.bn1);
                 n2 = ceil_div(m.rows, ts.bm2) * ceil_div(d, ts.bn2);
@@ -196,12 +196,18 @@ __device__ void write_tables(CountFn count, const int* off, const int* kk_s, con
         }
         if (s >= hs && s < nseg) offsets[s - hs] = off[s - hs];
         const int i1 = wave_incl_scan(n1), i2 = wave_incl_scan(n2);
+        const int i3 = wave_incl_scan(n3), i4 = wave_incl_scan(n4);
         if (s < nseg) {
             t1start[s] = c1 + i1 - n1;
             t2start[s] = c2 + i2 - n2;
+            m.prow0 = s < hs ? 0 : c3 + i3 - n3;
+            m.rt0 = s < hs ? 0 : c4 + i4 - n4;
+            seg[s] = m;
         }
         c1 += __shfl(i1, 63, 64);
         c2 += __shfl(i2, 63, 64);
+        c3 += __shfl(i3, 63, 64);
+        c4 += __shfl(i4, 63, 64);
     }
     if (lane == 0) {
         offsets[E] = P;

@@ -32,11 +32,13 @@ EXPORTED = ("flexmoe_workspace_bytes", "flexmoe_rank_reorder", "flexmoe_set_budg
             "flexmoe_layer_forward", "flexmoe_keep_from_ratio", "flexmoe_last_error",
             "flexmoe_timing_enable", "flexmoe_timing_read", "flexmoe_clipped_channels",
             "flexmoe_export_clipped", "flexmoe_layer_forward_clipped",
-            "flexmoe_layer_forward_bucketed")
+            "flexmoe_layer_forward_bucketed", "flexmoe_saliency_workspace_bytes",
+            "flexmoe_channel_saliency")
 
 # kernel indices of flexmoe_kernel_times
 KERNELS = ("route", "dispatch_scan", "dispatch_scatter", "gate_up", "down", "combine",
-           "gate_up_shared", "down_shared")
+           "gate_up_shared", "down_shared", "sal_transpose", "sal_prep", "sal_dgrad", "sal_wgrad",
+           "sal_reduce")
 
 
 class FlexMoEError(RuntimeError):
@@ -51,7 +53,7 @@ class flexmoe_layer_desc(ctypes.Structure):
 
 
 class flexmoe_kernel_times(ctypes.Structure):
-    _fields_ = [("ms", ctypes.c_double * 8), ("launches", ctypes.c_int64 * 8)]
+    _fields_ = [("ms", ctypes.c_double * len(KERNELS)), ("launches", ctypes.c_int64 * len(KERNELS))]
 
 
 class flexmoe_route_out(ctypes.Structure):
@@ -95,6 +97,11 @@ def lib():
         L.flexmoe_layer_forward_bucketed.argtypes = ([D, i32] + [vp] * 6 + [i32] + [vp] * 5
                                                      + [sz, ctypes.POINTER(flexmoe_route_out), vp])
         L.flexmoe_layer_forward_bucketed.restype = ctypes.c_int
+        L.flexmoe_saliency_workspace_bytes.argtypes = [D, i32]
+        L.flexmoe_saliency_workspace_bytes.restype = sz
+        L.flexmoe_channel_saliency.argtypes = ([D, i32] + [vp] * 9 + [ctypes.c_float] + [vp] * 2
+                                               + [sz, vp])
+        L.flexmoe_channel_saliency.restype = ctypes.c_int
         L.flexmoe_keep_from_ratio.argtypes = [ctypes.c_double, i32]
         L.flexmoe_keep_from_ratio.restype = ctypes.c_int
         L.flexmoe_timing_enable.argtypes = [ctypes.c_int]
@@ -233,6 +240,22 @@ def flexmoe_layer_forward_bucketed(desc, T, x, logits, w_gate_r, w_up_r, w_down_
         _stream(stream)))
 
 
+def flexmoe_saliency_workspace_bytes(desc: flexmoe_layer_desc, T: int) -> int:
+    n = lib().flexmoe_saliency_workspace_bytes(ctypes.byref(desc), int(T))
+    if n == 0:
+        raise FlexMoEError(-2, lib().flexmoe_last_error().decode())
+    return n
+
+
+def flexmoe_channel_saliency(desc, T, x, logits, w_gate, w_up, w_down, ws_gate, ws_up, ws_down,
+                             y_target, scale, scores, workspace, workspace_bytes=None, stream=None):
+    nbytes = workspace.numel() * workspace.element_size() if workspace_bytes is None else workspace_bytes
+    _check(lib().flexmoe_channel_saliency(ctypes.byref(desc), int(T), _p(x), _p(logits), _p(w_gate),
+                                          _p(w_up), _p(w_down), _p(ws_gate), _p(ws_up), _p(ws_down),
+                                          _p(y_target), float(scale), _p(scores), _p(workspace), nbytes,
+                                          _stream(stream)))
+
+
 class ClippedWeights:
     """The packed weights of one exported budget (offline clipping) and its
     device keep table."""
@@ -304,6 +327,39 @@ class Layer:
                               self.keep if keep is None else keep, self.ws_gate, self.ws_up,
                               self.ws_down, y, self.workspace, dbg=dbg, stream=stream)
         return y
+
+
+class Saliency:
+    """Channel ranking on the device (Sec. 3.1): the running Eq. 2 scores of
+    one layer over calibration batches, then the reorder of Eq. 3.
+
+    Holds the score table and a saliency workspace for up to max_tokens
+    tokens per batch; the weights are those of `layer` (original order).
+    """
+
+    def __init__(self, layer: "Layer", max_tokens: int):
+        import torch
+        self.layer = layer
+        self.desc = make_desc(layer.desc.d, layer.desc.E, layer.desc.I, layer.desc.top_k,
+                              layer.desc.I_shared, layer.desc.dtype, layer.desc.norm_topk, max_tokens)
+        nbytes = flexmoe_saliency_workspace_bytes(self.desc, max_tokens)
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=layer.device)
+        self.scores = torch.zeros((layer.desc.E, layer.desc.I), dtype=torch.float32, device=layer.device)
+
+    def add_batch(self, x, logits, y_target, scale=1.0, stream=None):
+        L = self.layer
+        flexmoe_channel_saliency(self.desc, x.shape[0], x, logits, L.w_gate, L.w_up, L.w_down, L.ws_gate,
+                                 L.ws_up, L.ws_down, y_target, scale, self.scores, self.workspace,
+                                 stream=stream)
+
+    def rank_reorder(self, stream=None):
+        """Ranked copies of the layer's weights and the permutation (Eq. 3)."""
+        import torch
+        L = self.layer
+        out = [torch.empty_like(w) for w in (L.w_gate, L.w_up, L.w_down)]
+        perm = torch.empty((L.desc.E, L.desc.I), dtype=torch.int32, device=L.device)
+        flexmoe_rank_reorder(L.desc, self.scores, L.w_gate, L.w_up, L.w_down, *out, perm, stream=stream)
+        return (*out, perm)
 
 
 def to_device(a: np.ndarray, device="cuda"):

@@ -204,6 +204,33 @@ def make_tokens(cfg: LayerConfig, T: Optional[int] = None, batch: int = -1,
     return _as_dtype(x, cfg.dtype), np.ascontiguousarray(lg)
 
 
+_TID_TARGET = 16
+_TID_CALIB_BATCH = 200  # calibration batch b of the saliency uses 200 + 2b and 201 + 2b
+
+
+def make_target(cfg: LayerConfig, T: Optional[int] = None, std: float = 0.05, batch: int = -1):
+    """Target [T][d] fp32 of the layer-level loss L = 1/2 sum_t ||Y_t - target_t||^2
+    the channel saliency is measured with: seeded Gaussian noise of the given std.
+    batch >= 0: the target of calibration batch `batch`."""
+    T = cfg.T if T is None else T
+    tid = _TID_TARGET if batch < 0 else _TID_CALIB_BATCH + 2 * batch + 1
+    return _normal(cfg.config_id, tid, T * cfg.d, std).reshape(T, cfg.d)
+
+
+def make_calibration_batch(cfg: LayerConfig, batch: int, T: Optional[int] = None,
+                           bias: Optional[np.ndarray] = None):
+    """Tokens x [T][d] and logits [T][E] of calibration batch `batch` (same
+    distributions as make_tokens, independent draws)."""
+    T = cfg.T if T is None else T
+    if bias is None:
+        bias = router_bias(cfg)
+    g = rng_for(cfg.config_id, _TID_CALIB_BATCH + 2 * batch)
+    x = g.standard_normal(T * cfg.d, dtype=np.float32).reshape(T, cfg.d) * np.float32(cfg.x_std)
+    lg = g.standard_normal(T * cfg.E, dtype=np.float32).reshape(T, cfg.E) * np.float32(cfg.logit_std)
+    lg = (lg + bias[None, :]).astype(np.float32)
+    return _as_dtype(x, cfg.dtype), np.ascontiguousarray(lg)
+
+
 def make_expert_weights(cfg: LayerConfig):
     """w_gate, w_up [E][I][d]; w_down [E][d][I] (output rows, channel columns).
 
