@@ -19,6 +19,11 @@ results (the nested 100/80/60/40/20 % tables) go into `per_budget`, each with
 the same budget run offline (exported as compact weights: the paper's static
 checkpoint mode) and the online/offline throughput ratio, and with the
 paper's bucketed kernel design (width groups, aligned widths) as an ablation.
+`saliency` times the one-time channel ranking on the device: the Eq. 2
+saliency of every routed channel over calibration batches of the workload's
+size (a layer-level squared-error loss against a seeded target), with the
+roofline of its dominant kernel (the weight-gradient GEMMs with the fused
+saliency reduction), the reorder of Eq. 3, and the oracle on a sample.
 """
 import argparse
 import hashlib
@@ -54,6 +59,10 @@ def parse():
     ap.add_argument("--copies", type=int, default=3, help="weight copies rotated over the steps")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-per-budget", action="store_true")
+    ap.add_argument("--no-saliency", action="store_true", help="skip the channel-saliency measurement")
+    ap.add_argument("--saliency-T", type=int, default=0,
+                    help="tokens per calibration batch of the saliency (default: the workload's T)")
+    ap.add_argument("--saliency-steps", type=int, default=10)
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-baseline work")
     ap.add_argument("--bucket-align", type=int, default=128,
                     help="k_align of the bucketed ablation in the per-budget results")
@@ -255,6 +264,111 @@ def cpu_baseline(wl, keep, target_s):
                        % (what, t))
 
 
+def saliency_section(wl, args):
+    """Channel ranking on the device (Eq. 2 saliency over calibration batches,
+    then the reorder of Eq. 3), timed per calibration batch."""
+    torch, fm, synth, cfg = wl.torch, wl.fm, wl.synth, wl.cfg
+    T = args.saliency_T or wl.T
+    bias = synth.router_bias(cfg)
+    nb = 4
+    batches = []
+    for b in range(nb):
+        x, lg = synth.make_calibration_batch(cfg, b, T, bias=bias)
+        batches.append((fm.to_device(x), fm.to_device(lg), fm.to_device(synth.make_target(cfg, T, batch=b))))
+    wl.use_copy(0)
+    sal = fm.Saliency(wl.layer, T)
+    steps = args.saliency_steps
+
+    def run(k, timed_kernels=False):
+        if timed_kernels:
+            fm.flexmoe_timing_enable(True)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(k):
+            x, lg, tg = batches[i % nb]
+            sal.add_batch(x, lg, tg, scale=1.0 / k)
+        e1.record()
+        torch.cuda.synchronize()
+        kt = None
+        if timed_kernels:
+            kt = fm.flexmoe_timing_read()
+            fm.flexmoe_timing_enable(False)
+        return e0.elapsed_time(e1), kt
+
+    run(2)
+    sal.scores.zero_()
+    ms, _ = run(steps)
+    _, kt = run(steps, timed_kernels=True)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    ranked = sal.rank_reorder()
+    e1.record()
+    torch.cuda.synchronize()
+    rank_ms = e0.elapsed_time(e1)
+    del ranked
+    ms_b = ms / steps
+    A = T * cfg.top_k
+    d, I, Is = cfg.d, cfg.I, cfg.I_shared
+    f_fwd = 6 * d * A * I + 6 * d * T * Is
+    f_dgrad = 2 * d * A * I
+    f_wgrad = 6 * d * A * I           # three weight gradients, every routed expert at full width
+    f_all = f_fwd + f_dgrad + f_wgrad
+    wg_ms, wg_n = kt["sal_wgrad"]
+    dg_ms, dg_n = kt["sal_dgrad"]
+    kms = {k: v[0] / max(v[1], 1) for k, v in kt.items() if v[1]}
+    wg_avg = wg_ms / max(wg_n, 1)
+    roof = dict(kernel="wgrad GEMMs + Eq. 2 reduction (sal_wgrad_kernel)", bound="mfma",
+                achieved=f_wgrad / (wg_avg / 1e3) / 1e12, peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
+                avg_launch_ms=wg_avg, flops_per_launch=f_wgrad,
+                theta_bytes_per_launch=3 * cfg.E * I * d * 2)
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    dg_avg = dg_ms / max(dg_n, 1)
+    out = dict(calibration_tokens=T, batches_timed=steps, ms_per_batch=ms_b, tokens_per_s=T / (ms_b / 1e3),
+               tflops=f_all / (ms_b / 1e3) / 1e12, frac_mfma=f_all / (ms_b / 1e3) / 1e12 / PEAK_BF16_TFLOPS,
+               flops_per_batch=f_all, rank_reorder_ms=rank_ms, roofline_wgrad=roof,
+               dgrad_tflops=f_dgrad / (dg_avg / 1e3) / 1e12, kernels_ms=kms,
+               loss="1/2 sum_t ||Y_t - target_t||^2 with a seeded Gaussian target (std 0.05)")
+    log("[bench] saliency: %d tokens/batch, %.4f ms/batch, %.0f tokens/s, %.1f TFLOP/s overall; wgrad %.4f ms "
+        "(%.1f TFLOP/s), dgrad %.4f ms (%.1f TFLOP/s); rank+reorder %.3f ms"
+        % (T, ms_b, T / (ms_b / 1e3), out["tflops"], wg_avg, roof["achieved"], dg_avg, out["dgrad_tflops"],
+           rank_ms))
+    for k, v in kms.items():
+        log("[bench]   saliency %-17s %8.4f ms" % (k, v))
+    if not args.no_cpu:
+        out["cpu_baseline"] = saliency_cpu_baseline(wl, T, args.cpu_seconds)
+        log("[bench] saliency CPU oracle: %.2f tokens/s on %d threads" % (out["cpu_baseline"]["value"],
+                                                                           out["cpu_baseline"]["cores"]))
+    return out
+
+
+def saliency_cpu_baseline(wl, T, target_s):
+    """The oracle's Eq. 2 on the first S tokens of calibration batch 0."""
+    import oracle
+    cfg, synth = wl.cfg, wl.synth
+    x, lg = synth.make_calibration_batch(cfg, 0, T)
+    tg = synth.make_target(cfg, T, batch=0)
+
+    def run(S):
+        t0 = time.time()
+        oracle.channel_saliency([(x[:S], lg[:S], tg[:S])], *wl.w, cfg.top_k, cfg.norm_topk, *wl.s)
+        return time.time() - t0
+
+    # a per-batch fixed part (the Eq. 2 sums over every weight) plus a
+    # per-token part: two probe sizes size the timed sample
+    Sa, Sb = min(64, T), min(256, T)
+    ta = run(Sa)
+    tb = run(Sb) if Sb != Sa else ta
+    c = max((tb - ta) / max(Sb - Sa, 1), 1e-6)
+    f = max(ta - c * Sa, 0.0)
+    S = int(min(T, max(Sb, (target_s - f) / c)))
+    t = run(S) if S != Sb else tb
+    return dict(value=S / t, unit="tokens/s", cores=oracle.num_threads(), kind="oracle",
+                sample="first %d of %d tokens of calibration batch 0, %.1f s (fp64); the whole batch would take "
+                       "about %.0f s (%.1f s per batch + %.2f ms per token)" % (S, T, t, f + c * T, f, c * 1e3))
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -399,6 +513,10 @@ def main():
                 "ragged/bucketed %.3f" % (name, synth.keep_fraction(wl.tables[name], cfg.I), widths, sb * 1e3,
                                           args.bucket_align, sk * 1e3, sk / sb))
 
+    saliency = None
+    if not args.no_saliency and bf16 and not wl.decode:
+        saliency = saliency_section(wl, args)
+
     if args.copy_calibration_mib > 0:
         n = args.copy_calibration_mib << 20
         src = torch.empty(n, dtype=torch.uint8, device="cuda")
@@ -435,6 +553,7 @@ def main():
         "layer": layer,
         "per_budget": per_budget,
         "action_set_ablation": action_ablation,
+        "saliency": saliency,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -74,10 +74,13 @@ __device__ __forceinline__ void nt_rows(int wave, int lane, int row_base, int va
 
 // The K loop of one tile whose waves multiply MFW 32-row A fragments each:
 // acc[i][j] = A rows wm*32*MFW + i*32 .. x B rows wn*WCOL + j*32 ...  The
-// schedule is the forward's (two LDS stages, fragments one step ahead).
-template <int MFW>
+// schedule is the forward's (two LDS stages, fragments one step ahead).  The
+// last two DMA slots of the loop (K tiles nk and nk+1, past the end) go to
+// tail(h, sa, sb) for h = 0, 1, which must issue exactly NI loads into each
+// of this wave's A and B parts of the freed stage (nk + h) % 2.
+template <int MFW, typename Tail>
 __device__ __forceinline__ void nt_mainloop(unsigned char* smem, const NTOperands& op, int wave, int lane,
-                                            floatx16 (&acc)[MFW][NF]) {
+                                            floatx16 (&acc)[MFW][NF], Tail&& tail) {
     constexpr int WR = 32 * MFW;
     constexpr int NMF = MFW * NF;
     constexpr int NRD = MFW + NF;
@@ -89,9 +92,14 @@ __device__ __forceinline__ void nt_mainloop(unsigned char* smem, const NTOperand
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
+    const int nk = ceil_div(op.K, BK);
     auto issue = [&](int kt, int stage) {
         unsigned char* sa = smem + stage * STAGE + wave * ROWS_PER_WAVE * ROWB;
         unsigned char* sb = sa + STAGE_A;
+        if (kt >= nk) {
+            tail(kt - nk, sa, sb);
+            return;
+        }
         const int k0 = kt * BK;
         const int lim = op.K - k0;
         const uint32_t soff = (uint32_t)k0 * 2u;
@@ -119,7 +127,6 @@ __device__ __forceinline__ void nt_mainloop(unsigned char* smem, const NTOperand
             for (int j = 0; j < NF; ++j)
                 acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][i], b[buf][j], acc[i][j], 0, 0, 0);
     };
-    const int nk = ceil_div(op.K, BK);
     issue(0, 0);
     issue(1, 1);
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(LOADS_PER_TILE));
@@ -144,6 +151,19 @@ __device__ __forceinline__ void nt_mainloop(unsigned char* smem, const NTOperand
     }
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // no DMA may outlive the workgroup's LDS
 }
+
+// Tail of a K loop that needs nothing after its last K tile: zero-page loads
+// keep the count of outstanding DMAs the schedule waits on.
+struct ZeroTail {
+    __amdgpu_buffer_rsrc_t r;
+    __device__ __forceinline__ void operator()(int, unsigned char* sa, unsigned char* sb) const {
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            load_lds16(r, kOOB, 0, sa + i * RPI * ROWB);
+            load_lds16(r, kOOB, 0, sb + i * RPI * ROWB);
+        }
+    }
+};
 
 // Runs `body` with the fragment count for a tile of `rows` A rows (the two
 // M-waves cover 64*MFW rows).
@@ -194,7 +214,7 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void sal_dgrad_kernel(SalD
     by_rows(sm.rows - mtile * BM, [&](auto tag) {
         constexpr int MFW = decltype(tag)::value;
         floatx16 acc[MFW][NF];
-        nt_mainloop<MFW>(smem, op, wave, lane, acc);
+        nt_mainloop<MFW>(smem, op, wave, lane, acc, ZeroTail{op.ra});
         // epilogue: lane -> channel c, register v -> row 8(v/4) + 4(lane/32) + v%4
         const int prow = packed_width(sm.rows);
 #pragma unroll
@@ -277,27 +297,46 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void sal_wgrad_kernel(SalW
     nt_rows(wave, lane, mtile * BM, p.d, p.ldt, op.aoff, op.acol);
     nt_rows(wave, lane, ntile * BN, p.I, p.ldt, op.boff, bcol);
 
+    // theta = W[c][m] of the tile's 256 channels x 256 hidden units (gate, up
+    // or the transposed down weight), brought into the two operand stages by
+    // the loop's last two DMA slots, while its last K tiles are multiplied.
+    // Stage (nk + h) % 2 holds channels h*128 .. +128, one 512-byte row each,
+    // 16-byte chunk pos of row r holding hidden units 8 * (pos ^ (r % 32)) ..
     const bf16_t* W = p.w[mat] + (size_t)e * p.I * p.d;
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(W, (size_t)p.I * p.d);
+    auto theta_tail = [&](int h, unsigned char* sa, unsigned char* sb) {
+#pragma unroll
+        for (int i = 0; i < NI; ++i)
+#pragma unroll
+            for (int part = 0; part < 2; ++part) {
+                const int tr = part * 64 + wave * 8 + 2 * i + (lane >> 5);  // theta row of the stage
+                const int c = ntile * BN + h * 128 + tr;
+                const int m = mtile * BM + ((lane & 31) ^ (tr & 31)) * 8;
+                const uint32_t off = c < p.I && m < p.d ? (uint32_t)(((size_t)c * p.d + m) * 2) : kOOB;
+                load_lds16(rw, off, 0, (part ? sb : sa) + i * RPI * ROWB);
+            }
+    };
+    const int nk = ceil_div(op.K, BK);
     by_rows(p.d - mtile * BM, [&](auto tag) {
         constexpr int MFW = decltype(tag)::value;
         floatx16 acc[MFW][NF];
-        nt_mainloop<MFW>(smem, op, wave, lane, acc);
-        // epilogue: theta is W[c][m] (gate, up, or the transposed down
-        // weight), read as runs of 4 hidden units m matching the accumulator
+        nt_mainloop<MFW>(smem, op, wave, lane, acc, theta_tail);
+        barrier_no_fence();  // every wave's theta DMAs have landed
+        // epilogue: lane -> channel c, register v -> hidden unit
+        // 8(v/4) + 4(lane/32) + v%4 of a fragment; (theta * dW)^2 summed
         float part[NF];
 #pragma unroll
         for (int j = 0; j < NF; ++j) {
             part[j] = 0.f;
-            const int c = ntile * BN + wn * WCOL + j * 32 + (lane & 31);
-            if (c >= p.I) continue;
-            const bf16_t* wr = W + (size_t)c * p.d;
+            const int cl = wn * WCOL + j * 32 + (lane & 31);  // channel within the tile
+            const unsigned char* trow = smem + ((nk + (cl >> 7)) & 1) * STAGE + (cl & 127) * 512;
 #pragma unroll
             for (int i = 0; i < MFW; ++i)
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const int m0 = mtile * BM + wm * 32 * MFW + i * 32 + q * 8 + (lane >> 5) * 4;
-                    if (m0 >= p.d) continue;
-                    const uint2 th = *reinterpret_cast<const uint2*>(wr + m0);
+                    const int ml = wm * 32 * MFW + i * 32 + q * 8 + (lane >> 5) * 4;
+                    const uint2 th = *reinterpret_cast<const uint2*>(
+                        trow + (((ml >> 3) ^ (cl & 31)) << 4) + (ml & 7) * 2);
                     const float t0 = lo_bf16(th.x) * acc[i][j][q * 4 + 0];
                     const float t1 = hi_bf16(th.x) * acc[i][j][q * 4 + 1];
                     const float t2 = lo_bf16(th.y) * acc[i][j][q * 4 + 2];
