@@ -59,7 +59,11 @@ def lib():
         L.oracle_num_threads.argtypes = []
         L.oracle_layer_grads.argtypes = [i] * 8 + [p] * 14
         L.oracle_channel_saliency.argtypes = [i] * 4 + [p] * 7
-        for f in (L.oracle_route, L.oracle_dispatch, L.oracle_layer_forward,
+        L.oracle_sample_actions.argtypes = [i, i, p, i, p, p, ctypes.c_double, p, p, p]
+        L.oracle_masked_backward.argtypes = [i] * 8 + [p] * 13
+        L.oracle_action_grad.argtypes = [i, i, p, i, p, p, ctypes.c_double, p, p, ctypes.c_longlong,
+                                         ctypes.c_double, ctypes.c_double, p, p, p]
+        for f in (L.oracle_sample_actions, L.oracle_masked_backward, L.oracle_action_grad,L.oracle_route, L.oracle_dispatch, L.oracle_layer_forward,
                   L.oracle_rank_reorder, L.oracle_keep_from_ratio, L.oracle_num_threads,
                   L.oracle_layer_grads, L.oracle_channel_saliency):
             f.restype = ctypes.c_int
@@ -239,6 +243,69 @@ def channel_saliency(batches, w_gate, w_up, w_down, top_k, norm_topk,
                                     y_target, ws_gate, ws_up, ws_down)
         total += channel_saliency_from_grads(w_gate, w_up, w_down, gg, gu, gd)
     return total / max(len(batches), 1)
+
+
+def sample_actions(ratios, I, alpha, gumbel, tau):
+    """Eq. 5: (keep [E] int32, action [E] int32, z_soft [E][K] fp64)."""
+    alpha = np.ascontiguousarray(alpha, dtype=np.float32)
+    gumbel = np.ascontiguousarray(gumbel, dtype=np.float32)
+    E, K = alpha.shape
+    r = np.ascontiguousarray(ratios, dtype=np.float64)
+    keep = np.empty(E, np.int32)
+    act = np.empty(E, np.int32)
+    zs = np.empty((E, K), np.float64)
+    rc = lib().oracle_sample_actions(E, K, _ptr(r), int(I), _ptr(alpha), _ptr(gumbel), float(tau),
+                                     _ptr(keep), _ptr(zs), _ptr(act))
+    if rc != 0:
+        raise ValueError("oracle_sample_actions failed (%d)" % rc)
+    return keep, act, zs
+
+
+def masked_backward(x, logits, w_gate, w_up, w_down, keep, top_k, norm_topk, dy,
+                    ws_gate=None, ws_up=None, ws_down=None):
+    """Backward of the masked layer for the upstream gradient dy [T][d] fp32:
+    (dx [T][d], dlogits [T][E], dmask [E][I]), fp64."""
+    x = np.ascontiguousarray(x)
+    dtype = _dtype_of(x)
+    logits = np.ascontiguousarray(logits, dtype=np.float32)
+    T, d = x.shape
+    E, I, _ = w_gate.shape
+    I_s = 0 if ws_gate is None else ws_gate.shape[0]
+    dy = np.ascontiguousarray(dy, dtype=np.float32)
+    keep = np.ascontiguousarray(keep, dtype=np.int32)
+    dx = np.empty((T, d), np.float64)
+    dl = np.empty((T, E), np.float64)
+    dm = np.empty((E, I), np.float64)
+    rc = lib().oracle_masked_backward(
+        T, d, E, I, top_k, I_s, dtype, int(norm_topk), _ptr(x), _ptr(logits),
+        _ptr(np.ascontiguousarray(w_gate)), _ptr(np.ascontiguousarray(w_up)),
+        _ptr(np.ascontiguousarray(w_down)), _ptr(keep),
+        _ptr(None if ws_gate is None else np.ascontiguousarray(ws_gate)),
+        _ptr(None if ws_up is None else np.ascontiguousarray(ws_up)),
+        _ptr(None if ws_down is None else np.ascontiguousarray(ws_down)),
+        _ptr(dy), _ptr(dx), _ptr(dl), _ptr(dm))
+    if rc != 0:
+        raise ValueError("oracle_masked_backward failed (%d)" % rc)
+    return dx, dl, dm
+
+
+def action_grad(ratios, I, alpha, gumbel, tau, dmask, counts, assignments, lambda_cost, beta):
+    """Eqs. 5-8: (dalpha [E][K] fp64, cost C, entropy H)."""
+    alpha = np.ascontiguousarray(alpha, dtype=np.float32)
+    gumbel = np.ascontiguousarray(gumbel, dtype=np.float32)
+    E, K = alpha.shape
+    r = np.ascontiguousarray(ratios, dtype=np.float64)
+    dm = np.ascontiguousarray(dmask, dtype=np.float64)
+    cnt = np.ascontiguousarray(counts, dtype=np.int32)
+    da = np.empty((E, K), np.float64)
+    c = np.zeros(1, np.float64)
+    h = np.zeros(1, np.float64)
+    rc = lib().oracle_action_grad(E, K, _ptr(r), int(I), _ptr(alpha), _ptr(gumbel), float(tau), _ptr(dm),
+                                  _ptr(cnt), int(assignments), float(lambda_cost), float(beta), _ptr(da),
+                                  _ptr(c), _ptr(h))
+    if rc != 0:
+        raise ValueError("oracle_action_grad failed (%d)" % rc)
+    return da, float(c[0]), float(h[0])
 
 
 def packed_width(k: int) -> int:

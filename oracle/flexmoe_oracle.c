@@ -24,7 +24,12 @@
  *     down column j) of (theta * dL/dtheta)^2.  The paper's loss is the
  *     language-model loss; here it is the layer-level
  *     L = 1/2 sum_t ||y_t - y_target_t||^2, with the gradients written out
- *     by the chain rule (router weights and logits are inputs, not trained).
+ *     by the chain rule (router weights and logits are inputs, not trained);
+ *   - action learning (Sec. 3.2, Eqs. 5-8): the straight-through Gumbel-softmax
+ *     sample of one discrete width per expert, the backward of the masked
+ *     layer (input, router-logit and mask gradients), and the gradient of the
+ *     action logits through the straight-through estimator plus the
+ *     load-weighted cost and the entropy regulariser.
  *
  * Readings where the paper is silent (each listed with its reason in the
  * design notes):
@@ -446,6 +451,281 @@ int oracle_channel_saliency(int d, int E, int I, int dtype, const void *w_gate, 
             s[(size_t)e * I + j] = acc;
         }
     }
+    return 0;
+}
+
+/* Eq. 5: per expert, z_soft = softmax((alpha + g) / tau) over the K actions
+ * and the hard action k* = argmax; the sampled width is ceil(r_k* * I).  The
+ * argmax is taken on the fp32 sums alpha + g (the softmax is monotone in
+ * them), the first index on ties.  alpha, gumbel [E][K] fp32; ratio [K];
+ * keep [E], action [E] (int32), z_soft [E][K] fp64 (any may be NULL). */
+int oracle_keep_from_ratio(double r, int I);
+int oracle_sample_actions(int E, int K, const double *ratio, int I, const float *alpha,
+                          const float *gumbel, double tau, int32_t *keep, double *z_soft,
+                          int32_t *action)
+{
+    if (E < 1 || K < 1 || I < 1 || !ratio || !alpha || !gumbel || !(tau > 0.0))
+        return -1;
+    for (int e = 0; e < E; ++e) {
+        const float *a = alpha + (size_t)e * K, *g = gumbel + (size_t)e * K;
+        int best = 0;
+        for (int k = 1; k < K; ++k)
+            if (a[k] + g[k] > a[best] + g[best])
+                best = k;
+        double m = -INFINITY, z = 0.0;
+        for (int k = 0; k < K; ++k)
+            if (((double)a[k] + g[k]) / tau > m)
+                m = ((double)a[k] + g[k]) / tau;
+        for (int k = 0; k < K; ++k)
+            z += exp(((double)a[k] + g[k]) / tau - m);
+        if (z_soft)
+            for (int k = 0; k < K; ++k)
+                z_soft[(size_t)e * K + k] = exp(((double)a[k] + g[k]) / tau - m) / z;
+        if (action)
+            action[e] = best;
+        if (keep)
+            keep[e] = oracle_keep_from_ratio(ratio[best], I);
+    }
+    return 0;
+}
+
+/* Backward of the masked layer for an upstream gradient dY [T][d] (Sec. 3.2:
+ * the sampled subnet's forward is the masked layer, h_c = M_c a_c with
+ * a_c = silu(g_c) u_c and the prefix mask M_c = [c < k_e]).  With
+ * dO_a = w_a dY_t and dh'_c = sum_n W_down[n][c] dO_a[n] for every channel:
+ *   dM[e][c]    = sum over e's assignments of dh'_c a_c   (all c < I)
+ *   dg_c, du_c  = M_c dh'_c u_c silu'(g_c),  M_c dh'_c silu(g_c)
+ *   dx_t       += sum_c dg_c W_gate[c] + du_c W_up[c]  (+ the shared expert's
+ *                 terms, with dO = dY_t and no mask)
+ *   dw_a        = <dY_t, O_a>, then through the router weights of
+ *                 oracle_route to the logits: with p = softmax(logits),
+ *                 w_j = p_{i_j} (/ sum_j p_{i_j} if norm_topk).
+ * Experts with k_e = 0 are skipped, as in the forward.  Outputs (fp64,
+ * overwritten): dx [T][d], dlogits [T][E], dmask [E][I]. */
+int oracle_masked_backward(int T, int d, int E, int I, int k, int I_s, int dtype, int norm_topk,
+                           const void *x, const float *logits, const void *w_gate,
+                           const void *w_up, const void *w_down, const int32_t *keep,
+                           const void *ws_gate, const void *ws_up, const void *ws_down,
+                           const float *dy, double *dx, double *dlogits, double *dmask)
+{
+    if (T < 0 || d < 1 || E < 1 || I < 1 || k < 1 || k > E || I_s < 0 || !keep || !dy || !dx ||
+        !dlogits || !dmask)
+        return -1;
+    for (int e = 0; e < E; ++e)
+        if (keep[e] < 0 || keep[e] > I)
+            return -3;
+    memset(dx, 0, (size_t)T * d * sizeof(double));
+    memset(dlogits, 0, (size_t)T * E * sizeof(double));
+    memset(dmask, 0, (size_t)E * I * sizeof(double));
+    if (T == 0)
+        return 0;
+    size_t A = (size_t)T * k;
+    int32_t *idx = (int32_t *)malloc(A * sizeof(int32_t));
+    double *w = (double *)malloc(A * sizeof(double));
+    int32_t *counts = (int32_t *)malloc((size_t)E * sizeof(int32_t));
+    int32_t *offsets = (int32_t *)malloc((size_t)(E + 1) * sizeof(int32_t));
+    int32_t *perm = (int32_t *)malloc(A * sizeof(int32_t));
+    int32_t *pos = (int32_t *)malloc(A * sizeof(int32_t));
+    double *dw = (double *)calloc(A, sizeof(double));
+    double *dxa = (double *)calloc(A * (size_t)d, sizeof(double)); /* per-assignment dx */
+    int rc = -1;
+    if (!idx || !w || !counts || !offsets || !perm || !pos || !dw || !dxa)
+        goto done;
+    if (oracle_route(T, E, k, logits, norm_topk, idx, w) != 0)
+        goto done;
+    if (oracle_dispatch(T, E, k, idx, keep, counts, offsets, perm, pos) < 0)
+        goto done;
+
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int e = 0; e < E; ++e) {
+        int kk = keep[e];
+        if (kk == 0)
+            continue;
+        double *g = (double *)malloc((size_t)I * sizeof(double));
+        double *u = (double *)malloc((size_t)I * sizeof(double));
+        double *h = (double *)malloc((size_t)I * sizeof(double));
+        const size_t wb = (size_t)e * I * d;
+        for (int p = offsets[e]; p < offsets[e + 1]; ++p) {
+            int a = perm[p], t = a / k;
+            const size_t xo = (size_t)t * d;
+            for (int c = 0; c < I; ++c) {
+                double gc = 0.0, uc = 0.0;
+                for (int i = 0; i < d; ++i) {
+                    double xi = elem(x, dtype, xo + i);
+                    gc += elem(w_gate, dtype, wb + (size_t)c * d + i) * xi;
+                    uc += elem(w_up, dtype, wb + (size_t)c * d + i) * xi;
+                }
+                g[c] = gc;
+                u[c] = uc;
+            }
+            /* dw_a = <dY_t, O_a>, O_a over the kept channels */
+            for (int c = 0; c < kk; ++c)
+                h[c] = g[c] / (1.0 + exp(-g[c])) * u[c];
+            double dwa = 0.0;
+            for (int n = 0; n < d; ++n) {
+                double o = 0.0;
+                for (int c = 0; c < kk; ++c)
+                    o += h[c] * elem(w_down, dtype, wb + (size_t)n * I + c);
+                dwa += (double)dy[xo + n] * o;
+            }
+            dw[a] = dwa;
+            for (int c = 0; c < I; ++c) {
+                double sg = 1.0 / (1.0 + exp(-g[c]));
+                double silu = g[c] * sg, dsilu = sg * (1.0 + g[c] * (1.0 - sg));
+                double dh = 0.0;
+                for (int n = 0; n < d; ++n)
+                    dh += elem(w_down, dtype, wb + (size_t)n * I + c) * w[a] * (double)dy[xo + n];
+                dmask[(size_t)e * I + c] += dh * silu * u[c];
+                if (c >= kk)
+                    continue;
+                double dg = dh * u[c] * dsilu, du = dh * silu;
+                for (int i = 0; i < d; ++i)
+                    dxa[(size_t)a * d + i] += dg * elem(w_gate, dtype, wb + (size_t)c * d + i) +
+                                              du * elem(w_up, dtype, wb + (size_t)c * d + i);
+            }
+        }
+        free(g);
+        free(u);
+        free(h);
+    }
+
+#pragma omp parallel for schedule(static)
+    for (int t = 0; t < T; ++t) {
+        double *dxt = dx + (size_t)t * d;
+        for (int j = 0; j < k; ++j)
+            for (int i = 0; i < d; ++i)
+                dxt[i] += dxa[((size_t)t * k + j) * d + i];
+        if (I_s > 0) {
+            const size_t xo = (size_t)t * d;
+            for (int c = 0; c < I_s; ++c) {
+                double gc = 0.0, uc = 0.0;
+                for (int i = 0; i < d; ++i) {
+                    double xi = elem(x, dtype, xo + i);
+                    gc += elem(ws_gate, dtype, (size_t)c * d + i) * xi;
+                    uc += elem(ws_up, dtype, (size_t)c * d + i) * xi;
+                }
+                double sg = 1.0 / (1.0 + exp(-gc));
+                double dh = 0.0;
+                for (int n = 0; n < d; ++n)
+                    dh += elem(ws_down, dtype, (size_t)n * I_s + c) * (double)dy[xo + n];
+                double dg = dh * uc * sg * (1.0 + gc * (1.0 - sg)), du = dh * gc * sg;
+                for (int i = 0; i < d; ++i)
+                    dxt[i] += dg * elem(ws_gate, dtype, (size_t)c * d + i) +
+                              du * elem(ws_up, dtype, (size_t)c * d + i);
+            }
+        }
+        /* router: softmax over all E, then the optional renormalisation */
+        const float *l = logits + (size_t)t * E;
+        double m = -INFINITY, z = 0.0;
+        for (int e = 0; e < E; ++e)
+            if ((double)l[e] > m)
+                m = (double)l[e];
+        for (int e = 0; e < E; ++e)
+            z += exp((double)l[e] - m);
+        double S = 0.0;
+        for (int j = 0; j < k; ++j)
+            S += exp((double)l[idx[(size_t)t * k + j]] - m) / z;
+        /* dL/dp_i for the selected experts */
+        double dwsum = 0.0;
+        for (int j = 0; j < k; ++j)
+            dwsum += dw[(size_t)t * k + j] * w[(size_t)t * k + j];
+        double dpp = 0.0; /* sum_i dL/dp_i * p_i */
+        double *dp = (double *)calloc((size_t)E, sizeof(double));
+        for (int j = 0; j < k; ++j) {
+            int e = idx[(size_t)t * k + j];
+            double g = norm_topk ? (dw[(size_t)t * k + j] - dwsum) / S : dw[(size_t)t * k + j];
+            dp[e] = g;
+            dpp += g * exp((double)l[e] - m) / z;
+        }
+        for (int e = 0; e < E; ++e) {
+            double pe = exp((double)l[e] - m) / z;
+            dlogits[(size_t)t * E + e] = pe * (dp[e] - dpp);
+        }
+        free(dp);
+    }
+    rc = 0;
+done:
+    free(idx);
+    free(w);
+    free(counts);
+    free(offsets);
+    free(perm);
+    free(pos);
+    free(dw);
+    free(dxa);
+    return rc;
+}
+
+/* Gradient of the action logits (Eqs. 5-8) for one layer:
+ *   quality term through the straight-through estimator (Eq. 6): the forward
+ *     mask is M = sum_k z~_k m(r_k), so dL/dz~_k = sum_{c < K_k} dmask[c]
+ *     (K_k = ceil(r_k I)); z~ passes it to z_soft unchanged, and
+ *     z_soft = softmax(s), s = (alpha + g) / tau gives
+ *     dalpha_k = z_soft_k (dz_k - sum_j z_soft_j dz_j) / tau;
+ *   cost (Eq. 7): C = sum_e q_e sum_k p_{e,k} r_k with p_e = softmax(alpha_e)
+ *     and q_e = counts_e / (T * top_k), constant in alpha:
+ *     dC/dalpha_{e,k} = q_e p_{e,k} (r_k - sum_j p_{e,j} r_j);
+ *   entropy (Eq. 8 and the text after it): H = (1/E) sum_e -sum_k p log p,
+ *     dH/dalpha_{e,k} = -(1/E) p_{e,k} (log p_{e,k} + H_e);
+ *   dalpha = dalpha_quality + lambda_cost dC/dalpha - beta dH/dalpha.
+ * dalpha [E][K] fp64; *cost = C, *entropy = H. */
+int oracle_action_grad(int E, int K, const double *ratio, int I, const float *alpha,
+                       const float *gumbel, double tau, const double *dmask,
+                       const int32_t *counts, long long assignments, double lambda_cost,
+                       double beta, double *dalpha, double *cost, double *entropy)
+{
+    if (E < 1 || K < 1 || I < 1 || !ratio || !alpha || !gumbel || !dmask || !counts || !dalpha ||
+        !(tau > 0.0) || assignments < 1)
+        return -1;
+    double *zs = (double *)malloc((size_t)E * K * sizeof(double));
+    if (!zs)
+        return -1;
+    oracle_sample_actions(E, K, ratio, I, alpha, gumbel, tau, NULL, zs, NULL);
+    double C = 0.0, H = 0.0;
+    for (int e = 0; e < E; ++e) {
+        const float *a = alpha + (size_t)e * K;
+        const double *z = zs + (size_t)e * K;
+        double dz[64], p[64];
+        if (K > 64) {
+            free(zs);
+            return -1;
+        }
+        for (int kk = 0; kk < K; ++kk) {
+            int w = oracle_keep_from_ratio(ratio[kk], I);
+            dz[kk] = 0.0;
+            for (int c = 0; c < w; ++c)
+                dz[kk] += dmask[(size_t)e * I + c];
+        }
+        double zdz = 0.0;
+        for (int kk = 0; kk < K; ++kk)
+            zdz += z[kk] * dz[kk];
+        double m = -INFINITY, Z = 0.0;
+        for (int kk = 0; kk < K; ++kk)
+            if ((double)a[kk] > m)
+                m = (double)a[kk];
+        for (int kk = 0; kk < K; ++kk)
+            Z += exp((double)a[kk] - m);
+        double rbar = 0.0, He = 0.0;
+        for (int kk = 0; kk < K; ++kk) {
+            p[kk] = exp((double)a[kk] - m) / Z;
+            rbar += p[kk] * ratio[kk];
+            He -= p[kk] > 0.0 ? p[kk] * log(p[kk]) : 0.0;
+        }
+        double q = (double)counts[e] / (double)assignments;
+        C += q * rbar;
+        H += He / E;
+        for (int kk = 0; kk < K; ++kk) {
+            double g_quality = z[kk] * (dz[kk] - zdz) / tau;
+            double g_cost = q * p[kk] * (ratio[kk] - rbar);
+            double g_ent = p[kk] > 0.0 ? -p[kk] * (log(p[kk]) + He) / E : 0.0;
+            dalpha[(size_t)e * K + kk] = g_quality + lambda_cost * g_cost - beta * g_ent;
+        }
+    }
+    if (cost)
+        *cost = C;
+    if (entropy)
+        *entropy = H;
+    free(zs);
     return 0;
 }
 

@@ -38,16 +38,31 @@ MUTANTS = {
                                "g_up[wb + (size_t)c * d + i] += dg * xi;"),
     "saliency_down_not_squared": ("acc += td * td;", "acc += fabs(td);"),
     "saliency_gate_term_dropped": ("acc += tg * tg + tu * tu;", "acc += tu * tu;"),
+    "dmask_only_kept_channels": ("dmask[(size_t)e * I + c] += dh * silu * u[c];",
+                                 "if (c < kk) dmask[(size_t)e * I + c] += dh * silu * u[c];"),
+    "router_grad_ignores_renorm": ("double g = norm_topk ? (dw[(size_t)t * k + j] - dwsum) / S : dw[(size_t)t * k + j];",
+                                   "double g = dw[(size_t)t * k + j];"),
+    "st_gradient_without_tau": ("double g_quality = z[kk] * (dz[kk] - zdz) / tau;",
+                                "double g_quality = z[kk] * (dz[kk] - zdz);"),
+    "entropy_gradient_sign": ("double g_ent = p[kk] > 0.0 ? -p[kk] * (log(p[kk]) + He) / E : 0.0;",
+                              "double g_ent = p[kk] > 0.0 ? p[kk] * (log(p[kk]) + He) / E : 0.0;"),
+    "cost_not_load_weighted": ("double q = (double)counts[e] / (double)assignments;", "double q = 1.0;"),
+    "sample_tie_takes_last": ("if (a[k] + g[k] > a[best] + g[best])", "if (a[k] + g[k] >= a[best] + g[best])"),
+    "shared_input_grad_dropped": ("                    dxt[i] += dg * elem(ws_gate, dtype, (size_t)c * d + i) +\n"
+                                  "                              du * elem(ws_up, dtype, (size_t)c * d + i);",
+                                  "                    dxt[i] += 0.0 * dg * elem(ws_gate, dtype, (size_t)c * d + i);"),
     "prefix_short_by_one": ("    for (int c = 0; c < kk; ++c) {\n        double g = 0.0, u = 0.0;",
                             "    for (int c = 0; c < kk; ++c) {\n        if (c == kk - 1 && kk > 1) { h[c] = 0; continue; }\n        double g = 0.0, u = 0.0;"),
 }
 
 
 def _run_pins(lib_path):
-    env = dict(os.environ, FLEXMOE_ORACLE_LIB=lib_path)
+    # small pin cases: one OpenMP thread per run (parallel test workers would oversubscribe)
+    env = dict(os.environ, FLEXMOE_ORACLE_LIB=lib_path, OMP_NUM_THREADS="1")
     return subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
                            os.path.join(ROOT, "tests", "test_oracle_pins.py"),
-                           os.path.join(ROOT, "tests", "test_saliency_pins.py")],
+                           os.path.join(ROOT, "tests", "test_saliency_pins.py"),
+                           os.path.join(ROOT, "tests", "test_action_pins.py")],
                           cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
 
 
