@@ -157,6 +157,93 @@ int flexmoe_channel_saliency(const flexmoe_layer_desc *desc, int32_t T, const vo
                              float *scores, void *workspace, size_t workspace_bytes,
                              void *stream);
 
+/* ---- Action learning on the device (Sec. 3.2, Eqs. 5-8) ------------------
+ * One training step of the per-expert width actions of a layer:
+ *   1. flexmoe_sample_actions: the hard straight-through Gumbel-softmax
+ *      sample (Eq. 5) of one action per expert, written as a device keep
+ *      table (no host round trip);
+ *   2. flexmoe_train_forward: the sampled subnet's forward (the masked layer
+ *      at that keep table), keeping what the backward needs in the workspace;
+ *   3. flexmoe_train_backward: for an upstream gradient dY, the input
+ *      gradient dx, the router-logit gradient and the mask gradient
+ *      dM[e][c] = dL/dM_{e,c} of the prefix mask (every channel c < I);
+ *   4. flexmoe_action_grad: the action-logit gradient through the
+ *      straight-through estimator (Eq. 6) plus lambda_cost times the
+ *      load-weighted cost of Eq. 7 minus beta times the entropy of the clean
+ *      action distribution, with the cost and entropy values.
+ * The weights are frozen (only the action logits learn), so their gradients
+ * are not formed; the transposed copies the backward reads are made once by
+ * flexmoe_transpose_weights.  bf16 layers only (FLEXMOE_EDTYPE otherwise).
+ *
+ * Actions: K <= FLEXMOE_MAX_ACTIONS retention ratios r_k in (0, 1]
+ * (FLEXMOE_EINVAL otherwise); action k keeps ceil(r_k I) channels
+ * (flexmoe_keep_from_ratio), at least one.  alpha, gumbel [E][K] fp32 on the
+ * device; gumbel holds the caller's Gumbel(0, 1) draws.  The hard sample is
+ * argmax_k (alpha + gumbel) in fp32, the first index on ties (the softmax of
+ * Eq. 5 is monotone in its argument). */
+#define FLEXMOE_MAX_ACTIONS 16
+typedef struct flexmoe_action_set {
+    int32_t K;
+    double ratio[FLEXMOE_MAX_ACTIONS];   /* fp64, so that the widths ceil(r I)
+                                            are those of the decimal ratios */
+} flexmoe_action_set;
+
+/* Transposed weight copies: w_gate_t, w_up_t [E][d][I]; w_down_t [E][I][d];
+ * ws_gate_t, ws_up_t [d][I_s]; ws_down_t [I_s][d] (shared ones NULL iff
+ * I_s == 0).  Outputs must not overlap inputs. */
+int flexmoe_transpose_weights(const flexmoe_layer_desc *desc, const void *w_gate, const void *w_up,
+                              const void *w_down, const void *ws_gate, const void *ws_up,
+                              const void *ws_down, void *w_gate_t, void *w_up_t, void *w_down_t,
+                              void *ws_gate_t, void *ws_up_t, void *ws_down_t, void *stream);
+
+/* Eq. 5: keep_dev[e] = ceil(r_{k*} I) with k* = argmax_k (alpha + gumbel);
+ * action_dev [E] int32 receives k* (may be NULL). */
+int flexmoe_sample_actions(const flexmoe_layer_desc *desc, const flexmoe_action_set *actions,
+                           const float *alpha, const float *gumbel, int32_t *keep_dev,
+                           int32_t *action_dev, void *stream);
+
+/* Workspace of flexmoe_train_forward/backward/action_grad for T tokens.  The
+ * forward writes it and the other two read it: keep it, and T and logits,
+ * unchanged between the calls of one step. */
+size_t flexmoe_train_workspace_bytes(const flexmoe_layer_desc *desc, int32_t T);
+
+/* The masked layer's forward at keep_dev (any 0 <= k_e <= I; an expert at 0
+ * is skipped and gets no mask gradient), y [T][d] bf16 as from
+ * flexmoe_layer_forward.  The gate/up GEMM computes every channel (the mask
+ * gradient needs g and u past the prefix); the down GEMM only the kept ones. */
+int flexmoe_train_forward(const flexmoe_layer_desc *desc, int32_t T, const void *x,
+                          const float *logits, const void *w_gate, const void *w_up,
+                          const void *w_down, const int32_t *keep_dev, const void *ws_gate,
+                          const void *ws_up, const void *ws_down, void *y, void *workspace,
+                          size_t workspace_bytes, void *stream);
+
+/* Backward of the forward above for dy [T][d] fp32 = dL/dY:
+ *   dx [T][d] fp32        dL/dx through the routed experts (kept channels)
+ *                         and the shared expert;
+ *   dlogits [T][E] fp32   dL/dlogits through the router weights (softmax over
+ *                         all E, then the top-k renormalisation if norm_topk);
+ *   dmask [E][I] fp32     dL/dM_{e,c} = sum over e's tokens of
+ *                         dh'_c silu(g_c) u_c, dh' = w dY W_down (every c).
+ * Arithmetic: fp32 accumulation; dO = w*dY, dY (shared), g, u, dG, dU are
+ * rounded to bf16 as MFMA operands; fixed summation orders. */
+int flexmoe_train_backward(const flexmoe_layer_desc *desc, int32_t T, const float *logits,
+                           const float *dy, const void *w_gate_t, const void *w_up_t,
+                           const void *w_down_t, const void *ws_gate_t, const void *ws_up_t,
+                           const void *ws_down_t, float *dx, float *dlogits, float *dmask,
+                           void *workspace, size_t workspace_bytes, void *stream);
+
+/* Eqs. 6-8 for this layer: dalpha [E][K] fp32 = (1/tau) z (dz - <z, dz>)
+ * with z = softmax((alpha + gumbel) / tau) and dz_k = sum_{c < ceil(r_k I)}
+ * dmask[e][c], plus lambda_cost q_e p_k (r_k - <p, r>) and
+ * beta p_k (log p_k + H_e) / E, where p = softmax(alpha),
+ * H_e = -<p, log p> and q_e = n_e / (T top_k) from the forward's routing.
+ * stats (may be NULL) [2] fp32 receives C = sum_e q_e <p_e, r> and
+ * H = mean_e H_e.  tau > 0 (FLEXMOE_EINVAL otherwise). */
+int flexmoe_action_grad(const flexmoe_layer_desc *desc, int32_t T, const flexmoe_action_set *actions,
+                        const float *alpha, const float *gumbel, float tau, float lambda_cost,
+                        float beta, const float *dmask, float *dalpha, float *stats,
+                        const void *workspace, size_t workspace_bytes, void *stream);
+
 /* Budget switch: validates 0 <= keep_host[e] <= I for every e on the host, then
  * writes the E counts into keep_dev [E] on `stream` (one small kernel whose
  * arguments carry the table, so keep_host may be reused as soon as the call
@@ -279,7 +366,11 @@ enum {
     FLEXMOE_K_SAL_DGRAD = 10,     /* saliency: dgrad GEMM + SwiGLU backward    */
     FLEXMOE_K_SAL_WGRAD = 11,     /* saliency: wgrad GEMMs + Eq. 2 reduction   */
     FLEXMOE_K_SAL_REDUCE = 12,    /* saliency: sum of the partial scores       */
-    FLEXMOE_K_COUNT = 13
+    FLEXMOE_K_ACT_DGRAD = 13,     /* training: dgrad + SwiGLU bwd + mask grad  */
+    FLEXMOE_K_ACT_DX = 14,        /* training: input-gradient GEMMs            */
+    FLEXMOE_K_ACT_OTHER = 15,     /* training: sampling, prep, combine bwd,
+                                     mask sums, action gradient              */
+    FLEXMOE_K_COUNT = 16
 };
 typedef struct flexmoe_kernel_times {
     double ms[FLEXMOE_K_COUNT];

@@ -21,6 +21,7 @@
 #include "flexmoe.h"
 #include "kernels.h"
 #include "saliency.h"
+#include "train.h"
 
 using namespace flexmoe;
 
@@ -839,7 +840,7 @@ int saliency_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, cons
     // 1. the transposed down weights (no dependence on the batch's routing)
     {
         KernelTimer kt(FLEXMOE_K_SAL_TRANSPOSE, s);
-        err = launch_transpose_down((const bf16_t*)w_down, wdt, D.E, D.d, D.I, s);
+        err = launch_transpose_batched((const bf16_t*)w_down, wdt, D.E, D.d, D.I, s);
     }
     if (err != hipSuccess) return hip_fail(err, "down-weight transpose launch");
 
@@ -956,6 +957,359 @@ int flexmoe_channel_saliency(const flexmoe_layer_desc* desc, int32_t T, const vo
                              float* scores, void* workspace, size_t workspace_bytes, void* stream) {
     return saliency_impl(desc, T, x, logits, w_gate, w_up, w_down, ws_gate, ws_up, ws_down, y_target, scale,
                          scores, workspace, workspace_bytes, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+// ---- action learning: training step of the masked layer --------------------
+struct TrainLayout {
+    Layout f;  // the forward's regions (shared expert unsplit)
+    size_t G, U, Gs, Us, dO, dYs, dG, dU, dGs, dUs, dXr, dXs, dmp, total;
+    long long rt;  // bound on the routed row tiles
+};
+
+TrainLayout train_layout(const flexmoe_layer_desc& D, int T) {
+    TrainLayout S{};
+    S.f = layout(D, T, (size_t)T);
+    S.rt = routed_row_tiles_ub(T, D.E, D.top_k, kTrainTile);
+    const size_t A = (size_t)T * D.top_k, d = D.d, I = D.I, Is = D.I_shared, Tz = T;
+    size_t off = S.f.total;
+    auto take = [&](size_t bytes) {
+        const size_t o = off;
+        off += align256(bytes);
+        return o;
+    };
+    S.G = take(A * I * 2);
+    S.U = take(A * I * 2);
+    S.Gs = take(Tz * Is * 2);
+    S.Us = take(Tz * Is * 2);
+    S.dO = take(A * d * 2);
+    S.dYs = take(Tz * d * 2);
+    S.dG = take(A * I * 2);
+    S.dU = take(A * I * 2);
+    S.dGs = take(Tz * Is * 2);
+    S.dUs = take(Tz * Is * 2);
+    S.dXr = take(A * d * 4);
+    S.dXs = take(Tz * d * 4);
+    S.dmp = take((size_t)S.rt * kTrainWaveM * I * 4);
+    S.total = off;
+    return S;
+}
+
+int check_train(const flexmoe_layer_desc* desc, int T) {
+    int rc = check_desc(desc);
+    if (rc) return rc;
+    if (desc->dtype != FLEXMOE_BF16) return fail(FLEXMOE_EDTYPE, "action learning runs on bf16 layers only");
+    if (T < 0) return fail(FLEXMOE_EINVAL, "T = %d is negative", T);
+    if (T > desc->max_tokens) return fail(FLEXMOE_ESHAPE, "T = %d exceeds max_tokens = %d", T, desc->max_tokens);
+    return FLEXMOE_OK;
+}
+
+int action_widths(const flexmoe_layer_desc& D, const flexmoe_action_set* a, ActionWidths& aw) {
+    if (!a) return fail(FLEXMOE_EINVAL, "actions is NULL");
+    if (a->K < 1 || a->K > FLEXMOE_MAX_ACTIONS)
+        return fail(FLEXMOE_EINVAL, "K = %d actions outside [1, %d]", a->K, FLEXMOE_MAX_ACTIONS);
+    aw = ActionWidths{};
+    aw.K = a->K;
+    for (int k = 0; k < a->K; ++k) {
+        const double r = a->ratio[k];
+        if (!(r > 0.0 && r <= 1.0)) return fail(FLEXMOE_EINVAL, "ratio[%d] = %g outside (0, 1]", k, r);
+        aw.ratio[k] = (float)a->ratio[k];
+        aw.width[k] = std::max(1, flexmoe_keep_from_ratio(r, D.I));
+    }
+    return FLEXMOE_OK;
+}
+
+struct TrainPtrs {
+    int32_t *idx, *counts, *offsets, *perm, *pos, *plan, *blockcnt, *blockbase, *t1, *t2;
+    float* wts;
+    SegMeta* seg;
+    bf16_t *H, *Hs, *O, *Os, *G, *U, *Gs, *Us, *dO, *dYs, *dG, *dU, *dGs, *dUs;
+    float *dXr, *dXs, *dmp;
+};
+
+TrainPtrs train_ptrs(const TrainLayout& S, void* workspace) {
+    char* ws = (char*)workspace;
+    const Layout& L = S.f;
+    TrainPtrs P;
+    P.idx = (int32_t*)(ws + L.idx);
+    P.wts = (float*)(ws + L.wts);
+    P.blockcnt = (int32_t*)(ws + L.blockcnt);
+    P.blockbase = (int32_t*)(ws + L.blockbase);
+    P.counts = (int32_t*)(ws + L.counts);
+    P.offsets = (int32_t*)(ws + L.offsets);
+    P.perm = (int32_t*)(ws + L.perm);
+    P.pos = (int32_t*)(ws + L.pos);
+    P.seg = (SegMeta*)(ws + L.seg);
+    P.t1 = (int32_t*)(ws + L.t1);
+    P.t2 = (int32_t*)(ws + L.t2);
+    P.plan = (int32_t*)(ws + L.plan);
+    P.H = (bf16_t*)(ws + L.H);
+    P.Hs = (bf16_t*)(ws + L.Hs);
+    P.O = (bf16_t*)(ws + L.O);
+    P.Os = (bf16_t*)(ws + L.Os);
+    P.G = (bf16_t*)(ws + S.G);
+    P.U = (bf16_t*)(ws + S.U);
+    P.Gs = (bf16_t*)(ws + S.Gs);
+    P.Us = (bf16_t*)(ws + S.Us);
+    P.dO = (bf16_t*)(ws + S.dO);
+    P.dYs = (bf16_t*)(ws + S.dYs);
+    P.dG = (bf16_t*)(ws + S.dG);
+    P.dU = (bf16_t*)(ws + S.dU);
+    P.dGs = (bf16_t*)(ws + S.dGs);
+    P.dUs = (bf16_t*)(ws + S.dUs);
+    P.dXr = (float*)(ws + S.dXr);
+    P.dXs = (float*)(ws + S.dXs);
+    P.dmp = (float*)(ws + S.dmp);
+    return P;
+}
+
+int check_workspace(const TrainLayout& S, const void* workspace, size_t bytes) {
+    if (!workspace || bytes < S.total)
+        return fail(FLEXMOE_EWORKSPACE, "workspace of %zu bytes given, %zu needed", bytes, S.total);
+    if (((uintptr_t)workspace) & 255) return fail(FLEXMOE_EWORKSPACE, "workspace is not 256-byte aligned");
+    return FLEXMOE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int flexmoe_transpose_weights(const flexmoe_layer_desc* desc, const void* w_gate, const void* w_up,
+                              const void* w_down, const void* ws_gate, const void* ws_up, const void* ws_down,
+                              void* w_gate_t, void* w_up_t, void* w_down_t, void* ws_gate_t, void* ws_up_t,
+                              void* ws_down_t, void* stream) {
+    int rc = check_train(desc, 0);
+    if (rc) return rc;
+    const flexmoe_layer_desc& D = *desc;
+    if (!w_gate || !w_up || !w_down || !w_gate_t || !w_up_t || !w_down_t)
+        return fail(FLEXMOE_EINVAL, "transpose_weights: a routed weight pointer is NULL");
+    const bool has_shared = D.I_shared > 0;
+    const bool all_sh = ws_gate && ws_up && ws_down && ws_gate_t && ws_up_t && ws_down_t;
+    const bool any_sh = ws_gate || ws_up || ws_down || ws_gate_t || ws_up_t || ws_down_t;
+    if (has_shared ? !all_sh : any_sh)
+        return fail(FLEXMOE_EINVAL, "shared weights and their copies must be given iff I_shared > 0");
+    for (const void* ptr : {w_gate, w_up, w_down, ws_gate, ws_up, ws_down, (const void*)w_gate_t,
+                            (const void*)w_up_t, (const void*)w_down_t, (const void*)ws_gate_t,
+                            (const void*)ws_up_t, (const void*)ws_down_t})
+        if (((uintptr_t)ptr) & 15) return fail(FLEXMOE_EINVAL, "weights must be 16-byte aligned");
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t err;
+    struct {
+        const void* src;
+        void* dst;
+        int batch, rows, cols;
+    } jobs[] = {{w_gate, w_gate_t, D.E, D.I, D.d},        {w_up, w_up_t, D.E, D.I, D.d},
+                {w_down, w_down_t, D.E, D.d, D.I},        {ws_gate, ws_gate_t, 1, D.I_shared, D.d},
+                {ws_up, ws_up_t, 1, D.I_shared, D.d},     {ws_down, ws_down_t, 1, D.d, D.I_shared}};
+    for (auto& j : jobs) {
+        if (!j.src) continue;
+        if ((err = launch_transpose_batched((const bf16_t*)j.src, (bf16_t*)j.dst, j.batch, j.rows, j.cols, s)) !=
+            hipSuccess)
+            return hip_fail(err, "weight transpose launch");
+    }
+    return FLEXMOE_OK;
+}
+
+int flexmoe_sample_actions(const flexmoe_layer_desc* desc, const flexmoe_action_set* actions, const float* alpha,
+                           const float* gumbel, int32_t* keep_dev, int32_t* action_dev, void* stream) {
+    int rc = check_train(desc, 0);
+    if (rc) return rc;
+    ActionWidths aw;
+    if ((rc = action_widths(*desc, actions, aw)) != FLEXMOE_OK) return rc;
+    if (!alpha || !gumbel || !keep_dev) return fail(FLEXMOE_EINVAL, "sample_actions: a pointer is NULL");
+    KernelTimer kt(FLEXMOE_K_ACT_OTHER, (hipStream_t)stream);
+    const hipError_t err = launch_sample_actions(aw, alpha, gumbel, desc->E, keep_dev, action_dev,
+                                                 (hipStream_t)stream);
+    if (err != hipSuccess) return hip_fail(err, "sample_actions launch");
+    return FLEXMOE_OK;
+}
+
+size_t flexmoe_train_workspace_bytes(const flexmoe_layer_desc* desc, int32_t T) {
+    if (check_train(desc, T) != FLEXMOE_OK) return 0;
+    return train_layout(*desc, T).total;
+}
+
+int flexmoe_train_forward(const flexmoe_layer_desc* desc, int32_t T, const void* x, const float* logits,
+                          const void* w_gate, const void* w_up, const void* w_down, const int32_t* keep_dev,
+                          const void* ws_gate, const void* ws_up, const void* ws_down, void* y, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+    int rc = check_train(desc, T);
+    if (rc) return rc;
+    const flexmoe_layer_desc& D = *desc;
+    if (T == 0) return FLEXMOE_OK;
+    if (!x || !logits || !w_gate || !w_up || !w_down || !keep_dev || !y)
+        return fail(FLEXMOE_EINVAL, "train_forward: an input/output pointer is NULL");
+    for (const void* ptr : {x, w_gate, w_up, w_down, ws_gate, ws_up, ws_down, (const void*)y})
+        if (((uintptr_t)ptr) & 15) return fail(FLEXMOE_EINVAL, "x, weights and y must be 16-byte aligned");
+    if (((uintptr_t)logits) & 3 || ((uintptr_t)keep_dev) & 3)
+        return fail(FLEXMOE_EINVAL, "logits and keep_dev must be 4-byte aligned");
+    const bool has_shared = D.I_shared > 0;
+    if (has_shared != (ws_gate && ws_up && ws_down) || (!has_shared && (ws_gate || ws_up || ws_down)))
+        return fail(FLEXMOE_EINVAL, "shared weights must be given iff I_shared > 0");
+    const TrainLayout S = train_layout(D, T);
+    if ((rc = check_workspace(S, workspace, workspace_bytes)) != FLEXMOE_OK) return rc;
+    TrainPtrs P = train_ptrs(S, workspace);
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t err;
+    const int hs = has_shared ? 1 : 0, nseg = D.E + hs;
+
+    // segments in expert order, the gate/up GEMM over all I channels
+    KeepArgs order, full;
+    for (int e = 0; e < kMaxExperts; ++e) {
+        order.v[e] = e < D.E ? e : 0;
+        full.v[e] = e < D.E ? D.I : 0;
+    }
+    set_keep_kernel<<<1, kMaxExperts, 0, s>>>(P.plan, order, D.E);
+    set_keep_kernel<<<1, kMaxExperts, 0, s>>>(P.plan + D.E, full, D.E);
+    if ((err = hipGetLastError()) != hipSuccess) return hip_fail(err, "plan upload");
+    const TileShape ts{kBigBM1, kBigBN1, kBigBM2, kBigBN2, 0};
+    static_assert(kBigBM1 == kTrainTile, "segment row tiles (rt0) are counted in training tile rows");
+    const int NB = num_chunks(T);
+    if ((long long)T * D.top_k <= kSmallAssign) {
+        KernelTimer kt(FLEXMOE_K_ROUTE, s);
+        dispatch_small_kernel<<<1, 64 * kSmallWaves, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, keep_dev, D.I,
+                                                             D.I_shared, D.d, ts, 0x7fffffff, P.plan, 0, P.idx,
+                                                             P.wts, P.counts, P.perm, P.pos, P.offsets, P.seg,
+                                                             P.t1, P.t2);
+        if ((err = hipGetLastError()) != hipSuccess) return hip_fail(err, "dispatch launch");
+    } else {
+        {
+            KernelTimer kt(FLEXMOE_K_ROUTE, s);
+            route_kernel<<<NB, 64 * kRouteTokens, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, P.idx, P.wts,
+                                                          P.blockcnt, NB);
+            err = hipGetLastError();
+        }
+        if (err != hipSuccess) return hip_fail(err, "route launch");
+        {
+            KernelTimer kt(FLEXMOE_K_DISPATCH_SCAN, s);
+            dispatch_scan_kernel<<<D.E, 256, 0, s>>>(P.blockcnt, NB, P.blockbase, P.counts);
+            err = hipGetLastError();
+        }
+        if (err != hipSuccess) return hip_fail(err, "dispatch scan launch");
+        {
+            KernelTimer kt(FLEXMOE_K_DISPATCH_SCATTER, s);
+            dispatch_scatter_kernel<<<NB, 64, 0, s>>>(P.idx, keep_dev, P.counts, P.blockbase, T, D.E, D.top_k,
+                                                      D.I, D.I_shared, D.d, NB, ts, 0x7fffffff, P.plan, P.perm,
+                                                      P.pos, P.offsets, P.seg, P.t1, P.t2);
+            err = hipGetLastError();
+        }
+        if (err != hipSuccess) return hip_fail(err, "dispatch scatter launch");
+    }
+    const long long g1 = routed_row_tiles_ub(T, D.E, D.top_k, ts.bm1) * ceil_div(D.I, ts.bn1) +
+                         (has_shared ? (long long)ceil_div(T, ts.bm1) * ceil_div(D.I_shared, ts.bn1) : 0);
+    const long long g2s = has_shared ? (long long)ceil_div(T, ts.bm2) * ceil_div(D.d, ts.bn2) : 0;
+    const long long g2 = routed_row_tiles_ub(T, D.E, D.top_k, ts.bm2) * ceil_div(D.d, ts.bn2) + g2s;
+    if (g1 > 0x7fffffffLL || g2 > 0x7fffffffLL) return fail(FLEXMOE_ESHAPE, "tile grid too large");
+    {
+        Gemm1Params<bf16_t> p1{(const bf16_t*)x, (const bf16_t*)w_gate, (const bf16_t*)w_up, (const bf16_t*)ws_gate,
+                               (const bf16_t*)ws_up, P.perm, P.seg, P.t1, P.H, P.Hs, D.d, D.I, D.I_shared, D.E,
+                               D.top_k, nseg, T, kPartRange, 0, nseg, 0, 0, nullptr, nullptr, nullptr, 0,
+                               P.G, P.U, P.Gs, P.Us};
+        KernelTimer kt(FLEXMOE_K_GATE_UP, s);
+        err = launch_gemm1_big_train_rm(p1, (int)g1, s);
+    }
+    if (err != hipSuccess) return hip_fail(err, "training gate/up GEMM launch");
+    if ((err = launch_seg_use_kept(P.seg, nseg, s)) != hipSuccess) return hip_fail(err, "segment width launch");
+    {
+        Gemm2Params<bf16_t> p2{P.H, P.Hs, (const bf16_t*)w_down, (const bf16_t*)ws_down, P.seg, P.t2, P.O, P.Os,
+                               D.d, D.I, D.I_shared, D.E, nseg, T, 0, kPartRange, 0, nseg, (int)g2s, 0};
+        KernelTimer kt(FLEXMOE_K_DOWN, s);
+        err = launch_gemm2_big(p2, (int)g2, s);
+    }
+    if (err != hipSuccess) return hip_fail(err, "down GEMM launch");
+    {
+        KernelTimer kt(FLEXMOE_K_COMBINE, s);
+        err = launch_combine(P.O, P.Os, P.pos, P.wts, T, D.top_k, D.d, has_shared ? 1 : 0, D.dtype, y, s);
+    }
+    if (err != hipSuccess) return hip_fail(err, "combine launch");
+    return FLEXMOE_OK;
+}
+
+int flexmoe_train_backward(const flexmoe_layer_desc* desc, int32_t T, const float* logits, const float* dy,
+                           const void* w_gate_t, const void* w_up_t, const void* w_down_t, const void* ws_gate_t,
+                           const void* ws_up_t, const void* ws_down_t, float* dx, float* dlogits, float* dmask,
+                           void* workspace, size_t workspace_bytes, void* stream) {
+    int rc = check_train(desc, T);
+    if (rc) return rc;
+    const flexmoe_layer_desc& D = *desc;
+    if (T == 0) return FLEXMOE_OK;
+    if (!logits || !dy || !w_gate_t || !w_up_t || !w_down_t || !dx || !dlogits || !dmask)
+        return fail(FLEXMOE_EINVAL, "train_backward: an input/output pointer is NULL");
+    for (const void* ptr : {(const void*)dy, w_gate_t, w_up_t, w_down_t, ws_gate_t, ws_up_t, ws_down_t,
+                            (const void*)dx})
+        if (((uintptr_t)ptr) & 15) return fail(FLEXMOE_EINVAL, "dy, dx and weights must be 16-byte aligned");
+    if (((uintptr_t)logits) & 3 || ((uintptr_t)dlogits) & 3 || ((uintptr_t)dmask) & 3)
+        return fail(FLEXMOE_EINVAL, "logits, dlogits and dmask must be 4-byte aligned");
+    const bool has_shared = D.I_shared > 0;
+    if (has_shared != (ws_gate_t && ws_up_t && ws_down_t) || (!has_shared && (ws_gate_t || ws_up_t || ws_down_t)))
+        return fail(FLEXMOE_EINVAL, "shared weight copies must be given iff I_shared > 0");
+    const TrainLayout S = train_layout(D, T);
+    if ((rc = check_workspace(S, workspace, workspace_bytes)) != FLEXMOE_OK) return rc;
+    TrainPtrs P = train_ptrs(S, workspace);
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t err;
+    const int hs = has_shared ? 1 : 0, nseg = D.E + hs;
+    const int A = T * D.top_k;
+    const int nI = ceil_div(D.I, kTrainTile), nIs = ceil_div(std::max(D.I_shared, 1), kTrainTile);
+    const int nD = ceil_div(D.d, kTrainTile);
+    const long long sh_rows = has_shared ? ceil_div(T, kTrainTile) : 0;
+    const long long tiles_dgrad = sh_rows * nIs + S.rt * nI;
+    const long long tiles_dx = sh_rows * nD + S.rt * nD;
+    if (tiles_dgrad > 0x7fffffffLL || tiles_dx > 0x7fffffffLL) return fail(FLEXMOE_ESHAPE, "tile grid too large");
+    {
+        KernelTimer kt(FLEXMOE_K_ACT_OTHER, s);
+        err = launch_train_prep(dy, P.perm, P.wts, P.offsets + D.E, A, T, D.d, D.top_k, P.dO,
+                                has_shared ? P.dYs : nullptr, s);
+    }
+    if (err != hipSuccess) return hip_fail(err, "backward prep launch");
+    {
+        ActDgradParams pd{P.dO, P.dYs, (const bf16_t*)w_down_t, (const bf16_t*)ws_down_t, P.G, P.U, P.Gs, P.Us,
+                          P.seg, P.dG, P.dU, P.dGs, P.dUs, P.dmp, hs, nseg, D.d, D.I, D.I_shared, T, nI, nIs};
+        KernelTimer kt(FLEXMOE_K_ACT_DGRAD, s);
+        err = launch_act_dgrad(pd, tiles_dgrad, s);
+    }
+    if (err != hipSuccess) return hip_fail(err, "dgrad launch");
+    {
+        ActDxParams px{P.dG, P.dU, P.dGs, P.dUs, (const bf16_t*)w_gate_t, (const bf16_t*)w_up_t,
+                       (const bf16_t*)ws_gate_t, (const bf16_t*)ws_up_t, P.seg, P.dXr, P.dXs, hs, nseg, D.d, D.I,
+                       D.I_shared, T, nD};
+        KernelTimer kt(FLEXMOE_K_ACT_DX, s);
+        err = launch_act_dx(px, tiles_dx, s);
+    }
+    if (err != hipSuccess) return hip_fail(err, "dx launch");
+    {
+        KernelTimer kt(FLEXMOE_K_ACT_OTHER, s);
+        err = launch_combine_backward(P.dXr, has_shared ? P.dXs : nullptr, P.O, P.pos, P.idx, P.wts, logits, dy, T,
+                                      D.E, D.top_k, D.d, D.norm_topk, dx, dlogits, s);
+        if (err == hipSuccess) err = launch_dmask_reduce(P.dmp, P.seg, hs, D.E, D.I, dmask, s);
+    }
+    if (err != hipSuccess) return hip_fail(err, "combine backward launch");
+    return FLEXMOE_OK;
+}
+
+int flexmoe_action_grad(const flexmoe_layer_desc* desc, int32_t T, const flexmoe_action_set* actions,
+                        const float* alpha, const float* gumbel, float tau, float lambda_cost, float beta,
+                        const float* dmask, float* dalpha, float* stats, const void* workspace,
+                        size_t workspace_bytes, void* stream) {
+    int rc = check_train(desc, T);
+    if (rc) return rc;
+    const flexmoe_layer_desc& D = *desc;
+    ActionWidths aw;
+    if ((rc = action_widths(D, actions, aw)) != FLEXMOE_OK) return rc;
+    if (!(tau > 0.f)) return fail(FLEXMOE_EINVAL, "tau = %g must be positive", (double)tau);
+    if (T < 1) return fail(FLEXMOE_EINVAL, "T = %d: the load ratios need at least one token", T);
+    if (!alpha || !gumbel || !dmask || !dalpha) return fail(FLEXMOE_EINVAL, "action_grad: a pointer is NULL");
+    const TrainLayout S = train_layout(D, T);
+    if ((rc = check_workspace(S, workspace, workspace_bytes)) != FLEXMOE_OK) return rc;
+    const int32_t* counts = (const int32_t*)((const char*)workspace + S.f.counts);
+    KernelTimer kt(FLEXMOE_K_ACT_OTHER, (hipStream_t)stream);
+    const hipError_t err = launch_action_grad(aw, alpha, gumbel, tau, dmask, counts, (long long)T * D.top_k, D.E,
+                                              D.I, lambda_cost, beta, dalpha, stats, (hipStream_t)stream);
+    if (err != hipSuccess) return hip_fail(err, "action_grad launch");
+    return FLEXMOE_OK;
 }
 
 }  // extern "C"

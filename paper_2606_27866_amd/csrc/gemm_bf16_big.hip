@@ -119,7 +119,10 @@ __device__ __forceinline__ void train_store_transposed(const Gemm1Params<bf16_t>
     }
 }
 
-template <bool kGateUp, bool kTrain = false>
+// kTrain: 0 = inference; 1 = also the transposed g, u, h of the routed rows
+// (channel saliency); 2 = also g and u of every row, row-major (the masked
+// layer's training backward).
+template <bool kGateUp, int kTrain = 0>
 __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Gemm2Params<bf16_t>& p2,
                                          unsigned char* smem) {
     const int d = kGateUp ? p1.d : p2.d;
@@ -333,7 +336,35 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
                     *reinterpret_cast<uint2*>(hr + ch) = make_uint2(w[0], w[1]);
                 }
             }
-            if constexpr (kTrain) {
+            if constexpr (kTrain == 2) {
+                // g and u for the training backward, in H's layout
+                bf16_t* Gb = shared ? p1.Gs : p1.G + (size_t)sm.row0 * p1.I;
+                bf16_t* Ub = shared ? p1.Us : p1.U + (size_t)sm.row0 * p1.I;
+#pragma unroll
+                for (int i = 0; i < MFW; ++i) {
+                    const int row = row_l + i * 32;
+                    if (row >= sm.rows) continue;
+#pragma unroll
+                    for (int jj = 0; jj < NF / 2; ++jj)
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const int ch = ntile * (BN / 2) + wn * (WCOL / 2) + jj * 32 + q * 8 + sub;
+                            if (ch >= sm.kg) continue;
+                            uint32_t gw[2], uw[2];
+#pragma unroll
+                            for (int h = 0; h < 2; ++h) {
+                                const int v = q * 4 + h * 2;
+                                gw[h] = (uint32_t)f32_to_bf16(acc[i][jj][v]) |
+                                        ((uint32_t)f32_to_bf16(acc[i][jj][v + 1]) << 16);
+                                uw[h] = (uint32_t)f32_to_bf16(acc[i][jj + NF / 2][v]) |
+                                        ((uint32_t)f32_to_bf16(acc[i][jj + NF / 2][v + 1]) << 16);
+                            }
+                            *reinterpret_cast<uint2*>(Gb + (size_t)row * ldh + ch) = make_uint2(gw[0], gw[1]);
+                            *reinterpret_cast<uint2*>(Ub + (size_t)row * ldh + ch) = make_uint2(uw[0], uw[1]);
+                        }
+                }
+            }
+            if constexpr (kTrain == 1) {
                 // transposed copies of g, u and h for the backward GEMMs,
                 // element [c][prow0 + row], zero in the rows up to the
                 // segment's padded height.  Each is staged through LDS as a
@@ -380,7 +411,14 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void gemm1_big_kernel(Gemm
 // transposed g, u and h copies of the routed segments (Gemm1Params).
 __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void gemm1_big_train_kernel(Gemm1Params<bf16_t> p) {
     __shared__ __attribute__((aligned(1024))) unsigned char smem[NSTAGE * STAGE];
-    big_tile<true, true>(p, Gemm2Params<bf16_t>{}, smem);
+    big_tile<true, 1>(p, Gemm2Params<bf16_t>{}, smem);
+}
+
+// The gate/up GEMM of the masked layer's training forward: the same tiles,
+// plus g and u of every row (Gemm1Params).
+__global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void gemm1_big_train_rm_kernel(Gemm1Params<bf16_t> p) {
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[NSTAGE * STAGE];
+    big_tile<true, 2>(p, Gemm2Params<bf16_t>{}, smem);
 }
 
 __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void gemm2_big_kernel(Gemm2Params<bf16_t> p) {
@@ -399,6 +437,13 @@ hipError_t launch_gemm1_big_train(const Gemm1Params<bf16_t>& p, int grid, hipStr
     if (grid <= 0) return hipSuccess;
     const int g = (grid + 8 * XCD_GROUP - 1) / (8 * XCD_GROUP) * (8 * XCD_GROUP);
     gemm1_big_train_kernel<<<g, THREADS, 0, s>>>(p);
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm1_big_train_rm(const Gemm1Params<bf16_t>& p, int grid, hipStream_t s) {
+    if (grid <= 0) return hipSuccess;
+    const int g = (grid + 8 * XCD_GROUP - 1) / (8 * XCD_GROUP) * (8 * XCD_GROUP);
+    gemm1_big_train_rm_kernel<<<g, THREADS, 0, s>>>(p);
     return hipGetLastError();
 }
 

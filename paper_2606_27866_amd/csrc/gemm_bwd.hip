@@ -23,6 +23,7 @@
 //          transposed copies, zero-padded to a multiple of 8).
 #include "mfma_tile.h"
 #include "saliency.h"
+#include "train.h"
 
 namespace flexmoe {
 
@@ -78,19 +79,24 @@ __device__ __forceinline__ void nt_rows(int wave, int lane, int row_base, int va
 // last two DMA slots of the loop (K tiles nk and nk+1, past the end) go to
 // tail(h, sa, sb) for h = 0, 1, which must issue exactly NI loads into each
 // of this wave's A and B parts of the freed stage (nk + h) % 2.
-template <int MFW, typename Tail>
+// kSwap: the A fragment is the MFMA's first operand (lane -> B row, registers
+// -> runs of 4 A rows); otherwise the B fragment is (lane -> A row, registers
+// -> runs of 4 B rows).  zero = false continues accumulating into acc.
+template <int MFW, bool kSwap = true, typename Tail>
 __device__ __forceinline__ void nt_mainloop(unsigned char* smem, const NTOperands& op, int wave, int lane,
-                                            floatx16 (&acc)[MFW][NF], Tail&& tail) {
+                                            floatx16 (&acc)[MFW][NF], Tail&& tail, bool zero = true) {
     constexpr int WR = 32 * MFW;
     constexpr int NMF = MFW * NF;
     constexpr int NRD = MFW + NF;
     const int wm = wave / WN, wn = wave % WN;
+    if (zero) {
 #pragma unroll
-    for (int i = 0; i < MFW; ++i)
+        for (int i = 0; i < MFW; ++i)
 #pragma unroll
-        for (int j = 0; j < NF; ++j)
+            for (int j = 0; j < NF; ++j)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+                for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+    }
 
     const int nk = ceil_div(op.K, BK);
     auto issue = [&](int kt, int stage) {
@@ -125,7 +131,8 @@ __device__ __forceinline__ void nt_mainloop(unsigned char* smem, const NTOperand
         for (int i = 0; i < MFW; ++i)
 #pragma unroll
             for (int j = 0; j < NF; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][i], b[buf][j], acc[i][j], 0, 0, 0);
+                acc[i][j] = kSwap ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][i], b[buf][j], acc[i][j], 0, 0, 0)
+                                  : __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[buf][j], a[buf][i], acc[i][j], 0, 0, 0);
     };
     issue(0, 0);
     issue(1, 1);
@@ -353,6 +360,214 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void sal_wgrad_kernel(SalW
                 if (c < p.I) part_out[(size_t)c * MP + mtile * WM + wm] = part[j];
             }
     });
+}
+
+// ---- training backward of the masked layer ---------------------------------
+namespace {
+// Tile L of the training backward's tile list: the shared expert's tiles
+// first (ceil(T/256) row tiles x nsh column tiles), then the routed segments'
+// (row tiles numbered by SegMeta::rt0, x nr column tiles).  False past the end.
+__device__ __forceinline__ bool train_tile(const SegMeta* seg, int hs, int nseg, int T, int Is, int nsh, int nr,
+                                           int L, SegMeta& sm, int& mtile, int& ntile) {
+    if (hs) {
+        const int mt = ceil_div(T, BM), sh = mt * nsh;
+        if (L < sh) {
+            sm = SegMeta{0, T, Is, 0, Is, -1, 0, 0};
+            mtile = L % mt;
+            ntile = L / mt;
+            return true;
+        }
+        L -= sh;
+    }
+    int lo = hs, hi = nseg - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (seg[mid].rt0 * nr <= L) lo = mid;
+        else hi = mid - 1;
+    }
+    sm = seg[lo];
+    const int mt = ceil_div(sm.rows, BM);
+    const int local = L - sm.rt0 * nr;
+    if (local >= mt * nr) return false;
+    ntile = local / mt;
+    mtile = local % mt;
+    return true;
+}
+}  // namespace
+
+// dgrad + SwiGLU backward + mask gradient; tile = 256 rows x 256 channels.
+// The B fragment goes first: lane -> row, registers -> runs of 4 channels,
+// matching the row-major g, u, dG and dU (8-byte accesses).
+__global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void act_dgrad_kernel(ActDgradParams p) {
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[NSTAGE * STAGE];
+    SegMeta sm;
+    int mtile, ntile;
+    if (!train_tile(p.seg, p.hs, p.nseg, p.T, p.Is, p.nIs, p.nI, xcd_tile(), sm, mtile, ntile)) return;
+    const bool shared = sm.e < 0;
+    const int C = shared ? p.Is : p.I;  // channels (row length of g, u, dG, dU)
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+    const int wm = wave / WN, wn = wave % WN;
+
+    NTOperands op;
+    op.K = p.d;
+    const bf16_t* A = shared ? p.dYs : p.dO + (size_t)sm.row0 * p.d;
+    const bf16_t* B = shared ? p.wsdt : p.wdt + (size_t)sm.e * p.I * p.d;
+    op.ra = make_rsrc(A, (size_t)sm.rows * p.d);
+    op.rb = make_rsrc(B, (size_t)C * p.d);
+    int bcol[NI];
+    nt_rows(wave, lane, mtile * BM, sm.rows, p.d, op.aoff, op.acol);
+    nt_rows(wave, lane, ntile * BN, C, p.d, op.boff, bcol);
+
+    const size_t rbase = shared ? 0 : (size_t)sm.row0;
+    const bf16_t* G = shared ? p.Gs : p.G;
+    const bf16_t* U = shared ? p.Us : p.U;
+    bf16_t* dG = shared ? p.dGs : p.dG;
+    bf16_t* dU = shared ? p.dUs : p.dU;
+    const int kk = sm.kk;                        // mask: channels below kk are kept
+    const int kk8 = min(packed_width(kk), C);    // dG/dU columns the dx GEMM reads
+    by_rows(sm.rows - mtile * BM, [&](auto tag) {
+        constexpr int MFW = decltype(tag)::value;
+        floatx16 acc[MFW][NF];
+        nt_mainloop<MFW, false>(smem, op, wave, lane, acc, ZeroTail{op.ra});
+        // epilogue: lane -> row (lane%32 of a fragment), register v ->
+        // channel 8(v/4) + 4(lane/32) + v%4 of a 32-channel fragment
+        float msum[NF][16];
+#pragma unroll
+        for (int j = 0; j < NF; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) msum[j][v] = 0.f;
+#pragma unroll
+        for (int i = 0; i < MFW; ++i) {
+            const int row = mtile * BM + wm * 32 * MFW + i * 32 + (lane & 31);
+            if (row >= sm.rows) continue;
+            const size_t ro = (rbase + row) * (size_t)C;
+#pragma unroll
+            for (int j = 0; j < NF; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int c0 = ntile * BN + wn * WCOL + j * 32 + q * 8 + (lane >> 5) * 4;
+                    if (c0 >= C) continue;
+                    const uint2 gv = *reinterpret_cast<const uint2*>(G + ro + c0);
+                    const uint2 uv = *reinterpret_cast<const uint2*>(U + ro + c0);
+                    const float g[4] = {lo_bf16(gv.x), hi_bf16(gv.x), lo_bf16(gv.y), hi_bf16(gv.y)};
+                    const float u[4] = {lo_bf16(uv.x), hi_bf16(uv.x), lo_bf16(uv.y), hi_bf16(uv.y)};
+                    uint32_t dg[2] = {0u, 0u}, du[2] = {0u, 0u};
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const float x = g[r];
+                        const float sg = 1.0f / (1.0f + __builtin_amdgcn_exp2f(-x * 1.4426950408889634f));
+                        const float dh = acc[i][j][q * 4 + r];
+                        msum[j][q * 4 + r] += dh * (x * sg) * u[r];
+                        const bool kept = c0 + r < kk;
+                        const float vg = kept ? dh * u[r] * (sg * (1.0f + x * (1.0f - sg))) : 0.f;
+                        const float vu = kept ? dh * (x * sg) : 0.f;
+                        dg[r >> 1] |= (uint32_t)f32_to_bf16(vg) << (16 * (r & 1));
+                        du[r >> 1] |= (uint32_t)f32_to_bf16(vu) << (16 * (r & 1));
+                    }
+                    if (c0 < kk8) {
+                        *reinterpret_cast<uint2*>(dG + ro + c0) = make_uint2(dg[0], dg[1]);
+                        *reinterpret_cast<uint2*>(dU + ro + c0) = make_uint2(du[0], du[1]);
+                    }
+                }
+        }
+        if (shared) return;
+        // mask-gradient partial sums: over the 32 rows of the lane group
+#pragma unroll
+        for (int j = 0; j < NF; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                float t = msum[j][v];
+#pragma unroll
+                for (int o = 1; o < 32; o <<= 1) t += __shfl_xor(t, o, 64);
+                msum[j][v] = t;
+            }
+        if ((lane & 31) == 0) {
+            float* out = p.dmp + ((size_t)(sm.rt0 + mtile) * kTrainWaveM + wm) * p.I;
+#pragma unroll
+            for (int j = 0; j < NF; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int c = ntile * BN + wn * WCOL + j * 32 + q * 8 + (lane >> 5) * 4 + r;
+                        if (c < p.I) out[c] = msum[j][q * 4 + r];
+                    }
+        }
+    });
+}
+
+// dX = dG W_gate + dU W_up over the kept channels; tile = 256 rows x 256
+// hidden units, two K loops into one accumulator.
+__global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void act_dx_kernel(ActDxParams p) {
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[NSTAGE * STAGE];
+    SegMeta sm;
+    int mtile, ntile;
+    if (!train_tile(p.seg, p.hs, p.nseg, p.T, p.Is, p.nD, p.nD, xcd_tile(), sm, mtile, ntile)) return;
+    const bool shared = sm.e < 0;
+    const int C = shared ? p.Is : p.I;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+    const int wm = wave / WN, wn = wave % WN;
+    const size_t rbase = shared ? 0 : (size_t)sm.row0;
+
+    NTOperands og, ou;
+    og.K = ou.K = sm.kk;
+    const bf16_t* Ag = (shared ? p.dGs : p.dG) + rbase * C;
+    const bf16_t* Au = (shared ? p.dUs : p.dU) + rbase * C;
+    const bf16_t* Bg = shared ? p.wsgt : p.wgt + (size_t)sm.e * p.d * p.I;
+    const bf16_t* Bu = shared ? p.wsut : p.wut + (size_t)sm.e * p.d * p.I;
+    og.ra = make_rsrc(Ag, (size_t)sm.rows * C);
+    ou.ra = make_rsrc(Au, (size_t)sm.rows * C);
+    og.rb = make_rsrc(Bg, (size_t)p.d * C);
+    ou.rb = make_rsrc(Bu, (size_t)p.d * C);
+    int bcol[NI];
+    nt_rows(wave, lane, mtile * BM, sm.rows, C, og.aoff, og.acol);
+    nt_rows(wave, lane, ntile * BN, p.d, C, og.boff, bcol);
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+        ou.aoff[i] = og.aoff[i];
+        ou.boff[i] = og.boff[i];
+        ou.acol[i] = og.acol[i];
+    }
+    float* out = (shared ? p.dXs : p.dXr) + rbase * p.d;
+    by_rows(sm.rows - mtile * BM, [&](auto tag) {
+        constexpr int MFW = decltype(tag)::value;
+        floatx16 acc[MFW][NF];
+        nt_mainloop<MFW, false>(smem, og, wave, lane, acc, ZeroTail{og.ra});
+        // every wave is past its last LDS read before the second loop refills the stages
+        __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+        barrier_no_fence();
+        nt_mainloop<MFW, false>(smem, ou, wave, lane, acc, ZeroTail{ou.ra}, false);
+        // epilogue: lane -> row, registers -> runs of 4 hidden units
+#pragma unroll
+        for (int i = 0; i < MFW; ++i) {
+            const int row = mtile * BM + wm * 32 * MFW + i * 32 + (lane & 31);
+            if (row >= sm.rows) continue;
+#pragma unroll
+            for (int j = 0; j < NF; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int n0 = ntile * BN + wn * WCOL + j * 32 + q * 8 + (lane >> 5) * 4;
+                    if (n0 >= p.d) continue;
+                    *reinterpret_cast<float4*>(out + (size_t)row * p.d + n0) =
+                        make_float4(acc[i][j][q * 4], acc[i][j][q * 4 + 1], acc[i][j][q * 4 + 2],
+                                    acc[i][j][q * 4 + 3]);
+                }
+        }
+    });
+}
+
+hipError_t launch_act_dgrad(const ActDgradParams& p, long long tiles, hipStream_t s) {
+    if (tiles <= 0) return hipSuccess;
+    const long long g = (tiles + 8 * XCD_GROUP - 1) / (8 * XCD_GROUP) * (8 * XCD_GROUP);
+    act_dgrad_kernel<<<(int)g, THREADS, 0, s>>>(p);
+    return hipGetLastError();
+}
+
+hipError_t launch_act_dx(const ActDxParams& p, long long tiles, hipStream_t s) {
+    if (tiles <= 0) return hipSuccess;
+    const long long g = (tiles + 8 * XCD_GROUP - 1) / (8 * XCD_GROUP) * (8 * XCD_GROUP);
+    act_dx_kernel<<<(int)g, THREADS, 0, s>>>(p);
+    return hipGetLastError();
 }
 
 hipError_t launch_sal_dgrad(const SalDgradParams& p, long long tiles, hipStream_t s) {

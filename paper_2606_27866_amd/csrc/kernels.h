@@ -47,6 +47,13 @@ struct Gemm1Params {
     T* ut;
     T* ht;
     int ldt;
+    // Training forward of the masked layer (launch_gemm1_big_train_rm): g and
+    // u of every row in the layout of H and Hs -- routed [A][I], shared
+    // [T][I_s] -- for every channel the GEMM computes (c < kg).
+    T* G;
+    T* U;
+    T* Gs;
+    T* Us;
 };
 
 // Down GEMM: O[row][n] = sum_{c < k_s} H[row][c] * W_down[n][c].  O holds one

@@ -54,7 +54,6 @@ hipError_t launch_gemm1_big_train(const Gemm1Params<bf16_t>& p, int grid, hipStr
 hipError_t launch_sal_dgrad(const SalDgradParams& p, long long tiles, hipStream_t s);
 hipError_t launch_sal_wgrad(const SalWgradParams& p, hipStream_t s);
 hipError_t launch_sal_prep(const SalPrepParams& p, hipStream_t s);
-hipError_t launch_transpose_down(const bf16_t* wd, bf16_t* wdt, int E, int d, int I, hipStream_t s);
 hipError_t launch_sal_reduce(const float* partial, int E, int I, int parts, float scale, float* scores,
                              hipStream_t s);
 // dY = (the combined layer output in fp32, before any rounding) - target.

@@ -1,13 +1,15 @@
 // Data movement of the channel saliency (FlexMoE Sec. 3.1, Eq. 2) around
 // its backward GEMMs (gemm_bwd.hip):
-//   - a transposed copy of the routed down weights, W_down^T [E][I][d], the
-//     B operand of the dgrad and the theta of the down matrix's saliency;
+//   - transposed weight copies (W_down^T [E][I][d] is the B operand of the
+//     dgrad and the theta of the down matrix's saliency; the training
+//     backward also takes W_gate^T and W_up^T);
 //   - transposed copies of x and of dO = w_a dY_t for the routed rows, whose
 //     segments become the reduction dimension of the wgrad, and dO itself;
 //   - the final sum of the wgrad tiles' partial scores.
 // Transposes go through a 64 x 64 LDS tile with 16-byte global accesses on
 // both sides.
 #include "saliency.h"
+#include "train.h"
 
 namespace flexmoe {
 
@@ -31,9 +33,11 @@ __device__ __forceinline__ uint4 pack8(const bf16_t* v) {
 }
 }  // namespace
 
-// W_down [E][d][I] -> W_down^T [E][I][d]; block (channel tile, unit tile, e).
-__global__ __launch_bounds__(TTHREADS) void transpose_down_kernel(const bf16_t* __restrict__ wd,
-                                                                  bf16_t* __restrict__ wdt, int d, int I) {
+// src [batch][R][C] -> dst [batch][C][R] (e.g. W_down [E][d][I] -> W_down^T
+// [E][I][d]); block (column tile, row tile, batch).  The names below follow
+// that example: rows n < d, columns c < I.
+__global__ __launch_bounds__(TTHREADS) void transpose_batched_kernel(const bf16_t* __restrict__ wd,
+                                                                     bf16_t* __restrict__ wdt, int d, int I) {
     __shared__ bf16_t tile[TT][TPAD];
     const size_t e = blockIdx.z;
     const int c0 = blockIdx.x * TT, n0 = blockIdx.y * TT;
@@ -129,9 +133,11 @@ __global__ __launch_bounds__(256) void sal_reduce_kernel(const float* __restrict
     scores[i] += scale * s;
 }
 
-hipError_t launch_transpose_down(const bf16_t* wd, bf16_t* wdt, int E, int d, int I, hipStream_t s) {
-    const dim3 grid(ceil_div(I, TT), ceil_div(d, TT), E);
-    transpose_down_kernel<<<grid, TTHREADS, 0, s>>>(wd, wdt, d, I);
+hipError_t launch_transpose_batched(const bf16_t* src, bf16_t* dst, int batch, int rows, int cols,
+                                    hipStream_t s) {
+    if (batch <= 0 || rows <= 0 || cols <= 0) return hipSuccess;
+    const dim3 grid(ceil_div(cols, TT), ceil_div(rows, TT), batch);
+    transpose_batched_kernel<<<grid, TTHREADS, 0, s>>>(src, dst, rows, cols);
     return hipGetLastError();
 }
 

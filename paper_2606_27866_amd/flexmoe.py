@@ -33,12 +33,15 @@ EXPORTED = ("flexmoe_workspace_bytes", "flexmoe_rank_reorder", "flexmoe_set_budg
             "flexmoe_timing_enable", "flexmoe_timing_read", "flexmoe_clipped_channels",
             "flexmoe_export_clipped", "flexmoe_layer_forward_clipped",
             "flexmoe_layer_forward_bucketed", "flexmoe_saliency_workspace_bytes",
-            "flexmoe_channel_saliency")
+            "flexmoe_channel_saliency", "flexmoe_transpose_weights", "flexmoe_sample_actions",
+            "flexmoe_train_workspace_bytes", "flexmoe_train_forward", "flexmoe_train_backward",
+            "flexmoe_action_grad")
 
 # kernel indices of flexmoe_kernel_times
 KERNELS = ("route", "dispatch_scan", "dispatch_scatter", "gate_up", "down", "combine",
            "gate_up_shared", "down_shared", "sal_transpose", "sal_prep", "sal_dgrad", "sal_wgrad",
-           "sal_reduce")
+           "sal_reduce", "act_dgrad", "act_dx", "act_other")
+MAX_ACTIONS = 16
 
 
 class FlexMoEError(RuntimeError):
@@ -54,6 +57,18 @@ class flexmoe_layer_desc(ctypes.Structure):
 
 class flexmoe_kernel_times(ctypes.Structure):
     _fields_ = [("ms", ctypes.c_double * len(KERNELS)), ("launches", ctypes.c_int64 * len(KERNELS))]
+
+
+class flexmoe_action_set(ctypes.Structure):
+    _fields_ = [("K", ctypes.c_int32), ("ratio", ctypes.c_double * MAX_ACTIONS)]
+
+
+def make_actions(ratios) -> flexmoe_action_set:
+    a = flexmoe_action_set()
+    a.K = len(ratios)
+    for i, r in enumerate(ratios):
+        a.ratio[i] = float(r)
+    return a
 
 
 class flexmoe_route_out(ctypes.Structure):
@@ -102,6 +117,20 @@ def lib():
         L.flexmoe_channel_saliency.argtypes = ([D, i32] + [vp] * 9 + [ctypes.c_float] + [vp] * 2
                                                + [sz, vp])
         L.flexmoe_channel_saliency.restype = ctypes.c_int
+        AS = ctypes.POINTER(flexmoe_action_set)
+        f32 = ctypes.c_float
+        L.flexmoe_transpose_weights.argtypes = [D] + [vp] * 13
+        L.flexmoe_transpose_weights.restype = ctypes.c_int
+        L.flexmoe_sample_actions.argtypes = [D, AS] + [vp] * 5
+        L.flexmoe_sample_actions.restype = ctypes.c_int
+        L.flexmoe_train_workspace_bytes.argtypes = [D, i32]
+        L.flexmoe_train_workspace_bytes.restype = sz
+        L.flexmoe_train_forward.argtypes = [D, i32] + [vp] * 11 + [sz, vp]
+        L.flexmoe_train_forward.restype = ctypes.c_int
+        L.flexmoe_train_backward.argtypes = [D, i32] + [vp] * 12 + [sz, vp]
+        L.flexmoe_train_backward.restype = ctypes.c_int
+        L.flexmoe_action_grad.argtypes = [D, i32, AS, vp, vp, f32, f32, f32, vp, vp, vp, vp, sz, vp]
+        L.flexmoe_action_grad.restype = ctypes.c_int
         L.flexmoe_keep_from_ratio.argtypes = [ctypes.c_double, i32]
         L.flexmoe_keep_from_ratio.restype = ctypes.c_int
         L.flexmoe_timing_enable.argtypes = [ctypes.c_int]
@@ -256,6 +285,52 @@ def flexmoe_channel_saliency(desc, T, x, logits, w_gate, w_up, w_down, ws_gate, 
                                           _stream(stream)))
 
 
+def _nbytes(t, given):
+    return t.numel() * t.element_size() if given is None else given
+
+
+def flexmoe_transpose_weights(desc, w_gate, w_up, w_down, ws_gate, ws_up, ws_down, w_gate_t, w_up_t, w_down_t,
+                              ws_gate_t, ws_up_t, ws_down_t, stream=None):
+    _check(lib().flexmoe_transpose_weights(ctypes.byref(desc), *[_p(t) for t in (
+        w_gate, w_up, w_down, ws_gate, ws_up, ws_down, w_gate_t, w_up_t, w_down_t, ws_gate_t, ws_up_t,
+        ws_down_t)], _stream(stream)))
+
+
+def flexmoe_sample_actions(desc, actions, alpha, gumbel, keep_dev, action_dev=None, stream=None):
+    _check(lib().flexmoe_sample_actions(ctypes.byref(desc), ctypes.byref(actions), _p(alpha), _p(gumbel),
+                                        _p(keep_dev), _p(action_dev), _stream(stream)))
+
+
+def flexmoe_train_workspace_bytes(desc, T: int) -> int:
+    n = lib().flexmoe_train_workspace_bytes(ctypes.byref(desc), int(T))
+    if n == 0:
+        raise FlexMoEError(-2, lib().flexmoe_last_error().decode())
+    return n
+
+
+def flexmoe_train_forward(desc, T, x, logits, w_gate, w_up, w_down, keep_dev, ws_gate, ws_up, ws_down, y,
+                          workspace, workspace_bytes=None, stream=None):
+    _check(lib().flexmoe_train_forward(ctypes.byref(desc), int(T), _p(x), _p(logits), _p(w_gate), _p(w_up),
+                                       _p(w_down), _p(keep_dev), _p(ws_gate), _p(ws_up), _p(ws_down), _p(y),
+                                       _p(workspace), _nbytes(workspace, workspace_bytes), _stream(stream)))
+
+
+def flexmoe_train_backward(desc, T, logits, dy, w_gate_t, w_up_t, w_down_t, ws_gate_t, ws_up_t, ws_down_t, dx,
+                           dlogits, dmask, workspace, workspace_bytes=None, stream=None):
+    _check(lib().flexmoe_train_backward(ctypes.byref(desc), int(T), _p(logits), _p(dy), _p(w_gate_t),
+                                        _p(w_up_t), _p(w_down_t), _p(ws_gate_t), _p(ws_up_t), _p(ws_down_t),
+                                        _p(dx), _p(dlogits), _p(dmask), _p(workspace),
+                                        _nbytes(workspace, workspace_bytes), _stream(stream)))
+
+
+def flexmoe_action_grad(desc, T, actions, alpha, gumbel, tau, lambda_cost, beta, dmask, dalpha, stats,
+                        workspace, workspace_bytes=None, stream=None):
+    _check(lib().flexmoe_action_grad(ctypes.byref(desc), int(T), ctypes.byref(actions), _p(alpha), _p(gumbel),
+                                     float(tau), float(lambda_cost), float(beta), _p(dmask), _p(dalpha),
+                                     _p(stats), _p(workspace), _nbytes(workspace, workspace_bytes),
+                                     _stream(stream)))
+
+
 class ClippedWeights:
     """The packed weights of one exported budget (offline clipping) and its
     device keep table."""
@@ -360,6 +435,76 @@ class Saliency:
         perm = torch.empty((L.desc.E, L.desc.I), dtype=torch.int32, device=L.device)
         flexmoe_rank_reorder(L.desc, self.scores, L.w_gate, L.w_up, L.w_down, *out, perm, stream=stream)
         return (*out, perm)
+
+
+class ActionLearner:
+    """One layer's action-learning step on the device (Sec. 3.2): sample the
+    per-expert widths (Eq. 5), run the sampled subnet forward, backward for
+    an upstream gradient, and the action-logit gradient (Eqs. 6-8).
+
+    Holds the transposed weight copies (made once: the weights are frozen),
+    the sampled keep table and a training workspace for up to max_tokens.
+    """
+
+    def __init__(self, layer: "Layer", max_tokens: int, ratios):
+        import torch
+        self.layer = layer
+        D = layer.desc
+        self.desc = make_desc(D.d, D.E, D.I, D.top_k, D.I_shared, D.dtype, D.norm_topk, max_tokens)
+        self.actions = make_actions(ratios)
+        dev = layer.device
+        nbytes = flexmoe_train_workspace_bytes(self.desc, max_tokens)
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        bf = layer.tdtype
+        self.wt = [torch.empty((D.E, D.d, D.I), dtype=bf, device=dev),
+                   torch.empty((D.E, D.d, D.I), dtype=bf, device=dev),
+                   torch.empty((D.E, D.I, D.d), dtype=bf, device=dev)]
+        if D.I_shared:
+            self.wst = [torch.empty((D.d, D.I_shared), dtype=bf, device=dev),
+                        torch.empty((D.d, D.I_shared), dtype=bf, device=dev),
+                        torch.empty((D.I_shared, D.d), dtype=bf, device=dev)]
+        else:
+            self.wst = [None, None, None]
+        self.keep = torch.zeros((D.E,), dtype=torch.int32, device=dev)
+        self.action = torch.zeros((D.E,), dtype=torch.int32, device=dev)
+        self.T = 0
+
+    def transpose_weights(self, stream=None):
+        L = self.layer
+        flexmoe_transpose_weights(self.desc, L.w_gate, L.w_up, L.w_down, L.ws_gate, L.ws_up, L.ws_down,
+                                  *self.wt, *self.wst, stream=stream)
+
+    def sample(self, alpha, gumbel, stream=None):
+        flexmoe_sample_actions(self.desc, self.actions, alpha, gumbel, self.keep, self.action, stream=stream)
+
+    def forward(self, x, logits, y=None, keep=None, stream=None):
+        import torch
+        L = self.layer
+        self.T = x.shape[0]
+        if y is None:
+            y = torch.empty((self.T, self.desc.d), dtype=L.tdtype, device=L.device)
+        flexmoe_train_forward(self.desc, self.T, x, logits, L.w_gate, L.w_up, L.w_down,
+                              self.keep if keep is None else keep, L.ws_gate, L.ws_up, L.ws_down, y,
+                              self.workspace, stream=stream)
+        return y
+
+    def backward(self, logits, dy, stream=None):
+        import torch
+        D, dev = self.desc, self.layer.device
+        dx = torch.empty((self.T, D.d), dtype=torch.float32, device=dev)
+        dl = torch.empty((self.T, D.E), dtype=torch.float32, device=dev)
+        dm = torch.empty((D.E, D.I), dtype=torch.float32, device=dev)
+        flexmoe_train_backward(D, self.T, logits, dy, *self.wt, *self.wst, dx, dl, dm, self.workspace,
+                               stream=stream)
+        return dx, dl, dm
+
+    def action_grad(self, alpha, gumbel, tau, lambda_cost, beta, dmask, stream=None):
+        import torch
+        dalpha = torch.empty_like(alpha)
+        stats = torch.empty((2,), dtype=torch.float32, device=alpha.device)
+        flexmoe_action_grad(self.desc, self.T, self.actions, alpha, gumbel, tau, lambda_cost, beta, dmask, dalpha,
+                            stats, self.workspace, stream=stream)
+        return dalpha, stats
 
 
 def to_device(a: np.ndarray, device="cuda"):

@@ -217,6 +217,21 @@ def make_target(cfg: LayerConfig, T: Optional[int] = None, std: float = 0.05, ba
     return _normal(cfg.config_id, tid, T * cfg.d, std).reshape(T, cfg.d)
 
 
+_TID_ALPHA = 17
+_TID_GUMBEL = 18
+
+
+def make_action_inputs(cfg: LayerConfig, K: int, step: int = 0, alpha_std: float = 1.0):
+    """Action logits alpha [E][K] (Gaussian) and the Gumbel(0, 1) draws of one
+    sampling step [E][K] (-log(-log U), U uniform in (0, 1)), both fp32."""
+    alpha = _normal(cfg.config_id, _TID_ALPHA, cfg.E * K, alpha_std).reshape(cfg.E, K)
+    g = rng_for(cfg.config_id, _TID_GUMBEL + 1000 * step)
+    u = g.random(cfg.E * K, dtype=np.float64)
+    u = np.clip(u, 1e-12, 1.0 - 1e-12)
+    gumbel = (-np.log(-np.log(u))).astype(np.float32).reshape(cfg.E, K)
+    return alpha, gumbel
+
+
 def make_calibration_batch(cfg: LayerConfig, batch: int, T: Optional[int] = None,
                            bias: Optional[np.ndarray] = None):
     """Tokens x [T][d] and logits [T][E] of calibration batch `batch` (same
