@@ -24,6 +24,9 @@ saliency of every routed channel over calibration batches of the workload's
 size (a layer-level squared-error loss against a seeded target), with the
 roofline of its dominant kernel (the weight-gradient GEMMs with the fused
 saliency reduction), the reorder of Eq. 3, and the oracle on a sample.
+`action_learning` times one action-learning step of the layer on the device:
+the Gumbel-max width sample of every expert, the sampled subnet's forward,
+its backward for a fixed upstream gradient, and the action-logit gradient.
 """
 import argparse
 import hashlib
@@ -63,6 +66,8 @@ def parse():
     ap.add_argument("--saliency-T", type=int, default=0,
                     help="tokens per calibration batch of the saliency (default: the workload's T)")
     ap.add_argument("--saliency-steps", type=int, default=10)
+    ap.add_argument("--no-action", action="store_true", help="skip the action-learning step measurement")
+    ap.add_argument("--action-steps", type=int, default=10)
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-baseline work")
     ap.add_argument("--bucket-align", type=int, default=128,
                     help="k_align of the bucketed ablation in the per-budget results")
@@ -343,6 +348,103 @@ def saliency_section(wl, args):
     return out
 
 
+def action_section(wl, args):
+    """One action-learning step of the layer on the device (Sec. 3.2): the
+    Gumbel-max sample of every expert's width (Eq. 5), the sampled subnet's
+    forward, its backward for a fixed synthetic upstream gradient, and the
+    action-logit gradient (Eqs. 6-8).  Fresh Gumbel draws every step, so the
+    widths change from step to step."""
+    torch, fm, synth, cfg = wl.torch, wl.fm, wl.synth, wl.cfg
+    T = wl.T
+    ratios = synth.ACTION_RATIOS
+    K = len(ratios)
+    nsteps = 8
+    alpha, _ = synth.make_action_inputs(cfg, K)
+    gumbels = [fm.to_device(synth.make_action_inputs(cfg, K, step=i)[1]) for i in range(nsteps)]
+    ad = fm.to_device(alpha)
+    x, lg = wl.xd[0]
+    dy = fm.to_device(synth.make_target(cfg, T, std=1e-3))   # a fixed upstream gradient dL/dY
+    wl.use_copy(0)
+    lr = fm.ActionLearner(wl.layer, T, ratios)
+    lr.transpose_weights()
+    y = torch.empty((T, cfg.d), dtype=wl.layer.tdtype, device="cuda")
+    tau, lam, beta = 1.0, 0.1, 0.01
+
+    def step(i):
+        lr.sample(ad, gumbels[i % nsteps])
+        lr.forward(x, lg, y=y)
+        _, _, dm = lr.backward(lg, dy)
+        lr.action_grad(ad, gumbels[i % nsteps], tau, lam, beta, dm)
+
+    def run(k, timed_kernels=False):
+        if timed_kernels:
+            fm.flexmoe_timing_enable(True)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(k):
+            step(i)
+        e1.record()
+        torch.cuda.synchronize()
+        kt = None
+        if timed_kernels:
+            kt = fm.flexmoe_timing_read()
+            fm.flexmoe_timing_enable(False)
+        return e0.elapsed_time(e1), kt
+
+    run(2)
+    steps = args.action_steps
+    ms, _ = run(steps)
+    _, kt = run(steps, timed_kernels=True)
+    # algorithmic work of the average step: the sampled widths of each step
+    # and the routed counts (fixed: the batch does not change)
+    n = wl.counts(0, "kept100")
+    A_I = 0
+    nk = 0
+    for i in range(steps):
+        keep, _, _ = _sample_host(synth, cfg, ratios, alpha, i % nsteps)
+        nk += int((n * keep).sum())
+        A_I += int(n.sum()) * cfg.I
+    nk /= steps
+    A_I /= steps
+    d, Is = cfg.d, cfg.I_shared
+    f_fwd = 4 * d * A_I + 2 * d * nk + 6 * d * T * Is        # gate/up at full width, down at the kept width
+    f_dgrad = 2 * d * A_I + 2 * d * T * Is
+    f_dx = 4 * d * nk + 4 * d * T * Is
+    f_all = f_fwd + f_dgrad + f_dx
+    ms_s = ms / steps
+    kms = {k: v[0] / max(v[1], 1) for k, v in kt.items() if v[1]}
+    dg_ms = kms.get("act_dgrad", float("nan"))
+    dx_ms = kms.get("act_dx", float("nan"))
+    gu_ms = kms.get("gate_up", float("nan"))
+    out = dict(tokens=T, steps_timed=steps, ms_per_step=ms_s, tokens_per_s=T / (ms_s / 1e3),
+               tflops=f_all / (ms_s / 1e3) / 1e12, frac_mfma=f_all / (ms_s / 1e3) / 1e12 / PEAK_BF16_TFLOPS,
+               flops_per_step=f_all, mean_kept_fraction=nk / A_I, ratios=list(ratios),
+               roofline_dgrad=dict(kernel="dgrad + SwiGLU backward + mask gradient (act_dgrad_kernel)",
+                                   bound="mfma", achieved=f_dgrad / (dg_ms / 1e3) / 1e12, peak=PEAK_BF16_TFLOPS,
+                                   unit="TFLOP/s", frac=f_dgrad / (dg_ms / 1e3) / 1e12 / PEAK_BF16_TFLOPS,
+                                   avg_launch_ms=dg_ms, flops_per_launch=f_dgrad),
+               dx_tflops=f_dx / (dx_ms / 1e3) / 1e12, gate_up_tflops=4 * d * (A_I + T * Is) / (gu_ms / 1e3) / 1e12,
+               kernels_ms=kms,
+               upstream_gradient="fixed seeded Gaussian dL/dY (std 1e-3); Gumbel draws change every step")
+    log("[bench] action step: %.4f ms/step, %.0f tokens/s, %.1f TFLOP/s; dgrad %.4f ms (%.1f TFLOP/s), dx %.4f ms "
+        "(%.1f TFLOP/s), gate/up %.4f ms; mean kept fraction %.3f"
+        % (ms_s, T / (ms_s / 1e3), out["tflops"], dg_ms, out["roofline_dgrad"]["achieved"], dx_ms,
+           out["dx_tflops"], gu_ms, nk / A_I))
+    for k, v in kms.items():
+        log("[bench]   action %-17s %8.4f ms" % (k, v))
+    return out
+
+
+def _sample_host(synth, cfg, ratios, alpha, step):
+    """The widths the device samples at `step` (same fp32 argmax), for the
+    algorithmic flop count."""
+    _, gumbel = synth.make_action_inputs(cfg, len(ratios), step=step)
+    widths = np.array([int(np.ceil(r * cfg.I - 1e-9)) for r in ratios], np.int64)
+    act = np.argmax(alpha + gumbel, axis=1)
+    return widths[act], act, None
+
+
 def saliency_cpu_baseline(wl, T, target_s):
     """The oracle's Eq. 2 on the first S tokens of calibration batch 0."""
     import oracle
@@ -516,6 +618,9 @@ def main():
     saliency = None
     if not args.no_saliency and bf16 and not wl.decode:
         saliency = saliency_section(wl, args)
+    action = None
+    if not args.no_action and bf16 and not wl.decode:
+        action = action_section(wl, args)
 
     if args.copy_calibration_mib > 0:
         n = args.copy_calibration_mib << 20
@@ -554,6 +659,7 @@ def main():
         "per_budget": per_budget,
         "action_set_ablation": action_ablation,
         "saliency": saliency,
+        "action_learning": action,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
