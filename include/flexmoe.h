@@ -238,11 +238,13 @@ int flexmoe_train_backward(const flexmoe_layer_desc *desc, int32_t T, const floa
  * beta p_k (log p_k + H_e) / E, where p = softmax(alpha),
  * H_e = -<p, log p> and q_e = n_e / (T top_k) from the forward's routing.
  * stats (may be NULL) [2] fp32 receives C = sum_e q_e <p_e, r> and
- * H = mean_e H_e.  tau > 0 (FLEXMOE_EINVAL otherwise). */
+ * H = mean_e H_e.  tau > 0 (FLEXMOE_EINVAL otherwise).  The workspace is the
+ * step's training workspace: its routing counts are read and a small region
+ * of it is written. */
 int flexmoe_action_grad(const flexmoe_layer_desc *desc, int32_t T, const flexmoe_action_set *actions,
                         const float *alpha, const float *gumbel, float tau, float lambda_cost,
                         float beta, const float *dmask, float *dalpha, float *stats,
-                        const void *workspace, size_t workspace_bytes, void *stream);
+                        void *workspace, size_t workspace_bytes, void *stream);
 
 /* Budget switch: validates 0 <= keep_host[e] <= I for every e on the host, then
  * writes the E counts into keep_dev [E] on `stream` (one small kernel whose

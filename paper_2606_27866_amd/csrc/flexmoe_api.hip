@@ -966,7 +966,7 @@ namespace {
 // ---- action learning: training step of the masked layer --------------------
 struct TrainLayout {
     Layout f;  // the forward's regions (shared expert unsplit)
-    size_t G, U, Gs, Us, dO, dYs, dG, dU, dGs, dUs, dXr, dXs, dmp, total;
+    size_t G, U, Gs, Us, dO, dYs, dG, dU, dGs, dUs, dXr, dXs, dmp, stat, total;
     long long rt;  // bound on the routed row tiles
 };
 
@@ -994,6 +994,7 @@ TrainLayout train_layout(const flexmoe_layer_desc& D, int T) {
     S.dXr = take(A * d * 4);
     S.dXs = take(Tz * d * 4);
     S.dmp = take((size_t)S.rt * kTrainWaveM * I * 4);
+    S.stat = take((size_t)D.E * 2 * 4);
     S.total = off;
     return S;
 }
@@ -1292,7 +1293,7 @@ int flexmoe_train_backward(const flexmoe_layer_desc* desc, int32_t T, const floa
 
 int flexmoe_action_grad(const flexmoe_layer_desc* desc, int32_t T, const flexmoe_action_set* actions,
                         const float* alpha, const float* gumbel, float tau, float lambda_cost, float beta,
-                        const float* dmask, float* dalpha, float* stats, const void* workspace,
+                        const float* dmask, float* dalpha, float* stats, void* workspace,
                         size_t workspace_bytes, void* stream) {
     int rc = check_train(desc, T);
     if (rc) return rc;
@@ -1305,9 +1306,11 @@ int flexmoe_action_grad(const flexmoe_layer_desc* desc, int32_t T, const flexmoe
     const TrainLayout S = train_layout(D, T);
     if ((rc = check_workspace(S, workspace, workspace_bytes)) != FLEXMOE_OK) return rc;
     const int32_t* counts = (const int32_t*)((const char*)workspace + S.f.counts);
+    float* per_expert = (float*)((char*)workspace + S.stat);
     KernelTimer kt(FLEXMOE_K_ACT_OTHER, (hipStream_t)stream);
     const hipError_t err = launch_action_grad(aw, alpha, gumbel, tau, dmask, counts, (long long)T * D.top_k, D.E,
-                                              D.I, lambda_cost, beta, dalpha, stats, (hipStream_t)stream);
+                                              D.I, lambda_cost, beta, dalpha, per_expert, stats,
+                                              (hipStream_t)stream);
     if (err != hipSuccess) return hip_fail(err, "action_grad launch");
     return FLEXMOE_OK;
 }

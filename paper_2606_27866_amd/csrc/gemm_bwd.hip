@@ -182,10 +182,17 @@ __device__ __forceinline__ void by_rows(int rows, F&& body) {
     else body(std::integral_constant<int, 1>{});
 }
 
-__device__ __forceinline__ int xcd_tile() {
+// Tile of this workgroup when groups of `group` consecutive tiles go to one
+// XCD (workgroup b runs on XCD b % 8): tiles that share operands then share
+// that XCD's L2.  The grid is a multiple of 8 * group (xcd_grid).
+__device__ __forceinline__ int xcd_tile(int group = XCD_GROUP) {
     const int jb = blockIdx.x >> 3;
-    return (jb / XCD_GROUP) * (8 * XCD_GROUP) + (blockIdx.x & 7) * XCD_GROUP + jb % XCD_GROUP;
+    return (jb / group) * (8 * group) + (blockIdx.x & 7) * group + jb % group;
 }
+long long xcd_grid(long long tiles, int group) { return (tiles + 8LL * group - 1) / (8LL * group) * (8LL * group); }
+// Tiles per XCD group of the dgrad kernels: about one routed expert (two
+// row tiles x all channel tiles), whose tiles share its rows of dO.
+__host__ __device__ __forceinline__ int dgrad_group(int n_ct) { return 2 * n_ct; }
 
 __device__ __forceinline__ float lo_bf16(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float hi_bf16(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -194,7 +201,7 @@ __device__ __forceinline__ float hi_bf16(uint32_t w) { return __uint_as_float(w 
 // ---- dgrad: one tile = 256 rows of a routed segment x 256 channels --------
 __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void sal_dgrad_kernel(SalDgradParams p) {
     __shared__ __attribute__((aligned(1024))) unsigned char smem[NSTAGE * STAGE];
-    const int L = xcd_tile();
+    const int L = xcd_tile(dgrad_group(p.nI));
     // routed segment: the last one whose first tile is at or before L
     int lo = p.hs, hi = p.nseg - 1;
     while (lo < hi) {
@@ -271,7 +278,9 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void sal_dgrad_kernel(SalD
 // (matrix, expert) ----------------------------------------------------------
 __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void sal_wgrad_kernel(SalWgradParams p) {
     __shared__ __attribute__((aligned(1024))) unsigned char smem[NSTAGE * STAGE];
-    const int L = xcd_tile();
+    // all tiles of one (matrix, expert) on one XCD: they share its x^T (or
+    // dO^T) rows and its dG^T (dU^T, h^T) rows
+    const int L = xcd_tile(p.nI * p.nM);
     if (L >= 3 * p.E * p.nI * p.nM) return;
     const int mtile = L % p.nM;
     int rest = L / p.nM;
@@ -402,7 +411,8 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void act_dgrad_kernel(ActD
     __shared__ __attribute__((aligned(1024))) unsigned char smem[NSTAGE * STAGE];
     SegMeta sm;
     int mtile, ntile;
-    if (!train_tile(p.seg, p.hs, p.nseg, p.T, p.Is, p.nIs, p.nI, xcd_tile(), sm, mtile, ntile)) return;
+    if (!train_tile(p.seg, p.hs, p.nseg, p.T, p.Is, p.nIs, p.nI, xcd_tile(dgrad_group(p.nI)), sm, mtile, ntile))
+        return;
     const bool shared = sm.e < 0;
     const int C = shared ? p.Is : p.I;  // channels (row length of g, u, dG, dU)
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
@@ -502,7 +512,8 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void act_dx_kernel(ActDxPa
     __shared__ __attribute__((aligned(1024))) unsigned char smem[NSTAGE * STAGE];
     SegMeta sm;
     int mtile, ntile;
-    if (!train_tile(p.seg, p.hs, p.nseg, p.T, p.Is, p.nD, p.nD, xcd_tile(), sm, mtile, ntile)) return;
+    if (!train_tile(p.seg, p.hs, p.nseg, p.T, p.Is, p.nD, p.nD, xcd_tile(dgrad_group(p.nD)), sm, mtile, ntile))
+        return;
     const bool shared = sm.e < 0;
     const int C = shared ? p.Is : p.I;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
@@ -558,21 +569,21 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void act_dx_kernel(ActDxPa
 
 hipError_t launch_act_dgrad(const ActDgradParams& p, long long tiles, hipStream_t s) {
     if (tiles <= 0) return hipSuccess;
-    const long long g = (tiles + 8 * XCD_GROUP - 1) / (8 * XCD_GROUP) * (8 * XCD_GROUP);
+    const long long g = xcd_grid(tiles, dgrad_group(p.nI));
     act_dgrad_kernel<<<(int)g, THREADS, 0, s>>>(p);
     return hipGetLastError();
 }
 
 hipError_t launch_act_dx(const ActDxParams& p, long long tiles, hipStream_t s) {
     if (tiles <= 0) return hipSuccess;
-    const long long g = (tiles + 8 * XCD_GROUP - 1) / (8 * XCD_GROUP) * (8 * XCD_GROUP);
+    const long long g = xcd_grid(tiles, dgrad_group(p.nD));
     act_dx_kernel<<<(int)g, THREADS, 0, s>>>(p);
     return hipGetLastError();
 }
 
 hipError_t launch_sal_dgrad(const SalDgradParams& p, long long tiles, hipStream_t s) {
     if (tiles <= 0) return hipSuccess;
-    const long long g = (tiles + 8 * XCD_GROUP - 1) / (8 * XCD_GROUP) * (8 * XCD_GROUP);
+    const long long g = xcd_grid(tiles, dgrad_group(p.nI));
     sal_dgrad_kernel<<<(int)g, THREADS, 0, s>>>(p);
     return hipGetLastError();
 }
@@ -580,7 +591,7 @@ hipError_t launch_sal_dgrad(const SalDgradParams& p, long long tiles, hipStream_
 hipError_t launch_sal_wgrad(const SalWgradParams& p, hipStream_t s) {
     const long long tiles = 3LL * p.E * p.nI * p.nM;
     if (tiles <= 0) return hipSuccess;
-    const long long g = (tiles + 8 * XCD_GROUP - 1) / (8 * XCD_GROUP) * (8 * XCD_GROUP);
+    const long long g = xcd_grid(tiles, p.nI * p.nM);
     sal_wgrad_kernel<<<(int)g, THREADS, 0, s>>>(p);
     return hipGetLastError();
 }

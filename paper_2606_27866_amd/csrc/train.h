@@ -75,9 +75,11 @@ hipError_t launch_dmask_reduce(const float* dmp, const SegMeta* seg, int hs, int
                                hipStream_t s);
 hipError_t launch_sample_actions(const ActionWidths& aw, const float* alpha, const float* gumbel, int E,
                                  int32_t* keep, int32_t* action, hipStream_t s);
+// per_expert: [E][2] scratch for the cost and entropy of each expert
 hipError_t launch_action_grad(const ActionWidths& aw, const float* alpha, const float* gumbel, float tau,
                               const float* dmask, const int32_t* counts, long long assignments, int E, int I,
-                              float lambda_cost, float beta, float* dalpha, float* stats, hipStream_t s);
+                              float lambda_cost, float beta, float* dalpha, float* per_expert, float* stats,
+                              hipStream_t s);
 hipError_t launch_transpose_batched(const bf16_t* src, bf16_t* dst, int batch, int rows, int cols,
                                     hipStream_t s);
 

@@ -194,85 +194,86 @@ __global__ __launch_bounds__(256) void dmask_reduce_kernel(const float* __restri
     dmask[(size_t)e * I + c] = s;
 }
 
-// One wave per expert (16 waves, experts strided): Eqs. 6-8.
+// One wave per expert: Eqs. 6-8.
 //   dz_k = sum_{c < width_k} dmask[e][c]
 //   z = softmax((alpha + g) / tau), dalpha_quality = z (dz - <z, dz>) / tau
 //   p = softmax(alpha), rbar = <p, r>, H_e = -<p, log p>, q = counts / (T k)
 //   dalpha = dalpha_quality + lambda q p (r - rbar) + beta p (log p + H_e) / E
-// stats = (C = sum_e q rbar, H = mean_e H_e), summed in expert order.
-constexpr int kGradWaves = 16;
-__global__ __launch_bounds__(64 * kGradWaves) void action_grad_kernel(
-    ActionWidths aw, const float* __restrict__ alpha, const float* __restrict__ gumbel, float tau,
-    const float* __restrict__ dmask, const int32_t* __restrict__ counts, float inv_assign, int E, int I,
-    float lambda_cost, float beta, float* __restrict__ dalpha, float* __restrict__ stats) {
-    __shared__ float ce[kMaxExperts], he[kMaxExperts];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+// per_expert[e] = (q rbar, H_e), summed by action_stats_kernel.
+__global__ __launch_bounds__(64) void action_grad_kernel(ActionWidths aw, const float* __restrict__ alpha,
+                                                         const float* __restrict__ gumbel, float tau,
+                                                         const float* __restrict__ dmask,
+                                                         const int32_t* __restrict__ counts, float inv_assign,
+                                                         int E, int I, float lambda_cost, float beta,
+                                                         float* __restrict__ dalpha, float* __restrict__ per_expert) {
+    const int e = blockIdx.x, lane = threadIdx.x;
     const int K = aw.K;
     int wmax = 0;
     for (int k = 0; k < K; ++k) wmax = max(wmax, aw.width[k]);
-    for (int e = wave; e < E; e += kGradWaves) {
-        float dz[kMaxActions];
+    float dz[kMaxActions];
 #pragma unroll
-        for (int k = 0; k < kMaxActions; ++k) dz[k] = 0.f;
-        for (int c = lane; c < wmax; c += 64) {
-            const float v = dmask[(size_t)e * I + c];
-#pragma unroll
-            for (int k = 0; k < kMaxActions; ++k)
-                if (k < K && c < aw.width[k]) dz[k] += v;
-        }
+    for (int k = 0; k < kMaxActions; ++k) dz[k] = 0.f;
+#pragma unroll 8
+    for (int c = lane; c < wmax; c += 64) {
+        const float v = dmask[(size_t)e * I + c];
 #pragma unroll
         for (int k = 0; k < kMaxActions; ++k)
-            if (k < K) dz[k] = wave_sum_f(dz[k]);
-        const float* a = alpha + (size_t)e * K;
-        const float* g = gumbel + (size_t)e * K;
-        float sm = -INFINITY, am = -INFINITY;
-        for (int k = 0; k < K; ++k) {
-            sm = fmaxf(sm, (a[k] + g[k]) / tau);
-            am = fmaxf(am, a[k]);
-        }
-        float zsum = 0.f, psum = 0.f;
-        for (int k = 0; k < K; ++k) {
-            zsum += expf((a[k] + g[k]) / tau - sm);
-            psum += expf(a[k] - am);
-        }
-        float zdz = 0.f, rbar = 0.f, H = 0.f;
+            if (k < K && c < aw.width[k]) dz[k] += v;
+    }
 #pragma unroll
-        for (int k = 0; k < kMaxActions; ++k) {
-            if (k >= K) break;
+    for (int k = 0; k < kMaxActions; ++k)
+        if (k < K) dz[k] = wave_sum_f(dz[k]);
+    const float* a = alpha + (size_t)e * K;
+    const float* g = gumbel + (size_t)e * K;
+    float sm = -INFINITY, am = -INFINITY;
+    for (int k = 0; k < K; ++k) {
+        sm = fmaxf(sm, (a[k] + g[k]) / tau);
+        am = fmaxf(am, a[k]);
+    }
+    float zsum = 0.f, psum = 0.f;
+    for (int k = 0; k < K; ++k) {
+        zsum += expf((a[k] + g[k]) / tau - sm);
+        psum += expf(a[k] - am);
+    }
+    float zdz = 0.f, rbar = 0.f, H = 0.f;
+#pragma unroll
+    for (int k = 0; k < kMaxActions; ++k) {
+        if (k >= K) break;
+        const float z = expf((a[k] + g[k]) / tau - sm) / zsum;
+        const float p = expf(a[k] - am) / psum;
+        zdz += z * dz[k];
+        rbar += p * aw.ratio[k];
+        H -= p > 0.f ? p * logf(p) : 0.f;
+    }
+    const float q = (float)counts[e] * inv_assign;
+#pragma unroll
+    for (int k = 0; k < kMaxActions; ++k) {
+        if (k >= K) break;
+        if (lane == k) {
             const float z = expf((a[k] + g[k]) / tau - sm) / zsum;
             const float p = expf(a[k] - am) / psum;
-            zdz += z * dz[k];
-            rbar += p * aw.ratio[k];
-            H -= p > 0.f ? p * logf(p) : 0.f;
-        }
-        const float q = (float)counts[e] * inv_assign;
-#pragma unroll
-        for (int k = 0; k < kMaxActions; ++k) {
-            if (k >= K) break;
-            if (lane == k) {
-                const float z = expf((a[k] + g[k]) / tau - sm) / zsum;
-                const float p = expf(a[k] - am) / psum;
-                const float gq = z * (dz[k] - zdz) / tau;
-                const float gc = q * p * (aw.ratio[k] - rbar);
-                const float ge = p > 0.f ? p * (logf(p) + H) / (float)E : 0.f;
-                dalpha[(size_t)e * K + k] = gq + lambda_cost * gc + beta * ge;
-            }
-        }
-        if (lane == 0) {
-            ce[e] = q * rbar;
-            he[e] = H;
+            const float gq = z * (dz[k] - zdz) / tau;
+            const float gc = q * p * (aw.ratio[k] - rbar);
+            const float ge = p > 0.f ? p * (logf(p) + H) / (float)E : 0.f;
+            dalpha[(size_t)e * K + k] = gq + lambda_cost * gc + beta * ge;
         }
     }
-    __syncthreads();
-    if (threadIdx.x == 0 && stats) {
-        float C = 0.f, H = 0.f;
-        for (int e = 0; e < E; ++e) {
-            C += ce[e];
-            H += he[e];
-        }
-        stats[0] = C;
-        stats[1] = H / (float)E;
+    if (lane == 0) {
+        per_expert[2 * e] = q * rbar;
+        per_expert[2 * e + 1] = H;
     }
+}
+
+// stats = (C = sum_e q rbar, H = mean_e H_e), summed in expert order.
+__global__ void action_stats_kernel(const float* __restrict__ per_expert, int E, float* __restrict__ stats) {
+    if (threadIdx.x != 0) return;
+    float C = 0.f, H = 0.f;
+    for (int e = 0; e < E; ++e) {
+        C += per_expert[2 * e];
+        H += per_expert[2 * e + 1];
+    }
+    stats[0] = C;
+    stats[1] = H / (float)E;
 }
 
 hipError_t launch_sample_actions(const ActionWidths& aw, const float* alpha, const float* gumbel, int E,
@@ -314,10 +315,13 @@ hipError_t launch_dmask_reduce(const float* dmp, const SegMeta* seg, int hs, int
 
 hipError_t launch_action_grad(const ActionWidths& aw, const float* alpha, const float* gumbel, float tau,
                               const float* dmask, const int32_t* counts, long long assignments, int E, int I,
-                              float lambda_cost, float beta, float* dalpha, float* stats, hipStream_t s) {
-    action_grad_kernel<<<1, 64 * kGradWaves, 0, s>>>(aw, alpha, gumbel, tau, dmask, counts,
-                                                     1.0f / (float)assignments, E, I, lambda_cost, beta,
-                                                     dalpha, stats);
+                              float lambda_cost, float beta, float* dalpha, float* per_expert, float* stats,
+                              hipStream_t s) {
+    action_grad_kernel<<<E, 64, 0, s>>>(aw, alpha, gumbel, tau, dmask, counts, 1.0f / (float)assignments, E, I,
+                                        lambda_cost, beta, dalpha, per_expert);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess || !stats) return err;
+    action_stats_kernel<<<1, 64, 0, s>>>(per_expert, E, stats);
     return hipGetLastError();
 }
 
