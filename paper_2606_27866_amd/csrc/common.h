@@ -116,6 +116,18 @@ __device__ __forceinline__ int find_segment(const int32_t* tstart, int nseg, int
     return lo;
 }
 
+// Fragment-blocked layout of a [rows][C] bf16 matrix (C a multiple of 8):
+// 32-row x 8-column blocks of 512 bytes, block (r/32, c/8) at element
+// ((r/32) * (C/8) + c/8) * 256, and inside it element
+// (((c/4) % 2) * 32 + r % 32) * 4 + c % 4 -- the order in which a wave's 64
+// lanes hold runs of 4 consecutive columns of 32 rows (lane -> row lane % 32,
+// columns 4 * (lane / 32) ..), so that the wave's 8-byte accesses cover 512
+// contiguous bytes.  R rows take ceil(R/32) * 32 * C elements.
+__host__ __device__ __forceinline__ size_t frag_blocked(size_t r, int c, int C) {
+    return (((r >> 5) * (size_t)(C >> 3) + (size_t)(c >> 3)) << 8) + (size_t)((((c >> 2) & 1) << 5) + (r & 31)) * 4 +
+           (c & 3);
+}
+
 // Zero the bf16 elements at positions >= nvalid of an 8-element vector.
 __device__ __forceinline__ u32x4 mask_tail_bf16(u32x4 v, int nvalid) {
 #pragma unroll

@@ -981,10 +981,11 @@ TrainLayout train_layout(const flexmoe_layer_desc& D, int T) {
         off += align256(bytes);
         return o;
     };
-    S.G = take(A * I * 2);
-    S.U = take(A * I * 2);
-    S.Gs = take(Tz * Is * 2);
-    S.Us = take(Tz * Is * 2);
+    const size_t A32 = (A + 31) & ~size_t(31), T32 = (Tz + 31) & ~size_t(31);  // fragment-blocked rows
+    S.G = take(A32 * I * 2);
+    S.U = take(A32 * I * 2);
+    S.Gs = take(T32 * Is * 2);
+    S.Us = take(T32 * Is * 2);
     S.dO = take(A * d * 2);
     S.dYs = take(Tz * d * 2);
     S.dG = take(A * I * 2);

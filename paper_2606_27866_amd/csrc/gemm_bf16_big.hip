@@ -337,9 +337,11 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
                 }
             }
             if constexpr (kTrain == 2) {
-                // g and u for the training backward, in H's layout
-                bf16_t* Gb = shared ? p1.Gs : p1.G + (size_t)sm.row0 * p1.I;
-                bf16_t* Ub = shared ? p1.Us : p1.U + (size_t)sm.row0 * p1.I;
+                // g and u for the training backward, in the fragment-blocked
+                // layout (common.h) over the routed row space (or the tokens)
+                bf16_t* Gb = shared ? p1.Gs : p1.G;
+                bf16_t* Ub = shared ? p1.Us : p1.U;
+                const size_t rbase = shared ? 0 : (size_t)sm.row0;
 #pragma unroll
                 for (int i = 0; i < MFW; ++i) {
                     const int row = row_l + i * 32;
@@ -359,8 +361,9 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
                                 uw[h] = (uint32_t)f32_to_bf16(acc[i][jj + NF / 2][v]) |
                                         ((uint32_t)f32_to_bf16(acc[i][jj + NF / 2][v + 1]) << 16);
                             }
-                            *reinterpret_cast<uint2*>(Gb + (size_t)row * ldh + ch) = make_uint2(gw[0], gw[1]);
-                            *reinterpret_cast<uint2*>(Ub + (size_t)row * ldh + ch) = make_uint2(uw[0], uw[1]);
+                            const size_t off = frag_blocked(rbase + row, ch, ldh);
+                            *reinterpret_cast<uint2*>(Gb + off) = make_uint2(gw[0], gw[1]);
+                            *reinterpret_cast<uint2*>(Ub + off) = make_uint2(uw[0], uw[1]);
                         }
                 }
             }

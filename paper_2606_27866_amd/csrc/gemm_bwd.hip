@@ -405,10 +405,17 @@ __device__ __forceinline__ bool train_tile(const SegMeta* seg, int hs, int nseg,
 }  // namespace
 
 // dgrad + SwiGLU backward + mask gradient; tile = 256 rows x 256 channels.
-// The B fragment goes first: lane -> row, registers -> runs of 4 channels,
-// matching the row-major g, u, dG and dU (8-byte accesses).
+// The B fragment goes first: lane -> row, registers -> runs of 4 channels.
+// g and u are read in their fragment-blocked layout (a wave's 8-byte reads
+// cover 512 contiguous bytes); dG and dU are staged through LDS, half of the
+// tile's channels at a time, and stored as whole 16-byte row pieces.
+constexpr int DG_PITCH = BN / 2 + 8;                  // staged row (bf16): 272 bytes, 16-byte aligned
+constexpr int DG_STAGE = BM * DG_PITCH * 2;           // one staged array
+constexpr int DG_SMEM = (2 * DG_STAGE > NSTAGE * STAGE) ? 2 * DG_STAGE : NSTAGE * STAGE;
+static_assert(DG_SMEM <= 160 * 1024, "the dgrad LDS fits one compute unit");
+
 __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void act_dgrad_kernel(ActDgradParams p) {
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[NSTAGE * STAGE];
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[DG_SMEM];
     SegMeta sm;
     int mtile, ntile;
     if (!train_tile(p.seg, p.hs, p.nseg, p.T, p.Is, p.nIs, p.nI, xcd_tile(dgrad_group(p.nI)), sm, mtile, ntile))
@@ -435,50 +442,66 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void act_dgrad_kernel(ActD
     bf16_t* dU = shared ? p.dUs : p.dU;
     const int kk = sm.kk;                        // mask: channels below kk are kept
     const int kk8 = min(packed_width(kk), C);    // dG/dU columns the dx GEMM reads
+    bf16_t* stg = reinterpret_cast<bf16_t*>(smem);
+    bf16_t* stu = stg + BM * DG_PITCH;
     by_rows(sm.rows - mtile * BM, [&](auto tag) {
         constexpr int MFW = decltype(tag)::value;
         floatx16 acc[MFW][NF];
         nt_mainloop<MFW, false>(smem, op, wave, lane, acc, ZeroTail{op.ra});
+        // the stages are free once every wave is past its last fragment read
+        __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+        barrier_no_fence();
         // epilogue: lane -> row (lane%32 of a fragment), register v ->
         // channel 8(v/4) + 4(lane/32) + v%4 of a 32-channel fragment
         float msum[NF][16];
 #pragma unroll
-        for (int j = 0; j < NF; ++j)
+        for (int j = 0; j < NF; ++j) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) msum[j][v] = 0.f;
 #pragma unroll
-        for (int i = 0; i < MFW; ++i) {
-            const int row = mtile * BM + wm * 32 * MFW + i * 32 + (lane & 31);
-            if (row >= sm.rows) continue;
-            const size_t ro = (rbase + row) * (size_t)C;
-#pragma unroll
-            for (int j = 0; j < NF; ++j)
+            for (int i = 0; i < MFW; ++i) {
+                const int row = wm * 32 * MFW + i * 32 + (lane & 31);  // row of the tile
+                const int grow = mtile * BM + row;                     // row of the segment
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
+                    const int cl = wn * 32 + q * 8 + (lane >> 5) * 4;  // staged column of this half
                     const int c0 = ntile * BN + wn * WCOL + j * 32 + q * 8 + (lane >> 5) * 4;
-                    if (c0 >= C) continue;
-                    const uint2 gv = *reinterpret_cast<const uint2*>(G + ro + c0);
-                    const uint2 uv = *reinterpret_cast<const uint2*>(U + ro + c0);
-                    const float g[4] = {lo_bf16(gv.x), hi_bf16(gv.x), lo_bf16(gv.y), hi_bf16(gv.y)};
-                    const float u[4] = {lo_bf16(uv.x), hi_bf16(uv.x), lo_bf16(uv.y), hi_bf16(uv.y)};
                     uint32_t dg[2] = {0u, 0u}, du[2] = {0u, 0u};
+                    if (grow < sm.rows && c0 < C) {
+                        const size_t off = frag_blocked(rbase + grow, c0, C);
+                        const uint2 gv = *reinterpret_cast<const uint2*>(G + off);
+                        const uint2 uv = *reinterpret_cast<const uint2*>(U + off);
+                        const float g[4] = {lo_bf16(gv.x), hi_bf16(gv.x), lo_bf16(gv.y), hi_bf16(gv.y)};
+                        const float u[4] = {lo_bf16(uv.x), hi_bf16(uv.x), lo_bf16(uv.y), hi_bf16(uv.y)};
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const float x = g[r];
-                        const float sg = 1.0f / (1.0f + __builtin_amdgcn_exp2f(-x * 1.4426950408889634f));
-                        const float dh = acc[i][j][q * 4 + r];
-                        msum[j][q * 4 + r] += dh * (x * sg) * u[r];
-                        const bool kept = c0 + r < kk;
-                        const float vg = kept ? dh * u[r] * (sg * (1.0f + x * (1.0f - sg))) : 0.f;
-                        const float vu = kept ? dh * (x * sg) : 0.f;
-                        dg[r >> 1] |= (uint32_t)f32_to_bf16(vg) << (16 * (r & 1));
-                        du[r >> 1] |= (uint32_t)f32_to_bf16(vu) << (16 * (r & 1));
+                        for (int r = 0; r < 4; ++r) {
+                            const float x = g[r];
+                            const float sg = 1.0f / (1.0f + __builtin_amdgcn_exp2f(-x * 1.4426950408889634f));
+                            const float dh = acc[i][j][q * 4 + r];
+                            msum[j][q * 4 + r] += dh * (x * sg) * u[r];
+                            const bool kept = c0 + r < kk;
+                            const float vg = kept ? dh * u[r] * (sg * (1.0f + x * (1.0f - sg))) : 0.f;
+                            const float vu = kept ? dh * (x * sg) : 0.f;
+                            dg[r >> 1] |= (uint32_t)f32_to_bf16(vg) << (16 * (r & 1));
+                            du[r >> 1] |= (uint32_t)f32_to_bf16(vu) << (16 * (r & 1));
+                        }
                     }
-                    if (c0 < kk8) {
-                        *reinterpret_cast<uint2*>(dG + ro + c0) = make_uint2(dg[0], dg[1]);
-                        *reinterpret_cast<uint2*>(dU + ro + c0) = make_uint2(du[0], du[1]);
-                    }
+                    *reinterpret_cast<uint2*>(stg + row * DG_PITCH + cl) = make_uint2(dg[0], dg[1]);
+                    *reinterpret_cast<uint2*>(stu + row * DG_PITCH + cl) = make_uint2(du[0], du[1]);
                 }
+            }
+            __syncthreads();
+            // staged column cl of half j is channel ntile*BN + (cl/32)*WCOL + j*32 + cl%32
+            for (int k = threadIdx.x; k < BM * (BN / 2 / 8); k += THREADS) {
+                const int row = k / (BN / 2 / 8), cl = (k % (BN / 2 / 8)) * 8;
+                const int grow = mtile * BM + row;
+                const int c = ntile * BN + (cl / 32) * WCOL + j * 32 + cl % 32;
+                if (grow >= sm.rows || c >= kk8) continue;
+                const size_t o = (rbase + grow) * (size_t)C + c;
+                *reinterpret_cast<u32x4*>(dG + o) = *reinterpret_cast<const u32x4*>(stg + row * DG_PITCH + cl);
+                *reinterpret_cast<u32x4*>(dU + o) = *reinterpret_cast<const u32x4*>(stu + row * DG_PITCH + cl);
+            }
+            __syncthreads();
         }
         if (shared) return;
         // mask-gradient partial sums: over the 32 rows of the lane group

@@ -48,8 +48,9 @@ struct Gemm1Params {
     T* ht;
     int ldt;
     // Training forward of the masked layer (launch_gemm1_big_train_rm): g and
-    // u of every row in the layout of H and Hs -- routed [A][I], shared
-    // [T][I_s] -- for every channel the GEMM computes (c < kg).
+    // u of every row for every channel the GEMM computes (c < kg), in the
+    // fragment-blocked layout (common.h) of a routed [A][I] and a shared
+    // [T][I_s] matrix.
     T* G;
     T* U;
     T* Gs;

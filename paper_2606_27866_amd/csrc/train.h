@@ -21,9 +21,9 @@ struct ActDgradParams {
     const bf16_t* dYs;      // [T][d] dY, the shared expert's output gradient
     const bf16_t* wdt;      // [E][I][d] routed W_down^T
     const bf16_t* wsdt;     // [I_s][d] shared W_down^T
-    const bf16_t* G;        // [A][I] forward pre-activations (training forward)
-    const bf16_t* U;
-    const bf16_t* Gs;       // [T][I_s]
+    const bf16_t* G;        // [A][I] forward pre-activations (training forward),
+    const bf16_t* U;        //   fragment-blocked (common.h)
+    const bf16_t* Gs;       // [T][I_s], fragment-blocked
     const bf16_t* Us;
     const SegMeta* seg;
     bf16_t* dG;             // [A][I]: channels below packed_width(k) written
