@@ -398,14 +398,34 @@ BucketPlan make_plan(const int32_t* keep, int E, int I, int k_align) {
     return b;
 }
 
+// What the training forwards keep besides the output (TrainKeep::mode):
+//   1: transposed g, u, h of the routed rows (channel saliency), and the
+//      combine writes dY = y - target in fp32 instead of y;
+//   2: g and u of every row, fragment-blocked (the masked layer's backward);
+//      the gate/up GEMM computes all I channels of every active expert, the
+//      down GEMM only the kept ones.
+// Both always run the prefill tile kernels and an unsplit shared down GEMM
+// (one shared row set), so the workspace regions after the forward's are
+// those of layout(D, T, T).
+struct TrainKeep {
+    int mode;
+    bf16_t *gt, *ut, *ht;
+    int ldt;
+    bf16_t *G, *U, *Gs, *Us;
+    const float* y_target;
+    float* dy;
+};
+
 int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const float* logits,
                  const void* w_gate_r, const void* w_up_r, const void* w_down_r, const int32_t* keep_dev,
                  int clipped, int packed_limit, const int32_t* bucket_keep, int k_align,
                  const void* ws_gate, const void* ws_up, const void* ws_down, void* y, void* workspace,
-                 size_t workspace_bytes, const flexmoe_route_out* dbg, void* stream) {
+                 size_t workspace_bytes, const flexmoe_route_out* dbg, void* stream,
+                 const TrainKeep* tr = nullptr) {
     int rc = check_desc(desc);
     if (rc) return rc;
     const flexmoe_layer_desc& D = *desc;
+    const int train = tr ? tr->mode : 0;
     const bool bucketed = bucket_keep != nullptr;
     if (bucketed) {
         if (k_align < 1) return fail(FLEXMOE_EINVAL, "k_align = %d must be positive", k_align);
@@ -416,7 +436,7 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
     if (T < 0) return fail(FLEXMOE_EINVAL, "T = %d is negative", T);
     if (T > D.max_tokens) return fail(FLEXMOE_ESHAPE, "T = %d exceeds max_tokens = %d", T, D.max_tokens);
     if (T == 0) return FLEXMOE_OK;
-    if (!x || !logits || !w_gate_r || !w_up_r || !w_down_r || (!keep_dev && !bucketed) || !y)
+    if (!x || !logits || !w_gate_r || !w_up_r || !w_down_r || (!keep_dev && !bucketed) || (!y && train != 1))
         return fail(FLEXMOE_EINVAL, "forward: an input/output pointer is NULL");
     for (const void* ptr : {x, w_gate_r, w_up_r, w_down_r, ws_gate, ws_up, ws_down, (const void*)y})
         if (((uintptr_t)ptr) & 15) return fail(FLEXMOE_EINVAL, "x, weights and y must be 16-byte aligned");
@@ -425,7 +445,7 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
     const bool has_shared = D.I_shared > 0;
     if (has_shared != (ws_gate && ws_up && ws_down) || (!has_shared && (ws_gate || ws_up || ws_down)))
         return fail(FLEXMOE_EINVAL, "shared weights must be given iff I_shared > 0");
-    const Layout L = layout(D, T, (size_t)T * shared_parts(D, T));
+    const Layout L = layout(D, T, (size_t)T * (train ? 1 : shared_parts(D, T)));
     if (!workspace || workspace_bytes < L.total)
         return fail(FLEXMOE_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace_bytes, L.total);
     if (((uintptr_t)workspace) & 255) return fail(FLEXMOE_EWORKSPACE, "workspace is not 256-byte aligned");
@@ -467,9 +487,22 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
     const bool bf16 = D.dtype == FLEXMOE_BF16;
     // kernel family: weight streaming for decode-sized T, large MFMA tiles
     // otherwise (bf16); LDS-tiled FMA for fp32
-    const bool decode = bf16 && T <= kDecodeMaxT;
-    const int ks2 = shared_ks2(D, T);
-    const int parts = shared_parts(D, T);
+    const bool decode = bf16 && T <= kDecodeMaxT && !train;
+    const int ks2 = train ? 0 : shared_ks2(D, T);
+    const int parts = train ? (has_shared ? 1 : 0) : shared_parts(D, T);
+    if (train == 2) {
+        // every active expert's gate/up GEMM over all I channels, experts in id order
+        KeepArgs order, full;
+        for (int e = 0; e < kMaxExperts; ++e) {
+            order.v[e] = e < D.E ? e : 0;
+            full.v[e] = e < D.E ? D.I : 0;
+        }
+        plan = (int32_t*)(ws + L.plan);
+        set_keep_kernel<<<1, kMaxExperts, 0, (hipStream_t)stream>>>(plan, order, D.E);
+        set_keep_kernel<<<1, kMaxExperts, 0, (hipStream_t)stream>>>(plan + D.E, full, D.E);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return hip_fail(e, "plan upload");
+    }
     const TileShape ts = !bf16   ? TileShape{kF32BM, kF32BN, kF32BM, kF32BN, 0}
                          : decode ? TileShape{kDecodeMaxT, kDecBN, kDecodeMaxT, kDecBN, ks2}
                                   : TileShape{kBigBM1, kBigBN1, kBigBM2, kBigBN2, ks2};
@@ -497,11 +530,27 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
                                    (const bf16_t*)ws_gate, (const bf16_t*)ws_up, perm, seg, t1,
                                    (bf16_t*)(ws + L.H), (bf16_t*)(ws + L.Hs), D.d, D.I, D.I_shared, D.E,
                                    D.top_k, nseg, T, part, seg_lo, seg_hi, (int)g1s, clipped};
+            if (tr) {
+                p1.gt = tr->gt;
+                p1.ut = tr->ut;
+                p1.ht = tr->ht;
+                p1.ldt = tr->ldt;
+                p1.G = tr->G;
+                p1.U = tr->U;
+                p1.Gs = tr->Gs;
+                p1.Us = tr->Us;
+            }
             {
                 KernelTimer kt(k1, st);
-                e = decode ? launch_gemm1_decode(p1, (int)n1, st) : launch_gemm1_big(p1, (int)n1, st);
+                e = decode       ? launch_gemm1_decode(p1, (int)n1, st)
+                    : train == 1 ? launch_gemm1_big_train(p1, (int)n1, st)
+                    : train == 2 ? launch_gemm1_big_train_rm(p1, (int)n1, st)
+                                 : launch_gemm1_big(p1, (int)n1, st);
             }
             if (e != hipSuccess) return hip_fail(e, "gate/up GEMM launch");
+            // the masked layer's down GEMM reduces over the kept channels only
+            if (train == 2 && !sh && (e = launch_seg_use_kept(seg, nseg, st)) != hipSuccess)
+                return hip_fail(e, "segment width launch");
             Gemm2Params<bf16_t> p2{(const bf16_t*)(ws + L.H), (const bf16_t*)(ws + L.Hs),
                                    (const bf16_t*)w_down_r, (const bf16_t*)ws_down, seg, t2, (bf16_t*)O,
                                    (bf16_t*)Os, D.d, D.I, D.I_shared, D.E, nseg, T, ks2, part, seg_lo,
@@ -542,7 +591,10 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
     // shared experts whose gate/up GEMM alone fills fewer than kSideWaves
     // waves of tiles.  Past that, one launch over all segments keeps each
     // XCD's L2 serving one GEMM at a time.
-    const bool use_side = has_shared && (decode || g1s < (long long)kSideWaves * kComputeUnits);
+    // The training forwards compute every routed channel (the routed GEMMs
+    // alone fill the chip): one launch over all segments there (measured 2 %
+    // faster than the split on the Qwen1.5 shape).
+    const bool use_side = has_shared && !train && (decode || g1s < (long long)kSideWaves * kComputeUnits);
     SideStream* side = nullptr;
     std::unique_lock<std::mutex> side_lock;
     if (use_side) {
@@ -629,7 +681,9 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
     }
     {
         KernelTimer kt(FLEXMOE_K_COMBINE, s);
-        err = launch_combine(O, Os, pos, wts, T, D.top_k, D.d, parts, D.dtype, y, s);
+        err = train == 1 ? launch_combine_residual((const bf16_t*)O, (const bf16_t*)Os, pos, wts, T, D.top_k, D.d,
+                                                   parts, tr->y_target, tr->dy, s)
+                         : launch_combine(O, Os, pos, wts, T, D.top_k, D.d, parts, D.dtype, y, s);
     }
     if (err != hipSuccess) return hip_fail(err, "combine launch");
 
@@ -807,22 +861,10 @@ int saliency_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, cons
     hipStream_t s = (hipStream_t)stream;
     char* ws = (char*)workspace;
     const Layout& L = S.f;
-    int32_t* idx = (int32_t*)(ws + L.idx);
     float* wts = (float*)(ws + L.wts);
-    int32_t* blockcnt = (int32_t*)(ws + L.blockcnt);
-    int32_t* blockbase = (int32_t*)(ws + L.blockbase);
-    int32_t* counts = (int32_t*)(ws + L.counts);
-    int32_t* offsets = (int32_t*)(ws + L.offsets);
     int32_t* perm = (int32_t*)(ws + L.perm);
-    int32_t* pos = (int32_t*)(ws + L.pos);
     SegMeta* seg = (SegMeta*)(ws + L.seg);
-    int32_t* t1 = (int32_t*)(ws + L.t1);
-    int32_t* t2 = (int32_t*)(ws + L.t2);
     int32_t* keep = (int32_t*)(ws + L.keep);
-    bf16_t* H = (bf16_t*)(ws + L.H);
-    bf16_t* Hs = (bf16_t*)(ws + L.Hs);
-    bf16_t* O = (bf16_t*)(ws + L.O);
-    bf16_t* Os = (bf16_t*)(ws + L.Os);
     float* dy = (float*)(ws + S.dy);
     bf16_t* dO = (bf16_t*)(ws + S.dO);
     bf16_t* xt = (bf16_t*)(ws + S.xt);
@@ -844,76 +886,22 @@ int saliency_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, cons
     }
     if (err != hipSuccess) return hip_fail(err, "down-weight transpose launch");
 
-    // 2. routing and dispatch of the unpruned layer (every k_e = I), with the
-    //    prefill tile shapes and the shared expert's down GEMM unsplit
+    // 2. the unpruned layer's forward (every k_e = I), keeping transposed g,
+    //    u, h of the routed rows, with dY = Y - target from its combine
     KeepArgs ka;
     for (int e = 0; e < kMaxExperts; ++e) ka.v[e] = e < D.E ? D.I : 0;
     set_keep_kernel<<<1, kMaxExperts, 0, s>>>(keep, ka, D.E);
     if ((err = hipGetLastError()) != hipSuccess) return hip_fail(err, "keep upload");
-    const TileShape ts{kBigBM1, kBigBN1, kBigBM2, kBigBN2, 0};
     static_assert(kBigBM1 == kSalTile, "segment row tiles (rt0) are counted in saliency tile rows");
-    const int NB = num_chunks(T);
-    if ((long long)T * D.top_k <= kSmallAssign) {
-        KernelTimer kt(FLEXMOE_K_ROUTE, s);
-        dispatch_small_kernel<<<1, 64 * kSmallWaves, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, keep, D.I,
-                                                             D.I_shared, D.d, ts, 0x7fffffff, nullptr, 0, idx,
-                                                             wts, counts, perm, pos, offsets, seg, t1, t2);
-        if ((err = hipGetLastError()) != hipSuccess) return hip_fail(err, "dispatch launch");
-    } else {
-        {
-            KernelTimer kt(FLEXMOE_K_ROUTE, s);
-            route_kernel<<<NB, 64 * kRouteTokens, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, idx, wts,
-                                                          blockcnt, NB);
-            err = hipGetLastError();
-        }
-        if (err != hipSuccess) return hip_fail(err, "route launch");
-        {
-            KernelTimer kt(FLEXMOE_K_DISPATCH_SCAN, s);
-            dispatch_scan_kernel<<<D.E, 256, 0, s>>>(blockcnt, NB, blockbase, counts);
-            err = hipGetLastError();
-        }
-        if (err != hipSuccess) return hip_fail(err, "dispatch scan launch");
-        {
-            KernelTimer kt(FLEXMOE_K_DISPATCH_SCATTER, s);
-            dispatch_scatter_kernel<<<NB, 64, 0, s>>>(idx, keep, counts, blockbase, T, D.E, D.top_k, D.I,
-                                                      D.I_shared, D.d, NB, ts, 0x7fffffff, nullptr, perm, pos,
-                                                      offsets, seg, t1, t2);
-            err = hipGetLastError();
-        }
-        if (err != hipSuccess) return hip_fail(err, "dispatch scatter launch");
-    }
-
-    // 3. the forward, keeping transposed g, u, h of the routed rows
-    const long long g1 = routed_row_tiles_ub(T, D.E, D.top_k, ts.bm1) * ceil_div(D.I, ts.bn1) +
-                         (has_shared ? (long long)ceil_div(T, ts.bm1) * ceil_div(D.I_shared, ts.bn1) : 0);
-    const long long g2s = has_shared ? (long long)ceil_div(T, ts.bm2) * ceil_div(D.d, ts.bn2) : 0;
-    const long long g2 = routed_row_tiles_ub(T, D.E, D.top_k, ts.bm2) * ceil_div(D.d, ts.bn2) + g2s;
+    const TrainKeep tk{1, gt, ut, ht, S.ldt, nullptr, nullptr, nullptr, nullptr, y_target, dy};
+    rc = forward_impl(desc, T, x, logits, w_gate, w_up, w_down, keep, 0, 0x7fffffff, nullptr, 0, ws_gate, ws_up,
+                      ws_down, nullptr, workspace, workspace_bytes, nullptr, stream, &tk);
+    if (rc != FLEXMOE_OK) return rc;
     const long long gd = routed_row_tiles_ub(T, D.E, D.top_k, kSalTile) * S.nI;
-    if (g1 > 0x7fffffffLL || g2 > 0x7fffffffLL || gd > 0x7fffffffLL ||
-        3LL * D.E * S.nI * S.nM > 0x7fffffffLL)
+    if (gd > 0x7fffffffLL || 3LL * D.E * S.nI * S.nM > 0x7fffffffLL)
         return fail(FLEXMOE_ESHAPE, "tile grid too large");
-    {
-        Gemm1Params<bf16_t> p1{(const bf16_t*)x, (const bf16_t*)w_gate, (const bf16_t*)w_up,
-                               (const bf16_t*)ws_gate, (const bf16_t*)ws_up, perm, seg, t1, H, Hs, D.d, D.I,
-                               D.I_shared, D.E, D.top_k, nseg, T, kPartRange, 0, nseg, 0, 0, gt, ut, ht, S.ldt};
-        KernelTimer kt(FLEXMOE_K_GATE_UP, s);
-        err = launch_gemm1_big_train(p1, (int)g1, s);
-    }
-    if (err != hipSuccess) return hip_fail(err, "training gate/up GEMM launch");
-    {
-        Gemm2Params<bf16_t> p2{H, Hs, (const bf16_t*)w_down, (const bf16_t*)ws_down, seg, t2, O, Os, D.d, D.I,
-                               D.I_shared, D.E, nseg, T, 0, kPartRange, 0, nseg, (int)g2s, 0};
-        KernelTimer kt(FLEXMOE_K_DOWN, s);
-        err = launch_gemm2_big(p2, (int)g2, s);
-    }
-    if (err != hipSuccess) return hip_fail(err, "down GEMM launch");
-    {
-        KernelTimer kt(FLEXMOE_K_COMBINE, s);
-        err = launch_combine_residual(O, Os, pos, wts, T, D.top_k, D.d, has_shared ? 1 : 0, y_target, dy, s);
-    }
-    if (err != hipSuccess) return hip_fail(err, "residual launch");
 
-    // 4. backward: transposed x and dO, dgrad + SwiGLU backward, wgrad + Eq. 2
+    // 3. backward: transposed x and dO, dgrad + SwiGLU backward, wgrad + Eq. 2
     {
         SalPrepParams pp{(const bf16_t*)x, dy, perm, wts, seg, xt, dot, dO, D.d, D.top_k, hs, nseg, S.ldt};
         KernelTimer kt(FLEXMOE_K_SAL_PREP, s);
@@ -1154,80 +1142,10 @@ int flexmoe_train_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
     const TrainLayout S = train_layout(D, T);
     if ((rc = check_workspace(S, workspace, workspace_bytes)) != FLEXMOE_OK) return rc;
     TrainPtrs P = train_ptrs(S, workspace);
-    hipStream_t s = (hipStream_t)stream;
-    hipError_t err;
-    const int hs = has_shared ? 1 : 0, nseg = D.E + hs;
-
-    // segments in expert order, the gate/up GEMM over all I channels
-    KeepArgs order, full;
-    for (int e = 0; e < kMaxExperts; ++e) {
-        order.v[e] = e < D.E ? e : 0;
-        full.v[e] = e < D.E ? D.I : 0;
-    }
-    set_keep_kernel<<<1, kMaxExperts, 0, s>>>(P.plan, order, D.E);
-    set_keep_kernel<<<1, kMaxExperts, 0, s>>>(P.plan + D.E, full, D.E);
-    if ((err = hipGetLastError()) != hipSuccess) return hip_fail(err, "plan upload");
-    const TileShape ts{kBigBM1, kBigBN1, kBigBM2, kBigBN2, 0};
     static_assert(kBigBM1 == kTrainTile, "segment row tiles (rt0) are counted in training tile rows");
-    const int NB = num_chunks(T);
-    if ((long long)T * D.top_k <= kSmallAssign) {
-        KernelTimer kt(FLEXMOE_K_ROUTE, s);
-        dispatch_small_kernel<<<1, 64 * kSmallWaves, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, keep_dev, D.I,
-                                                             D.I_shared, D.d, ts, 0x7fffffff, P.plan, 0, P.idx,
-                                                             P.wts, P.counts, P.perm, P.pos, P.offsets, P.seg,
-                                                             P.t1, P.t2);
-        if ((err = hipGetLastError()) != hipSuccess) return hip_fail(err, "dispatch launch");
-    } else {
-        {
-            KernelTimer kt(FLEXMOE_K_ROUTE, s);
-            route_kernel<<<NB, 64 * kRouteTokens, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, P.idx, P.wts,
-                                                          P.blockcnt, NB);
-            err = hipGetLastError();
-        }
-        if (err != hipSuccess) return hip_fail(err, "route launch");
-        {
-            KernelTimer kt(FLEXMOE_K_DISPATCH_SCAN, s);
-            dispatch_scan_kernel<<<D.E, 256, 0, s>>>(P.blockcnt, NB, P.blockbase, P.counts);
-            err = hipGetLastError();
-        }
-        if (err != hipSuccess) return hip_fail(err, "dispatch scan launch");
-        {
-            KernelTimer kt(FLEXMOE_K_DISPATCH_SCATTER, s);
-            dispatch_scatter_kernel<<<NB, 64, 0, s>>>(P.idx, keep_dev, P.counts, P.blockbase, T, D.E, D.top_k,
-                                                      D.I, D.I_shared, D.d, NB, ts, 0x7fffffff, P.plan, P.perm,
-                                                      P.pos, P.offsets, P.seg, P.t1, P.t2);
-            err = hipGetLastError();
-        }
-        if (err != hipSuccess) return hip_fail(err, "dispatch scatter launch");
-    }
-    const long long g1 = routed_row_tiles_ub(T, D.E, D.top_k, ts.bm1) * ceil_div(D.I, ts.bn1) +
-                         (has_shared ? (long long)ceil_div(T, ts.bm1) * ceil_div(D.I_shared, ts.bn1) : 0);
-    const long long g2s = has_shared ? (long long)ceil_div(T, ts.bm2) * ceil_div(D.d, ts.bn2) : 0;
-    const long long g2 = routed_row_tiles_ub(T, D.E, D.top_k, ts.bm2) * ceil_div(D.d, ts.bn2) + g2s;
-    if (g1 > 0x7fffffffLL || g2 > 0x7fffffffLL) return fail(FLEXMOE_ESHAPE, "tile grid too large");
-    {
-        Gemm1Params<bf16_t> p1{(const bf16_t*)x, (const bf16_t*)w_gate, (const bf16_t*)w_up, (const bf16_t*)ws_gate,
-                               (const bf16_t*)ws_up, P.perm, P.seg, P.t1, P.H, P.Hs, D.d, D.I, D.I_shared, D.E,
-                               D.top_k, nseg, T, kPartRange, 0, nseg, 0, 0, nullptr, nullptr, nullptr, 0,
-                               P.G, P.U, P.Gs, P.Us};
-        KernelTimer kt(FLEXMOE_K_GATE_UP, s);
-        err = launch_gemm1_big_train_rm(p1, (int)g1, s);
-    }
-    if (err != hipSuccess) return hip_fail(err, "training gate/up GEMM launch");
-    if ((err = launch_seg_use_kept(P.seg, nseg, s)) != hipSuccess) return hip_fail(err, "segment width launch");
-    {
-        Gemm2Params<bf16_t> p2{P.H, P.Hs, (const bf16_t*)w_down, (const bf16_t*)ws_down, P.seg, P.t2, P.O, P.Os,
-                               D.d, D.I, D.I_shared, D.E, nseg, T, 0, kPartRange, 0, nseg, (int)g2s, 0};
-        KernelTimer kt(FLEXMOE_K_DOWN, s);
-        err = launch_gemm2_big(p2, (int)g2, s);
-    }
-    if (err != hipSuccess) return hip_fail(err, "down GEMM launch");
-    {
-        KernelTimer kt(FLEXMOE_K_COMBINE, s);
-        err = launch_combine(P.O, P.Os, P.pos, P.wts, T, D.top_k, D.d, has_shared ? 1 : 0, D.dtype, y, s);
-    }
-    if (err != hipSuccess) return hip_fail(err, "combine launch");
-    return FLEXMOE_OK;
+    const TrainKeep tk{2, nullptr, nullptr, nullptr, 0, P.G, P.U, P.Gs, P.Us, nullptr, nullptr};
+    return forward_impl(desc, T, x, logits, w_gate, w_up, w_down, keep_dev, 0, 0x7fffffff, nullptr, 0, ws_gate,
+                        ws_up, ws_down, y, workspace, workspace_bytes, nullptr, stream, &tk);
 }
 
 int flexmoe_train_backward(const flexmoe_layer_desc* desc, int32_t T, const float* logits, const float* dy,
