@@ -334,7 +334,8 @@ def saliency_section(wl, args):
                tflops=f_all / (ms_b / 1e3) / 1e12, frac_mfma=f_all / (ms_b / 1e3) / 1e12 / PEAK_BF16_TFLOPS,
                flops_per_batch=f_all, rank_reorder_ms=rank_ms, roofline_wgrad=roof,
                dgrad_tflops=f_dgrad / (dg_avg / 1e3) / 1e12, kernels_ms=kms,
-               loss="1/2 sum_t ||Y_t - target_t||^2 with a seeded Gaussian target (std 0.05)")
+               loss="1/2 sum_t ||Y_t - target_t||^2 with a seeded Gaussian target (std 0.05)",
+               w_down_t="made once for the ranking set (flexmoe_transpose_weights), not per batch")
     log("[bench] saliency: %d tokens/batch, %.4f ms/batch, %.0f tokens/s, %.1f TFLOP/s overall; wgrad %.4f ms "
         "(%.1f TFLOP/s), dgrad %.4f ms (%.1f TFLOP/s); rank+reorder %.3f ms"
         % (T, ms_b, T / (ms_b / 1e3), out["tflops"], wg_avg, roof["achieved"], dg_avg, out["dgrad_tflops"],

@@ -145,17 +145,20 @@ int flexmoe_rank_reorder(const flexmoe_layer_desc *desc, const float *scores,
  * in every GEMM; g, u, h, dO = w*dY, dG and dU are rounded to bf16 as MFMA
  * operands; Y and dY stay fp32; the squares and their sums are fp32, summed in
  * a fixed order (repeated calls give identical bits).
+ * w_down_t: W_down^T [E][I][d] as written by flexmoe_transpose_weights, or
+ * NULL, in which case every call writes that copy into its workspace (a
+ * ranking set of several batches makes it once and passes it).
  * Workspace: flexmoe_saliency_workspace_bytes(desc, T), 256-byte aligned; it
- * holds a transposed copy of W_down (E*I*d bf16) besides per-token buffers.
+ * holds room for that copy (E*I*d bf16) besides per-token buffers.
  * Shapes: the bf16 rules of the forward, and
  * max(d, I) * (T*top_k + 7*E rounded up to 8) < 2^30 (FLEXMOE_ESHAPE). */
 size_t flexmoe_saliency_workspace_bytes(const flexmoe_layer_desc *desc, int32_t T);
 int flexmoe_channel_saliency(const flexmoe_layer_desc *desc, int32_t T, const void *x,
                              const float *logits, const void *w_gate, const void *w_up,
-                             const void *w_down, const void *ws_gate, const void *ws_up,
-                             const void *ws_down, const float *y_target, float scale,
-                             float *scores, void *workspace, size_t workspace_bytes,
-                             void *stream);
+                             const void *w_down, const void *w_down_t, const void *ws_gate,
+                             const void *ws_up, const void *ws_down, const float *y_target,
+                             float scale, float *scores, void *workspace,
+                             size_t workspace_bytes, void *stream);
 
 /* ---- Action learning on the device (Sec. 3.2, Eqs. 5-8) ------------------
  * One training step of the per-expert width actions of a layer:
@@ -189,8 +192,10 @@ typedef struct flexmoe_action_set {
 } flexmoe_action_set;
 
 /* Transposed weight copies: w_gate_t, w_up_t [E][d][I]; w_down_t [E][I][d];
- * ws_gate_t, ws_up_t [d][I_s]; ws_down_t [I_s][d] (shared ones NULL iff
- * I_s == 0).  Outputs must not overlap inputs. */
+ * ws_gate_t, ws_up_t [d][I_s]; ws_down_t [I_s][d].  Each (input, output) pair
+ * is given or NULL together (the training backward needs all of them; the
+ * saliency only the down one); shared pairs only if I_s > 0.  Outputs must not
+ * overlap inputs. */
 int flexmoe_transpose_weights(const flexmoe_layer_desc *desc, const void *w_gate, const void *w_up,
                               const void *w_down, const void *ws_gate, const void *ws_up,
                               const void *ws_down, void *w_gate_t, void *w_up_t, void *w_down_t,

@@ -836,9 +836,9 @@ int check_saliency_shape(const flexmoe_layer_desc& D, int T) {
 }
 
 int saliency_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const float* logits,
-                  const void* w_gate, const void* w_up, const void* w_down, const void* ws_gate,
-                  const void* ws_up, const void* ws_down, const float* y_target, float scale, float* scores,
-                  void* workspace, size_t workspace_bytes, void* stream) {
+                  const void* w_gate, const void* w_up, const void* w_down, const void* w_down_t,
+                  const void* ws_gate, const void* ws_up, const void* ws_down, const float* y_target, float scale,
+                  float* scores, void* workspace, size_t workspace_bytes, void* stream) {
     int rc = check_desc(desc);
     if (rc) return rc;
     const flexmoe_layer_desc& D = *desc;
@@ -846,7 +846,7 @@ int saliency_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, cons
     if (T == 0) return FLEXMOE_OK;
     if (!x || !logits || !w_gate || !w_up || !w_down || !y_target || !scores)
         return fail(FLEXMOE_EINVAL, "saliency: an input/output pointer is NULL");
-    for (const void* ptr : {x, w_gate, w_up, w_down, ws_gate, ws_up, ws_down, (const void*)y_target})
+    for (const void* ptr : {x, w_gate, w_up, w_down, w_down_t, ws_gate, ws_up, ws_down, (const void*)y_target})
         if (((uintptr_t)ptr) & 15) return fail(FLEXMOE_EINVAL, "x, weights and y_target must be 16-byte aligned");
     if (((uintptr_t)logits) & 3 || ((uintptr_t)scores) & 3)
         return fail(FLEXMOE_EINVAL, "logits and scores must be 4-byte aligned");
@@ -874,17 +874,17 @@ int saliency_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, cons
     bf16_t* ht = (bf16_t*)(ws + S.ht);
     bf16_t* dgt = (bf16_t*)(ws + S.dgt);
     bf16_t* dut = (bf16_t*)(ws + S.dut);
-    bf16_t* wdt = (bf16_t*)(ws + S.wdt);
+    const bf16_t* wdt = w_down_t ? (const bf16_t*)w_down_t : (const bf16_t*)(ws + S.wdt);
     float* partial = (float*)(ws + S.partial);
     const int hs = has_shared ? 1 : 0, nseg = D.E + hs;
     hipError_t err;
 
-    // 1. the transposed down weights (no dependence on the batch's routing)
-    {
+    // 1. the transposed down weights, unless the caller made them
+    if (!w_down_t) {
         KernelTimer kt(FLEXMOE_K_SAL_TRANSPOSE, s);
-        err = launch_transpose_batched((const bf16_t*)w_down, wdt, D.E, D.d, D.I, s);
+        err = launch_transpose_batched((const bf16_t*)w_down, (bf16_t*)(ws + S.wdt), D.E, D.d, D.I, s);
+        if (err != hipSuccess) return hip_fail(err, "down-weight transpose launch");
     }
-    if (err != hipSuccess) return hip_fail(err, "down-weight transpose launch");
 
     // 2. the unpruned layer's forward (every k_e = I), keeping transposed g,
     //    u, h of the routed rows, with dY = Y - target from its combine
@@ -940,11 +940,11 @@ size_t flexmoe_saliency_workspace_bytes(const flexmoe_layer_desc* desc, int32_t 
 }
 
 int flexmoe_channel_saliency(const flexmoe_layer_desc* desc, int32_t T, const void* x, const float* logits,
-                             const void* w_gate, const void* w_up, const void* w_down, const void* ws_gate,
-                             const void* ws_up, const void* ws_down, const float* y_target, float scale,
-                             float* scores, void* workspace, size_t workspace_bytes, void* stream) {
-    return saliency_impl(desc, T, x, logits, w_gate, w_up, w_down, ws_gate, ws_up, ws_down, y_target, scale,
-                         scores, workspace, workspace_bytes, stream);
+                             const void* w_gate, const void* w_up, const void* w_down, const void* w_down_t,
+                             const void* ws_gate, const void* ws_up, const void* ws_down, const float* y_target,
+                             float scale, float* scores, void* workspace, size_t workspace_bytes, void* stream) {
+    return saliency_impl(desc, T, x, logits, w_gate, w_up, w_down, w_down_t, ws_gate, ws_up, ws_down, y_target,
+                         scale, scores, workspace, workspace_bytes, stream);
 }
 
 }  // extern "C"
@@ -1074,13 +1074,14 @@ int flexmoe_transpose_weights(const flexmoe_layer_desc* desc, const void* w_gate
     int rc = check_train(desc, 0);
     if (rc) return rc;
     const flexmoe_layer_desc& D = *desc;
-    if (!w_gate || !w_up || !w_down || !w_gate_t || !w_up_t || !w_down_t)
-        return fail(FLEXMOE_EINVAL, "transpose_weights: a routed weight pointer is NULL");
-    const bool has_shared = D.I_shared > 0;
-    const bool all_sh = ws_gate && ws_up && ws_down && ws_gate_t && ws_up_t && ws_down_t;
-    const bool any_sh = ws_gate || ws_up || ws_down || ws_gate_t || ws_up_t || ws_down_t;
-    if (has_shared ? !all_sh : any_sh)
-        return fail(FLEXMOE_EINVAL, "shared weights and their copies must be given iff I_shared > 0");
+    const void* pairs[6][2] = {{w_gate, w_gate_t}, {w_up, w_up_t},   {w_down, w_down_t},
+                               {ws_gate, ws_gate_t}, {ws_up, ws_up_t}, {ws_down, ws_down_t}};
+    for (int i = 0; i < 6; ++i) {
+        if ((pairs[i][0] == nullptr) != (pairs[i][1] == nullptr))
+            return fail(FLEXMOE_EINVAL, "transpose_weights: a weight and its copy must be given together");
+        if (i >= 3 && pairs[i][0] && D.I_shared == 0)
+            return fail(FLEXMOE_EINVAL, "transpose_weights: shared weights given but I_shared = 0");
+    }
     for (const void* ptr : {w_gate, w_up, w_down, ws_gate, ws_up, ws_down, (const void*)w_gate_t,
                             (const void*)w_up_t, (const void*)w_down_t, (const void*)ws_gate_t,
                             (const void*)ws_up_t, (const void*)ws_down_t})

@@ -114,7 +114,7 @@ def lib():
         L.flexmoe_layer_forward_bucketed.restype = ctypes.c_int
         L.flexmoe_saliency_workspace_bytes.argtypes = [D, i32]
         L.flexmoe_saliency_workspace_bytes.restype = sz
-        L.flexmoe_channel_saliency.argtypes = ([D, i32] + [vp] * 9 + [ctypes.c_float] + [vp] * 2
+        L.flexmoe_channel_saliency.argtypes = ([D, i32] + [vp] * 10 + [ctypes.c_float] + [vp] * 2
                                                + [sz, vp])
         L.flexmoe_channel_saliency.restype = ctypes.c_int
         AS = ctypes.POINTER(flexmoe_action_set)
@@ -276,13 +276,13 @@ def flexmoe_saliency_workspace_bytes(desc: flexmoe_layer_desc, T: int) -> int:
     return n
 
 
-def flexmoe_channel_saliency(desc, T, x, logits, w_gate, w_up, w_down, ws_gate, ws_up, ws_down,
+def flexmoe_channel_saliency(desc, T, x, logits, w_gate, w_up, w_down, w_down_t, ws_gate, ws_up, ws_down,
                              y_target, scale, scores, workspace, workspace_bytes=None, stream=None):
     nbytes = workspace.numel() * workspace.element_size() if workspace_bytes is None else workspace_bytes
     _check(lib().flexmoe_channel_saliency(ctypes.byref(desc), int(T), _p(x), _p(logits), _p(w_gate),
-                                          _p(w_up), _p(w_down), _p(ws_gate), _p(ws_up), _p(ws_down),
-                                          _p(y_target), float(scale), _p(scores), _p(workspace), nbytes,
-                                          _stream(stream)))
+                                          _p(w_up), _p(w_down), _p(w_down_t), _p(ws_gate), _p(ws_up),
+                                          _p(ws_down), _p(y_target), float(scale), _p(scores), _p(workspace),
+                                          nbytes, _stream(stream)))
 
 
 def _nbytes(t, given):
@@ -412,19 +412,24 @@ class Saliency:
     tokens per batch; the weights are those of `layer` (original order).
     """
 
-    def __init__(self, layer: "Layer", max_tokens: int):
+    def __init__(self, layer: "Layer", max_tokens: int, transpose_once: bool = True):
         import torch
         self.layer = layer
-        self.desc = make_desc(layer.desc.d, layer.desc.E, layer.desc.I, layer.desc.top_k,
-                              layer.desc.I_shared, layer.desc.dtype, layer.desc.norm_topk, max_tokens)
+        D = layer.desc
+        self.desc = make_desc(D.d, D.E, D.I, D.top_k, D.I_shared, D.dtype, D.norm_topk, max_tokens)
         nbytes = flexmoe_saliency_workspace_bytes(self.desc, max_tokens)
         self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=layer.device)
-        self.scores = torch.zeros((layer.desc.E, layer.desc.I), dtype=torch.float32, device=layer.device)
+        self.scores = torch.zeros((D.E, D.I), dtype=torch.float32, device=layer.device)
+        self.w_down_t = None
+        if transpose_once:   # W_down^T made once for the whole ranking set
+            self.w_down_t = torch.empty((D.E, D.I, D.d), dtype=layer.tdtype, device=layer.device)
+            flexmoe_transpose_weights(self.desc, None, None, layer.w_down, None, None, None,
+                                      None, None, self.w_down_t, None, None, None)
 
     def add_batch(self, x, logits, y_target, scale=1.0, stream=None):
         L = self.layer
-        flexmoe_channel_saliency(self.desc, x.shape[0], x, logits, L.w_gate, L.w_up, L.w_down, L.ws_gate,
-                                 L.ws_up, L.ws_down, y_target, scale, self.scores, self.workspace,
+        flexmoe_channel_saliency(self.desc, x.shape[0], x, logits, L.w_gate, L.w_up, L.w_down, self.w_down_t,
+                                 L.ws_gate, L.ws_up, L.ws_down, y_target, scale, self.scores, self.workspace,
                                  stream=stream)
 
     def rank_reorder(self, stream=None):

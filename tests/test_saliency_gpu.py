@@ -28,20 +28,20 @@ ABS_TOL = 1e-4   # times the expert's largest score
 def test_saliency_rejects_bad_arguments_on_host():
     f32 = fm.make_desc(64, 4, 64, 2, 0, fm.FLEXMOE_F32, 1, 16)
     with pytest.raises(fm.FlexMoEError) as ei:
-        fm.flexmoe_channel_saliency(f32, 4, *([0x1000] * 8), 0x1000, 1.0, 0x1000, 0x1000,
+        fm.flexmoe_channel_saliency(f32, 4, *([0x1000] * 9), 0x1000, 1.0, 0x1000, 0x1000,
                                     workspace_bytes=1 << 30, stream=0)
     assert ei.value.code == -5
     bf = fm.make_desc(64, 4, 64, 2, 0, fm.FLEXMOE_BF16, 1, 16)
     with pytest.raises(fm.FlexMoEError) as ei:  # T above max_tokens
-        fm.flexmoe_channel_saliency(bf, 17, *([0x1000] * 5), None, None, None, 0x1000, 1.0, 0x1000, 0x1000,
+        fm.flexmoe_channel_saliency(bf, 17, *([0x1000] * 5), None, None, None, None, 0x1000, 1.0, 0x1000, 0x1000,
                                     workspace_bytes=1 << 30, stream=0)
     assert ei.value.code == -2
     with pytest.raises(fm.FlexMoEError) as ei:  # workspace too small
-        fm.flexmoe_channel_saliency(bf, 16, *([0x1000] * 5), None, None, None, 0x1000, 1.0, 0x1000, 0x1000,
+        fm.flexmoe_channel_saliency(bf, 16, *([0x1000] * 5), None, None, None, None, 0x1000, 1.0, 0x1000, 0x1000,
                                     workspace_bytes=256, stream=0)
     assert ei.value.code == -4
     with pytest.raises(fm.FlexMoEError) as ei:  # shared weights without a shared expert
-        fm.flexmoe_channel_saliency(bf, 16, *([0x1000] * 8), 0x1000, 1.0, 0x1000, 0x1000,
+        fm.flexmoe_channel_saliency(bf, 16, *([0x1000] * 9), 0x1000, 1.0, 0x1000, 0x1000,
                                     workspace_bytes=1 << 30, stream=0)
     assert ei.value.code == -1
     # the workspace grows with T and T = 0 needs only the fixed part
@@ -84,7 +84,8 @@ def test_gpu_saliency_and_rank_match_oracle(spec):
 
     layer = fm.Layer(d, E, I, k, I_s, synth.BF16, norm, max_tokens=T)
     layer.set_weights(*[fm.to_device(a) if a is not None else None for a in (*w, *s)])
-    sal = fm.Saliency(layer, T)
+    # the first case makes W_down^T inside every call, the others once up front
+    sal = fm.Saliency(layer, T, transpose_once=CASES.index(spec) > 0)
     say(name, "T", T, "d", d, "E", E, "I", I, "k", k, "I_s", I_s)
     dev = [fm.to_device(a) for a in (x, lg, tgt, x2, lg2, tgt2)]
     sal.add_batch(dev[0], dev[1], dev[2])
