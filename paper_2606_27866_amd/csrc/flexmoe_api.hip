@@ -399,8 +399,9 @@ BucketPlan make_plan(const int32_t* keep, int E, int I, int k_align) {
 }
 
 // What the training forwards keep besides the output (TrainKeep::mode):
-//   1: transposed g, u, h of the routed rows (channel saliency), and the
-//      combine writes dY = y - target in fp32 instead of y;
+//   1: g, u of the routed rows (fragment-blocked) and their h transposed
+//      (channel saliency); the combine writes dY = y - target in fp32
+//      instead of y;
 //   2: g and u of every row, fragment-blocked (the masked layer's backward);
 //      the gate/up GEMM computes all I channels of every active expert, the
 //      down GEMM only the kept ones.
@@ -409,10 +410,10 @@ BucketPlan make_plan(const int32_t* keep, int E, int I, int k_align) {
 // those of layout(D, T, T).
 struct TrainKeep {
     int mode;
-    bf16_t *gt, *ut, *ht;
+    bf16_t *G, *U, *Gs, *Us;  // fragment-blocked g, u
+    bf16_t* ht;               // mode 1: transposed h
     int ldt;
-    bf16_t *G, *U, *Gs, *Us;
-    const float* y_target;
+    const float* y_target;    // mode 1
     float* dy;
 };
 
@@ -531,8 +532,6 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
                                    (bf16_t*)(ws + L.H), (bf16_t*)(ws + L.Hs), D.d, D.I, D.I_shared, D.E,
                                    D.top_k, nseg, T, part, seg_lo, seg_hi, (int)g1s, clipped};
             if (tr) {
-                p1.gt = tr->gt;
-                p1.ut = tr->ut;
                 p1.ht = tr->ht;
                 p1.ldt = tr->ldt;
                 p1.G = tr->G;
@@ -788,7 +787,7 @@ namespace {
 // ---- channel saliency -------------------------------------------------------
 struct SalLayout {
     Layout f;  // the forward's regions (shared expert unsplit)
-    size_t dy, dO, xt, dot, gt, ut, ht, dgt, dut, wdt, partial, total;
+    size_t dy, dO, xt, dot, G, U, ht, dgt, dut, wdt, partial, total;
     int ldt, nI, nM;
 };
 
@@ -815,8 +814,9 @@ SalLayout sal_layout(const flexmoe_layer_desc& D, int T) {
     S.dO = take(A * d * 2);
     S.xt = take(d * ldt * 2);
     S.dot = take(d * ldt * 2);
-    S.gt = take(I * ldt * 2);
-    S.ut = take(I * ldt * 2);
+    const size_t A32 = (A + 31) & ~size_t(31);  // fragment-blocked rows
+    S.G = take(A32 * I * 2);
+    S.U = take(A32 * I * 2);
     S.ht = take(I * ldt * 2);
     S.dgt = take(I * ldt * 2);
     S.dut = take(I * ldt * 2);
@@ -869,8 +869,8 @@ int saliency_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, cons
     bf16_t* dO = (bf16_t*)(ws + S.dO);
     bf16_t* xt = (bf16_t*)(ws + S.xt);
     bf16_t* dot = (bf16_t*)(ws + S.dot);
-    bf16_t* gt = (bf16_t*)(ws + S.gt);
-    bf16_t* ut = (bf16_t*)(ws + S.ut);
+    bf16_t* G = (bf16_t*)(ws + S.G);
+    bf16_t* U = (bf16_t*)(ws + S.U);
     bf16_t* ht = (bf16_t*)(ws + S.ht);
     bf16_t* dgt = (bf16_t*)(ws + S.dgt);
     bf16_t* dut = (bf16_t*)(ws + S.dut);
@@ -893,7 +893,7 @@ int saliency_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, cons
     set_keep_kernel<<<1, kMaxExperts, 0, s>>>(keep, ka, D.E);
     if ((err = hipGetLastError()) != hipSuccess) return hip_fail(err, "keep upload");
     static_assert(kBigBM1 == kSalTile, "segment row tiles (rt0) are counted in saliency tile rows");
-    const TrainKeep tk{1, gt, ut, ht, S.ldt, nullptr, nullptr, nullptr, nullptr, y_target, dy};
+    const TrainKeep tk{1, G, U, nullptr, nullptr, ht, S.ldt, y_target, dy};
     rc = forward_impl(desc, T, x, logits, w_gate, w_up, w_down, keep, 0, 0x7fffffff, nullptr, 0, ws_gate, ws_up,
                       ws_down, nullptr, workspace, workspace_bytes, nullptr, stream, &tk);
     if (rc != FLEXMOE_OK) return rc;
@@ -909,7 +909,8 @@ int saliency_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, cons
     }
     if (err != hipSuccess) return hip_fail(err, "saliency prep launch");
     {
-        SalDgradParams pd{dO, wdt, seg, gt, ut, dgt, dut, hs, nseg, D.d, D.I, S.ldt, S.nI};
+        ActDgradParams pd{dO, nullptr, wdt, nullptr, G, U, nullptr, nullptr, seg, dgt, dut, nullptr, nullptr,
+                          nullptr, hs, nseg, D.d, D.I, D.I_shared, T, S.nI, 1, S.ldt};
         KernelTimer kt(FLEXMOE_K_SAL_DGRAD, s);
         err = launch_sal_dgrad(pd, gd, s);
     }
@@ -1144,7 +1145,7 @@ int flexmoe_train_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
     if ((rc = check_workspace(S, workspace, workspace_bytes)) != FLEXMOE_OK) return rc;
     TrainPtrs P = train_ptrs(S, workspace);
     static_assert(kBigBM1 == kTrainTile, "segment row tiles (rt0) are counted in training tile rows");
-    const TrainKeep tk{2, nullptr, nullptr, nullptr, 0, P.G, P.U, P.Gs, P.Us, nullptr, nullptr};
+    const TrainKeep tk{2, P.G, P.U, P.Gs, P.Us, nullptr, 0, nullptr, nullptr};
     return forward_impl(desc, T, x, logits, w_gate, w_up, w_down, keep_dev, 0, 0x7fffffff, nullptr, 0, ws_gate,
                         ws_up, ws_down, y, workspace, workspace_bytes, nullptr, stream, &tk);
 }
@@ -1188,7 +1189,7 @@ int flexmoe_train_backward(const flexmoe_layer_desc* desc, int32_t T, const floa
     if (err != hipSuccess) return hip_fail(err, "backward prep launch");
     {
         ActDgradParams pd{P.dO, P.dYs, (const bf16_t*)w_down_t, (const bf16_t*)ws_down_t, P.G, P.U, P.Gs, P.Us,
-                          P.seg, P.dG, P.dU, P.dGs, P.dUs, P.dmp, hs, nseg, D.d, D.I, D.I_shared, T, nI, nIs};
+                          P.seg, P.dG, P.dU, P.dGs, P.dUs, P.dmp, hs, nseg, D.d, D.I, D.I_shared, T, nI, nIs, 0};
         KernelTimer kt(FLEXMOE_K_ACT_DGRAD, s);
         err = launch_act_dgrad(pd, tiles_dgrad, s);
     }

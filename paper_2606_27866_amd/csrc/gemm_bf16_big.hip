@@ -68,60 +68,53 @@ constexpr int STAGE = STAGE_A + BN * ROWB;  // 64 KB
 constexpr int XCD_GROUP = 8;                // consecutive tiles kept on one XCD
 }  // namespace
 
-// Training forward: the tile's g, u and h (256 rows x 128 channels) written
-// transposed through an LDS staging tile, one array at a time.  In the
-// accumulator, lane -> row lane%32 of a 32-row fragment, register v ->
-// channel (v/4)*8 + (lane/32)*4 + v%4 of the wave's 32 gate (jj = 0) and up
-// (jj = NF/2) channels.
+// Saliency forward: the tile's h (256 rows x 128 channels) written
+// transposed through an LDS staging tile.  In the accumulator, lane -> row
+// lane%32 of a 32-row fragment, register v -> channel (v/4)*8 + (lane/32)*4 +
+// v%4 of the wave's 32 gate (jj = 0) and up (jj = NF/2) channels.
 constexpr int TROW = 256 + 8;  // staging row pitch (bf16): 4 rows apart = 16 banks apart
 static_assert(128 * TROW * 2 <= NSTAGE * STAGE, "the staging tile fits in the operand stages");
 
 template <int MFW, typename Acc>
-__device__ __forceinline__ void train_store_transposed(const Gemm1Params<bf16_t>& p, const SegMeta& sm,
-                                                       const Acc& acc, unsigned char* smem, int mtile,
-                                                       int ntile, int wave, int lane) {
+__device__ __forceinline__ void train_store_h_transposed(const Gemm1Params<bf16_t>& p, const SegMeta& sm,
+                                                         const Acc& acc, unsigned char* smem, int mtile,
+                                                         int ntile, int wave, int lane) {
     constexpr int WR = 32 * MFW;
     const int wm = wave / WN, wn = wave % WN;
     bf16_t* st = reinterpret_cast<bf16_t*>(smem);
     const int tile_rows = sm.rows - mtile * BM;            // real rows of this tile
     const int pvalid = packed_width(sm.rows) - mtile * BM;  // rows written (padding included)
     const int ch_tile = ntile * (BN / 2);
-    bf16_t* outs[3] = {p.gt, p.ut, p.ht};
     // the operand stages are free once every wave is past its last fragment read
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     barrier_no_fence();
 #pragma unroll
-    for (int arr = 0; arr < 3; ++arr) {
+    for (int i = 0; i < MFW; ++i) {
+        const int row = wm * WR + i * 32 + (lane & 31);
+        const bool real = row < tile_rows;
 #pragma unroll
-        for (int i = 0; i < MFW; ++i) {
-            const int row = wm * WR + i * 32 + (lane & 31);
-            const bool real = row < tile_rows;
+        for (int q = 0; q < 4; ++q)
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int cl = wn * (WCOL / 2) + q * 8 + (lane >> 5) * 4 + r;
-                    const float g = acc[i][0][q * 4 + r], u = acc[i][NF / 2][q * 4 + r];
-                    const float v = arr == 0 ? g : arr == 1 ? u : silu_fast(g) * u;
-                    st[cl * TROW + row] = real ? f32_to_bf16(v) : (bf16_t)0;
-                }
-        }
-        __syncthreads();
-        bf16_t* out = outs[arr] + (size_t)sm.prow0 + mtile * BM;
-        for (int k = threadIdx.x; k < (BN / 2) * (BM / 8); k += THREADS) {
-            const int cl = k / (BM / 8), r0 = (k % (BM / 8)) * 8;
-            const int ch = ch_tile + cl;
-            if (r0 >= pvalid || ch >= sm.kg) continue;
-            *reinterpret_cast<u32x4*>(out + (size_t)ch * p.ldt + r0) =
-                *reinterpret_cast<const u32x4*>(st + cl * TROW + r0);
-        }
-        __syncthreads();
+            for (int r = 0; r < 4; ++r) {
+                const int cl = wn * (WCOL / 2) + q * 8 + (lane >> 5) * 4 + r;
+                const float g = acc[i][0][q * 4 + r], u = acc[i][NF / 2][q * 4 + r];
+                st[cl * TROW + row] = real ? f32_to_bf16(silu_fast(g) * u) : (bf16_t)0;
+            }
+    }
+    __syncthreads();
+    bf16_t* out = p.ht + (size_t)sm.prow0 + mtile * BM;
+    for (int k = threadIdx.x; k < (BN / 2) * (BM / 8); k += THREADS) {
+        const int cl = k / (BM / 8), r0 = (k % (BM / 8)) * 8;
+        const int ch = ch_tile + cl;
+        if (r0 >= pvalid || ch >= sm.kg) continue;
+        *reinterpret_cast<u32x4*>(out + (size_t)ch * p.ldt + r0) =
+            *reinterpret_cast<const u32x4*>(st + cl * TROW + r0);
     }
 }
 
-// kTrain: 0 = inference; 1 = also the transposed g, u, h of the routed rows
-// (channel saliency); 2 = also g and u of every row, row-major (the masked
-// layer's training backward).
+// kTrain: 0 = inference; 1 = also g and u of the routed rows
+// (fragment-blocked) and their h transposed (channel saliency); 2 = also g
+// and u of every row, fragment-blocked (the masked layer's training backward).
 template <bool kGateUp, int kTrain = 0>
 __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Gemm2Params<bf16_t>& p2,
                                          unsigned char* smem) {
@@ -336,7 +329,7 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
                     *reinterpret_cast<uint2*>(hr + ch) = make_uint2(w[0], w[1]);
                 }
             }
-            if constexpr (kTrain == 2) {
+            if (kTrain == 2 || (kTrain == 1 && !shared)) {
                 // g and u for the training backward, in the fragment-blocked
                 // layout (common.h) over the routed row space (or the tokens)
                 bf16_t* Gb = shared ? p1.Gs : p1.G;
@@ -368,12 +361,11 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
                 }
             }
             if constexpr (kTrain == 1) {
-                // transposed copies of g, u and h for the backward GEMMs,
-                // element [c][prow0 + row], zero in the rows up to the
-                // segment's padded height.  Each is staged through LDS as a
-                // [128 channels][256 rows] tile so that global stores are
-                // whole 16-byte row pieces.
-                if (!shared) train_store_transposed<MFW>(p1, sm, acc, smem, mtile, ntile, wave, lane);
+                // h transposed for the weight-gradient GEMMs, element
+                // [c][prow0 + row], zero in the rows up to the segment's padded
+                // height, staged through LDS as a [128 channels][256 rows] tile
+                // so that global stores are whole 16-byte row pieces
+                if (!shared) train_store_h_transposed<MFW>(p1, sm, acc, smem, mtile, ntile, wave, lane);
             }
         } else {
             bf16_t* Ob = shared ? p2.Os + (size_t)split * p2.tokens * d : p2.O + (size_t)sm.row0 * d;

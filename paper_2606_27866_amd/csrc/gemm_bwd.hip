@@ -3,19 +3,19 @@
 // e with dO_a = w_a dY_t (one row per routed assignment):
 //   dgrad:  dH[a][c] = sum_n dO_a[n] W_down[n][c]; fused epilogue
 //           dG = dH u silu'(g), dU = dH silu(g)           (SwiGLU backward)
+//           (the same kernel serves the masked layer's training backward)
 //   wgrad:  dW_gate[c][i] = sum_a dG[a][c] x_a[i], dW_up likewise with dU,
 //           dW_down[n][c] = sum_a dO_a[n] h_a[c]; fused epilogue
 //           s[e][c] += sum over the tile of (theta * dW)^2  (Eq. 2)
 // so the weight gradients are never written: each wgrad tile reduces its
 // 256 x 256 block of (theta * g)^2 to one partial sum per channel.
 //
-// Both kernels are "NT" GEMMs: A rows and B rows are contiguous in K, staged
-// by the same LDS pipeline as the forward's big tiles (mfma_tile.h: 256 x 256
-// x 64 tiles, 8 waves as 2 x 4, direct-to-LDS DMA, two stages, fragments one
-// step ahead).  The MFMA takes the A fragment first, so a lane's accumulator
-// holds one B row (a channel) and runs of 4 consecutive A rows: the
-// transposed stores of the dgrad epilogue and the weight reads of the wgrad
-// epilogue are 8-byte accesses.
+// All are "NT" GEMMs: A rows and B rows are contiguous in K, staged by the
+// same LDS pipeline as the forward's big tiles (mfma_tile.h: 256 x 256 x 64
+// tiles, 8 waves as 2 x 4, direct-to-LDS DMA, two stages, fragments one step
+// ahead).  In the wgrad the MFMA takes the A fragment first, so a lane's
+// accumulator holds one B row (a channel) and runs of 4 consecutive A rows,
+// and the weight reads of its epilogue are 8-byte accesses.
 //   dgrad: A = dO [A][d] (a segment's rows), B = W_down^T [E][I][d] (a
 //          transposed copy of the down weights), K = d.
 //   wgrad: A = x^T or dO^T [d][ldt], B = dG^T, dU^T or h^T [I][ldt], with a
@@ -198,82 +198,6 @@ __device__ __forceinline__ float lo_bf16(uint32_t w) { return __uint_as_float(w 
 __device__ __forceinline__ float hi_bf16(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 }  // namespace
 
-// ---- dgrad: one tile = 256 rows of a routed segment x 256 channels --------
-__global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void sal_dgrad_kernel(SalDgradParams p) {
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[NSTAGE * STAGE];
-    const int L = xcd_tile(dgrad_group(p.nI));
-    // routed segment: the last one whose first tile is at or before L
-    int lo = p.hs, hi = p.nseg - 1;
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (p.seg[mid].rt0 * p.nI <= L) lo = mid;
-        else hi = mid - 1;
-    }
-    const SegMeta sm = p.seg[lo];
-    const int mt = ceil_div(sm.rows, BM);
-    const int local = L - sm.rt0 * p.nI;
-    if (local >= mt * p.nI) return;  // past the last tile (or an empty segment)
-    const int ntile = local / mt, mtile = local % mt;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
-
-    NTOperands op;
-    op.K = p.d;
-    op.ra = make_rsrc(p.dO + (size_t)sm.row0 * p.d, (size_t)sm.rows * p.d);
-    op.rb = make_rsrc(p.wdt + (size_t)sm.e * p.I * p.d, (size_t)p.I * p.d);
-    int bcol[NI];
-    nt_rows(wave, lane, mtile * BM, sm.rows, p.d, op.aoff, op.acol);
-    nt_rows(wave, lane, ntile * BN, p.I, p.d, op.boff, bcol);  // same chunk columns as A
-
-    const int wm = wave / WN, wn = wave % WN;
-    by_rows(sm.rows - mtile * BM, [&](auto tag) {
-        constexpr int MFW = decltype(tag)::value;
-        floatx16 acc[MFW][NF];
-        nt_mainloop<MFW>(smem, op, wave, lane, acc, ZeroTail{op.ra});
-        // epilogue: lane -> channel c, register v -> row 8(v/4) + 4(lane/32) + v%4
-        const int prow = packed_width(sm.rows);
-#pragma unroll
-        for (int j = 0; j < NF; ++j) {
-            const int c = ntile * BN + wn * WCOL + j * 32 + (lane & 31);
-            if (c >= p.I) continue;
-            const size_t base = (size_t)c * p.ldt + sm.prow0;
-#pragma unroll
-            for (int i = 0; i < MFW; ++i)
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int r0 = mtile * BM + wm * 32 * MFW + i * 32 + q * 8 + (lane >> 5) * 4;
-                    if (r0 >= prow) continue;
-                    const uint2 gv = *reinterpret_cast<const uint2*>(p.gt + base + r0);
-                    const uint2 uv = *reinterpret_cast<const uint2*>(p.ut + base + r0);
-                    const float g[4] = {lo_bf16(gv.x), hi_bf16(gv.x), lo_bf16(gv.y), hi_bf16(gv.y)};
-                    const float u[4] = {lo_bf16(uv.x), hi_bf16(uv.x), lo_bf16(uv.y), hi_bf16(uv.y)};
-                    uint32_t dg[2], du[2];
-#pragma unroll
-                    for (int h = 0; h < 2; ++h) {
-                        uint32_t pg = 0, pu = 0;
-#pragma unroll
-                        for (int r = 0; r < 2; ++r) {
-                            const int rr = h * 2 + r;
-                            float vg = 0.f, vu = 0.f;
-                            if (r0 + rr < sm.rows) {
-                                const float x = g[rr];
-                                const float sg = 1.0f / (1.0f + __builtin_amdgcn_exp2f(-x * 1.4426950408889634f));
-                                const float dh = acc[i][j][q * 4 + rr];
-                                vg = dh * u[rr] * (sg * (1.0f + x * (1.0f - sg)));
-                                vu = dh * (x * sg);
-                            }
-                            pg |= (uint32_t)f32_to_bf16(vg) << (16 * r);
-                            pu |= (uint32_t)f32_to_bf16(vu) << (16 * r);
-                        }
-                        dg[h] = pg;
-                        du[h] = pu;
-                    }
-                    *reinterpret_cast<uint2*>(p.dgt + base + r0) = make_uint2(dg[0], dg[1]);
-                    *reinterpret_cast<uint2*>(p.dut + base + r0) = make_uint2(du[0], du[1]);
-                }
-        }
-    });
-}
-
 // ---- wgrad + saliency: one tile = 256 hidden units x 256 channels of one
 // (matrix, expert) ----------------------------------------------------------
 __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void sal_wgrad_kernel(SalWgradParams p) {
@@ -377,8 +301,8 @@ namespace {
 // first (ceil(T/256) row tiles x nsh column tiles), then the routed segments'
 // (row tiles numbered by SegMeta::rt0, x nr column tiles).  False past the end.
 __device__ __forceinline__ bool train_tile(const SegMeta* seg, int hs, int nseg, int T, int Is, int nsh, int nr,
-                                           int L, SegMeta& sm, int& mtile, int& ntile) {
-    if (hs) {
+                                           int L, SegMeta& sm, int& mtile, int& ntile, bool with_shared = true) {
+    if (hs && with_shared) {
         const int mt = ceil_div(T, BM), sh = mt * nsh;
         if (L < sh) {
             sm = SegMeta{0, T, Is, 0, Is, -1, 0, 0};
@@ -404,21 +328,31 @@ __device__ __forceinline__ bool train_tile(const SegMeta* seg, int hs, int nseg,
 }
 }  // namespace
 
-// dgrad + SwiGLU backward + mask gradient; tile = 256 rows x 256 channels.
-// The B fragment goes first: lane -> row, registers -> runs of 4 channels.
-// g and u are read in their fragment-blocked layout (a wave's 8-byte reads
-// cover 512 contiguous bytes); dG and dU are staged through LDS, half of the
-// tile's channels at a time, and stored as whole 16-byte row pieces.
+// dgrad + SwiGLU backward; tile = 256 rows x 256 channels.  The B fragment
+// goes first: lane -> row, registers -> runs of 4 channels.  g and u are read
+// in their fragment-blocked layout (a wave's 8-byte reads cover 512
+// contiguous bytes); dG and dU are staged through LDS, half of the tile's
+// channels at a time, and stored as whole 16-byte pieces.
+//   kMode 2 (masked layer's training backward): shared expert included, the
+//     mask gradient's partial sums, dG/dU row-major [rows][C] over the kept
+//     channels;
+//   kMode 1 (channel saliency): routed segments only, every channel kept,
+//     dG/dU transposed -- [c][prow0 + r] of [I][ldt], zero in each segment's
+//     padding rows -- for the weight-gradient GEMMs.
 constexpr int DG_PITCH = BN / 2 + 8;                  // staged row (bf16): 272 bytes, 16-byte aligned
 constexpr int DG_STAGE = BM * DG_PITCH * 2;           // one staged array
 constexpr int DG_SMEM = (2 * DG_STAGE > NSTAGE * STAGE) ? 2 * DG_STAGE : NSTAGE * STAGE;
+constexpr int DG_TPITCH = BM + 8;                     // transposed staging row (bf16): 4 rows = 16 banks
+static_assert(2 * (BN / 2) * DG_TPITCH * 2 <= DG_SMEM, "the transposed staging fits");
 static_assert(DG_SMEM <= 160 * 1024, "the dgrad LDS fits one compute unit");
 
-__global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void act_dgrad_kernel(ActDgradParams p) {
+template <int kMode>
+__global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void dgrad_kernel(ActDgradParams p) {
     __shared__ __attribute__((aligned(1024))) unsigned char smem[DG_SMEM];
     SegMeta sm;
     int mtile, ntile;
-    if (!train_tile(p.seg, p.hs, p.nseg, p.T, p.Is, p.nIs, p.nI, xcd_tile(dgrad_group(p.nI)), sm, mtile, ntile))
+    if (!train_tile(p.seg, p.hs, p.nseg, p.T, p.Is, p.nIs, p.nI, xcd_tile(dgrad_group(p.nI)), sm, mtile, ntile,
+                    kMode == 2))
         return;
     const bool shared = sm.e < 0;
     const int C = shared ? p.Is : p.I;  // channels (row length of g, u, dG, dU)
@@ -443,7 +377,7 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void act_dgrad_kernel(ActD
     const int kk = sm.kk;                        // mask: channels below kk are kept
     const int kk8 = min(packed_width(kk), C);    // dG/dU columns the dx GEMM reads
     bf16_t* stg = reinterpret_cast<bf16_t*>(smem);
-    bf16_t* stu = stg + BM * DG_PITCH;
+    bf16_t* stu = stg + (kMode == 2 ? BM * DG_PITCH : (BN / 2) * DG_TPITCH);
     by_rows(sm.rows - mtile * BM, [&](auto tag) {
         constexpr int MFW = decltype(tag)::value;
         floatx16 acc[MFW][NF];
@@ -478,7 +412,7 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void act_dgrad_kernel(ActD
                             const float x = g[r];
                             const float sg = 1.0f / (1.0f + __builtin_amdgcn_exp2f(-x * 1.4426950408889634f));
                             const float dh = acc[i][j][q * 4 + r];
-                            msum[j][q * 4 + r] += dh * (x * sg) * u[r];
+                            if constexpr (kMode == 2) msum[j][q * 4 + r] += dh * (x * sg) * u[r];
                             const bool kept = c0 + r < kk;
                             const float vg = kept ? dh * u[r] * (sg * (1.0f + x * (1.0f - sg))) : 0.f;
                             const float vu = kept ? dh * (x * sg) : 0.f;
@@ -486,24 +420,46 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void act_dgrad_kernel(ActD
                             du[r >> 1] |= (uint32_t)f32_to_bf16(vu) << (16 * (r & 1));
                         }
                     }
-                    *reinterpret_cast<uint2*>(stg + row * DG_PITCH + cl) = make_uint2(dg[0], dg[1]);
-                    *reinterpret_cast<uint2*>(stu + row * DG_PITCH + cl) = make_uint2(du[0], du[1]);
+                    if constexpr (kMode == 2) {
+                        *reinterpret_cast<uint2*>(stg + row * DG_PITCH + cl) = make_uint2(dg[0], dg[1]);
+                        *reinterpret_cast<uint2*>(stu + row * DG_PITCH + cl) = make_uint2(du[0], du[1]);
+                    } else {  // staged transposed: [channel][row]
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            stg[(cl + r) * DG_TPITCH + row] = (bf16_t)(dg[r >> 1] >> (16 * (r & 1)));
+                            stu[(cl + r) * DG_TPITCH + row] = (bf16_t)(du[r >> 1] >> (16 * (r & 1)));
+                        }
+                    }
                 }
             }
             __syncthreads();
             // staged column cl of half j is channel ntile*BN + (cl/32)*WCOL + j*32 + cl%32
-            for (int k = threadIdx.x; k < BM * (BN / 2 / 8); k += THREADS) {
-                const int row = k / (BN / 2 / 8), cl = (k % (BN / 2 / 8)) * 8;
-                const int grow = mtile * BM + row;
-                const int c = ntile * BN + (cl / 32) * WCOL + j * 32 + cl % 32;
-                if (grow >= sm.rows || c >= kk8) continue;
-                const size_t o = (rbase + grow) * (size_t)C + c;
-                *reinterpret_cast<u32x4*>(dG + o) = *reinterpret_cast<const u32x4*>(stg + row * DG_PITCH + cl);
-                *reinterpret_cast<u32x4*>(dU + o) = *reinterpret_cast<const u32x4*>(stu + row * DG_PITCH + cl);
+            if constexpr (kMode == 2) {
+                for (int k = threadIdx.x; k < BM * (BN / 2 / 8); k += THREADS) {
+                    const int row = k / (BN / 2 / 8), cl = (k % (BN / 2 / 8)) * 8;
+                    const int grow = mtile * BM + row;
+                    const int c = ntile * BN + (cl / 32) * WCOL + j * 32 + cl % 32;
+                    if (grow >= sm.rows || c >= kk8) continue;
+                    const size_t o = (rbase + grow) * (size_t)C + c;
+                    *reinterpret_cast<u32x4*>(dG + o) = *reinterpret_cast<const u32x4*>(stg + row * DG_PITCH + cl);
+                    *reinterpret_cast<u32x4*>(dU + o) = *reinterpret_cast<const u32x4*>(stu + row * DG_PITCH + cl);
+                }
+            } else {
+                // rows up to the segment's padded height (zeros past its rows)
+                const int pvalid = packed_width(sm.rows) - mtile * BM;
+                const size_t col = (size_t)sm.prow0 + mtile * BM;
+                for (int k = threadIdx.x; k < (BN / 2) * (BM / 8); k += THREADS) {
+                    const int cl = k / (BM / 8), r0 = (k % (BM / 8)) * 8;
+                    const int c = ntile * BN + (cl / 32) * WCOL + j * 32 + cl % 32;
+                    if (r0 >= pvalid || c >= C) continue;
+                    const size_t o = (size_t)c * p.ldt + col + r0;
+                    *reinterpret_cast<u32x4*>(dG + o) = *reinterpret_cast<const u32x4*>(stg + cl * DG_TPITCH + r0);
+                    *reinterpret_cast<u32x4*>(dU + o) = *reinterpret_cast<const u32x4*>(stu + cl * DG_TPITCH + r0);
+                }
             }
             __syncthreads();
         }
-        if (shared) return;
+        if (kMode == 1 || shared) return;
         // mask-gradient partial sums: over the 32 rows of the lane group
 #pragma unroll
         for (int j = 0; j < NF; ++j)
@@ -593,7 +549,14 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void act_dx_kernel(ActDxPa
 hipError_t launch_act_dgrad(const ActDgradParams& p, long long tiles, hipStream_t s) {
     if (tiles <= 0) return hipSuccess;
     const long long g = xcd_grid(tiles, dgrad_group(p.nI));
-    act_dgrad_kernel<<<(int)g, THREADS, 0, s>>>(p);
+    dgrad_kernel<2><<<(int)g, THREADS, 0, s>>>(p);
+    return hipGetLastError();
+}
+
+hipError_t launch_sal_dgrad(const ActDgradParams& p, long long tiles, hipStream_t s) {
+    if (tiles <= 0) return hipSuccess;
+    const long long g = xcd_grid(tiles, dgrad_group(p.nI));
+    dgrad_kernel<1><<<(int)g, THREADS, 0, s>>>(p);
     return hipGetLastError();
 }
 
@@ -601,13 +564,6 @@ hipError_t launch_act_dx(const ActDxParams& p, long long tiles, hipStream_t s) {
     if (tiles <= 0) return hipSuccess;
     const long long g = xcd_grid(tiles, dgrad_group(p.nD));
     act_dx_kernel<<<(int)g, THREADS, 0, s>>>(p);
-    return hipGetLastError();
-}
-
-hipError_t launch_sal_dgrad(const SalDgradParams& p, long long tiles, hipStream_t s) {
-    if (tiles <= 0) return hipSuccess;
-    const long long g = xcd_grid(tiles, dgrad_group(p.nI));
-    sal_dgrad_kernel<<<(int)g, THREADS, 0, s>>>(p);
     return hipGetLastError();
 }
 

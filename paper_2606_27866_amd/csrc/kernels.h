@@ -39,22 +39,19 @@ struct Gemm1Params {
     int seg_lo, seg_hi;         // kPartRange: the segments covered
     int shared_tiles;           // tiles of the shared segment (kPartShared)
     int clipped;                // routed weights in the clipped layout (see RoutedWeights)
-    // Training forward only (launch_gemm1_big_train): the routed segments'
-    // pre-activations g, u and activations h, transposed -- element
-    // [c][prow0 + r] for row r of a segment -- with zeros in the rows
-    // [rows, packed_width(rows)) of each segment.  Row stride ldt.
-    T* gt;
-    T* ut;
-    T* ht;
-    int ldt;
-    // Training forward of the masked layer (launch_gemm1_big_train_rm): g and
-    // u of every row for every channel the GEMM computes (c < kg), in the
-    // fragment-blocked layout (common.h) of a routed [A][I] and a shared
-    // [T][I_s] matrix.
+    // Training forwards: g and u for every channel the GEMM computes (c < kg),
+    // in the fragment-blocked layout (common.h) of a routed [A][I] and a shared
+    // [T][I_s] matrix (launch_gemm1_big_train: routed rows only;
+    // launch_gemm1_big_train_rm: all rows).
     T* G;
     T* U;
     T* Gs;
     T* Us;
+    // launch_gemm1_big_train only: the routed rows' activations h transposed --
+    // element [c][prow0 + r] for row r of a segment -- with zeros in the rows
+    // [rows, packed_width(rows)) of each segment.  Row stride ldt.
+    T* ht;
+    int ldt;
 };
 
 // Down GEMM: O[row][n] = sum_{c < k_s} H[row][c] * W_down[n][c].  O holds one

@@ -3,26 +3,12 @@
 // loss, reduced to one score per hidden channel of every routed expert.
 #pragma once
 
-#include "kernels.h"
+#include "train.h"
 
 namespace flexmoe {
 
 constexpr int kSalTile = 256;   // rows x channels of the dgrad and wgrad tiles
 constexpr int kSalWaveM = 2;    // partial sums per channel from one wgrad tile
-
-// dgrad with the SwiGLU backward fused: per routed segment,
-// dH = dO W_down (all I channels), then dG, dU transposed.
-struct SalDgradParams {
-    const bf16_t* dO;       // [A][d] routed rows in dispatch order: w_a * dY_t
-    const bf16_t* wdt;      // [E][I][d] transposed routed down weights
-    const SegMeta* seg;
-    const bf16_t* gt;       // [I][ldt] transposed pre-activations g, u (training forward)
-    const bf16_t* ut;
-    bf16_t* dgt;            // [I][ldt] transposed dG, dU, zero in each segment's padding rows
-    bf16_t* dut;
-    int hs, nseg;           // first routed segment, number of segments
-    int d, I, ldt, nI;      // nI = ceil(I / kSalTile)
-};
 
 // wgrad of the three routed matrices with the Eq. 2 reduction fused; tile
 // (mat, e, channel tile, hidden-unit tile) writes kSalWaveM partial sums per
@@ -51,7 +37,6 @@ struct SalPrepParams {
 };
 
 hipError_t launch_gemm1_big_train(const Gemm1Params<bf16_t>& p, int grid, hipStream_t s);
-hipError_t launch_sal_dgrad(const SalDgradParams& p, long long tiles, hipStream_t s);
 hipError_t launch_sal_wgrad(const SalWgradParams& p, hipStream_t s);
 hipError_t launch_sal_prep(const SalPrepParams& p, hipStream_t s);
 hipError_t launch_sal_reduce(const float* partial, int E, int I, int parts, float scale, float* scores,

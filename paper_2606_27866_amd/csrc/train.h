@@ -32,6 +32,7 @@ struct ActDgradParams {
     bf16_t* dUs;
     float* dmp;             // [routed row tiles][kTrainWaveM][I] mask-gradient partial sums
     int hs, nseg, d, I, Is, T, nI, nIs;   // nI = ceil(I / kTrainTile), nIs likewise
+    int ldt;                // launch_sal_dgrad: dG, dU are [I][ldt], written transposed
 };
 
 // dx rows: dX = dG W_gate + dU W_up, K = k (routed) or I_s (shared).
@@ -58,6 +59,10 @@ struct ActionWidths {
 
 hipError_t launch_gemm1_big_train_rm(const Gemm1Params<bf16_t>& p, int grid, hipStream_t s);
 hipError_t launch_act_dgrad(const ActDgradParams& p, long long tiles, hipStream_t s);
+// The channel saliency's dgrad (the same kernel): routed segments only, no
+// mask, dG and dU written transposed -- element [c][prow0 + r] of [I][ldt],
+// zeros in each segment's padding rows -- and no mask gradient (dmp unused).
+hipError_t launch_sal_dgrad(const ActDgradParams& p, long long tiles, hipStream_t s);
 hipError_t launch_act_dx(const ActDxParams& p, long long tiles, hipStream_t s);
 // seg[s].kg = seg[s].kk: the down GEMM of the training forward reduces over
 // the kept channels only (the gate/up GEMM computed all of them)
