@@ -67,6 +67,9 @@ def parse():
                     help="tokens per calibration batch of the saliency (default: the workload's T)")
     ap.add_argument("--saliency-steps", type=int, default=10)
     ap.add_argument("--no-action", action="store_true", help="skip the action-learning step measurement")
+    ap.add_argument("--graphs", action="store_true",
+                    help="decode: replay each step from a HIP graph (captured through torch.cuda.graph); "
+                         "measured no faster than eager calls, whose launches already overlap")
     ap.add_argument("--action-steps", type=int, default=10)
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-baseline work")
     ap.add_argument("--bucket-align", type=int, default=128,
@@ -197,6 +200,36 @@ class Workload:
             fm.flexmoe_timing_enable(False)
         return ms, kt
 
+    def capture_graphs(self, keep_names, n):
+        """One HIP graph per step of a period of n decode steps: the budget
+        upload (when tables switch) and the layer forward of batch b with
+        weight copy b % copies, captured through torch.cuda.graph."""
+        torch = self.torch
+        switching = len(keep_names) > 1
+        self.graphs = []
+        for b in range(n):
+            self.use_copy(b)
+            x, lg = self.xd[b % len(self.xd)]
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                if switching:
+                    self.layer.set_budget(self.tables[keep_names[b % len(keep_names)]])
+                self.layer.forward(x, lg, y=self.y, keep=None if switching else self.keep_dev[keep_names[0]])
+            self.graphs.append(g)
+        torch.cuda.synchronize()
+
+    def run_graphs(self, steps):
+        torch = self.torch
+        torch.cuda.synchronize()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        ev0.record()
+        for i in range(steps):
+            self.graphs[i % len(self.graphs)].replay()
+        ev1.record()
+        torch.cuda.synchronize()
+        return ev0.elapsed_time(ev1)
+
     def run_bucketed(self, steps, table_name, k_align):
         """Time `steps` forwards of the bucketed ablation (width groups, one
         launch pair each, widths aligned up to k_align)."""
@@ -269,11 +302,11 @@ def cpu_baseline(wl, keep, target_s):
                        % (what, t))
 
 
-def saliency_section(wl, args):
+def saliency_section(wl, args, T=None, with_cpu=True):
     """Channel ranking on the device (Eq. 2 saliency over calibration batches,
     then the reorder of Eq. 3), timed per calibration batch."""
     torch, fm, synth, cfg = wl.torch, wl.fm, wl.synth, wl.cfg
-    T = args.saliency_T or wl.T
+    T = T or args.saliency_T or wl.T
     bias = synth.router_bias(cfg)
     nb = 4
     batches = []
@@ -342,7 +375,9 @@ def saliency_section(wl, args):
            rank_ms))
     for k, v in kms.items():
         log("[bench]   saliency %-17s %8.4f ms" % (k, v))
-    if not args.no_cpu:
+    del sal, batches
+    torch.cuda.empty_cache()
+    if with_cpu and not args.no_cpu:
         out["cpu_baseline"] = saliency_cpu_baseline(wl, T, args.cpu_seconds)
         log("[bench] saliency CPU oracle: %.2f tokens/s on %d threads" % (out["cpu_baseline"]["value"],
                                                                            out["cpu_baseline"]["cores"]))
@@ -515,6 +550,19 @@ def main():
     value = wl.T * args.steps / (ms / 1e3)
     log("[bench] %s: %.4f ms/step, %.0f tokens/s (%.4f ms/step with per-kernel events)"
         % (args.workload, ms_step, value, ms_inst / args.steps))
+    eager_ms_step = ms_step
+    graphs = False
+    if wl.decode and args.graphs:
+        # decode steps are short: replaying each step's launches from a HIP
+        # graph removes the host's launch gaps between its kernels
+        wl.capture_graphs(keep_names, 64)
+        wl.run_graphs(args.warmup)
+        ms_g = wl.run_graphs(args.steps)
+        graphs = True
+        ms_step = ms_g / args.steps
+        value = wl.T * args.steps / (ms_g / 1e3)
+        log("[bench] %s: %.4f ms/step, %.0f tokens/s replayed from HIP graphs (eager %.4f ms/step)"
+            % (args.workload, ms_step, value, eager_ms_step))
     for kname, (kms, cnt) in kt.items():
         if cnt:
             log("[bench]   %-17s %8.4f ms avg over %d launches" % (kname, kms / cnt, cnt))
@@ -619,6 +667,10 @@ def main():
     saliency = None
     if not args.no_saliency and bf16 and not wl.decode:
         saliency = saliency_section(wl, args)
+        if not args.saliency_T:
+            # a calibration batch four times the workload's: Eq. 2 reads every
+            # weight once per batch, which larger batches amortise
+            saliency["batch_x4"] = saliency_section(wl, args, T=4 * wl.T, with_cpu=False)
     action = None
     if not args.no_action and bf16 and not wl.decode:
         action = action_section(wl, args)
@@ -654,7 +706,8 @@ def main():
         "config": {"workload": args.workload, "T": wl.T, "d": cfg.d, "E": cfg.E, "I": cfg.I,
                    "top_k": cfg.top_k, "I_shared": cfg.I_shared,
                    "keep_table": "+".join(keep_names) if wl.decode else wl.table_name,
-                   "weight_copies": args.copies},
+                   "weight_copies": args.copies, "hip_graphs": graphs},
+        "eager_ms_per_step": eager_ms_step,
         "roofline": roof,
         "layer": layer,
         "per_budget": per_budget,
