@@ -7,7 +7,11 @@
  * the expert weights (Eq. 3); a budget is the per-expert keep-count array
  * k[E] (the hardened action mask of Eqs. 9-10 expressed as channel counts).
  * Switching budgets rewrites only that array: no weight is moved, which is the
- * online clipping mode of Sec. 4.4 (Table 3).
+ * online clipping mode of Sec. 4.4 (Table 3).  Around that forward: the
+ * offline-clipped mode (Table 2), the bucketed kernel design of App. C.3 as an
+ * ablation, the channel saliency of Eq. 2 on the device, and one
+ * action-learning step (Eqs. 5-8): sampled widths, the masked layer's
+ * training forward and backward, and the action-logit gradient.
  *
  * General rules for every entry point
  *   - All pointers except the descriptor, the host keep table of
@@ -22,7 +26,8 @@
  *     two GEMMs on a second stream of the same device (forked from `stream` by
  *     an event before routing, joined by an event before the combine): it does
  *     so for T <= 64 and while the shared expert's gate/up GEMM has fewer than
- *     1024 tiles.  The library creates that stream on first use per device
+ *     1024 tiles (the training forwards never do).  The library creates that
+ *     stream on first use per device
  *     (default priority) and keeps it for the life of the process; forwards
  *     on one device share it, so concurrent forwards on one device also
  *     serialise their shared-expert GEMMs.
@@ -32,6 +37,10 @@
  *     an argument error has enqueued nothing.  Device-resident data (logits,
  *     keep counts) is not inspected by the host; keep counts read on the device
  *     are clamped to [0, I] so that no access leaves its buffer.
+ *   - No call allocates, frees, synchronises or sets memory with a memset:
+ *     the calls can be captured into a HIP graph (the side stream joins the
+ *     capture through its fork and join events; create it with one eager call
+ *     before capturing).
  *   - x, weights and y must be 16-byte aligned; logits and keep arrays 4-byte
  *     aligned (FLEXMOE_EINVAL otherwise); the workspace 256-byte aligned.
  *
