@@ -1013,11 +1013,13 @@ int action_widths(const flexmoe_layer_desc& D, const flexmoe_action_set* a, Acti
     return FLEXMOE_OK;
 }
 
+// The regions of the training workspace the backward reads or writes (the
+// forward's own regions are carved by forward_impl).
 struct TrainPtrs {
-    int32_t *idx, *counts, *offsets, *perm, *pos, *plan, *blockcnt, *blockbase, *t1, *t2;
+    int32_t *idx, *offsets, *perm, *pos;
     float* wts;
     SegMeta* seg;
-    bf16_t *H, *Hs, *O, *Os, *G, *U, *Gs, *Us, *dO, *dYs, *dG, *dU, *dGs, *dUs;
+    bf16_t *O, *G, *U, *Gs, *Us, *dO, *dYs, *dG, *dU, *dGs, *dUs;
     float *dXr, *dXs, *dmp;
 };
 
@@ -1027,20 +1029,11 @@ TrainPtrs train_ptrs(const TrainLayout& S, void* workspace) {
     TrainPtrs P;
     P.idx = (int32_t*)(ws + L.idx);
     P.wts = (float*)(ws + L.wts);
-    P.blockcnt = (int32_t*)(ws + L.blockcnt);
-    P.blockbase = (int32_t*)(ws + L.blockbase);
-    P.counts = (int32_t*)(ws + L.counts);
     P.offsets = (int32_t*)(ws + L.offsets);
     P.perm = (int32_t*)(ws + L.perm);
     P.pos = (int32_t*)(ws + L.pos);
     P.seg = (SegMeta*)(ws + L.seg);
-    P.t1 = (int32_t*)(ws + L.t1);
-    P.t2 = (int32_t*)(ws + L.t2);
-    P.plan = (int32_t*)(ws + L.plan);
-    P.H = (bf16_t*)(ws + L.H);
-    P.Hs = (bf16_t*)(ws + L.Hs);
     P.O = (bf16_t*)(ws + L.O);
-    P.Os = (bf16_t*)(ws + L.Os);
     P.G = (bf16_t*)(ws + S.G);
     P.U = (bf16_t*)(ws + S.U);
     P.Gs = (bf16_t*)(ws + S.Gs);
