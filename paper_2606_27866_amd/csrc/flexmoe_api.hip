@@ -525,6 +525,8 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
         const bool sh = part == kPartShared;
         const int k1 = sh ? FLEXMOE_K_GATE_UP_SHARED : FLEXMOE_K_GATE_UP;
         const int k2 = sh ? FLEXMOE_K_DOWN_SHARED : FLEXMOE_K_DOWN;
+        // the shared expert at 17..64 tokens: 64-wide tiles sharing the token rows
+        const bool wide = decode && sh && T > kDecodeWideT;
         hipError_t e;
         if (bf16) {
             Gemm1Params<bf16_t> p1{(const bf16_t*)x, (const bf16_t*)w_gate_r, (const bf16_t*)w_up_r,
@@ -541,7 +543,8 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
             }
             {
                 KernelTimer kt(k1, st);
-                e = decode       ? launch_gemm1_decode(p1, (int)n1, st)
+                e = wide         ? launch_gemm1_decode_wide(p1, st)
+                    : decode     ? launch_gemm1_decode(p1, (int)n1, st)
                     : train == 1 ? launch_gemm1_big_train(p1, (int)n1, st)
                     : train == 2 ? launch_gemm1_big_train_rm(p1, (int)n1, st)
                                  : launch_gemm1_big(p1, (int)n1, st);
@@ -556,7 +559,9 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
                                    seg_hi, (int)g2s, clipped};
             {
                 KernelTimer kt(k2, st);
-                e = decode ? launch_gemm2_decode(p2, (int)n2, st) : launch_gemm2_big(p2, (int)n2, st);
+                e = wide     ? launch_gemm2_decode_wide(p2, st)
+                    : decode ? launch_gemm2_decode(p2, (int)n2, st)
+                             : launch_gemm2_big(p2, (int)n2, st);
             }
             if (e != hipSuccess) return hip_fail(e, "down GEMM launch");
         } else {

@@ -24,7 +24,9 @@
 //   expert's reduction is split into chunks of I channels (one routed
 //   expert's worth), each chunk writing its own partial rows, which the
 //   combine sums in a fixed order.
-#include "kernels.h"
+#include <type_traits>
+
+#include "mfma_tile.h"
 
 namespace flexmoe {
 
@@ -211,6 +213,186 @@ __global__ __launch_bounds__(64 * DWAVES) void gemm2_decode_kernel(Gemm2Params<b
     }
 }
 
+// ---- The shared expert at more than kDecodeWideT tokens: wide tiles ------
+//
+// With 17..64 tokens the 16-channel tiles above read every token row once
+// per 16 weight rows -- two to four times the weight bytes, from L2, one
+// 16-token block after another.  The shared expert's GEMMs then take tiles
+// of 64 channels (gate/up) or 64 output columns (down): wave w owns 16 of
+// them over the whole reduction, and the four waves share the token rows
+// through LDS.  Per 256-deep K batch the workgroup copies rows [64][256]
+// into LDS once (buffer_load ... lds); the next batch's rows and weights are
+// in flight while the current batch is multiplied.  LDS row r keeps its 16-B
+// chunk c at position c ^ (r & 15): the 16 lanes of one fragment read (16
+// rows, one chunk) then cover all 64 banks.
+namespace {
+constexpr int WCH = 64;                            // channels / output columns per wide tile
+constexpr int WKB = 256;                           // K per batch
+constexpr int WROWB = WKB * 2;                     // LDS bytes per staged row
+constexpr int WSTAGE = kDecodeMaxT * WROWB;        // one batch of every row: 32 KB
+constexpr int WDMA = WSTAGE / (16 * 64 * DWAVES);  // DMA instructions per lane per batch
+static_assert(2 * WROWB == 16 * 64 && WDMA * DWAVES * 16 * 64 == WSTAGE,
+              "a DMA instruction fills two staged rows; the waves fill the stage");
+}  // namespace
+
+template <bool kGateUp>
+__device__ __forceinline__ void wide_tile(const Gemm1Params<bf16_t>& p1, const Gemm2Params<bf16_t>& p2,
+                                          unsigned char* smem) {
+    using namespace mfma;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+    const int R = kGateUp ? p1.tokens : p2.tokens;      // token rows, <= kDecodeMaxT
+    const int nrows = kGateUp ? p1.Is : p2.d;           // weight rows: channels or output columns
+    const int ntiles = ceil_div(nrows, WCH);
+    int tile = blockIdx.x, split = 0;
+    if (!kGateUp) {
+        split = tile / ntiles;
+        tile -= split * ntiles;
+    }
+    // the reduction: all of d (gate/up) or channel chunk `split` of I_s (down)
+    const int ks = kGateUp ? p1.d : (p2.ks2 > 0 ? p2.ks2 : p2.Is);
+    const int kbeg = kGateUp ? 0 : split * ks;
+    if (kbeg >= (kGateUp ? p1.d : p2.Is)) return;  // workgroup-uniform
+    const int K = kGateUp ? p1.d : min(p2.Is - kbeg, ks);
+    const int ld = kGateUp ? p1.d : p2.Is;  // row stride of the token rows and of the weights
+
+    // token rows: x [T][d] or the shared activations Hs [T][I_s] from kbeg
+    const bf16_t* A = kGateUp ? p1.x : p2.Hs + kbeg;
+    const __amdgpu_buffer_rsrc_t ra = make_rsrc(A, (size_t)R * ld - kbeg);
+    // DMA instruction i of this wave fills staged rows 2*(wave*WDMA + i) and
+    // the next; lane -> row lane/32, LDS chunk lane%32
+    uint32_t aoff[WDMA];
+    int acol[WDMA];
+#pragma unroll
+    for (int i = 0; i < WDMA; ++i) {
+        const int r = 2 * (wave * WDMA + i) + (lane >> 5);
+        const int c = (lane & 31) ^ (r & 15);
+        acol[i] = c * 8;
+        aoff[i] = r < R ? (uint32_t)(((size_t)r * ld + c * 8) * 2) : kOOB;
+    }
+    // weights: this wave's 16 rows; lane -> row lane%16, K group lane/16
+    const int wrow = tile * WCH + wave * 16 + (lane & 15);
+    const int g8 = (lane >> 4) * 8;
+    const __amdgpu_buffer_rsrc_t rw0 = make_rsrc(kGateUp ? p1.sg : p2.sd, (size_t)nrows * ld);
+    const __amdgpu_buffer_rsrc_t rw1 = make_rsrc(kGateUp ? p1.su : p2.sd, (size_t)nrows * ld);
+    const uint32_t woff = wrow < nrows ? (uint32_t)(((size_t)wrow * ld + kbeg + g8) * 2) : kOOB;
+
+    const int nb = ceil_div(K, WKB);
+    constexpr int NW = kGateUp ? 2 : 1;  // weight matrices
+
+    auto issue_rows = [&](int b) {
+        unsigned char* st = smem + (b & 1) * WSTAGE + wave * WDMA * 1024;
+        const int k0 = b * WKB, lim = K - k0;
+#pragma unroll
+        for (int i = 0; i < WDMA; ++i)
+            load_lds16(ra, acol[i] < lim ? aoff[i] : kOOB, (uint32_t)k0 * 2u, st + i * 1024);
+    };
+    // weights of step j of batch b into w[.][j]
+    auto load_step = [&](int b, int j, u32x4 (&w)[NW][8]) {
+        const int k0 = b * WKB;
+        const uint32_t off = k0 + 32 * j + g8 < K ? woff + (uint32_t)(k0 + 32 * j) * 2u : kOOB;
+        w[0][j] = __builtin_amdgcn_raw_buffer_load_b128(rw0, off, 0, 0);
+        if constexpr (NW == 2) w[NW - 1][j] = __builtin_amdgcn_raw_buffer_load_b128(rw1, off, 0, 0);
+    };
+
+    // The K loop and epilogue for NF 16-token blocks (the rows R fill NF blocks).
+    auto run = [&](auto nf_tag) {
+        constexpr int NF = decltype(nf_tag)::value;
+        floatx4 acc[NW][NF];
+#pragma unroll
+        for (int m = 0; m < NW; ++m)
+#pragma unroll
+            for (int f = 0; f < NF; ++f) acc[m][f] = floatx4{0.f, 0.f, 0.f, 0.f};
+        // One weight buffer: once step j of batch b has been multiplied, its
+        // registers are reloaded with step j of batch b+1, so a batch's
+        // weights are requested one batch ahead.  The token fragments of step
+        // j+1 are read from LDS while step j multiplies.
+        u32x4 w[NW][8];
+        auto compute = [&](int b) {
+            const unsigned char* st = smem + (b & 1) * WSTAGE + (lane & 15) * WROWB;
+            bf16x8 xf[2][NF];
+            auto read = [&](int j, bf16x8 (&x)[NF]) {
+                const int c = (4 * j + (lane >> 4)) ^ (lane & 15);
+#pragma unroll
+                for (int f = 0; f < NF; ++f)
+                    x[f] = as_frag(*reinterpret_cast<const u32x4*>(st + f * 16 * WROWB + c * 16));
+            };
+            read(0, xf[0]);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                if (j + 1 < 8) read(j + 1, xf[(j + 1) & 1]);
+#pragma unroll
+                for (int f = 0; f < NF; ++f)
+#pragma unroll
+                    for (int m = 0; m < NW; ++m)
+                        acc[m][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_frag(w[m][j]), xf[j & 1][f],
+                                                                            acc[m][f], 0, 0, 0);
+                load_step(b + 1, j, w);  // past the last batch: zero-page loads
+                // order: next step's LDS reads, this step's MFMAs, the reloads
+                if (j + 1 < 8) __builtin_amdgcn_sched_group_barrier(0x100, NF, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, NF * NW, 0);
+                __builtin_amdgcn_sched_group_barrier(0x020, NW, 0);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        };
+        issue_rows(0);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) load_step(0, j, w);
+        for (int b = 0; b < nb; ++b) {
+            // batch b's rows are in LDS once every wave's row DMAs are done:
+            // only batch b's weight loads (issued after them) may be
+            // outstanding; this wave's LDS reads of batch b-1 are finished, so
+            // after the barrier batch b+1's rows may refill that stage
+            __builtin_amdgcn_s_waitcnt(waitcnt_vm(8 * NW) & kWaitLgkm0);
+            barrier_no_fence();
+            // unconditional, so that the compiler's count of outstanding loads
+            // stays exact: past the last batch the rows and weights are all
+            // masked and read the zero page
+            issue_rows(b + 1);
+            compute(b);
+        }
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // no DMA may outlive the workgroup's LDS
+
+        // D[m][n]: lane holds weight rows 4*(lane/16) + i of token n = lane%16
+        const int col = tile * WCH + wave * 16 + 4 * (lane >> 4);  // col % 4 == 0, nrows % 8 == 0
+        if (col >= nrows) return;
+#pragma unroll
+        for (int f = 0; f < NF; ++f) {
+            const int r = f * 16 + (lane & 15);
+            if (r >= R) continue;
+            uint32_t v[2];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                float lo, hi;
+                if constexpr (kGateUp) {
+                    lo = silu_fast(acc[0][f][2 * h]) * acc[1][f][2 * h];
+                    hi = silu_fast(acc[0][f][2 * h + 1]) * acc[1][f][2 * h + 1];
+                } else {
+                    lo = acc[0][f][2 * h];
+                    hi = acc[0][f][2 * h + 1];
+                }
+                v[h] = (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+            }
+            bf16_t* dst = kGateUp ? p1.Hs + (size_t)r * p1.Is + col
+                                  : p2.Os + ((size_t)split * p2.tokens + r) * p2.d + col;
+            *reinterpret_cast<uint2*>(dst) = make_uint2(v[0], v[1]);
+        }
+    };
+    if (R > 48) run(std::integral_constant<int, 4>{});
+    else if (R > 32) run(std::integral_constant<int, 3>{});
+    else if (R > 16) run(std::integral_constant<int, 2>{});
+    else run(std::integral_constant<int, 1>{});
+}
+
+__global__ __launch_bounds__(64 * DWAVES) void gemm1_decode_wide_kernel(Gemm1Params<bf16_t> p) {
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * WSTAGE];
+    wide_tile<true>(p, Gemm2Params<bf16_t>{}, smem);
+}
+
+__global__ __launch_bounds__(64 * DWAVES) void gemm2_decode_wide_kernel(Gemm2Params<bf16_t> p) {
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * WSTAGE];
+    wide_tile<false>(Gemm1Params<bf16_t>{}, p, smem);
+}
+
 hipError_t launch_gemm1_decode(const Gemm1Params<bf16_t>& p, int tiles, hipStream_t s) {
     if (tiles <= 0) return hipSuccess;
     gemm1_decode_kernel<<<tiles, 64 * DWAVES, 0, s>>>(p);
@@ -220,6 +402,19 @@ hipError_t launch_gemm1_decode(const Gemm1Params<bf16_t>& p, int tiles, hipStrea
 hipError_t launch_gemm2_decode(const Gemm2Params<bf16_t>& p, int tiles, hipStream_t s) {
     if (tiles <= 0) return hipSuccess;
     gemm2_decode_kernel<<<tiles, 64 * DWAVES, 0, s>>>(p);
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm1_decode_wide(const Gemm1Params<bf16_t>& p, hipStream_t s) {
+    if (p.tokens <= 0 || p.tokens > kDecodeMaxT || p.Is <= 0) return hipSuccess;
+    gemm1_decode_wide_kernel<<<ceil_div(p.Is, WCH), 64 * DWAVES, 0, s>>>(p);
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm2_decode_wide(const Gemm2Params<bf16_t>& p, hipStream_t s) {
+    if (p.tokens <= 0 || p.tokens > kDecodeMaxT || p.Is <= 0) return hipSuccess;
+    const int parts = p.ks2 > 0 ? ceil_div(p.Is, p.ks2) : 1;
+    gemm2_decode_wide_kernel<<<ceil_div(p.d, WCH) * parts, 64 * DWAVES, 0, s>>>(p);
     return hipGetLastError();
 }
 

@@ -124,6 +124,22 @@ def test_bf16_token_counts(T):
     check_y(y, ref, BF16_TOL)
 
 
+@pytest.mark.parametrize("T", [17, 31, 33, 49, 64])
+def test_bf16_shared_expert_wide_decode_tiles(T):
+    """17..64 tokens: the shared expert's GEMMs take 64-wide tiles.  d = 264
+    leaves a partial 256-deep K batch, I_s = 216 a partial channel tile and a
+    ragged last reduction chunk (chunks of I = 40 channels), and T a partial
+    16-token block."""
+    cfg, x, lg, w, s = mini_layer("wide%d" % T, 64, 264, 6, 40, 2, 216, config_id=72)
+    x, lg = x[:T], lg[:T]
+    g = gpu_layer_for(cfg, w, s, max_tokens=64)
+    for keep in (np.full(6, 40, np.int32), np.array([40, 0, 17, 8, 1, 33], np.int32)):
+        y, r = g.forward(x, lg, keep)
+        ref, rr = oracle_ref(cfg, x, lg, w, s, keep)
+        check_route(r, rr)
+        check_y(y, ref, BF16_TOL)
+
+
 def test_all_tokens_on_one_expert_and_ties():
     cfg, x, lg, w, s = mini_layer("skew", 257, 128, 8, 128, 2, 0, config_id=71)
     g = gpu_layer_for(cfg, w, s)
