@@ -504,9 +504,19 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return hip_fail(e, "plan upload");
     }
+    // 17..64 tokens: 64-wide weight-streaming tiles whose workgroup shares the
+    // token rows through LDS (16-wide tiles each re-read every row of their
+    // segment).  The shared expert (T rows) takes them from 17 tokens on; the
+    // routed experts once they average 8 rows (fewer rows leave little to
+    // share, and the wider tiles hold more LDS per compute unit).
+    const bool wide_sh = decode && T > kDecodeWideT;
+    const bool wide_rt = wide_sh && (long long)T * D.top_k >= 8LL * D.E;
+    const int dbn = wide_rt ? kDecWideBN : kDecBN;
     const TileShape ts = !bf16   ? TileShape{kF32BM, kF32BN, kF32BM, kF32BN, 0}
-                         : decode ? TileShape{kDecodeMaxT, kDecBN, kDecodeMaxT, kDecBN, ks2}
+                         : decode ? TileShape{kDecodeMaxT, dbn, kDecodeMaxT, dbn, ks2}
                                   : TileShape{kBigBM1, kBigBN1, kBigBM2, kBigBN2, ks2};
+    // the shared expert's tile width (its tiles are counted here, not by the dispatch)
+    const int sbn1 = wide_sh ? kDecWideBN : ts.bn1, sbn2 = wide_sh ? kDecWideBN : ts.bn2;
 
     hipError_t err;
     // grid upper bounds from host-known sizes: the routed part's from the
@@ -515,8 +525,8 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
     const long long rt2 = routed_row_tiles_ub(T, D.E, D.top_k, ts.bm2);
     const long long g1r = rt1 * ceil_div(D.I, ts.bn1);
     const long long g2r = rt2 * ceil_div(D.d, ts.bn2);
-    const long long g1s = has_shared ? (long long)ceil_div(T, ts.bm1) * ceil_div(D.I_shared, ts.bn1) : 0;
-    const long long g2s = has_shared ? (long long)ceil_div(T, ts.bm2) * ceil_div(D.d, ts.bn2) * parts : 0;
+    const long long g1s = has_shared ? (long long)ceil_div(T, ts.bm1) * ceil_div(D.I_shared, sbn1) : 0;
+    const long long g2s = has_shared ? (long long)ceil_div(T, ts.bm2) * ceil_div(D.d, sbn2) * parts : 0;
     if (g1r + g1s > 0x7fffffffLL || g2r + g2s > 0x7fffffffLL) return fail(FLEXMOE_ESHAPE, "tile grid too large");
 
     // The two GEMMs over one part of the tile list (n1, n2 workgroups), on
@@ -525,8 +535,7 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
         const bool sh = part == kPartShared;
         const int k1 = sh ? FLEXMOE_K_GATE_UP_SHARED : FLEXMOE_K_GATE_UP;
         const int k2 = sh ? FLEXMOE_K_DOWN_SHARED : FLEXMOE_K_DOWN;
-        // the shared expert at 17..64 tokens: 64-wide tiles sharing the token rows
-        const bool wide = decode && sh && T > kDecodeWideT;
+        const bool wide = sh ? wide_sh : wide_rt;
         hipError_t e;
         if (bf16) {
             Gemm1Params<bf16_t> p1{(const bf16_t*)x, (const bf16_t*)w_gate_r, (const bf16_t*)w_up_r,
@@ -543,7 +552,7 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
             }
             {
                 KernelTimer kt(k1, st);
-                e = wide         ? launch_gemm1_decode_wide(p1, st)
+                e = wide         ? launch_gemm1_decode_wide(p1, (int)n1, st)
                     : decode     ? launch_gemm1_decode(p1, (int)n1, st)
                     : train == 1 ? launch_gemm1_big_train(p1, (int)n1, st)
                     : train == 2 ? launch_gemm1_big_train_rm(p1, (int)n1, st)
@@ -559,7 +568,7 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
                                    seg_hi, (int)g2s, clipped};
             {
                 KernelTimer kt(k2, st);
-                e = wide     ? launch_gemm2_decode_wide(p2, st)
+                e = wide     ? launch_gemm2_decode_wide(p2, (int)n2, st)
                     : decode ? launch_gemm2_decode(p2, (int)n2, st)
                              : launch_gemm2_big(p2, (int)n2, st);
             }

@@ -213,81 +213,119 @@ __global__ __launch_bounds__(64 * DWAVES) void gemm2_decode_kernel(Gemm2Params<b
     }
 }
 
-// ---- The shared expert at more than kDecodeWideT tokens: wide tiles ------
+// ---- More than kDecodeWideT tokens: wide tiles ---------------------------
 //
-// With 17..64 tokens the 16-channel tiles above read every token row once
-// per 16 weight rows -- two to four times the weight bytes, from L2, one
-// 16-token block after another.  The shared expert's GEMMs then take tiles
-// of 64 channels (gate/up) or 64 output columns (down): wave w owns 16 of
-// them over the whole reduction, and the four waves share the token rows
-// through LDS.  Per 256-deep K batch the workgroup copies rows [64][256]
-// into LDS once (buffer_load ... lds); the next batch's rows and weights are
-// in flight while the current batch is multiplied.  LDS row r keeps its 16-B
-// chunk c at position c ^ (r & 15): the 16 lanes of one fragment read (16
-// rows, one chunk) then cover all 64 banks.
+// With 17..64 tokens the 16-channel tiles above read a segment's token rows
+// once per 16 weight rows -- for the shared expert two to four times the
+// weight bytes, from L2, one 16-token block after another.  The GEMMs then
+// take tiles of 64 channels (gate/up) or 64 output columns (down): wave w
+// owns 16 of them over the whole reduction, and the four waves share the
+// segment's token rows through LDS.  Per 256-deep K batch the workgroup
+// copies the rows into LDS once (buffer_load ... lds; as many 16-row blocks
+// as T needs, so small batches keep more workgroups per compute unit); the
+// next batch's rows and weights are in flight while the current batch is
+// multiplied.  LDS row r keeps its 16-B chunk c at position c ^ (r & 15):
+// the 16 lanes of one fragment read (16 rows, one chunk) then cover all 64
+// banks.
 namespace {
-constexpr int WCH = 64;                            // channels / output columns per wide tile
-constexpr int WKB = 256;                           // K per batch
-constexpr int WROWB = WKB * 2;                     // LDS bytes per staged row
-constexpr int WSTAGE = kDecodeMaxT * WROWB;        // one batch of every row: 32 KB
-constexpr int WDMA = WSTAGE / (16 * 64 * DWAVES);  // DMA instructions per lane per batch
-static_assert(2 * WROWB == 16 * 64 && WDMA * DWAVES * 16 * 64 == WSTAGE,
-              "a DMA instruction fills two staged rows; the waves fill the stage");
+constexpr int WCH = kDecWideBN;         // channels / output columns per wide tile
+constexpr int WKB = 256;                // K per batch
+constexpr int WSTEPS = WKB / 32;        // MFMA steps per batch
+constexpr int WROWB = WKB * 2;          // LDS bytes per staged row
+constexpr int WCHUNKS = WROWB / 16;     // 16-byte chunks per staged row
+constexpr int WRPI = 1024 / WROWB;      // staged rows one DMA instruction (64 lanes x 16 B) fills
+static_assert(WCHUNKS % 16 == 0 && 1024 % WROWB == 0,
+              "the chunk swizzle XORs with 4 row bits; a DMA instruction fills whole rows");
 }  // namespace
 
-template <bool kGateUp>
+// 16-row blocks staged per batch for a launch over T tokens (every segment
+// has at most T rows) and the dynamic LDS that takes: two stages.
+__host__ __device__ __forceinline__ int wide_blocks(int tokens) { return ceil_div(min(tokens, kDecodeMaxT), 16); }
+__host__ __device__ __forceinline__ size_t wide_lds_bytes(int tokens) {
+    return (size_t)2 * wide_blocks(tokens) * 16 * WROWB;
+}
+
+// SB: 16-row blocks staged per batch, wide_blocks(T) (a template parameter:
+// a fixed count of row copies keeps the compiler's count of outstanding loads
+// exact).
+template <bool kGateUp, int SB>
 __device__ __forceinline__ void wide_tile(const Gemm1Params<bf16_t>& p1, const Gemm2Params<bf16_t>& p2,
                                           unsigned char* smem) {
     using namespace mfma;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
-    const int R = kGateUp ? p1.tokens : p2.tokens;      // token rows, <= kDecodeMaxT
-    const int nrows = kGateUp ? p1.Is : p2.d;           // weight rows: channels or output columns
-    const int ntiles = ceil_div(nrows, WCH);
-    int tile = blockIdx.x, split = 0;
-    if (!kGateUp) {
-        split = tile / ntiles;
-        tile -= split * ntiles;
+    int s, local;  // one row tile per segment (rows <= 64): `local` numbers the segment's 64-wide tiles
+    SegMeta sm;
+    if (!(kGateUp ? tile_of(p1, blockIdx.x, s, sm, local) : tile_of(p2, blockIdx.x, s, sm, local))) return;
+    const bool shared = sm.e < 0;
+    const int R = sm.rows;  // token rows, <= kDecodeMaxT
+    const int d = kGateUp ? p1.d : p2.d;
+    // weight rows of the tile: channels c < kg (gate/up) or output columns n < d (down)
+    const int nrows = kGateUp ? sm.kg : d;
+    int tile = local, split = 0;
+    if (!kGateUp) {  // the shared expert's split reduction: chunk `split`
+        const int nt = ceil_div(d, WCH);
+        split = local / nt;
+        tile = local - split * nt;
     }
-    // the reduction: all of d (gate/up) or channel chunk `split` of I_s (down)
-    const int ks = kGateUp ? p1.d : (p2.ks2 > 0 ? p2.ks2 : p2.Is);
-    const int kbeg = kGateUp ? 0 : split * ks;
-    if (kbeg >= (kGateUp ? p1.d : p2.Is)) return;  // workgroup-uniform
-    const int K = kGateUp ? p1.d : min(p2.Is - kbeg, ks);
-    const int ld = kGateUp ? p1.d : p2.Is;  // row stride of the token rows and of the weights
+    // the reduction: all of d (gate/up), the kept channels (routed down) or
+    // channel chunk `split` of I_s (shared down)
+    const int ks = kGateUp ? d : shared ? (p2.ks2 > 0 ? p2.ks2 : p2.Is) : sm.kg;
+    const int kbeg = split * ks;
+    const int K = kGateUp ? d : shared ? min(p2.Is - kbeg, ks) : sm.kg;
+    if (K <= 0) return;  // workgroup-uniform
 
-    // token rows: x [T][d] or the shared activations Hs [T][I_s] from kbeg
-    const bf16_t* A = kGateUp ? p1.x : p2.Hs + kbeg;
-    const __amdgpu_buffer_rsrc_t ra = make_rsrc(A, (size_t)R * ld - kbeg);
-    // DMA instruction i of this wave fills staged rows 2*(wave*WDMA + i) and
-    // the next; lane -> row lane/32, LDS chunk lane%32
-    uint32_t aoff[WDMA];
-    int acol[WDMA];
+    // token rows: x [T][d] (routed rows gathered through perm), the routed
+    // activations H [A][I] of the segment, or the shared Hs [T][I_s] from kbeg
+    const int lda = kGateUp ? d : shared ? p2.Is : p2.I;
+    const bf16_t* A = kGateUp ? p1.x : shared ? p2.Hs + kbeg : p2.H + (size_t)sm.row0 * p2.I;
+    const size_t aext = kGateUp ? (size_t)p1.tokens * d : (size_t)R * lda - kbeg;
+    const __amdgpu_buffer_rsrc_t ra = make_rsrc(A, aext);
+    // Staged rows: SB 16-row blocks; each wave issues NDMA DMA instructions
+    // per batch, instruction i filling staged rows WRPI*(wave*NDMA + i) ..
+    // +WRPI; lane -> row lane/WCHUNKS, LDS chunk lane%WCHUNKS.
+    constexpr int stage_bytes = SB * 16 * WROWB;
+    constexpr int NDMA = SB * 16 / (DWAVES * WRPI);
+    static_assert(NDMA * DWAVES * WRPI == SB * 16, "the waves' DMAs fill the stage");
+    uint32_t aoff[NDMA];
+    int acol[NDMA];
 #pragma unroll
-    for (int i = 0; i < WDMA; ++i) {
-        const int r = 2 * (wave * WDMA + i) + (lane >> 5);
-        const int c = (lane & 31) ^ (r & 15);
+    for (int i = 0; i < NDMA; ++i) {
+        const int r = WRPI * (wave * NDMA + i) + lane / WCHUNKS;
+        const int c = (lane % WCHUNKS) ^ (r & 15);
         acol[i] = c * 8;
-        aoff[i] = r < R ? (uint32_t)(((size_t)r * ld + c * 8) * 2) : kOOB;
+        aoff[i] = kOOB;
+        if (r < R) {
+            int src = r;
+            if (kGateUp && !shared)
+                src = (int)min((unsigned)(p1.perm[sm.row0 + r] / p1.top_k), (unsigned)(p1.tokens - 1));
+            aoff[i] = (uint32_t)(((size_t)src * lda + c * 8) * 2);
+        }
     }
     // weights: this wave's 16 rows; lane -> row lane%16, K group lane/16
+    const RoutedWeights rw = kGateUp ? (shared ? RoutedWeights{0, p1.Is, 0} : routed_weights(p1, sm))
+                                     : (shared ? RoutedWeights{0, 0, p2.Is} : routed_weights(p2, sm));
+    const int ldw = kGateUp ? d : rw.ldd;  // weight row stride
+    const bf16_t* W0 = kGateUp ? (shared ? p1.sg : p1.wg + rw.base) : (shared ? p2.sd : p2.wd + rw.base);
+    const bf16_t* W1 = kGateUp ? (shared ? p1.su : p1.wu + rw.base) : W0;
+    const size_t wext = kGateUp ? (size_t)rw.rows * d : (size_t)d * ldw;
+    const __amdgpu_buffer_rsrc_t rw0 = make_rsrc(W0, wext);
+    const __amdgpu_buffer_rsrc_t rw1 = make_rsrc(W1, wext);
     const int wrow = tile * WCH + wave * 16 + (lane & 15);
     const int g8 = (lane >> 4) * 8;
-    const __amdgpu_buffer_rsrc_t rw0 = make_rsrc(kGateUp ? p1.sg : p2.sd, (size_t)nrows * ld);
-    const __amdgpu_buffer_rsrc_t rw1 = make_rsrc(kGateUp ? p1.su : p2.sd, (size_t)nrows * ld);
-    const uint32_t woff = wrow < nrows ? (uint32_t)(((size_t)wrow * ld + kbeg + g8) * 2) : kOOB;
+    const uint32_t woff = wrow < nrows ? (uint32_t)(((size_t)wrow * ldw + kbeg + g8) * 2) : kOOB;
 
     const int nb = ceil_div(K, WKB);
     constexpr int NW = kGateUp ? 2 : 1;  // weight matrices
 
     auto issue_rows = [&](int b) {
-        unsigned char* st = smem + (b & 1) * WSTAGE + wave * WDMA * 1024;
+        unsigned char* st = smem + (b & 1) * stage_bytes + wave * NDMA * 1024;
         const int k0 = b * WKB, lim = K - k0;
 #pragma unroll
-        for (int i = 0; i < WDMA; ++i)
+        for (int i = 0; i < NDMA; ++i)
             load_lds16(ra, acol[i] < lim ? aoff[i] : kOOB, (uint32_t)k0 * 2u, st + i * 1024);
     };
     // weights of step j of batch b into w[.][j]
-    auto load_step = [&](int b, int j, u32x4 (&w)[NW][8]) {
+    auto load_step = [&](int b, int j, u32x4 (&w)[NW][WSTEPS]) {
         const int k0 = b * WKB;
         const uint32_t off = k0 + 32 * j + g8 < K ? woff + (uint32_t)(k0 + 32 * j) * 2u : kOOB;
         w[0][j] = __builtin_amdgcn_raw_buffer_load_b128(rw0, off, 0, 0);
@@ -306,9 +344,9 @@ __device__ __forceinline__ void wide_tile(const Gemm1Params<bf16_t>& p1, const G
         // registers are reloaded with step j of batch b+1, so a batch's
         // weights are requested one batch ahead.  The token fragments of step
         // j+1 are read from LDS while step j multiplies.
-        u32x4 w[NW][8];
+        u32x4 w[NW][WSTEPS];
         auto compute = [&](int b) {
-            const unsigned char* st = smem + (b & 1) * WSTAGE + (lane & 15) * WROWB;
+            const unsigned char* st = smem + (b & 1) * stage_bytes + (lane & 15) * WROWB;
             bf16x8 xf[2][NF];
             auto read = [&](int j, bf16x8 (&x)[NF]) {
                 const int c = (4 * j + (lane >> 4)) ^ (lane & 15);
@@ -318,8 +356,8 @@ __device__ __forceinline__ void wide_tile(const Gemm1Params<bf16_t>& p1, const G
             };
             read(0, xf[0]);
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                if (j + 1 < 8) read(j + 1, xf[(j + 1) & 1]);
+            for (int j = 0; j < WSTEPS; ++j) {
+                if (j + 1 < WSTEPS) read(j + 1, xf[(j + 1) & 1]);
 #pragma unroll
                 for (int f = 0; f < NF; ++f)
 #pragma unroll
@@ -328,7 +366,7 @@ __device__ __forceinline__ void wide_tile(const Gemm1Params<bf16_t>& p1, const G
                                                                             acc[m][f], 0, 0, 0);
                 load_step(b + 1, j, w);  // past the last batch: zero-page loads
                 // order: next step's LDS reads, this step's MFMAs, the reloads
-                if (j + 1 < 8) __builtin_amdgcn_sched_group_barrier(0x100, NF, 0);
+                if (j + 1 < WSTEPS) __builtin_amdgcn_sched_group_barrier(0x100, NF, 0);
                 __builtin_amdgcn_sched_group_barrier(0x008, NF * NW, 0);
                 __builtin_amdgcn_sched_group_barrier(0x020, NW, 0);
                 __builtin_amdgcn_sched_barrier(0);
@@ -336,13 +374,13 @@ __device__ __forceinline__ void wide_tile(const Gemm1Params<bf16_t>& p1, const G
         };
         issue_rows(0);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) load_step(0, j, w);
+        for (int j = 0; j < WSTEPS; ++j) load_step(0, j, w);
         for (int b = 0; b < nb; ++b) {
             // batch b's rows are in LDS once every wave's row DMAs are done:
             // only batch b's weight loads (issued after them) may be
             // outstanding; this wave's LDS reads of batch b-1 are finished, so
             // after the barrier batch b+1's rows may refill that stage
-            __builtin_amdgcn_s_waitcnt(waitcnt_vm(8 * NW) & kWaitLgkm0);
+            __builtin_amdgcn_s_waitcnt(waitcnt_vm(WSTEPS * NW) & kWaitLgkm0);
             barrier_no_fence();
             // unconditional, so that the compiler's count of outstanding loads
             // stays exact: past the last batch the rows and weights are all
@@ -352,9 +390,15 @@ __device__ __forceinline__ void wide_tile(const Gemm1Params<bf16_t>& p1, const G
         }
         __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // no DMA may outlive the workgroup's LDS
 
-        // D[m][n]: lane holds weight rows 4*(lane/16) + i of token n = lane%16
-        const int col = tile * WCH + wave * 16 + 4 * (lane >> 4);  // col % 4 == 0, nrows % 8 == 0
-        if (col >= nrows) return;
+        // D[m][n]: lane holds weight rows 4*(lane/16) + i of token n = lane%16.
+        // gate/up writes channels below kk8 = the GEMM width rounded up to 8
+        // (the down GEMM reads whole 16-byte chunks), zeros from kk on; col
+        // and kk8 are multiples of 4 and 8, so a lane's run of 4 is wholly
+        // inside or outside.
+        const int col = tile * WCH + wave * 16 + 4 * (lane >> 4);
+        const int ldh = kGateUp ? (shared ? p1.Is : p1.I) : d;
+        const int lim = kGateUp ? min((sm.kg + 7) & ~7, ldh) : d;  // d % 8 == 0
+        if (col >= lim) return;
 #pragma unroll
         for (int f = 0; f < NF; ++f) {
             const int r = f * 16 + (lane & 15);
@@ -364,33 +408,41 @@ __device__ __forceinline__ void wide_tile(const Gemm1Params<bf16_t>& p1, const G
             for (int h = 0; h < 2; ++h) {
                 float lo, hi;
                 if constexpr (kGateUp) {
-                    lo = silu_fast(acc[0][f][2 * h]) * acc[1][f][2 * h];
-                    hi = silu_fast(acc[0][f][2 * h + 1]) * acc[1][f][2 * h + 1];
+                    lo = col + 2 * h < sm.kk ? silu_fast(acc[0][f][2 * h]) * acc[1][f][2 * h] : 0.f;
+                    hi = col + 2 * h + 1 < sm.kk ? silu_fast(acc[0][f][2 * h + 1]) * acc[1][f][2 * h + 1] : 0.f;
                 } else {
                     lo = acc[0][f][2 * h];
                     hi = acc[0][f][2 * h + 1];
                 }
                 v[h] = (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
             }
-            bf16_t* dst = kGateUp ? p1.Hs + (size_t)r * p1.Is + col
-                                  : p2.Os + ((size_t)split * p2.tokens + r) * p2.d + col;
+            bf16_t* dst;
+            if constexpr (kGateUp)
+                dst = (shared ? p1.Hs : p1.H + (size_t)sm.row0 * p1.I) + (size_t)r * ldh + col;
+            else
+                dst = (shared ? p2.Os + (size_t)split * p2.tokens * d : p2.O + (size_t)sm.row0 * d) +
+                      (size_t)r * d + col;
             *reinterpret_cast<uint2*>(dst) = make_uint2(v[0], v[1]);
         }
     };
-    if (R > 48) run(std::integral_constant<int, 4>{});
-    else if (R > 32) run(std::integral_constant<int, 3>{});
-    else if (R > 16) run(std::integral_constant<int, 2>{});
+    // R <= tokens, so NF = ceil(R/16) <= SB
+    if (SB >= 4 && R > 48) run(std::integral_constant<int, SB >= 4 ? 4 : 1>{});
+    else if (SB >= 3 && R > 32) run(std::integral_constant<int, SB >= 3 ? 3 : 1>{});
+    else if (SB >= 2 && R > 16) run(std::integral_constant<int, SB >= 2 ? 2 : 1>{});
     else run(std::integral_constant<int, 1>{});
 }
 
+// LDS: wide_lds_bytes(tokens), dynamic; SB = wide_blocks(tokens).
+template <int SB>
 __global__ __launch_bounds__(64 * DWAVES) void gemm1_decode_wide_kernel(Gemm1Params<bf16_t> p) {
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * WSTAGE];
-    wide_tile<true>(p, Gemm2Params<bf16_t>{}, smem);
+    extern __shared__ __attribute__((aligned(1024))) unsigned char wide_smem[];
+    wide_tile<true, SB>(p, Gemm2Params<bf16_t>{}, wide_smem);
 }
 
+template <int SB>
 __global__ __launch_bounds__(64 * DWAVES) void gemm2_decode_wide_kernel(Gemm2Params<bf16_t> p) {
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * WSTAGE];
-    wide_tile<false>(Gemm1Params<bf16_t>{}, p, smem);
+    extern __shared__ __attribute__((aligned(1024))) unsigned char wide_smem[];
+    wide_tile<false, SB>(Gemm1Params<bf16_t>{}, p, wide_smem);
 }
 
 hipError_t launch_gemm1_decode(const Gemm1Params<bf16_t>& p, int tiles, hipStream_t s) {
@@ -405,16 +457,27 @@ hipError_t launch_gemm2_decode(const Gemm2Params<bf16_t>& p, int tiles, hipStrea
     return hipGetLastError();
 }
 
-hipError_t launch_gemm1_decode_wide(const Gemm1Params<bf16_t>& p, hipStream_t s) {
-    if (p.tokens <= 0 || p.tokens > kDecodeMaxT || p.Is <= 0) return hipSuccess;
-    gemm1_decode_wide_kernel<<<ceil_div(p.Is, WCH), 64 * DWAVES, 0, s>>>(p);
+hipError_t launch_gemm1_decode_wide(const Gemm1Params<bf16_t>& p, int tiles, hipStream_t s) {
+    if (tiles <= 0 || p.tokens <= 0 || p.tokens > kDecodeMaxT) return hipSuccess;
+    const size_t lds = wide_lds_bytes(p.tokens);
+    switch (wide_blocks(p.tokens)) {
+        case 1: gemm1_decode_wide_kernel<1><<<tiles, 64 * DWAVES, lds, s>>>(p); break;
+        case 2: gemm1_decode_wide_kernel<2><<<tiles, 64 * DWAVES, lds, s>>>(p); break;
+        case 3: gemm1_decode_wide_kernel<3><<<tiles, 64 * DWAVES, lds, s>>>(p); break;
+        default: gemm1_decode_wide_kernel<4><<<tiles, 64 * DWAVES, lds, s>>>(p); break;
+    }
     return hipGetLastError();
 }
 
-hipError_t launch_gemm2_decode_wide(const Gemm2Params<bf16_t>& p, hipStream_t s) {
-    if (p.tokens <= 0 || p.tokens > kDecodeMaxT || p.Is <= 0) return hipSuccess;
-    const int parts = p.ks2 > 0 ? ceil_div(p.Is, p.ks2) : 1;
-    gemm2_decode_wide_kernel<<<ceil_div(p.d, WCH) * parts, 64 * DWAVES, 0, s>>>(p);
+hipError_t launch_gemm2_decode_wide(const Gemm2Params<bf16_t>& p, int tiles, hipStream_t s) {
+    if (tiles <= 0 || p.tokens <= 0 || p.tokens > kDecodeMaxT) return hipSuccess;
+    const size_t lds = wide_lds_bytes(p.tokens);
+    switch (wide_blocks(p.tokens)) {
+        case 1: gemm2_decode_wide_kernel<1><<<tiles, 64 * DWAVES, lds, s>>>(p); break;
+        case 2: gemm2_decode_wide_kernel<2><<<tiles, 64 * DWAVES, lds, s>>>(p); break;
+        case 3: gemm2_decode_wide_kernel<3><<<tiles, 64 * DWAVES, lds, s>>>(p); break;
+        default: gemm2_decode_wide_kernel<4><<<tiles, 64 * DWAVES, lds, s>>>(p); break;
+    }
     return hipGetLastError();
 }
 

@@ -122,8 +122,9 @@ constexpr int kF32BM = 64, kF32BN = 64;
 constexpr int kBigBM1 = 256, kBigBN1 = 128, kBigBM2 = 256, kBigBN2 = 256;
 constexpr int kDecodeMaxT = 64;     // T at or below which the weight-streaming kernels run
 constexpr int kDecBN = 16;          // their channels / output columns per tile
-constexpr int kDecodeWideT = 16;    // above this many tokens the shared expert's weight-streaming
-                                    // GEMMs take 64-wide tiles (launch_gemm*_decode_wide)
+constexpr int kDecodeWideT = 16;    // above this many tokens the weight-streaming GEMMs take
+constexpr int kDecWideBN = 64;      // tiles of this many channels / output columns whose token
+                                    // rows are shared through LDS (launch_gemm*_decode_wide)
 
 __global__ void route_kernel(const float* logits, int T, int E, int k, int norm_topk, int32_t* idx,
                              float* wts, int32_t* blockcnt, int NB);
@@ -155,9 +156,9 @@ hipError_t launch_gemm1_big(const Gemm1Params<bf16_t>& p, int grid, hipStream_t 
 hipError_t launch_gemm2_big(const Gemm2Params<bf16_t>& p, int grid, hipStream_t s);
 hipError_t launch_gemm1_decode(const Gemm1Params<bf16_t>& p, int tiles, hipStream_t s);
 hipError_t launch_gemm2_decode(const Gemm2Params<bf16_t>& p, int tiles, hipStream_t s);
-// The shared expert alone at kDecodeWideT < T <= kDecodeMaxT (grid from p).
-hipError_t launch_gemm1_decode_wide(const Gemm1Params<bf16_t>& p, hipStream_t s);
-hipError_t launch_gemm2_decode_wide(const Gemm2Params<bf16_t>& p, hipStream_t s);
+// kDecodeWideT < T <= kDecodeMaxT: tiles of kDecWideBN channels / output columns.
+hipError_t launch_gemm1_decode_wide(const Gemm1Params<bf16_t>& p, int tiles, hipStream_t s);
+hipError_t launch_gemm2_decode_wide(const Gemm2Params<bf16_t>& p, int tiles, hipStream_t s);
 hipError_t launch_gemm1_f32(const Gemm1Params<float>& p, int grid, hipStream_t s);
 hipError_t launch_gemm2_f32(const Gemm2Params<float>& p, int grid, hipStream_t s);
 hipError_t launch_combine(const void* O, const void* Os, const int32_t* pos, const float* wts,

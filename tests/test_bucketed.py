@@ -29,6 +29,8 @@ CASES = [
     ("b_prefill", 300, 256, 8, 320, 2, 0, synth.BF16, 1),
     ("b_prefill_shared", 200, 512, 16, 192, 4, 256, synth.BF16, 0),
     ("b_decode", 8, 256, 16, 200, 4, 128, synth.BF16, 0),
+    # 17..64 tokens: 64-wide weight-streaming tiles
+    ("b_decode48", 48, 264, 12, 200, 4, 136, synth.BF16, 1),
 ]
 
 
