@@ -19,16 +19,21 @@
 namespace flexmoe {
 
 // Routing order: larger logit first, equal logits -> lower id, NaN last.
-__device__ __forceinline__ bool route_before(float va, int ia, float vb, int ib) {
-    const bool na = __builtin_isnan(va), nb = __builtin_isnan(vb);
-    if (na != nb) return nb;
-    if (!na && va != vb) return va > vb;
-    return ia < ib;
+// route_key maps a logit to an unsigned key with the same order: the bits of
+// a non-negative float with the sign bit set, those of a negative float
+// inverted, -0 as +0 (they compare equal), and 0 for NaN (below -inf, whose
+// key is 0x007fffff).  Expert a then comes before expert b exactly when
+// key_a > key_b, or key_a == key_b and a < b.
+__device__ __forceinline__ uint32_t route_key(float v) {
+    uint32_t u = __float_as_uint(v);
+    u = u == 0x80000000u ? 0u : u;
+    const uint32_t k = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+    return __builtin_isnan(v) ? 0u : k;
 }
 
-// Per-wave LDS scratch of route_token: the token's logits and the k slots.
+// Per-wave LDS scratch of route_token: the token's keys and the k slots.
 struct RouteScratch {
-    float v[kMaxExperts];
+    uint32_t key[kMaxExperts];
     float slot_v[kMaxTopK];
     int slot_id[kMaxTopK];
 };
@@ -44,41 +49,55 @@ __device__ __forceinline__ void load_logits(const float* __restrict__ l, int E, 
     }
 }
 
+// Ranks of this lane's experts lane + 64*q (q < NQ) among the E8 keys in LDS:
+// the number of experts ordered before each.  Every lane reads the same keys
+// (an LDS broadcast); two compares per pair, no branches.
+template <int NQ>
+__device__ __forceinline__ void rank_keys(const RouteScratch& rs, const uint32_t (&mk)[4], int E8, int lane,
+                                          int (&rank)[4]) {
+    for (int j0 = 0; j0 < E8; j0 += 8) {
+        const uint4 k0 = *reinterpret_cast<const uint4*>(&rs.key[j0]);
+        const uint4 k1 = *reinterpret_cast<const uint4*>(&rs.key[j0 + 4]);
+        const uint32_t o[8] = {k0.x, k0.y, k0.z, k0.w, k1.x, k1.y, k1.z, k1.w};
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const int me = lane + 64 * q;
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                rank[q] += (o[i] > mk[q]) + (o[i] == mk[q] && j0 + i < me);
+        }
+    }
+}
+
 // One wave routes one token whose logits are in v (load_logits): lane j < k
 // returns the j-th selected expert and its router weight.  Each lane ranks
 // its (up to four) experts by counting the experts ordered before them under
-// the total order above, reading the token's logits back from LDS (all lanes
-// read the same address: a broadcast).  Ranks are a permutation of 0..E-1,
-// so the expert of rank j < k fills slot j -- the top-k in order, with no
-// chain of cross-lane steps.  The LDS row is padded to a multiple of 8 with
-// NaN: a NaN whose id is at or past E is ordered after every expert, so the
-// padding never counts.  Softmax over all E experts, shifted by the largest
-// logit; with norm_topk the k weights are divided by their sum.
+// the order above, reading the token's keys back from LDS.  Ranks are a
+// permutation of 0..E-1, so the expert of rank j < k fills slot j -- the
+// top-k in order, with no chain of cross-lane steps.  The LDS row is padded
+// to a multiple of 8 with key 0 and ids at or past E, which no expert counts.
+// Softmax over all E experts, shifted by the largest logit; with norm_topk
+// the k weights are divided by their sum.
 __device__ __forceinline__ void route_token(const float (&v)[4], int E, int k, int norm_topk, int lane,
                                             RouteScratch& rs, int& my_id, float& my_w) {
     const int nq = ceil_div(E, 64);         // wave-uniform
     const int E8 = ceil_div(E, 8) * 8;      // <= kMaxExperts
+    uint32_t mk[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
         const int e = lane + 64 * q;
-        if (e < E) rs.v[e] = v[q];
-        else if (e < E8) rs.v[e] = __builtin_nanf("");
+        mk[q] = route_key(v[q]);
+        if (e < E) rs.key[e] = mk[q];
+        else if (e < E8) rs.key[e] = 0u;
     }
     __builtin_amdgcn_wave_barrier();
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
     int rank[4] = {0, 0, 0, 0};
-    for (int j0 = 0; j0 < E8; j0 += 8) {
-        const float4 o0 = *reinterpret_cast<const float4*>(&rs.v[j0]);
-        const float4 o1 = *reinterpret_cast<const float4*>(&rs.v[j0 + 4]);
-        const float o[8] = {o0.x, o0.y, o0.z, o0.w, o1.x, o1.y, o1.z, o1.w};
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            if (q >= nq) break;
-            int c = 0;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) c += route_before(o[i], j0 + i, v[q], lane + 64 * q) ? 1 : 0;
-            rank[q] += c;
-        }
+    switch (nq) {
+        case 1: rank_keys<1>(rs, mk, E8, lane, rank); break;
+        case 2: rank_keys<2>(rs, mk, E8, lane, rank); break;
+        case 3: rank_keys<3>(rs, mk, E8, lane, rank); break;
+        default: rank_keys<4>(rs, mk, E8, lane, rank); break;
     }
 #pragma unroll
     for (int q = 0; q < 4; ++q) {

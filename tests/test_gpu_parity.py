@@ -149,6 +149,15 @@ def test_all_tokens_on_one_expert_and_ties():
         "quantised_ties": np.round(lg * 2) / 2,
         "all_equal": np.zeros_like(lg),
         "nan_logit": np.where(np.arange(lg.shape[1])[None, :] == 3, np.float32(np.nan), lg),
+        # -0 and +0 compare equal: every token ties everywhere, so experts 0 and 1
+        "signed_zeros": np.where((np.arange(lg.shape[1])[None, :] + np.arange(lg.shape[0])[:, None]) % 2 == 0,
+                                 np.float32(-0.0), np.float32(0.0)).astype(np.float32),
+        # +inf first, -inf after every finite logit, NaN after -inf
+        "infinities": np.where(np.arange(lg.shape[1])[None, :] == 2, np.float32(-np.inf),
+                               np.where((np.arange(lg.shape[1])[None, :] == 5) & (np.arange(lg.shape[0])[:, None] % 2 == 0),
+                                        np.float32(np.inf),
+                                        np.where((np.arange(lg.shape[1])[None, :] == 6)
+                                                 & (np.arange(lg.shape[0])[:, None] % 3 == 0), np.float32(np.nan), lg))),
     }
     for name, l2 in cases.items():
         say("routing case", name)
@@ -158,7 +167,7 @@ def test_all_tokens_on_one_expert_and_ties():
         np.testing.assert_array_equal(r["topk_idx"], rr["idx"])
         np.testing.assert_array_equal(r["perm"], rr["perm"])
         np.testing.assert_array_equal(r["pos"], rr["pos"])
-        if name != "nan_logit":
+        if name not in ("nan_logit", "infinities"):  # weights of those rows are not finite
             check_route(r, rr)
             check_y(y, ref, BF16_TOL)
 
