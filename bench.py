@@ -45,6 +45,7 @@ PEAK_F32_TFLOPS = 157.3      # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
 RIDGE = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
 DECODE_MAX_T = 64            # the library runs its weight-streaming GEMMs for T <= 64 (bf16)
+DECODE_WIDE_T = 16           # above this many tokens with 64-wide tiles (the routed experts once T*k >= 8*E)
 
 
 def log(*a):
@@ -589,8 +590,13 @@ def main():
     roof["traffic"] = load_traffic(args.workload, wl.T, "+".join(keep_names))
     if not bf16:
         roof["kernel"] = "gate_up GEMM (gemm1_f32_kernel)"
-    elif wl.T <= DECODE_MAX_T:
+    elif wl.T <= DECODE_WIDE_T:
         roof["kernel"] = "gate_up GEMM (gemm1_decode_kernel)"
+    elif wl.T <= DECODE_MAX_T and wl.T * cfg.top_k >= 8 * cfg.E:
+        roof["kernel"] = "gate_up GEMM (gemm1_decode_wide_kernel)"
+    elif wl.T <= DECODE_MAX_T:
+        roof["kernel"] = ("gate_up GEMM (gemm1_decode_kernel for the routed experts, "
+                          "gemm1_decode_wide_kernel for the shared expert)")
     else:
         roof["kernel"] = "gate_up GEMM (gemm1_big_kernel)"
     roof["avg_launch_ms"] = gu_avg
