@@ -55,8 +55,9 @@ def log(*a):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=100,
+                    help="untimed steps first (the clocks and caches settle over ~100 steps)")
     ap.add_argument("--workload", default="qwen15_moe_a27b")
     ap.add_argument("--table", default=None, help="keep table (default: the workload's own, else kept100)")
     ap.add_argument("--decode-T", type=int, default=1, help="tokens per step of the decode workload")

@@ -48,6 +48,57 @@ __device__ __forceinline__ float4 combine_cols(const OutT* __restrict__ O, const
     return acc;
 }
 
+// bf16: columns n .. n+7 of token t (16-byte loads and stores), the same
+// arithmetic as combine_cols per column.
+__device__ __forceinline__ void combine_cols8(const bf16_t* __restrict__ O, const bf16_t* __restrict__ Os,
+                                              const int32_t* __restrict__ pos, const float* __restrict__ wts,
+                                              int T, int k, int d, int shared_parts, int t, int n, float (&acc)[8]) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+    for (int j = 0; j < k; ++j) {
+        const int p = pos[(size_t)t * k + j];
+        if (p < 0) continue;
+        const float w = wts[(size_t)t * k + j];
+        const uint4 v = *reinterpret_cast<const uint4*>(O + (size_t)p * d + n);
+        const uint32_t u[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            acc[2 * i] += w * __uint_as_float(u[i] << 16);
+            acc[2 * i + 1] += w * __uint_as_float(u[i] & 0xffff0000u);
+        }
+    }
+    float sh[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int q = 0; q < shared_parts; ++q) {
+        const uint4 v = *reinterpret_cast<const uint4*>(Os + ((size_t)q * T + t) * d + n);
+        const uint32_t u[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            sh[2 * i] += __uint_as_float(u[i] << 16);
+            sh[2 * i + 1] += __uint_as_float(u[i] & 0xffff0000u);
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] += sh[i];
+}
+
+// bf16 output: one 8-column group per thread (d % 8 == 0).
+__global__ __launch_bounds__(256) void combine_bf16_kernel(const bf16_t* __restrict__ O,
+                                                           const bf16_t* __restrict__ Os,
+                                                           const int32_t* __restrict__ pos,
+                                                           const float* __restrict__ wts, int T, int k, int d,
+                                                           int shared_parts, bf16_t* __restrict__ y) {
+    const int t = blockIdx.x;
+    const int n = (blockIdx.y * blockDim.x + threadIdx.x) * 8;
+    if (n >= d) return;
+    float acc[8];
+    combine_cols8(O, Os, pos, wts, T, k, d, shared_parts, t, n, acc);
+    uint32_t u[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        u[i] = (uint32_t)f32_to_bf16(acc[2 * i]) | ((uint32_t)f32_to_bf16(acc[2 * i + 1]) << 16);
+    *reinterpret_cast<uint4*>(y + (size_t)t * d + n) = make_uint4(u[0], u[1], u[2], u[3]);
+}
+
 template <typename OutT>
 __global__ __launch_bounds__(256) void combine_kernel(const OutT* __restrict__ O,
                                                       const OutT* __restrict__ Os,
@@ -103,8 +154,8 @@ hipError_t launch_combine(const void* O, const void* Os, const int32_t* pos, con
         combine_kernel<float><<<grid, 256, 0, s>>>((const float*)O, (const float*)Os, pos, wts, T, k, d,
                                                    shared_parts, (float*)y);
     else
-        combine_kernel<bf16_t><<<grid, 256, 0, s>>>((const bf16_t*)O, (const bf16_t*)Os, pos, wts, T, k, d,
-                                                    shared_parts, (bf16_t*)y);
+        combine_bf16_kernel<<<dim3(T, ceil_div(d, 8 * 256)), 256, 0, s>>>((const bf16_t*)O, (const bf16_t*)Os, pos,
+                                                                        wts, T, k, d, shared_parts, (bf16_t*)y);
     return hipGetLastError();
 }
 
