@@ -76,7 +76,7 @@ int check_desc(const flexmoe_layer_desc* D) {
 }
 
 struct Layout {
-    size_t idx, wts, blockcnt, blockbase, counts, offsets, perm, pos, seg, t1, t2, keep, plan, H, Hs, O, Os;
+    size_t idx, wts, blockcnt, blockbase, counts, offsets, perm, pos, seg, t1, t2, ord2, keep, plan, H, Hs, O, Os;
     size_t total;
 };
 
@@ -94,10 +94,11 @@ long long routed_row_tiles_ub(int T, int E, int k, int bm) {
 }
 
 // The shared expert's down reduction is split into chunks (each writing its
-// own partial rows, added by the combine) when one of its tiles would take
-// longer than a compute unit's average share of the down GEMM, which the host
-// estimates at full budget over MI355X's 256 compute units.  Chunks hold at
-// least kMinSplitK channels.
+// own partial rows, added by the combine in chunk order) while its tiles alone
+// cannot occupy MI355X's 256 compute units: ceil(256 / tiles) chunks of at
+// least kMinSplitK channels.  Its reductions are the longest of the launch
+// (I_s against the routed experts' k_e <= I), so without the split they set
+// the end of the down GEMM whenever the routed tiles finish first.
 constexpr int kComputeUnits = 256;
 constexpr int kMinSplitK = 1024;
 // Waves of shared-expert gate/up tiles below which the shared expert runs on
@@ -110,15 +111,9 @@ constexpr int kSideWaves = 4;
 int shared_ks2(const flexmoe_layer_desc& D, int T) {
     if (D.I_shared <= 0 || D.dtype != FLEXMOE_BF16) return 0;
     if (T <= kDecodeMaxT) return D.I;
-    const long long nd = ceil_div(D.d, kBigBN2);
-    const long long sh_tiles = (long long)ceil_div(T, kBigBM2) * nd;
+    const long long sh_tiles = (long long)ceil_div(T, kBigBM2) * ceil_div(D.d, kBigBN2);
     if (sh_tiles >= kComputeUnits) return 0;
-    const long long sh_steps = ceil_div(D.I_shared, 64);
-    const long long rt_tiles = routed_row_tiles_ub(T, D.E, D.top_k, kBigBM2) * nd;
-    const long long avg = (sh_tiles * sh_steps + rt_tiles * ceil_div(D.I, 64)) / kComputeUnits;
-    if (sh_steps <= avg) return 0;
-    const long long p = std::min<long long>(ceil_div((int)sh_steps, (int)std::max<long long>(avg, 16)),
-                                            D.I_shared / kMinSplitK);
+    const long long p = std::min<long long>(ceil_div(kComputeUnits, (int)sh_tiles), D.I_shared / kMinSplitK);
     if (p <= 1) return 0;
     return ceil_div(ceil_div(D.I_shared, (int)p), 64) * 64;
 }
@@ -168,6 +163,7 @@ Layout layout(const flexmoe_layer_desc& D, int T, size_t os_rows) {
     L.seg = take(nseg * sizeof(SegMeta));
     L.t1 = take((nseg + 1) * 4);
     L.t2 = take((nseg + 1) * 4);
+    L.ord2 = take(nseg * 4);
     L.keep = take((size_t)D.E * 4);      // bucketed forward: the uploaded keep table
     L.plan = take((size_t)D.E * 2 * 4);  // bucketed forward: segment order, GEMM widths
     L.H = take(A * (size_t)D.I * es);
@@ -464,6 +460,7 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
     SegMeta* seg = (SegMeta*)(ws + L.seg);
     int32_t* t1 = (int32_t*)(ws + L.t1);
     int32_t* t2 = (int32_t*)(ws + L.t2);
+    int32_t* ord2 = (int32_t*)(ws + L.ord2);
     void* O = ws + L.O;
     void* Os = ws + L.Os;
     int32_t* plan = nullptr;
@@ -566,6 +563,7 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
                                    (const bf16_t*)w_down_r, (const bf16_t*)ws_down, seg, t2, (bf16_t*)O,
                                    (bf16_t*)Os, D.d, D.I, D.I_shared, D.E, nseg, T, ks2, part, seg_lo,
                                    seg_hi, (int)g2s, clipped};
+            p2.order = ord2;
             {
                 KernelTimer kt(k2, st);
                 e = wide     ? launch_gemm2_decode_wide(p2, (int)n2, st)
@@ -587,6 +585,7 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
                                   (const float*)w_down_r, (const float*)ws_down, seg, t2, (float*)O,
                                   (float*)Os, D.d, D.I, D.I_shared, D.E, nseg, T, 0, part, seg_lo, seg_hi,
                                   (int)g2s, clipped};
+            p2.order = ord2;
             {
                 KernelTimer kt(k2, st);
                 e = launch_gemm2_f32(p2, (int)n2, st);
@@ -627,7 +626,7 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
         dispatch_small_kernel<<<1, 64 * kSmallWaves, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, keep_dev,
                                                              D.I, D.I_shared, D.d, ts, packed_limit, plan, 0,
                                                              idx, wts, counts, perm, pos, offsets, seg, t1,
-                                                             t2);
+                                                             t2, ord2);
         err = hipGetLastError();
         if (err != hipSuccess) return hip_fail(err, "dispatch launch");
     } else {
@@ -651,7 +650,7 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
         dispatch_small_kernel<<<1, 64 * kSmallWaves, 0, s>>>(logits, T, D.E, D.top_k, D.norm_topk, keep_dev,
                                                              D.I, D.I_shared, D.d, ts, packed_limit, plan, 1,
                                                              idx, wts, counts, perm, pos, offsets, seg, t1,
-                                                             t2);
+                                                             t2, ord2);
         err = hipGetLastError();
         if (err != hipSuccess) return hip_fail(err, "dispatch launch");
     } else if (!small) {
@@ -665,7 +664,7 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
             KernelTimer kt(FLEXMOE_K_DISPATCH_SCATTER, s);
             dispatch_scatter_kernel<<<NB, 64, 0, s>>>(idx, keep_dev, counts, blockbase, T, D.E, D.top_k,
                                                       D.I, D.I_shared, D.d, NB, ts, packed_limit, plan,
-                                                      perm, pos, offsets, seg, t1, t2);
+                                                      perm, pos, offsets, seg, t1, t2, ord2);
             err = hipGetLastError();
         }
         if (err != hipSuccess) return hip_fail(err, "dispatch scatter launch");

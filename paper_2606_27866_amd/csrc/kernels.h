@@ -74,6 +74,11 @@ struct Gemm2Params {
     int seg_lo, seg_hi;         // kPartRange: the segments covered
     int shared_tiles;           // tiles of the shared segment (kPartShared)
     int clipped;                // routed weights in the clipped layout (see RoutedWeights)
+    // Tile order (kPartRange): tstart, seg_lo and seg_hi count positions in
+    // this order of the segments (NULL: segment order).  The dispatch puts the
+    // shared expert first, then the routed experts by decreasing GEMM width:
+    // the longest reductions start first, so the launch ends evenly.
+    const int32_t* order = nullptr;
 };
 
 // Where routed expert e's weights live.  Ranked layout (online clipping):
@@ -94,6 +99,14 @@ __device__ __forceinline__ RoutedWeights routed_weights(const P& p, const SegMet
     return RoutedWeights{(size_t)sm.e * p.I * p.d, p.I, p.I};
 }
 
+// Segment at tile-order position i (down GEMM: Gemm2Params::order).
+__device__ __forceinline__ int order_of(const Gemm1Params<bf16_t>&, int i) { return i; }
+__device__ __forceinline__ int order_of(const Gemm1Params<float>&, int i) { return i; }
+template <typename T>
+__device__ __forceinline__ int order_of(const Gemm2Params<T>& p, int i) {
+    return p.order ? min(max(p.order[i], 0), p.nseg - 1) : i;
+}
+
 // Tile L of a launch -> segment s, its metadata and the tile's index inside
 // the segment.  False when L is past the launch's last tile (the caller's
 // workgroup then has nothing to do).  The shared segment's metadata is known
@@ -110,9 +123,10 @@ __device__ __forceinline__ bool tile_of(const P& p, int L, int& s, SegMeta& sm, 
     }
     L += p.tstart[p.seg_lo];
     if (L >= p.tstart[p.seg_hi]) return false;
-    s = find_segment(p.tstart, p.nseg, L);
+    const int i = find_segment(p.tstart, p.nseg, L);
+    s = order_of(p, i);
     sm = p.seg[s];
-    local = L - p.tstart[s];
+    local = L - p.tstart[i];
     return true;
 }
 
@@ -142,13 +156,13 @@ __global__ void dispatch_scatter_kernel(const int32_t* idx, const int32_t* keep,
                                         TileShape ts, int packed_limit, const int32_t* plan,
                                         int32_t* perm, int32_t* pos,
                                         int32_t* offsets, SegMeta* seg, int32_t* t1start,
-                                        int32_t* t2start);
+                                        int32_t* t2start, int32_t* order2);
 __global__ void dispatch_small_kernel(const float* logits, int T, int E, int k, int norm_topk,
                                       const int32_t* keep, int I, int I_shared, int d, TileShape ts,
                                       int packed_limit, const int32_t* plan, int pre_routed, int32_t* idx,
                                       float* wts, int32_t* counts,
                                       int32_t* perm, int32_t* pos, int32_t* offsets, SegMeta* seg,
-                                      int32_t* t1start, int32_t* t2start);
+                                      int32_t* t1start, int32_t* t2start, int32_t* order2);
 __global__ void set_keep_kernel(int32_t* keep, KeepArgs t, int E);
 
 // Launchers (defined next to their kernels).  Each returns the launch status.

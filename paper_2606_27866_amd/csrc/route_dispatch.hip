@@ -171,18 +171,21 @@ __device__ __forceinline__ int expert_offsets(CountFn count, const int32_t* __re
 }
 
 // One wave: segment table (shared expert first: its tiles carry the longest
-// reductions, so they start first) and the exclusive scans of both GEMMs'
-// tile counts, 64 segments per round.
+// reductions, so they start first), the exclusive scan of the gate/up GEMM's
+// tile counts in segment order, and the down GEMM's tile order (order2, see
+// Gemm2Params::order) with its tile counts scanned in that order, 64
+// segments per round.  n2s and ordl are LDS scratch of nseg entries.
 template <typename CountFn>
 __device__ void write_tables(CountFn count, const int* off, const int* kk_s, const int* ch0,
                              const int32_t* __restrict__ plan, int P, int T, int E, int I,
-                             int I_shared, int d, TileShape ts, int32_t* __restrict__ offsets,
-                             SegMeta* __restrict__ seg, int32_t* __restrict__ t1start,
-                             int32_t* __restrict__ t2start) {
+                             int I_shared, int d, TileShape ts, int* n2s, int* ordl,
+                             int32_t* __restrict__ offsets, SegMeta* __restrict__ seg,
+                             int32_t* __restrict__ t1start, int32_t* __restrict__ t2start,
+                             int32_t* __restrict__ order2) {
     const int lane = threadIdx.x & 63;
     const int hs = I_shared > 0 ? 1 : 0;
     const int nseg = E + hs;
-    int c1 = 0, c2 = 0, c3 = 0, c4 = 0;
+    int c1 = 0, c3 = 0, c4 = 0;
     for (int s0 = 0; s0 < nseg; s0 += 64) {
         const int s = s0 + lane;
         int n1 = 0, n2 = 0, n3 = 0, n4 = 0;
@@ -212,21 +215,50 @@ __device__ void write_tables(CountFn count, const int* off, const int* kk_s, con
                 n2 = ceil_div(m.rows, ts.bm2) * ceil_div(d, ts.bn2);
                 if (s < hs && ts.ks2 > 0) n2 *= ceil_div(m.kk, ts.ks2);
             }
+            n2s[s] = n2;
         }
         if (s >= hs && s < nseg) offsets[s - hs] = off[s - hs];
-        const int i1 = wave_incl_scan(n1), i2 = wave_incl_scan(n2);
+        const int i1 = wave_incl_scan(n1);
         const int i3 = wave_incl_scan(n3), i4 = wave_incl_scan(n4);
         if (s < nseg) {
             t1start[s] = c1 + i1 - n1;
-            t2start[s] = c2 + i2 - n2;
             m.prow0 = s < hs ? 0 : c3 + i3 - n3;
             m.rt0 = s < hs ? 0 : c4 + i4 - n4;
             seg[s] = m;
         }
         c1 += __shfl(i1, 63, 64);
-        c2 += __shfl(i2, 63, 64);
         c3 += __shfl(i3, 63, 64);
         c4 += __shfl(i4, 63, 64);
+    }
+    // The down GEMM's tile order: the shared expert, then the routed experts
+    // by decreasing width k_e (ties: lower id first), so that the longest
+    // reductions are handed out first.  The bucketed forward keeps its
+    // plan's order (one launch per width group).
+    for (int s0 = 0; s0 < nseg; s0 += 64) {
+        const int s = s0 + lane;
+        if (s >= nseg) continue;
+        int pos = s;
+        if (s >= hs && !plan) {
+            const int ks = kk_s[s - hs];
+            int r = 0;
+            for (int q = 0; q < E; ++q) {
+                const int kq = kk_s[q];
+                r += (kq > ks) + (kq == ks && q < s - hs);
+            }
+            pos = hs + r;
+        }
+        ordl[pos] = s;
+        order2[pos] = s;
+    }
+    __builtin_amdgcn_wave_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    int c2 = 0;
+    for (int i0 = 0; i0 < nseg; i0 += 64) {
+        const int i = i0 + lane;
+        const int n2 = i < nseg ? n2s[ordl[i]] : 0;
+        const int i2 = wave_incl_scan(n2);
+        if (i < nseg) t2start[i] = c2 + i2 - n2;
+        c2 += __shfl(i2, 63, 64);
     }
     if (lane == 0) {
         offsets[E] = P;
@@ -347,16 +379,19 @@ __global__ __launch_bounds__(64) void dispatch_scatter_kernel(
     int I, int I_shared, int d, int NB, TileShape ts, int packed_limit, const int32_t* __restrict__ plan,
     int32_t* __restrict__ perm,
     int32_t* __restrict__ pos, int32_t* __restrict__ offsets, SegMeta* __restrict__ seg,
-    int32_t* __restrict__ t1start, int32_t* __restrict__ t2start) {
+    int32_t* __restrict__ t1start, int32_t* __restrict__ t2start, int32_t* __restrict__ order2) {
     __shared__ int off[kMaxExperts];
     __shared__ int kk_s[kMaxExperts];
     __shared__ int ch0[kMaxExperts];
     __shared__ int run[kMaxExperts];
+    __shared__ int n2s[kMaxExperts + 1];
+    __shared__ int ordl[kMaxExperts + 1];
     auto count = [&](int e) { return counts[e]; };
     const int P = expert_offsets(count, keep, E, I, packed_limit, off, kk_s, ch0, run);
     __syncthreads();
     if (blockIdx.x == 0)
-        write_tables(count, off, kk_s, ch0, plan, P, T, E, I, I_shared, d, ts, offsets, seg, t1start, t2start);
+        write_tables(count, off, kk_s, ch0, plan, P, T, E, I, I_shared, d, ts, n2s, ordl, offsets, seg, t1start,
+                     t2start, order2);
     const int a0 = blockIdx.x * kRouteTokens * k;
     const int a1 = min((blockIdx.x + 1) * kRouteTokens, T) * k;
     auto base = [&](int e) { return off[e] + blockbase[(size_t)e * NB + blockIdx.x]; };
@@ -376,13 +411,16 @@ __global__ __launch_bounds__(64 * kSmallWaves) void dispatch_small_kernel(
     const int32_t* __restrict__ plan, int pre_routed, int32_t* __restrict__ idx, float* __restrict__ wts,
     int32_t* __restrict__ counts,
     int32_t* __restrict__ perm, int32_t* __restrict__ pos, int32_t* __restrict__ offsets,
-    SegMeta* __restrict__ seg, int32_t* __restrict__ t1start, int32_t* __restrict__ t2start) {
+    SegMeta* __restrict__ seg, int32_t* __restrict__ t1start, int32_t* __restrict__ t2start,
+    int32_t* __restrict__ order2) {
     __shared__ int hist[kSmallWaves][kMaxExperts];  // per-wave counts, then per-wave bases
     __shared__ int cnt[kMaxExperts];
     __shared__ int off[kMaxExperts];
     __shared__ int kk_s[kMaxExperts];
     __shared__ int ch0[kMaxExperts];
     __shared__ int run[kMaxExperts];
+    __shared__ int n2s[kMaxExperts + 1];
+    __shared__ int ordl[kMaxExperts + 1];
     __shared__ int32_t sidx[kSmallAssign];
     __shared__ RouteScratch rs[kSmallWaves];
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -432,7 +470,8 @@ __global__ __launch_bounds__(64 * kSmallWaves) void dispatch_small_kernel(
         const int P = expert_offsets(count, keep, E, I, packed_limit, off, kk_s, ch0, run);
         __builtin_amdgcn_wave_barrier();
         __atomic_signal_fence(__ATOMIC_SEQ_CST);
-        write_tables(count, off, kk_s, ch0, plan, P, T, E, I, I_shared, d, ts, offsets, seg, t1start, t2start);
+        write_tables(count, off, kk_s, ch0, plan, P, T, E, I, I_shared, d, ts, n2s, ordl, offsets, seg, t1start,
+                     t2start, order2);
     }
     __syncthreads();
     // this wave's running position inside each expert starts at its base
