@@ -63,8 +63,11 @@ __device__ __forceinline__ void reduce_waves(floatx4_t (&acc)[NACC], float4* red
 }
 }  // namespace
 
-__global__ __launch_bounds__(64 * DWAVES) void gemm1_decode_kernel(Gemm1Params<bf16_t> p) {
-    __shared__ float4 red[(DWAVES - 1) * 8 * 64];
+// NFM: most 16-token blocks a segment can hold (1 for T <= 16: the kernel
+// then needs far fewer registers and more workgroups fit per compute unit).
+template <int NFM>
+__global__ __launch_bounds__(64 * DWAVES, NFM == 1 ? 4 : 1) void gemm1_decode_kernel(Gemm1Params<bf16_t> p) {
+    __shared__ float4 red[(DWAVES - 1) * 2 * NFM * 64];
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     int s, ntile;  // one row tile per segment (rows <= 64): the local tile is the channel tile
     SegMeta sm;
@@ -77,11 +80,11 @@ __global__ __launch_bounds__(64 * DWAVES) void gemm1_decode_kernel(Gemm1Params<b
     const int g = lane >> 4;  // K group of this lane
     const int c = ntile * DCH + (lane & 15);
     const bool cval = c < sm.kg;  // channels the GEMM computes
-    const int nf = ceil_div(sm.rows, 16);  // 1..4 token blocks
+    const int nf = min(ceil_div(sm.rows, 16), NFM);  // token blocks (rows <= 16 * NFM)
 
-    const bf16_t* xrow[4];
+    const bf16_t* xrow[NFM];
 #pragma unroll
-    for (int f = 0; f < 4; ++f) {
+    for (int f = 0; f < NFM; ++f) {
         const int r = f * 16 + (lane & 15);
         xrow[f] = nullptr;
         if (f < nf && r < sm.rows) {
@@ -90,9 +93,9 @@ __global__ __launch_bounds__(64 * DWAVES) void gemm1_decode_kernel(Gemm1Params<b
             xrow[f] = p.x + (size_t)t * d;
         }
     }
-    floatx4_t acc[8];  // [0..3] gate, [4..7] up, per token block
+    floatx4_t acc[2 * NFM];  // [0, NFM) gate, [NFM, 2 NFM) up, per token block
 #pragma unroll
-    for (int i = 0; i < 8; ++i) acc[i] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < 2 * NFM; ++i) acc[i] = floatx4_t{0.f, 0.f, 0.f, 0.f};
     const u32x4 zero = {0u, 0u, 0u, 0u};
     const bf16_t* wgr = Wg + (size_t)c * d;
     const bf16_t* wur = Wu + (size_t)c * d;
@@ -106,7 +109,7 @@ __global__ __launch_bounds__(64 * DWAVES) void gemm1_decode_kernel(Gemm1Params<b
             wuv[j] = ok ? *reinterpret_cast<const u32x4*>(wur + k0 + j * 32) : zero;
         }
 #pragma unroll
-        for (int f = 0; f < 4; ++f) {
+        for (int f = 0; f < NFM; ++f) {
             if (f >= nf) break;  // workgroup-uniform
             u32x4 xv[8];
 #pragma unroll
@@ -115,7 +118,8 @@ __global__ __launch_bounds__(64 * DWAVES) void gemm1_decode_kernel(Gemm1Params<b
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 acc[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_frag(wgv[j]), as_frag(xv[j]), acc[f], 0, 0, 0);
-                acc[4 + f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_frag(wuv[j]), as_frag(xv[j]), acc[4 + f], 0, 0, 0);
+                acc[NFM + f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_frag(wuv[j]), as_frag(xv[j]), acc[NFM + f], 0, 0,
+                                                                       0);
             }
         }
     }
@@ -126,7 +130,7 @@ __global__ __launch_bounds__(64 * DWAVES) void gemm1_decode_kernel(Gemm1Params<b
     const int ldh = shared ? p.Is : p.I;
     const int kk8 = min((sm.kg + 7) & ~7, ldh);  // [kk, kk8) written as zeros
 #pragma unroll
-    for (int f = 0; f < 4; ++f) {
+    for (int f = 0; f < NFM; ++f) {
         if (f >= nf) break;
         const int r = f * 16 + (lane & 15);
         if (r >= sm.rows) continue;
@@ -134,13 +138,14 @@ __global__ __launch_bounds__(64 * DWAVES) void gemm1_decode_kernel(Gemm1Params<b
         for (int i = 0; i < 4; ++i) {
             const int ch = ntile * DCH + 4 * g + i;
             if (ch < kk8)
-                Hb[(size_t)r * ldh + ch] = ch < sm.kk ? f32_to_bf16(silu_fast(acc[f][i]) * acc[4 + f][i]) : (bf16_t)0;
+                Hb[(size_t)r * ldh + ch] = ch < sm.kk ? f32_to_bf16(silu_fast(acc[f][i]) * acc[NFM + f][i]) : (bf16_t)0;
         }
     }
 }
 
+template <int NFM>
 __global__ __launch_bounds__(64 * DWAVES) void gemm2_decode_kernel(Gemm2Params<bf16_t> p) {
-    __shared__ float4 red[(DWAVES - 1) * 4 * 64];
+    __shared__ float4 red[(DWAVES - 1) * NFM * 64];
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     int s, local;
     SegMeta sm;
@@ -158,16 +163,16 @@ __global__ __launch_bounds__(64 * DWAVES) void gemm2_decode_kernel(Gemm2Params<b
     const int g = lane >> 4;
     const int n = ntile * DCH + (lane & 15);
     const bool nval = n < d;
-    const int nf = ceil_div(sm.rows, 16);
-    const bf16_t* hrow[4];
+    const int nf = min(ceil_div(sm.rows, 16), NFM);
+    const bf16_t* hrow[NFM];
 #pragma unroll
-    for (int f = 0; f < 4; ++f) {
+    for (int f = 0; f < NFM; ++f) {
         const int r = f * 16 + (lane & 15);
         hrow[f] = (f < nf && r < sm.rows) ? Hb + (size_t)r * ldh : nullptr;
     }
-    floatx4_t acc[4];
+    floatx4_t acc[NFM];
 #pragma unroll
-    for (int f = 0; f < 4; ++f) acc[f] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+    for (int f = 0; f < NFM; ++f) acc[f] = floatx4_t{0.f, 0.f, 0.f, 0.f};
     const u32x4 zero = {0u, 0u, 0u, 0u};
     const bf16_t* wrow = Wd + (size_t)n * rw.ldd;
     // a chunk is used when it starts before kend; H is zero past k_e within
@@ -180,7 +185,7 @@ __global__ __launch_bounds__(64 * DWAVES) void gemm2_decode_kernel(Gemm2Params<b
         for (int j = 0; j < 8; ++j)
             wv[j] = (nval && k0 + j * 32 < kend) ? *reinterpret_cast<const u32x4*>(wrow + k0 + j * 32) : zero;
 #pragma unroll
-        for (int f = 0; f < 4; ++f) {
+        for (int f = 0; f < NFM; ++f) {
             if (f >= nf) break;
             u32x4 hv[8];
 #pragma unroll
@@ -196,7 +201,7 @@ __global__ __launch_bounds__(64 * DWAVES) void gemm2_decode_kernel(Gemm2Params<b
     // D[m][n']: lane holds output columns m = 4*(lane/16) + i of row n' = lane%16
     bf16_t* Ob = shared ? p.Os + (size_t)split * p.tokens * d : p.O + (size_t)sm.row0 * d;
 #pragma unroll
-    for (int f = 0; f < 4; ++f) {
+    for (int f = 0; f < NFM; ++f) {
         if (f >= nf) break;
         const int r = f * 16 + (lane & 15);
         if (r >= sm.rows) continue;
@@ -447,13 +452,15 @@ __global__ __launch_bounds__(64 * DWAVES) void gemm2_decode_wide_kernel(Gemm2Par
 
 hipError_t launch_gemm1_decode(const Gemm1Params<bf16_t>& p, int tiles, hipStream_t s) {
     if (tiles <= 0) return hipSuccess;
-    gemm1_decode_kernel<<<tiles, 64 * DWAVES, 0, s>>>(p);
+    if (p.tokens <= 16) gemm1_decode_kernel<1><<<tiles, 64 * DWAVES, 0, s>>>(p);
+    else gemm1_decode_kernel<4><<<tiles, 64 * DWAVES, 0, s>>>(p);
     return hipGetLastError();
 }
 
 hipError_t launch_gemm2_decode(const Gemm2Params<bf16_t>& p, int tiles, hipStream_t s) {
     if (tiles <= 0) return hipSuccess;
-    gemm2_decode_kernel<<<tiles, 64 * DWAVES, 0, s>>>(p);
+    if (p.tokens <= 16) gemm2_decode_kernel<1><<<tiles, 64 * DWAVES, 0, s>>>(p);
+    else gemm2_decode_kernel<4><<<tiles, 64 * DWAVES, 0, s>>>(p);
     return hipGetLastError();
 }
 
