@@ -45,7 +45,8 @@ PEAK_F32_TFLOPS = 157.3      # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
 RIDGE = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
 DECODE_MAX_T = 64            # the library runs its weight-streaming GEMMs for T <= 64 (bf16)
-DECODE_WIDE_T = 16           # above this many tokens with 64-wide tiles (the routed experts once T*k >= 8*E)
+DECODE_WIDE_T = 16           # above this many tokens the routed experts' take 64-wide tiles once T*k >= 8*E
+DECODE_WIDE_SHARED_T = 5     # above this many tokens the shared expert's take them
 
 
 def log(*a):
@@ -591,9 +592,10 @@ def main():
     roof["traffic"] = load_traffic(args.workload, wl.T, "+".join(keep_names))
     if not bf16:
         roof["kernel"] = "gate_up GEMM (gemm1_f32_kernel)"
-    elif wl.T <= DECODE_WIDE_T:
+    elif wl.T <= DECODE_WIDE_SHARED_T or (wl.T <= DECODE_MAX_T and not cfg.I_shared and
+                                          not (wl.T > DECODE_WIDE_T and wl.T * cfg.top_k >= 8 * cfg.E)):
         roof["kernel"] = "gate_up GEMM (gemm1_decode_kernel)"
-    elif wl.T <= DECODE_MAX_T and wl.T * cfg.top_k >= 8 * cfg.E:
+    elif wl.T <= DECODE_MAX_T and wl.T > DECODE_WIDE_T and wl.T * cfg.top_k >= 8 * cfg.E:
         roof["kernel"] = "gate_up GEMM (gemm1_decode_wide_kernel)"
     elif wl.T <= DECODE_MAX_T:
         roof["kernel"] = ("gate_up GEMM (gemm1_decode_kernel for the routed experts, "

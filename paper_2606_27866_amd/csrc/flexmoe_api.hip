@@ -501,13 +501,15 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return hip_fail(e, "plan upload");
     }
-    // 17..64 tokens: 64-wide weight-streaming tiles whose workgroup shares the
-    // token rows through LDS (16-wide tiles each re-read every row of their
-    // segment).  The shared expert (T rows) takes them from 17 tokens on; the
-    // routed experts once they average 8 rows (fewer rows leave little to
-    // share, and the wider tiles hold more LDS per compute unit).
-    const bool wide_sh = decode && T > kDecodeWideT;
-    const bool wide_rt = wide_sh && (long long)T * D.top_k >= 8LL * D.E;
+    // 64-wide weight-streaming tiles whose workgroup shares the token rows
+    // through LDS (16-wide tiles each re-read every row of their segment).
+    // The shared expert (T rows) takes them from 6 tokens on (measured on the
+    // Qwen2-57B shape: even at 4 tokens, 1.04x slower at 1 token, faster from
+    // 6); the routed experts above 16 tokens once they average 8 rows (fewer
+    // rows leave little to share, and the wider tiles hold more LDS per
+    // compute unit).
+    const bool wide_sh = decode && T > kDecodeWideSharedT;
+    const bool wide_rt = decode && T > kDecodeWideT && (long long)T * D.top_k >= 8LL * D.E;
     const int dbn = wide_rt ? kDecWideBN : kDecBN;
     const TileShape ts = !bf16   ? TileShape{kF32BM, kF32BN, kF32BM, kF32BN, 0}
                          : decode ? TileShape{kDecodeMaxT, dbn, kDecodeMaxT, dbn, ks2}

@@ -136,7 +136,9 @@ constexpr int kF32BM = 64, kF32BN = 64;
 constexpr int kBigBM1 = 256, kBigBN1 = 128, kBigBM2 = 256, kBigBN2 = 256;
 constexpr int kDecodeMaxT = 64;     // T at or below which the weight-streaming kernels run
 constexpr int kDecBN = 16;          // their channels / output columns per tile
-constexpr int kDecodeWideT = 16;    // above this many tokens the weight-streaming GEMMs take
+constexpr int kDecodeWideT = 16;    // above this many tokens the routed experts' weight-streaming
+                                    // GEMMs may take (once T * k >= 8 E)
+constexpr int kDecodeWideSharedT = 5;  // above this many tokens the shared expert's take
 constexpr int kDecWideBN = 64;      // tiles of this many channels / output columns whose token
                                     // rows are shared through LDS (launch_gemm*_decode_wide)
 

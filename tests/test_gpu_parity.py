@@ -124,9 +124,10 @@ def test_bf16_token_counts(T):
     check_y(y, ref, BF16_TOL)
 
 
-@pytest.mark.parametrize("T", [17, 31, 33, 49, 64])
+@pytest.mark.parametrize("T", [5, 6, 8, 17, 31, 33, 49, 64])
 def test_bf16_shared_expert_wide_decode_tiles(T):
-    """17..64 tokens: the shared expert's GEMMs take 64-wide tiles.  d = 264
+    """6..64 tokens: the shared expert's GEMMs take 64-wide tiles (the routed
+    experts' too from 24 tokens on at this E and k; 5 tokens: neither).  d = 264
     leaves a partial 256-deep K batch, I_s = 216 a partial channel tile and a
     ragged last reduction chunk (chunks of I = 40 channels), and T a partial
     16-token block."""
