@@ -218,12 +218,14 @@ __global__ __launch_bounds__(64 * DWAVES) void gemm2_decode_kernel(Gemm2Params<b
     }
 }
 
-// ---- More than kDecodeWideT tokens: wide tiles ---------------------------
+// ---- Wide tiles ------------------------------------------------------------
 //
-// With 17..64 tokens the 16-channel tiles above read a segment's token rows
-// once per 16 weight rows -- for the shared expert two to four times the
-// weight bytes, from L2, one 16-token block after another.  The GEMMs then
-// take tiles of 64 channels (gate/up) or 64 output columns (down): wave w
+// The 16-channel tiles above read a segment's token rows once per 16 weight
+// rows -- at 64 tokens, for the shared expert, four times the weight bytes,
+// from L2, one 16-token block after another.  With enough rows per segment
+// (the shared expert above kDecodeWideSharedT tokens, routed experts above
+// kDecodeWideT tokens once T * k >= 8 E) the GEMMs take tiles of 64
+// channels (gate/up) or 64 output columns (down) instead: wave w
 // owns 16 of them over the whole reduction, and the four waves share the
 // segment's token rows through LDS.  Per 256-deep K batch the workgroup
 // copies the rows into LDS once (buffer_load ... lds; as many 16-row blocks
