@@ -124,6 +124,20 @@ def test_bf16_token_counts(T):
     check_y(y, ref, BF16_TOL)
 
 
+def test_bf16_decode_shared_partial_rows_fit_a_smaller_token_count():
+    """The shared expert's down reduction at decode is split into chunks of
+    I channels up to 16 tokens and of 2I above: a workspace sized for 24
+    tokens (4 partial rows per token) must also hold 16 tokens' 8 each."""
+    cfg, x, lg, w, s = mini_layer("osrows", 24, 64, 4, 64, 2, 512, config_id=75)
+    g = gpu_layer_for(cfg, w, s, max_tokens=24)
+    keep = np.array([64, 7, 0, 40], np.int32)
+    for T in (16, 24, 16):
+        y, r = g.forward(x[:T], lg[:T], keep)
+        ref, rr = oracle_ref(cfg, x[:T], lg[:T], w, s, keep)
+        check_route(r, rr)
+        check_y(y, ref, BF16_TOL)
+
+
 @pytest.mark.parametrize("T", [5, 6, 8, 17, 31, 33, 49, 64])
 def test_bf16_shared_expert_wide_decode_tiles(T):
     """6..64 tokens: the shared expert's GEMMs take 64-wide tiles (the routed
