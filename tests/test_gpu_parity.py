@@ -11,7 +11,7 @@ import oracle
 from paper_2606_27866_amd import flexmoe as fm
 from paper_2606_27866_amd import synth
 from tests.gpu_util import (BF16_TOL, F32_TOL, GpuLayer, check_route, check_y, mini_layer,
-                            oracle_ref, say)
+                            oracle_ref, say, y_to_f64)
 
 pytestmark = pytest.mark.gpu
 
@@ -153,6 +153,40 @@ def test_bf16_shared_expert_wide_decode_tiles(T):
         ref, rr = oracle_ref(cfg, x, lg, w, s, keep)
         check_route(r, rr)
         check_y(y, ref, BF16_TOL)
+
+
+@pytest.mark.parametrize("T", [1, 4, 6, 16, 17, 40, 64])
+def test_bf16_decode_with_shared_expert_every_output_written(T):
+    """Decode-sized batches with a shared expert whose down reduction is
+    split into many row sets (chunks of I or 2I channels), across the 16- and
+    64-wide tile choices.  d = 328 leaves a last 64-column tile of 8 columns;
+    the tables prune every routed expert (the shared row sets alone make y),
+    keep one expert, mix widths, keep all.  Each call is repeated into
+    outputs filled with NaN and must write every element with the same bits."""
+    import torch
+    E, I = 12, 96
+    cfg, x, lg, w, s = mini_layer("dsh%d" % T, 64, 328, E, I, 4, 1184, config_id=91)
+    x, lg = x[:T], lg[:T]
+    g = gpu_layer_for(cfg, w, s, max_tokens=64)
+    one = np.zeros(E, np.int32)
+    one[int(np.argmax(lg[0]))] = I  # the first token's top expert
+    rng = np.random.default_rng(T)
+    tables = (np.zeros(E, np.int32), one, rng.integers(0, I + 1, size=E).astype(np.int32),
+              np.full(E, I, np.int32))
+    for keep in tables:
+        say("decode T", T, "keep", keep.tolist())
+        y, r = g.forward(x, lg, keep)
+        ref, rr = oracle_ref(cfg, x, lg, w, s, keep)
+        check_route(r, rr)
+        check_y(y, ref, BF16_TOL)
+        # the same call again, into outputs filled with NaN: every element
+        # is written, with the same bits
+        xd, ld = fm.to_device(x), fm.to_device(np.ascontiguousarray(lg, np.float32))
+        for _ in range(3):
+            yb = torch.full((T, cfg.d), float("nan"), dtype=torch.bfloat16, device="cuda")
+            g.layer.forward(xd, ld, y=yb)
+            torch.cuda.synchronize()
+            assert np.array_equal(y, y_to_f64(fm.to_host(yb)))
 
 
 def test_all_tokens_on_one_expert_and_ties():
