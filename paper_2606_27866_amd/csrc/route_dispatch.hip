@@ -234,21 +234,34 @@ __device__ void write_tables(CountFn count, const int* off, const int* kk_s, con
     // by decreasing width k_e (ties: lower id first), so that the longest
     // reductions are handed out first.  The bucketed forward keeps its
     // plan's order (one launch per width group).
-    for (int s0 = 0; s0 < nseg; s0 += 64) {
-        const int s = s0 + lane;
-        if (s >= nseg) continue;
-        int pos = s;
-        if (s >= hs && !plan) {
-            const int ks = kk_s[s - hs];
+    static_assert(kMaxExperts % 4 == 0, "the width reads below stay inside kk_s");
+    // Expert e's rank counts the experts ordered before it, reading the
+    // widths four at a time (kk_s is 16-byte aligned and holds kMaxExperts
+    // entries, so the last read stays inside it; entries at or past E are
+    // masked).
+    if (hs && lane == 0) {
+        ordl[0] = 0;
+        order2[0] = 0;
+    }
+    for (int e0 = 0; e0 < E; e0 += 64) {
+        const int e = e0 + lane;
+        if (e >= E) continue;
+        int pos = e;
+        if (!plan) {
+            const int ks = kk_s[e];
             int r = 0;
-            for (int q = 0; q < E; ++q) {
-                const int kq = kk_s[q];
-                r += (kq > ks) + (kq == ks && q < s - hs);
+#pragma unroll 4
+            for (int q0 = 0; q0 < E; q0 += 4) {
+                const int4 v = *reinterpret_cast<const int4*>(&kk_s[q0]);
+                const int kq[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    r += q0 + i < E && (kq[i] > ks || (kq[i] == ks && q0 + i < e));
             }
-            pos = hs + r;
+            pos = r;
         }
-        ordl[pos] = s;
-        order2[pos] = s;
+        ordl[hs + pos] = hs + e;
+        order2[hs + pos] = hs + e;
     }
     __builtin_amdgcn_wave_barrier();
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
@@ -381,7 +394,7 @@ __global__ __launch_bounds__(64) void dispatch_scatter_kernel(
     int32_t* __restrict__ pos, int32_t* __restrict__ offsets, SegMeta* __restrict__ seg,
     int32_t* __restrict__ t1start, int32_t* __restrict__ t2start, int32_t* __restrict__ order2) {
     __shared__ int off[kMaxExperts];
-    __shared__ int kk_s[kMaxExperts];
+    __shared__ __align__(16) int kk_s[kMaxExperts];
     __shared__ int ch0[kMaxExperts];
     __shared__ int run[kMaxExperts];
     __shared__ int n2s[kMaxExperts + 1];
@@ -416,7 +429,7 @@ __global__ __launch_bounds__(64 * kSmallWaves) void dispatch_small_kernel(
     __shared__ int hist[kSmallWaves][kMaxExperts];  // per-wave counts, then per-wave bases
     __shared__ int cnt[kMaxExperts];
     __shared__ int off[kMaxExperts];
-    __shared__ int kk_s[kMaxExperts];
+    __shared__ __align__(16) int kk_s[kMaxExperts];
     __shared__ int ch0[kMaxExperts];
     __shared__ int run[kMaxExperts];
     __shared__ int n2s[kMaxExperts + 1];
