@@ -49,32 +49,53 @@ __device__ __forceinline__ float4 combine_cols(const OutT* __restrict__ O, const
 }
 
 // bf16: columns n .. n+7 of token t (16-byte loads and stores), the same
-// arithmetic as combine_cols per column.
+// arithmetic as combine_cols per column.  The reads of up to 8 slots and 8
+// row sets are issued together (addresses of absent ones clamped to a valid
+// row, their values unused), so that a token's combine costs about two
+// memory round trips instead of one per slot.
 __device__ __forceinline__ void combine_cols8(const bf16_t* __restrict__ O, const bf16_t* __restrict__ Os,
                                               const int32_t* __restrict__ pos, const float* __restrict__ wts,
                                               int T, int k, int d, int shared_parts, int t, int n, float (&acc)[8]) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) acc[i] = 0.f;
-    for (int j = 0; j < k; ++j) {
-        const int p = pos[(size_t)t * k + j];
-        if (p < 0) continue;
-        const float w = wts[(size_t)t * k + j];
-        const uint4 v = *reinterpret_cast<const uint4*>(O + (size_t)p * d + n);
-        const uint32_t u[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            acc[2 * i] += w * __uint_as_float(u[i] << 16);
-            acc[2 * i + 1] += w * __uint_as_float(u[i] & 0xffff0000u);
-        }
-    }
     float sh[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int q = 0; q < shared_parts; ++q) {
-        const uint4 v = *reinterpret_cast<const uint4*>(Os + ((size_t)q * T + t) * d + n);
-        const uint32_t u[4] = {v.x, v.y, v.z, v.w};
+    const int nbat = max(ceil_div(k, 8), ceil_div(shared_parts, 8));
+    for (int b = 0; b < nbat; ++b) {
+        int p[8];
+        float w[8];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            sh[2 * i] += __uint_as_float(u[i] << 16);
-            sh[2 * i + 1] += __uint_as_float(u[i] & 0xffff0000u);
+        for (int jj = 0; jj < 8; ++jj) {
+            const int j = min(b * 8 + jj, k - 1);
+            p[jj] = pos[(size_t)t * k + j];
+            w[jj] = wts[(size_t)t * k + j];
+        }
+        uint4 v[8], sv[8];
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) {
+            v[jj] = *reinterpret_cast<const uint4*>(O + (size_t)max(p[jj], 0) * d + n);
+            const int q = min(b * 8 + jj, max(shared_parts - 1, 0));
+            sv[jj] = shared_parts > 0 ? *reinterpret_cast<const uint4*>(Os + ((size_t)q * T + t) * d + n)
+                                      : make_uint4(0u, 0u, 0u, 0u);
+        }
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) {
+            if (b * 8 + jj >= k || p[jj] < 0) continue;
+            const uint32_t u[4] = {v[jj].x, v[jj].y, v[jj].z, v[jj].w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                acc[2 * i] += w[jj] * __uint_as_float(u[i] << 16);
+                acc[2 * i + 1] += w[jj] * __uint_as_float(u[i] & 0xffff0000u);
+            }
+        }
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) {
+            if (b * 8 + jj >= shared_parts) continue;
+            const uint32_t u[4] = {sv[jj].x, sv[jj].y, sv[jj].z, sv[jj].w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                sh[2 * i] += __uint_as_float(u[i] << 16);
+                sh[2 * i + 1] += __uint_as_float(u[i] & 0xffff0000u);
+            }
         }
     }
 #pragma unroll
