@@ -26,29 +26,38 @@ F32 = 0
 BF16 = 1
 
 
-def build(force: bool = False) -> str:
+# The timing build of the CPU baseline: the same source with fp32
+# accumulators in the forward's dot products, -O3 -march=native.  The parity
+# checks use the fp64 build only.
+_LIB_F32ACC = os.path.join(_HERE, "liboracle_f32acc.so")
+_FLAGS = {"fp64": (_LIB, ["-O2"]),
+          "f32acc": (_LIB_F32ACC, ["-O3", "-march=native", "-DORACLE_ACC_F32"])}
+
+
+def build(force: bool = False, variant: str = "fp64") -> str:
     """Compile the oracle with gcc (OpenMP over independent tokens/rows)."""
-    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
-        tmp = _LIB + ".tmp%d" % os.getpid()
-        cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-Wall",
+    path, flags = _FLAGS[variant]
+    if force or not os.path.exists(path) or os.path.getmtime(path) < os.path.getmtime(_SRC):
+        tmp = path + ".tmp%d" % os.getpid()
+        cmd = ["gcc", *flags, "-fopenmp", "-fPIC", "-shared", "-std=c11", "-Wall",
                "-o", tmp, _SRC, "-lm"]
         subprocess.run(cmd, check=True)
-        os.replace(tmp, _LIB)
-    return _LIB
+        os.replace(tmp, path)
+    return path
 
 
-_lib = None
+_libs = {}
 
 
-def lib():
-    global _lib
-    if _lib is None:
-        if _LIB_OVERRIDE:
+def lib(variant: str = "fp64"):
+    if variant not in _libs:
+        if _LIB_OVERRIDE and variant == "fp64":
             L = ctypes.CDLL(_LIB_OVERRIDE)
         else:
-            if not os.path.exists(_LIB):
-                build()
-            L = ctypes.CDLL(_LIB)
+            path = _FLAGS[variant][0]
+            if not os.path.exists(path):
+                build(variant=variant)
+            L = ctypes.CDLL(path)
         p = ctypes.c_void_p
         i = ctypes.c_int
         L.oracle_route.argtypes = [i, i, i, p, i, p, p]
@@ -63,12 +72,22 @@ def lib():
         L.oracle_masked_backward.argtypes = [i] * 8 + [p] * 13
         L.oracle_action_grad.argtypes = [i, i, p, i, p, p, ctypes.c_double, p, p, ctypes.c_longlong,
                                          ctypes.c_double, ctypes.c_double, p, p, p]
-        for f in (L.oracle_sample_actions, L.oracle_masked_backward, L.oracle_action_grad,L.oracle_route, L.oracle_dispatch, L.oracle_layer_forward,
-                  L.oracle_rank_reorder, L.oracle_keep_from_ratio, L.oracle_num_threads,
-                  L.oracle_layer_grads, L.oracle_channel_saliency):
+        fns = [L.oracle_sample_actions, L.oracle_masked_backward, L.oracle_action_grad, L.oracle_route,
+               L.oracle_dispatch, L.oracle_layer_forward, L.oracle_rank_reorder, L.oracle_keep_from_ratio,
+               L.oracle_num_threads, L.oracle_layer_grads, L.oracle_channel_saliency]
+        if hasattr(L, "oracle_set_threads"):  # absent from older mutant copies
+            L.oracle_set_threads.argtypes = [i]
+            L.oracle_acc_f32.argtypes = []
+            fns += [L.oracle_set_threads, L.oracle_acc_f32]
+        for f in fns:
             f.restype = ctypes.c_int
-        _lib = L
-    return _lib
+        _libs[variant] = L
+    return _libs[variant]
+
+
+def set_threads(n: int, variant: str = "fp64") -> int:
+    """OpenMP threads of the oracle's loops (for CPU-baseline timing)."""
+    return int(lib(variant).oracle_set_threads(int(n)))
 
 
 def _ptr(a: Optional[np.ndarray]):
@@ -115,7 +134,7 @@ def dispatch(idx: np.ndarray, keep: np.ndarray, E: int):
 
 
 def layer_forward(x, logits, w_gate, w_up, w_down, keep, top_k, norm_topk,
-                  ws_gate=None, ws_up=None, ws_down=None, want_route=False):
+                  ws_gate=None, ws_up=None, ws_down=None, want_route=False, variant="fp64"):
     """Masked MoE layer: y [T][d] fp64 (unrounded).
 
     x [T][d]; logits [T][E] fp32; w_gate/w_up [E][I][d]; w_down [E][d][I];
@@ -144,7 +163,7 @@ def layer_forward(x, logits, w_gate, w_up, w_down, keep, top_k, norm_topk,
     offsets = np.empty(E + 1, dtype=np.int32)
     perm = np.empty(max(A, 1), dtype=np.int32)
     pos = np.empty(max(A, 1), dtype=np.int32)
-    rc = lib().oracle_layer_forward(
+    rc = lib(variant).oracle_layer_forward(
         T, d, E, I, top_k, I_s, dtype, int(norm_topk), _ptr(x), _ptr(logits),
         _ptr(np.ascontiguousarray(w_gate)), _ptr(np.ascontiguousarray(w_up)),
         _ptr(np.ascontiguousarray(w_down)), _ptr(keep),
@@ -346,5 +365,5 @@ def keep_from_ratio(r: float, I: int) -> int:
     return int(lib().oracle_keep_from_ratio(float(r), int(I)))
 
 
-def num_threads() -> int:
-    return int(lib().oracle_num_threads())
+def num_threads(variant: str = "fp64") -> int:
+    return int(lib(variant).oracle_num_threads())

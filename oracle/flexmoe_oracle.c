@@ -60,6 +60,16 @@
 #define ORACLE_F32 0
 #define ORACLE_BF16 1
 
+/* Accumulator of the forward's dot products.  The parity build accumulates
+ * in fp64 (acc_t = double); defining ORACLE_ACC_F32 builds the same source
+ * with fp32 accumulators, a build used only to time the CPU baseline.  Its
+ * outputs are never compared with anything. */
+#ifdef ORACLE_ACC_F32
+typedef float acc_t;
+#else
+typedef double acc_t;
+#endif
+
 /* Exact decode of one stored element to double (bf16 -> fp32 is a shift). */
 static double elem(const void *base, int dtype, size_t i)
 {
@@ -187,18 +197,18 @@ static void sliced_ffn(int d, int kk, int ld_down, int dtype, const void *x, siz
                        size_t wd_off, double *h, double *out)
 {
     for (int c = 0; c < kk; ++c) {
-        double g = 0.0, u = 0.0;
+        acc_t g = 0, u = 0;
         for (int i = 0; i < d; ++i) {
-            double xi = elem(x, dtype, x_off + i);
-            g += elem(wg, dtype, w_off + (size_t)c * d + i) * xi;
-            u += elem(wu, dtype, w_off + (size_t)c * d + i) * xi;
+            acc_t xi = (acc_t)elem(x, dtype, x_off + i);
+            g += (acc_t)elem(wg, dtype, w_off + (size_t)c * d + i) * xi;
+            u += (acc_t)elem(wu, dtype, w_off + (size_t)c * d + i) * xi;
         }
-        h[c] = g / (1.0 + exp(-g)) * u;
+        h[c] = g / (1.0 + exp(-(double)g)) * u;
     }
     for (int n = 0; n < d; ++n) {
-        double acc = 0.0;
+        acc_t acc = 0;
         for (int c = 0; c < kk; ++c)
-            acc += h[c] * elem(wd, dtype, wd_off + (size_t)n * ld_down + c);
+            acc += (acc_t)h[c] * (acc_t)elem(wd, dtype, wd_off + (size_t)n * ld_down + c);
         out[n] = acc;
     }
 }
@@ -797,4 +807,19 @@ int oracle_keep_from_ratio(double r, int I)
 int oracle_num_threads(void)
 {
     return omp_get_max_threads();
+}
+
+/* Sets the threads of the OpenMP loops (CPU-baseline timing at 1 thread and
+ * at all cores); returns the new count. */
+int oracle_set_threads(int n)
+{
+    if (n >= 1)
+        omp_set_num_threads(n);
+    return omp_get_max_threads();
+}
+
+/* 1 for the fp32-accumulator timing build, 0 for the fp64 parity build. */
+int oracle_acc_f32(void)
+{
+    return (int)(sizeof(acc_t) == sizeof(float));
 }

@@ -246,31 +246,64 @@ def make_calibration_batch(cfg: LayerConfig, batch: int, T: Optional[int] = None
     return _as_dtype(x, cfg.dtype), np.ascontiguousarray(lg)
 
 
+def _draw_all(specs):
+    """Draw several tensors at once, one thread each.
+
+    Each tensor has its own generator (its own seed), and NumPy's generators
+    and array arithmetic release the interpreter lock while they fill large
+    arrays, so the bytes are exactly those of drawing the tensors one after
+    another; only the wall time shrinks.  specs: (tensor_id, n, shape, dtype,
+    std) per tensor.
+    """
+    from concurrent.futures import ThreadPoolExecutor
+
+    def one(spec):
+        tid, n, shape, dtype, std, cid = spec
+        return _as_dtype(_normal(cid, tid, n, std).reshape(shape), dtype)
+
+    if len(specs) == 1:
+        return [one(specs[0])]
+    with ThreadPoolExecutor(len(specs)) as ex:
+        return list(ex.map(one, specs))
+
+
+def _expert_specs(cfg: LayerConfig):
+    E, I, d = cfg.E, cfg.I, cfg.d
+    return [(_TID_WGATE, E * I * d, (E, I, d), cfg.dtype, cfg.w_std, cfg.config_id),
+            (_TID_WUP, E * I * d, (E, I, d), cfg.dtype, cfg.w_std, cfg.config_id),
+            (_TID_WDOWN, E * d * I, (E, d, I), cfg.dtype, cfg.w_std, cfg.config_id)]
+
+
+def _shared_specs(cfg: LayerConfig):
+    Is, d = cfg.I_shared, cfg.d
+    return [(_TID_SGATE, Is * d, (Is, d), cfg.dtype, cfg.w_std, cfg.config_id),
+            (_TID_SUP, Is * d, (Is, d), cfg.dtype, cfg.w_std, cfg.config_id),
+            (_TID_SDOWN, d * Is, (d, Is), cfg.dtype, cfg.w_std, cfg.config_id)]
+
+
 def make_expert_weights(cfg: LayerConfig):
     """w_gate, w_up [E][I][d]; w_down [E][d][I] (output rows, channel columns).
 
     Random weights are exchangeable across channels, so they serve directly as
     an importance-ranked layer for the forward benchmarks.
     """
-    E, I, d = cfg.E, cfg.I, cfg.d
-    wg = _normal(cfg.config_id, _TID_WGATE, E * I * d, cfg.w_std).reshape(E, I, d)
-    wg = _as_dtype(wg, cfg.dtype)
-    wu = _normal(cfg.config_id, _TID_WUP, E * I * d, cfg.w_std).reshape(E, I, d)
-    wu = _as_dtype(wu, cfg.dtype)
-    wd = _normal(cfg.config_id, _TID_WDOWN, E * d * I, cfg.w_std).reshape(E, d, I)
-    wd = _as_dtype(wd, cfg.dtype)
-    return wg, wu, wd
+    return tuple(_draw_all(_expert_specs(cfg)))
 
 
 def make_shared_weights(cfg: LayerConfig):
     """ws_gate, ws_up [I_s][d]; ws_down [d][I_s]; None if the layer has none."""
     if cfg.I_shared == 0:
         return None, None, None
-    Is, d = cfg.I_shared, cfg.d
-    sg = _as_dtype(_normal(cfg.config_id, _TID_SGATE, Is * d, cfg.w_std).reshape(Is, d), cfg.dtype)
-    su = _as_dtype(_normal(cfg.config_id, _TID_SUP, Is * d, cfg.w_std).reshape(Is, d), cfg.dtype)
-    sd = _as_dtype(_normal(cfg.config_id, _TID_SDOWN, d * Is, cfg.w_std).reshape(d, Is), cfg.dtype)
-    return sg, su, sd
+    return tuple(_draw_all(_shared_specs(cfg)))
+
+
+def make_layer_weights(cfg: LayerConfig):
+    """(w_gate, w_up, w_down), (ws_gate, ws_up, ws_down): the same tensors as
+    make_expert_weights and make_shared_weights, all six drawn at once."""
+    specs = _expert_specs(cfg) + (_shared_specs(cfg) if cfg.I_shared else [])
+    out = _draw_all(specs)
+    shared = tuple(out[3:]) if cfg.I_shared else (None, None, None)
+    return tuple(out[:3]), shared
 
 
 def make_scores(cfg: LayerConfig, tie_every: int = 0) -> np.ndarray:

@@ -134,3 +134,42 @@ def test_traffic_records_name_their_workload():
         assert os.path.dirname(p) == os.path.join(ROOT, "profiles")
         assert wl in os.path.basename(p)
     assert bench.traffic_file("qwen2_57b_a14b_decode", 8).endswith("_T8.json")
+
+
+def test_default_run_is_the_largest_single_gpu_layer():
+    """With no flags the headline is the Mixtral-8x7B-shaped layer (T = 16384,
+    the largest configuration), with the further sections after it."""
+    a = bench.parse([])
+    assert a.workload == "mixtral_8x7b" and a.gpus == 1
+    cfg = synth.CONFIGS[a.workload]
+    assert cfg.T == max(c.T for c in synth.CONFIGS.values())
+    assert set(a.extras.split(",")) == {"qwen2_prefill", "decode", "qwen15"}
+    assert a.min_warmup_s >= 1.0   # warm-up lasts a while whatever --warmup says
+
+
+def test_step_stats_are_order_statistics_of_the_steps():
+    rng = np.random.default_rng(3)
+    ms = rng.uniform(1.0, 2.0, size=101)
+    st = bench.step_stats(list(ms))
+    s = np.sort(ms)
+    assert st["median"] == s[50] and st["n"] == 101
+    assert st["p10"] == pytest.approx(s[10]) and st["p90"] == pytest.approx(s[90])
+    assert st["p10"] <= st["median"] <= st["p90"]
+    assert st["mean"] == pytest.approx(ms.mean())
+
+
+@pytest.mark.parametrize("T,name", [(1, "gemm1_decode_kernel"), (5, "gemm1_decode_kernel"),
+                                    (8, "gemm1_decode_kernel for the routed experts, gemm1_decode_wide_kernel "
+                                        "for the shared expert"),
+                                    (64, "gemm1_decode_wide_kernel"), (65, "gemm1_big_kernel")])
+def test_gate_up_kernel_named_from_the_library_thresholds(T, name):
+    cfg = synth.CONFIGS["qwen2_57b_a14b_decode"]
+    assert bench.gate_up_kernel_name(cfg, T) == name
+    assert bench.gate_up_kernel_name(synth.CONFIGS["mixtral_8x7b"], 16384) == "gemm1_big_kernel"
+    assert bench.gate_up_kernel_name(synth.CONFIGS["tiny_fp32"], 64) == "gemm1_f32_kernel"
+
+
+def test_cpu_info_names_the_model_and_counts():
+    info = bench.cpu_info()
+    assert info["nproc"] >= 1 and 1 <= info["usable_cpus"] <= info["nproc"]
+    assert isinstance(info["cpu_model"], str) and info["cpu_model"]

@@ -3,7 +3,11 @@ configuration bench.py times.
 
 Routing and dispatch are checked bit-exactly for every token against the
 oracle's routing and dispatch; y is checked on sampled rows, which the oracle
-computes one by one (a token's output depends on that token only).
+computes one by one (a token's output depends on that token only).  The
+prefill rows include, for every active expert, the tokens of its first
+routed row, of the first row of its last (partial) 256-row tile and of its
+last routed row, so that every expert's tile edges are compared element by
+element.
 """
 import functools
 
@@ -21,8 +25,7 @@ pytestmark = pytest.mark.gpu
 def layer_inputs(name):
     cfg = synth.CONFIGS[name]
     say("generating", name)
-    w = synth.make_expert_weights(cfg)
-    s = synth.make_shared_weights(cfg)
+    w, s = synth.make_layer_weights(cfg)
     return cfg, w, s
 
 
@@ -31,6 +34,21 @@ def gpu_layer(name):
     cfg, w, s = layer_inputs(name)
     return GpuLayer(cfg.d, cfg.E, cfg.I, cfg.top_k, cfg.I_shared, cfg.dtype, cfg.norm_topk,
                     cfg.T, *w, *s)
+
+
+def edge_rows(cfg, lg, keep, tile_rows=256):
+    """Tokens at every active expert's segment edges in the oracle's own
+    dispatch: its first routed row, the first row of its last row tile and
+    its last routed row."""
+    idx, _ = oracle.route(lg, cfg.top_k, cfg.norm_topk)
+    _, offsets, perm, _ = oracle.dispatch(idx, keep, cfg.E)
+    rows = []
+    for e in range(cfg.E):
+        lo, hi = int(offsets[e]), int(offsets[e + 1])
+        if hi > lo:
+            last_tile = lo + (hi - lo - 1) // tile_rows * tile_rows
+            rows += [perm[lo] // cfg.top_k, perm[last_tile] // cfg.top_k, perm[hi - 1] // cfg.top_k]
+    return np.array(rows, dtype=np.int64)
 
 
 def check_all_routing(cfg, lg, keep, r):
@@ -59,7 +77,8 @@ def test_full_size_prefill(name, table):
     y, r = g.forward(x, lg, keep)
     check_all_routing(cfg, lg, keep, r)
     rng = np.random.default_rng(7)
-    rows = np.unique(np.concatenate([[0, cfg.T - 1], rng.choice(cfg.T, 8, replace=False)]))
+    rows = np.unique(np.concatenate([[0, cfg.T - 1], rng.choice(cfg.T, 8, replace=False),
+                                     edge_rows(cfg, lg, keep)]))
     say(name, table, "oracle on rows", rows.tolist())
     ref = oracle.layer_forward(x[rows], lg[rows], *w, keep, cfg.top_k, cfg.norm_topk, *s)
     check_y(y[rows], ref, BF16_TOL)

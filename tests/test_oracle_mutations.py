@@ -14,12 +14,12 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "flexmoe_oracle.c")
 
 MUTANTS = {
-    "silu_dropped": ("h[c] = g / (1.0 + exp(-g)) * u;", "h[c] = g * u;"),
-    "silu_sign": ("h[c] = g / (1.0 + exp(-g)) * u;", "h[c] = g / (1.0 + exp(g)) * u;"),
+    "silu_dropped": ("h[c] = g / (1.0 + exp(-(double)g)) * u;", "h[c] = g * u;"),
+    "silu_sign": ("h[c] = g / (1.0 + exp(-(double)g)) * u;", "h[c] = g / (1.0 + exp((double)g)) * u;"),
     "tie_break_reversed": ("    return ia < ib;\n}", "    return ia > ib;\n}"),
     "norm_flag_inverted": ("if (norm_topk)", "if (!norm_topk)"),
-    "down_transposed": ("acc += h[c] * elem(wd, dtype, wd_off + (size_t)n * ld_down + c);",
-                        "acc += h[c] * elem(wd, dtype, wd_off + (size_t)c * d + n);"),
+    "down_transposed": ("acc += (acc_t)h[c] * (acc_t)elem(wd, dtype, wd_off + (size_t)n * ld_down + c);",
+                        "acc += (acc_t)h[c] * (acc_t)elem(wd, dtype, wd_off + (size_t)c * d + n);"),
     "dispatch_unstable": ("int32_t p = offsets[e] + fill[e]++;",
                           "int32_t p = offsets[e + 1] - 1 - fill[e]++;"),
     "zero_expert_not_skipped": ("offsets[e] + (keep[e] > 0 ? counts[e] : 0)",
@@ -51,8 +51,8 @@ MUTANTS = {
     "shared_input_grad_dropped": ("                    dxt[i] += dg * elem(ws_gate, dtype, (size_t)c * d + i) +\n"
                                   "                              du * elem(ws_up, dtype, (size_t)c * d + i);",
                                   "                    dxt[i] += 0.0 * dg * elem(ws_gate, dtype, (size_t)c * d + i);"),
-    "prefix_short_by_one": ("    for (int c = 0; c < kk; ++c) {\n        double g = 0.0, u = 0.0;",
-                            "    for (int c = 0; c < kk; ++c) {\n        if (c == kk - 1 && kk > 1) { h[c] = 0; continue; }\n        double g = 0.0, u = 0.0;"),
+    "prefix_short_by_one": ("    for (int c = 0; c < kk; ++c) {\n        acc_t g = 0, u = 0;",
+                            "    for (int c = 0; c < kk; ++c) {\n        if (c == kk - 1 && kk > 1) { h[c] = 0; continue; }\n        acc_t g = 0, u = 0;"),
 }
 
 

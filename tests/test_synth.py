@@ -77,3 +77,18 @@ def test_action_keep_table_uses_only_action_widths():
         assert kept <= f + 1e-12 or (t == levels[0]).all()
         # one step wider on any expert would exceed the target (the walk stops at the first fit)
         assert kept > f - (levels[-1] - levels[0]) / (60 * 1408) - 1e-12 or (t == levels[0]).all()
+
+
+def test_concurrent_draws_equal_serial_draws():
+    """The weights drawn concurrently (one thread per tensor) are the bytes of
+    drawing each tensor alone, in any order, over several generation chunks."""
+    cfg = synth.small_config("conc", T=8, d=1024, E=3, I=6000, top_k=2, I_shared=4096, config_id=78)
+    (wg, wu, wd), (sg, su, sd) = synth.make_layer_weights(cfg)
+    assert wg.size > synth._CHUNK  # more than one chunk per tensor
+    serial = [synth._as_dtype(synth._normal(cfg.config_id, tid, a.size, cfg.w_std).reshape(a.shape), cfg.dtype)
+              for tid, a in ((synth._TID_SDOWN, sd), (synth._TID_WUP, wu), (synth._TID_WGATE, wg),
+                             (synth._TID_SGATE, sg), (synth._TID_WDOWN, wd), (synth._TID_SUP, su))]
+    for got, ref in zip((sd, wu, wg, sg, wd, su), serial):
+        assert got.dtype == np.uint16 and np.array_equal(got, ref)
+    assert all(np.array_equal(p, q) for p, q in zip(synth.make_expert_weights(cfg), (wg, wu, wd)))
+    assert all(np.array_equal(p, q) for p, q in zip(synth.make_shared_weights(cfg), (sg, su, sd)))
