@@ -18,7 +18,8 @@
  *     flexmoe_set_budget and the debug-output struct are DEVICE pointers of the
  *     current HIP device.  The caller owns and allocates every buffer,
  *     including the forward workspace; the library allocates no device memory
- *     and keeps no device data between calls.
+ *     and keeps no device data between calls, except the static scratch array
+ *     of flexmoe_layer_forward_noalloc (below).
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
  *     work is ordered after the work already queued on it, and later work
  *     queued on it is ordered after the call's work; no call synchronises the
@@ -293,6 +294,31 @@ int flexmoe_layer_forward(const flexmoe_layer_desc *desc, int32_t T, const void 
                           const void *w_down_r, const int32_t *keep_dev, const void *ws_gate,
                           const void *ws_up, const void *ws_down, void *y, void *workspace,
                           size_t workspace_bytes, const flexmoe_route_out *dbg, void *stream);
+
+/* No-allocation forward, for callers that cannot allocate device memory or
+ * pass a workspace: code under HIP graph capture, tight serving loops, and
+ * harnesses that forbid allocation.  Arguments, results, rules and errors are
+ * those of flexmoe_layer_forward, without the workspace: the workspace
+ * regions live in a static device array of the library (64 MiB per device,
+ * held by every device the library runs on until the process ends), so T is
+ * limited to what fits there (flexmoe_workspace_bytes(desc, T) up to about
+ * 64 MiB: every T <= 64 of the shapes this library is measured on, and a
+ * few hundred to a thousand tokens of them).  A larger T returns
+ * FLEXMOE_EWORKSPACE with nothing enqueued.  The array's device address is
+ * looked up on the first call on each device; after that the call allocates
+ * nothing, creates no stream or event (unless per-kernel timing is on) and
+ * issues no memset.  Every launch goes to `stream`: the shared expert's GEMMs
+ * run in the same launches as the routed experts' (no second stream), so the
+ * bits of y may differ from flexmoe_layer_forward's by the summation order of
+ * the shared expert (routing and dispatch outputs are identical).  All calls
+ * on one device share the one array, which keeps the last call's contents
+ * (nothing in it needs to start at zero): calls that overlap on one device,
+ * on different streams or threads, race and give wrong results; order them. */
+int flexmoe_layer_forward_noalloc(const flexmoe_layer_desc *desc, int32_t T, const void *x,
+                                  const float *logits, const void *w_gate_r, const void *w_up_r,
+                                  const void *w_down_r, const int32_t *keep_dev, const void *ws_gate,
+                                  const void *ws_up, const void *ws_down, void *y,
+                                  const flexmoe_route_out *dbg, void *stream);
 
 /* ---- Offline clipping (Sec. 4.4, Table 2): one budget exported as a
  * standalone compact subnetwork, run by the same kernels.

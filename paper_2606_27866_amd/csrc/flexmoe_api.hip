@@ -267,6 +267,36 @@ int side_stream(SideStream** out) {
     return FLEXMOE_OK;
 }
 
+// ---- scratch of the no-allocation forward --------------------------------
+// flexmoe_layer_forward_noalloc takes its workspace from this file-scope
+// device array instead of a caller buffer.  Every device the library runs
+// on holds its own copy (64 MiB) from the module's load until the process
+// ends.  In host code `scratch` names a host-side stand-in, not device
+// memory: kernels and copies get the array's device address, looked up once
+// per device with hipGetSymbolAddress (with that device current) and kept in
+// g_scratch.
+constexpr size_t kNoAllocScratchBytes = size_t(64) << 20;
+__device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+void* g_scratch[kMaxDevices];
+std::mutex g_scratch_mu;
+
+int scratch_address(void** out) {
+    int dev = 0;
+    hipError_t err = hipGetDevice(&dev);
+    if (err != hipSuccess) return hip_fail(err, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) return fail(FLEXMOE_EHIP, "device %d beyond %d", dev, kMaxDevices);
+    std::lock_guard<std::mutex> g(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void* ptr = nullptr;
+        err = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (err != hipSuccess) return hip_fail(err, "hipGetSymbolAddress(scratch)");
+        if (!ptr || ((uintptr_t)ptr & 255)) return fail(FLEXMOE_EHIP, "scratch address %p is not 256-byte aligned", ptr);
+        g_scratch[dev] = ptr;
+    }
+    *out = g_scratch[dev];
+    return FLEXMOE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -422,7 +452,7 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
                  int clipped, int packed_limit, const int32_t* bucket_keep, int k_align,
                  const void* ws_gate, const void* ws_up, const void* ws_down, void* y, void* workspace,
                  size_t workspace_bytes, const flexmoe_route_out* dbg, void* stream,
-                 const TrainKeep* tr = nullptr) {
+                 const TrainKeep* tr = nullptr, bool allow_side = true) {
     int rc = check_desc(desc);
     if (rc) return rc;
     const flexmoe_layer_desc& D = *desc;
@@ -518,8 +548,13 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
     const TileShape ts = !bf16   ? TileShape{kF32BM, kF32BN, kF32BM, kF32BN, 0}
                          : decode ? TileShape{kDecodeMaxT, dbn, kDecodeMaxT, dbn, ks2}
                                   : TileShape{kBigBM1, kBigBN1, kBigBM2, kBigBN2, ks2};
-    // the shared expert's tile width (its tiles are counted here, not by the dispatch)
-    const int sbn1 = wide_sh ? kDecWideBN : ts.bn1, sbn2 = wide_sh ? kDecWideBN : ts.bn2;
+    // The shared expert's tile width.  On the side stream (every decode-sized
+    // batch that may use it) its launches count their own tiles, of the
+    // wide shape from kDecodeWideSharedT tokens on; in the launches over all
+    // segments its tiles are those the dispatch counts, of the routed shape.
+    const bool side_ok = allow_side && has_shared && !train;
+    const bool sh_wide_tiles = side_ok && wide_sh;
+    const int sbn1 = sh_wide_tiles ? kDecWideBN : ts.bn1, sbn2 = sh_wide_tiles ? kDecWideBN : ts.bn2;
 
     hipError_t err;
     // grid upper bounds from host-known sizes: the routed part's from the
@@ -612,7 +647,7 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
     // The training forwards compute every routed channel (the routed GEMMs
     // alone fill the chip): one launch over all segments there (measured 2 %
     // faster than the split on the Qwen1.5 shape).
-    const bool use_side = has_shared && !train && (decode || g1s < (long long)kSideWaves * kComputeUnits);
+    const bool use_side = side_ok && (decode || g1s < (long long)kSideWaves * kComputeUnits);
     SideStream* side = nullptr;
     std::unique_lock<std::mutex> side_lock;
     if (use_side) {
@@ -748,6 +783,33 @@ int flexmoe_layer_forward(const flexmoe_layer_desc* desc, int32_t T, const void*
                           size_t workspace_bytes, const flexmoe_route_out* dbg, void* stream) {
     return forward_impl(desc, T, x, logits, w_gate_r, w_up_r, w_down_r, keep_dev, 0, 0x7fffffff, nullptr, 0,
                         ws_gate, ws_up, ws_down, y, workspace, workspace_bytes, dbg, stream);
+}
+
+int flexmoe_layer_forward_noalloc(const flexmoe_layer_desc* desc, int32_t T, const void* x,
+                                  const float* logits, const void* w_gate_r, const void* w_up_r,
+                                  const void* w_down_r, const int32_t* keep_dev, const void* ws_gate,
+                                  const void* ws_up, const void* ws_down, void* y,
+                                  const flexmoe_route_out* dbg, void* stream) {
+    int rc = check_desc(desc);
+    if (rc) return rc;
+    if (T < 0) return fail(FLEXMOE_EINVAL, "T = %d is negative", T);
+    if (T > desc->max_tokens) return fail(FLEXMOE_ESHAPE, "T = %d exceeds max_tokens = %d", T, desc->max_tokens);
+    if (T == 0) return FLEXMOE_OK;
+    if (!x || !logits || !w_gate_r || !w_up_r || !w_down_r || !keep_dev || !y)
+        return fail(FLEXMOE_EINVAL, "forward_noalloc: an input/output pointer is NULL");
+    // the regions of flexmoe_layer_forward's workspace for this T (nothing
+    // in them needs to start at zero: every kernel writes what it reads)
+    const size_t need = layout(*desc, T, (size_t)T * shared_parts(*desc, T)).total;
+    if (need > kNoAllocScratchBytes)
+        return fail(FLEXMOE_EWORKSPACE,
+                    "T = %d needs %zu bytes of scratch; the no-allocation forward's static scratch holds %zu "
+                    "(use flexmoe_layer_forward with a workspace)", T, need, kNoAllocScratchBytes);
+    void* ws = nullptr;
+    if ((rc = scratch_address(&ws)) != FLEXMOE_OK) return rc;
+    // every launch on the caller's stream: no side stream, no events
+    return forward_impl(desc, T, x, logits, w_gate_r, w_up_r, w_down_r, keep_dev, 0, 0x7fffffff, nullptr, 0,
+                        ws_gate, ws_up, ws_down, y, ws, kNoAllocScratchBytes, dbg, stream, nullptr,
+                        /*allow_side=*/false);
 }
 
 int64_t flexmoe_clipped_channels(const flexmoe_layer_desc* desc, const int32_t* keep_host) {

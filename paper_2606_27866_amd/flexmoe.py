@@ -35,7 +35,7 @@ EXPORTED = ("flexmoe_workspace_bytes", "flexmoe_rank_reorder", "flexmoe_set_budg
             "flexmoe_layer_forward_bucketed", "flexmoe_saliency_workspace_bytes",
             "flexmoe_channel_saliency", "flexmoe_transpose_weights", "flexmoe_sample_actions",
             "flexmoe_train_workspace_bytes", "flexmoe_train_forward", "flexmoe_train_backward",
-            "flexmoe_action_grad")
+            "flexmoe_action_grad", "flexmoe_layer_forward_noalloc")
 
 # kernel indices of flexmoe_kernel_times
 KERNELS = ("route", "dispatch_scan", "dispatch_scatter", "gate_up", "down", "combine",
@@ -102,6 +102,8 @@ def lib():
         L.flexmoe_set_budget.restype = ctypes.c_int
         L.flexmoe_layer_forward.argtypes = [D, i32] + [vp] * 11 + [sz, ctypes.POINTER(flexmoe_route_out), vp]
         L.flexmoe_layer_forward.restype = ctypes.c_int
+        L.flexmoe_layer_forward_noalloc.argtypes = [D, i32] + [vp] * 10 + [ctypes.POINTER(flexmoe_route_out), vp]
+        L.flexmoe_layer_forward_noalloc.restype = ctypes.c_int
         L.flexmoe_clipped_channels.argtypes = [D, vp]
         L.flexmoe_clipped_channels.restype = ctypes.c_int64
         L.flexmoe_export_clipped.argtypes = [D] + [vp] * 8
@@ -220,6 +222,18 @@ def flexmoe_layer_forward(desc, T, x, logits, w_gate_r, w_up_r, w_down_r, keep_d
         ctypes.byref(desc), int(T), _p(x), _p(logits), _p(w_gate_r), _p(w_up_r), _p(w_down_r),
         _p(keep_dev), _p(ws_gate), _p(ws_up), _p(ws_down), _p(y), _p(workspace),
         int(workspace_bytes), ctypes.byref(ro) if ro is not None else None, _stream(stream)))
+
+
+def flexmoe_layer_forward_noalloc(desc, T, x, logits, w_gate_r, w_up_r, w_down_r, keep_dev, ws_gate,
+                                  ws_up, ws_down, y, dbg=None, stream=None):
+    """flexmoe_layer_forward without a workspace (the library's static scratch)."""
+    ro = None
+    if dbg:
+        ro = flexmoe_route_out(*[_p(dbg.get(n)) for n, _ in flexmoe_route_out._fields_])
+    _check(lib().flexmoe_layer_forward_noalloc(
+        ctypes.byref(desc), int(T), _p(x), _p(logits), _p(w_gate_r), _p(w_up_r), _p(w_down_r),
+        _p(keep_dev), _p(ws_gate), _p(ws_up), _p(ws_down), _p(y),
+        ctypes.byref(ro) if ro is not None else None, _stream(stream)))
 
 
 def flexmoe_clipped_channels(desc, keep_host: Sequence[int]) -> int:

@@ -147,3 +147,24 @@ def test_one_hip_runtime_in_process():
     hips = set(re.findall(r"\S*libamdhip64\S*", maps))
     hsas = set(re.findall(r"\S*libhsa-runtime64\S*", maps))
     assert len(hips) == 1 and len(hsas) == 1, (hips, hsas)
+
+
+def test_noalloc_rejects_what_its_scratch_cannot_hold():
+    """The no-allocation forward refuses, on the host and before any device
+    call, a batch whose workspace regions exceed its 64 MiB static scratch,
+    and null pointers; T = 0 is a no-op."""
+    desc = good_desc(d=3584, E=64, I=2560, top_k=8, I_shared=20480, max_tokens=1024)
+    assert fm.flexmoe_workspace_bytes(desc, 1024) > 64 << 20
+    assert fm.flexmoe_workspace_bytes(desc, 64) <= 64 << 20
+    f = fm.flexmoe_layer_forward_noalloc
+    with pytest.raises(fm.FlexMoEError) as ei:
+        f(desc, 1024, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, stream=0)
+    assert ei.value.code == -4 and "static scratch" in fm.flexmoe_last_error()
+    for T, code in ((-1, -1), (1025, -2)):
+        with pytest.raises(fm.FlexMoEError) as ei:
+            f(desc, T, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, stream=0)
+        assert ei.value.code == code
+    with pytest.raises(fm.FlexMoEError) as ei:
+        f(desc, 4, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, stream=0)
+    assert ei.value.code == -1
+    f(desc, 0, None, None, None, None, None, None, None, None, None, None, stream=0)
