@@ -31,6 +31,9 @@ at 1, 8 and 64 tokens per step with the budget switching every step, the
 fixed-table and pointer-switch references and the cost of one budget
 switch), and `qwen15` (the Qwen1.5-MoE-A2.7B-shaped layer, T = 4096, with
 the device channel saliency of Eq. 2 and one action-learning step).
+`dense_gemm_reference` times the vendor library's dense bf16 GEMM
+(torch.matmul) on two dense shapes, as context for what a plain contraction
+reaches on the same GPU.
 """
 import argparse
 import hashlib
@@ -90,6 +93,10 @@ def parse(argv=None):
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target work of the main CPU baseline")
     ap.add_argument("--bucket-align", type=int, default=128,
                     help="k_align of the bucketed ablation in the per-budget results")
+    ap.add_argument("--no-dense-reference", action="store_true",
+                    help="skip timing the vendor library's dense bf16 GEMM (torch.matmul) on two reference shapes")
+    ap.add_argument("--dense-reference-only", action="store_true",
+                    help="only time the dense reference GEMMs (for a counter run of the vendor kernel)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after timing, copy this many MiB device-to-device once, so that a "
                          "counter run sees a plain copy of known size (HBM byte calibration)")
@@ -756,6 +763,43 @@ def saliency_cpu_baseline(wl, T, target_s):
                        "about %.0f s (%.1f s per batch + %.2f ms per token)" % (S, T, t, f + c * T, f, c * 1e3))
 
 
+DENSE_SHAPES = ((8192, 8192, 8192), (16384, 28672, 4096))
+
+
+def dense_reference(reps=25):
+    """The vendor library's dense bf16 GEMM (torch.matmul -> hipBLASLt) on two
+    dense shapes, the second one the Mixtral-shaped gate/up with every token
+    on one expert: the rate a plain contraction reaches on this GPU, as
+    context for the layer's roofline.  Not part of the layer's path."""
+    import torch
+    out = []
+    for M, N, K in DENSE_SHAPES:
+        g = torch.Generator(device="cuda")
+        g.manual_seed(M + N + K)
+        a = torch.randn(M, K, device="cuda", dtype=torch.bfloat16, generator=g)
+        b = torch.randn(N, K, device="cuda", dtype=torch.bfloat16, generator=g)
+        c = a @ b.t()
+        torch.cuda.synchronize()
+        t0 = time.time()
+        while time.time() - t0 < 1.0:
+            c = a @ b.t()
+            torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            c = a @ b.t()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        tf = 2.0 * M * N * K / (ms / 1e3) / 1e12
+        out.append(dict(M=M, N=N, K=K, ms=ms, tflops=tf, frac=tf / PEAK_BF16_TFLOPS))
+        log("[bench] dense reference (torch.matmul bf16) %dx%dx%d: %.4f ms, %.1f TFLOP/s (%.3f of bf16 peak)"
+            % (M, N, K, ms, tf, tf / PEAK_BF16_TFLOPS))
+        del a, b, c
+    torch.cuda.empty_cache()
+    return out
+
+
 def qwen2_prefill_section(args):
     """The Qwen2-57B-A14B-shaped layer (T = 8192, 64 experts of 2560
     channels, top-8, shared expert of 20480) at the five nested budgets.
@@ -872,6 +916,9 @@ def main(argv=None):
     from paper_2606_27866_amd import synth
     torch.cuda.set_device(0)
     fm.lib()
+    if args.dense_reference_only:
+        print(json.dumps({"dense_reference": dense_reference()}), flush=True)
+        return
     t_start = time.time()
     cfg = synth.CONFIGS[args.workload]
     decode_T = args.decode_T if args.workload == "qwen2_57b_a14b_decode" else None
@@ -933,6 +980,10 @@ def main(argv=None):
                         "qwen15": qwen15_section}[name](args)
         log("[bench] section %s done in %.1fs" % (name, time.time() - t0))
 
+    dense = None
+    if not args.no_dense_reference and args.workload == HEADLINE:
+        dense = dense_reference()
+
     out = {
         "metric": "masked MoE-layer tokens/s + % bf16 MFMA peak / % HBM BW, per budget",
         "value": value,
@@ -964,6 +1015,8 @@ def main(argv=None):
     if action is not None:
         out["action_learning"] = action
     out.update(extras)
+    if dense is not None:
+        out["dense_gemm_reference"] = dense
     out["wall_s"] = time.time() - t_start
     print(json.dumps(out), flush=True)
 

@@ -27,11 +27,13 @@
  *     two GEMMs on a second stream of the same device (forked from `stream` by
  *     an event before routing, joined by an event before the combine): it does
  *     so for T <= 64 and while the shared expert's gate/up GEMM has fewer than
- *     1024 tiles (the training forwards never do).  The library creates that
- *     stream on first use per device
- *     (default priority) and keeps it for the life of the process; forwards
- *     on one device share it, so concurrent forwards on one device also
- *     serialise their shared-expert GEMMs.
+ *     1024 tiles (the training forwards and flexmoe_layer_forward_noalloc
+ *     never do).  That stream, its two events and a mutex guarding the fork
+ *     and join are process-wide state of the library: created on first use
+ *     per device (default priority) and kept for the life of the process.
+ *     Forwards on one device share them, so concurrent forwards on one device
+ *     serialise their shared-expert GEMMs, and a graph capture of such a
+ *     forward needs one eager call first (to create the stream).
  *   - Return value 0 = success, otherwise one of the negative FLEXMOE_E* codes;
  *     flexmoe_last_error() then returns a message (thread-local).  Argument
  *     checks happen on the host before any device work: a call that returns
@@ -261,7 +263,10 @@ int flexmoe_action_grad(const flexmoe_layer_desc *desc, int32_t T, const flexmoe
                         float beta, const float *dmask, float *dalpha, float *stats,
                         void *workspace, size_t workspace_bytes, void *stream);
 
-/* Budget switch: validates 0 <= keep_host[e] <= I for every e on the host, then
+/* Budget switch (online clipping, Sec. 4.4 and Table 3: a new budget is a new
+ * per-expert width table, the hardened action mask of Eqs. 9-10 as channel
+ * counts, applied without moving any weight).
+ * Validates 0 <= keep_host[e] <= I for every e on the host, then
  * writes the E counts into keep_dev [E] on `stream` (one small kernel whose
  * arguments carry the table, so keep_host may be reused as soon as the call
  * returns).  A forward queued later on the same stream sees the new budget.
