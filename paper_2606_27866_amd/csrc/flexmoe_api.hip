@@ -569,6 +569,9 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
 
     // The two GEMMs over one part of the tile list (n1, n2 workgroups), on
     // one stream.
+    // the shared expert's GEMMs on the side stream (see below)
+    const bool use_side = side_ok && (decode || g1s < (long long)kSideWaves * kComputeUnits);
+
     auto gemms = [&](int part, int seg_lo, int seg_hi, long long n1, long long n2, hipStream_t st) -> int {
         const bool sh = part == kPartShared;
         const int k1 = sh ? FLEXMOE_K_GATE_UP_SHARED : FLEXMOE_K_GATE_UP;
@@ -609,7 +612,7 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
                 KernelTimer kt(k2, st);
                 e = wide     ? launch_gemm2_decode_wide(p2, (int)n2, st)
                     : decode ? launch_gemm2_decode(p2, (int)n2, st)
-                             : launch_gemm2_big(p2, (int)n2, st);
+                             : launch_gemm2_big(p2, (int)n2, st, !use_side);
             }
             if (e != hipSuccess) return hip_fail(e, "down GEMM launch");
         } else {
@@ -647,7 +650,6 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
     // The training forwards compute every routed channel (the routed GEMMs
     // alone fill the chip): one launch over all segments there (measured 2 %
     // faster than the split on the Qwen1.5 shape).
-    const bool use_side = side_ok && (decode || g1s < (long long)kSideWaves * kComputeUnits);
     SideStream* side = nullptr;
     std::unique_lock<std::mutex> side_lock;
     if (use_side) {

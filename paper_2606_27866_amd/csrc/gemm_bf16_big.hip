@@ -58,7 +58,7 @@ constexpr int WM = 2, WN = NWAVE / WM;      // wave grid
 static_assert(BM == WM * 128, "a full tile gives each M-wave four 32-row fragments");
 constexpr int NF = BN / (WN * 32);          // 32-column fragments per wave
 constexpr int WCOL = BN / WN;               // weight rows per wave
-constexpr int NSTAGE = 2;                   // LDS stages of BK-deep operand tiles
+constexpr int NSTAGE = 2;                   // LDS stages of BK-deep token-row (A) tiles
 constexpr int NSTEP = BK / 16;              // 16-deep MFMA steps per K tile
 static_assert(NSTEP == 4, "the K-loop schedule is laid out for four steps per K tile");
 constexpr int RPI = 64 / CHUNKS;            // LDS rows filled per DMA instruction
@@ -66,7 +66,12 @@ constexpr int ROWS_PER_WAVE = BM / NWAVE;   // A rows (and B rows) each wave loa
 constexpr int NI = ROWS_PER_WAVE / RPI;     // DMA instructions per wave per operand
 constexpr int LOADS_PER_TILE = 2 * NI;      // DMA instructions per lane per K tile
 constexpr int STAGE_A = BM * ROWB;          // 32 KB
-constexpr int STAGE = STAGE_A + BN * ROWB;  // 64 KB
+constexpr int STAGE_B = BN * ROWB;          // 32 KB
+// LDS of a workgroup with NSB stages of weight (B) tiles: 128 KB for two,
+// 160 KB -- all of a compute unit's LDS -- for three.
+template <int NSB>
+constexpr int smem_bytes() { return NSTAGE * STAGE_A + NSB * STAGE_B; }
+static_assert(smem_bytes<3>() <= 160 * 1024, "the stages fit the compute unit's LDS");
 constexpr int XCD_GROUP = 8;                // consecutive tiles kept on one XCD
 constexpr int ROW_GROUP = 4;                // row tiles of a segment walked before the next column
 }  // namespace
@@ -76,7 +81,7 @@ constexpr int ROW_GROUP = 4;                // row tiles of a segment walked bef
 // lane%32 of a 32-row fragment, register v -> channel (v/4)*8 + (lane/32)*4 +
 // v%4 of the wave's 32 gate (jj = 0) and up (jj = NF/2) channels.
 constexpr int TROW = 256 + 8;  // staging row pitch (bf16): 4 rows apart = 16 banks apart
-static_assert(128 * TROW * 2 <= NSTAGE * STAGE, "the staging tile fits in the operand stages");
+static_assert(128 * TROW * 2 <= smem_bytes<2>(), "the staging tile fits in the operand stages");
 
 template <int MFW, typename Acc>
 __device__ __forceinline__ void train_store_h_transposed(const Gemm1Params<bf16_t>& p, const SegMeta& sm,
@@ -118,7 +123,9 @@ __device__ __forceinline__ void train_store_h_transposed(const Gemm1Params<bf16_
 // kTrain: 0 = inference; 1 = also g and u of the routed rows
 // (fragment-blocked) and their h transposed (channel saliency); 2 = also g
 // and u of every row, fragment-blocked (the masked layer's training backward).
-template <bool kGateUp, int kTrain = 0>
+// NSB: LDS stages of weight tiles (2, or 3: the weights of K tile kt+3 are
+// requested with the token rows of kt+2, two tiles ahead of their use).
+template <bool kGateUp, int kTrain = 0, int NSB = 2>
 __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Gemm2Params<bf16_t>& p2,
                                          unsigned char* smem) {
     const int d = kGateUp ? p1.d : p2.d;
@@ -214,18 +221,20 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
     // DMA of K tile kt into a stage.  Chunks at or past K are masked as well,
     // and tiles past the end load nothing useful (their stage is never read),
     // so every tile issues exactly LOADS_PER_TILE loads.
-    auto issue = [&](int kt, int stage) {
-        unsigned char* sa = smem + stage * STAGE + wave * ROWS_PER_WAVE * ROWB;
-        unsigned char* sb = sa + STAGE_A;
-        const int k0 = kt * BK;
-        const int lim = K - k0;
-        const uint32_t soff = (uint32_t)k0 * 2u;
+    // The A stages come first in LDS, then the B stages.
+    auto issue_a = [&](int kt, int stage) {
+        unsigned char* sa = smem + stage * STAGE_A + wave * ROWS_PER_WAVE * ROWB;
+        const int lim = K - kt * BK;
+        const uint32_t soff = (uint32_t)(kt * BK) * 2u;
 #pragma unroll
-        for (int i = 0; i < NI; ++i) {
-            const bool kin = acol[i] < lim;  // A and B chunks share the column
-            load_lds16(ra, kin ? aoff[i] : kOOB, soff, sa + i * RPI * ROWB);
-            load_lds16(rb, kin ? boff[i] : kOOB, soff, sb + i * RPI * ROWB);
-        }
+        for (int i = 0; i < NI; ++i) load_lds16(ra, acol[i] < lim ? aoff[i] : kOOB, soff, sa + i * RPI * ROWB);
+    };
+    auto issue_b = [&](int kt, int stage) {
+        unsigned char* sb = smem + NSTAGE * STAGE_A + stage * STAGE_B + wave * ROWS_PER_WAVE * ROWB;
+        const int lim = K - kt * BK;
+        const uint32_t soff = (uint32_t)(kt * BK) * 2u;
+#pragma unroll
+        for (int i = 0; i < NI; ++i) load_lds16(rb, acol[i] < lim ? boff[i] : kOOB, soff, sb + i * RPI * ROWB);
     };
 
     const int wm = wave / WN, wn = wave % WN;
@@ -255,8 +264,8 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
                 for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
         bf16x8 a[2][MFW], b[2][NF];  // fragment buffers of alternate steps
         auto read_frags = [&](int kt, int ks, int buf) {
-            const unsigned char* sa = smem + (kt % NSTAGE) * STAGE;
-            const unsigned char* sb = sa + STAGE_A;
+            const unsigned char* sa = smem + (kt % NSTAGE) * STAGE_A;
+            const unsigned char* sb = smem + NSTAGE * STAGE_A + (kt % NSB) * STAGE_B;
             const int chunk = ks * 2 + (lane >> 5);
 #pragma unroll
             for (int i = 0; i < MFW; ++i) a[buf][i] = lds_frag(sa, wm * WR + i * 32 + (lane & 31), chunk);
@@ -280,9 +289,21 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
         // kt+1 has landed, so its fragments can be read.  Every iteration
         // issues one tile's DMAs (zero-page loads once past the end), so at
         // the wait no later tile's loads are outstanding (two stages).
-        issue(0, 0);
-        issue(1, 1);
-        __builtin_amdgcn_s_waitcnt(waitcnt_vm(LOADS_PER_TILE));  // tile 0 in
+        // With three B stages the weight tile kt+3 is requested together
+        // with token-row tile kt+2, two K tiles before its use: per
+        // iteration the loads go out as [A(kt+2), B(kt+3)], so at the wait
+        // only B(kt+2) -- issued last -- may still be outstanding.
+        // With three weight stages, weight tile kt+3 is requested after
+        // token-row tile kt+2: at the wait below only that last request may
+        // still be outstanding.
+        constexpr int AHEAD = NSB - NSTAGE;  // weight tiles further ahead (0 or 1)
+        static_assert(AHEAD == 0 || AHEAD == 1, "two or three weight stages");
+        issue_a(0, 0);
+        issue_b(0, 0);
+        issue_a(1, 1);
+        issue_b(1, 1);
+        if constexpr (AHEAD) issue_b(2, 2);
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm((2 + AHEAD) * NI));  // tile 0 in
         barrier_no_fence();
         read_frags(0, 0, 0);
         for (int kt = 0; kt < nk; ++kt) {
@@ -293,11 +314,12 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
                 sched_interleave<NMF, 0, NRD>();
                 __builtin_amdgcn_sched_barrier(0);
             }
-            __builtin_amdgcn_s_waitcnt(waitcnt_vm(0) & kWaitLgkm0);  // tile kt+1 in; own reads done
-            barrier_no_fence();  // all waves are done reading tile kt: its stage is free
+            __builtin_amdgcn_s_waitcnt(waitcnt_vm(AHEAD * NI) & kWaitLgkm0);  // tile kt+1 in; own reads done
+            barrier_no_fence();  // all waves are done reading tile kt: its stages are free
             __builtin_amdgcn_sched_barrier(0);
-            issue(kt + NSTAGE, kt % NSTAGE);
-            // after the last tile this reads a stale stage, whose values go unused
+            issue_a(kt + NSTAGE, kt % NSTAGE);
+            issue_b(kt + NSB, kt % NSB);
+            // after the last tile this reads stale stages, whose values go unused
             read_frags(kt + 1, 0, 0);
             mfma_step((NSTEP - 1) & 1);
             sched_interleave<NMF, LOADS_PER_TILE, NRD>();
@@ -413,27 +435,31 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
 }
 
 __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void gemm1_big_kernel(Gemm1Params<bf16_t> p) {
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[NSTAGE * STAGE];
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[smem_bytes<2>()];
     big_tile<true>(p, Gemm2Params<bf16_t>{}, smem);
 }
 
 // The gate/up GEMM of the training forward: the same tiles, plus the
 // transposed g, u and h copies of the routed segments (Gemm1Params).
 __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void gemm1_big_train_kernel(Gemm1Params<bf16_t> p) {
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[NSTAGE * STAGE];
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[smem_bytes<2>()];
     big_tile<true, 1>(p, Gemm2Params<bf16_t>{}, smem);
 }
 
 // The gate/up GEMM of the masked layer's training forward: the same tiles,
 // plus g and u of every row (Gemm1Params).
 __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void gemm1_big_train_rm_kernel(Gemm1Params<bf16_t> p) {
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[NSTAGE * STAGE];
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[smem_bytes<2>()];
     big_tile<true, 2>(p, Gemm2Params<bf16_t>{}, smem);
 }
 
+// NSB = 3 when the launch has the compute units to itself (its 160 KB of LDS
+// leave no room for a concurrent launch's workgroups): the down GEMM's long
+// reductions then run 2-3 % faster on the Mixtral and Qwen2-57B shapes.
+template <int NSB>
 __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void gemm2_big_kernel(Gemm2Params<bf16_t> p) {
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[NSTAGE * STAGE];
-    big_tile<false>(Gemm1Params<bf16_t>{}, p, smem);
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[smem_bytes<NSB>()];
+    big_tile<false, 0, NSB>(Gemm1Params<bf16_t>{}, p, smem);
 }
 
 hipError_t launch_gemm1_big(const Gemm1Params<bf16_t>& p, int grid, hipStream_t s) {
@@ -457,10 +483,11 @@ hipError_t launch_gemm1_big_train_rm(const Gemm1Params<bf16_t>& p, int grid, hip
     return hipGetLastError();
 }
 
-hipError_t launch_gemm2_big(const Gemm2Params<bf16_t>& p, int grid, hipStream_t s) {
+hipError_t launch_gemm2_big(const Gemm2Params<bf16_t>& p, int grid, hipStream_t s, bool alone) {
     if (grid <= 0) return hipSuccess;
     const int g = (grid + 8 * XCD_GROUP - 1) / (8 * XCD_GROUP) * (8 * XCD_GROUP);
-    gemm2_big_kernel<<<g, THREADS, 0, s>>>(p);
+    if (alone) gemm2_big_kernel<3><<<g, THREADS, 0, s>>>(p);
+    else gemm2_big_kernel<2><<<g, THREADS, 0, s>>>(p);
     return hipGetLastError();
 }
 
