@@ -74,15 +74,46 @@ struct TileShape {
                         // reductions of ks2 channels (one tile set each)
 };
 
-// Wave-wide inclusive prefix sum of an int (64 lanes).
+// Lane-shift building block of the wave scans: v of the lane DPP control
+// CTRL names (row_shr:n within rows of 16 lanes, or the gfx9 row broadcasts
+// of lane 15 / lane 31), 0 where that lane is outside the row or the row is
+// not in ROW_MASK.  A DPP move costs about as much as an ALU op, where a
+// ds_bpermute shuffle waits on the LDS crossbar.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ int dpp_shift(int v) {
+    return __builtin_amdgcn_update_dpp(0, v, CTRL, ROW_MASK, 0xf, false);
+}
+
+// Wave-wide inclusive prefix sum of an int (64 lanes, all active): a
+// Hillis-Steele scan inside each row of 16 lanes (row_shr 1, 2, 4, 8), then
+// row 0's total added to row 1 and row 2's to row 3 (row_bcast:15 into rows
+// 1 and 3), then the total of rows 0-1 to rows 2 and 3 (row_bcast:31).
 __device__ __forceinline__ int wave_incl_scan(int v) {
-    const int lane = threadIdx.x & 63;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        int n = __shfl_up(v, o, 64);
-        if (lane >= o) v += n;
-    }
+    v += dpp_shift<0x111, 0xf>(v);
+    v += dpp_shift<0x112, 0xf>(v);
+    v += dpp_shift<0x114, 0xf>(v);
+    v += dpp_shift<0x118, 0xf>(v);
+    v += dpp_shift<0x142, 0xa>(v);
+    v += dpp_shift<0x143, 0xc>(v);
     return v;
+}
+
+// Value of lane 63 (e.g. the total of an inclusive scan), in every lane.
+__device__ __forceinline__ int lane63(int v) { return __builtin_amdgcn_readlane(v, 63); }
+
+// Sum of a float over the wave (64 lanes, all active), in every lane: the
+// scan above on the float bits, read from lane 63.  The order of the
+// additions is fixed, so the sum is deterministic.
+__device__ __forceinline__ float wave_total_f(float v) {
+#define FLEXMOE_FSTEP(C, M) v += __int_as_float(dpp_shift<C, M>(__float_as_int(v)))
+    FLEXMOE_FSTEP(0x111, 0xf);
+    FLEXMOE_FSTEP(0x112, 0xf);
+    FLEXMOE_FSTEP(0x114, 0xf);
+    FLEXMOE_FSTEP(0x118, 0xf);
+    FLEXMOE_FSTEP(0x142, 0xa);
+    FLEXMOE_FSTEP(0x143, 0xc);
+#undef FLEXMOE_FSTEP
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
 }
 
 __device__ __forceinline__ int wave_sum(int v) {

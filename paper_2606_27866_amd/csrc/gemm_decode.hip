@@ -454,6 +454,7 @@ __global__ __launch_bounds__(64 * DWAVES) void gemm2_decode_wide_kernel(Gemm2Par
 
 hipError_t launch_gemm1_decode(const Gemm1Params<bf16_t>& p, int tiles, hipStream_t s) {
     if (tiles <= 0) return hipSuccess;
+    if (p.tokens <= kGemvMaxT) return launch_gemv1_decode(p, tiles, s);
     if (p.tokens <= 16) gemm1_decode_kernel<1><<<tiles, 64 * DWAVES, 0, s>>>(p);
     else gemm1_decode_kernel<4><<<tiles, 64 * DWAVES, 0, s>>>(p);
     return hipGetLastError();
@@ -461,6 +462,7 @@ hipError_t launch_gemm1_decode(const Gemm1Params<bf16_t>& p, int tiles, hipStrea
 
 hipError_t launch_gemm2_decode(const Gemm2Params<bf16_t>& p, int tiles, hipStream_t s) {
     if (tiles <= 0) return hipSuccess;
+    if (p.tokens <= kGemvMaxT) return launch_gemv2_decode(p, tiles, s);
     if (p.tokens <= 16) gemm2_decode_kernel<1><<<tiles, 64 * DWAVES, 0, s>>>(p);
     else gemm2_decode_kernel<4><<<tiles, 64 * DWAVES, 0, s>>>(p);
     return hipGetLastError();

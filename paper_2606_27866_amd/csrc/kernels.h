@@ -141,6 +141,8 @@ constexpr int kDecodeWideT = 16;    // above this many tokens the routed experts
 constexpr int kDecodeWideSharedT = 5;  // above this many tokens the shared expert's take
 constexpr int kDecWideBN = 64;      // tiles of this many channels / output columns whose token
                                     // rows are shared through LDS (launch_gemm*_decode_wide)
+constexpr int kGemvMaxT = 8;        // T at or below which the 16-wide weight-streaming tiles run
+                                    // on the vector ALUs (launch_gemv*_decode)
 
 __global__ void route_kernel(const float* logits, int T, int E, int k, int norm_topk, int32_t* idx,
                              float* wts, int32_t* blockcnt, int NB);
@@ -174,6 +176,10 @@ hipError_t launch_gemm1_big(const Gemm1Params<bf16_t>& p, int grid, hipStream_t 
 hipError_t launch_gemm2_big(const Gemm2Params<bf16_t>& p, int grid, hipStream_t s, bool alone);
 hipError_t launch_gemm1_decode(const Gemm1Params<bf16_t>& p, int tiles, hipStream_t s);
 hipError_t launch_gemm2_decode(const Gemm2Params<bf16_t>& p, int tiles, hipStream_t s);
+// T <= kGemvMaxT: the same tiles on the vector ALUs (launch_gemm*_decode
+// hands them over).
+hipError_t launch_gemv1_decode(const Gemm1Params<bf16_t>& p, int tiles, hipStream_t s);
+hipError_t launch_gemv2_decode(const Gemm2Params<bf16_t>& p, int tiles, hipStream_t s);
 // kDecodeWideT < T <= kDecodeMaxT: tiles of kDecWideBN channels / output columns.
 hipError_t launch_gemm1_decode_wide(const Gemm1Params<bf16_t>& p, int tiles, hipStream_t s);
 hipError_t launch_gemm2_decode_wide(const Gemm2Params<bf16_t>& p, int tiles, hipStream_t s);

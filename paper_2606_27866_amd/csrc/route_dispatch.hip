@@ -118,9 +118,9 @@ __device__ __forceinline__ void route_token(const float (&v)[4], int E, int k, i
 #pragma unroll
     for (int q = 0; q < 4; ++q)
         if (lane + 64 * q < E) z += expf(v[q] - m);
-    z = wave_sum_f(z);
+    z = wave_total_f(z);
     float w = lane < k ? expf(my_logit - m) / z : 0.0f;
-    if (norm_topk) w = w / wave_sum_f(w);
+    if (norm_topk) w = w / wave_total_f(w);
     my_w = w;
 }
 
@@ -129,16 +129,15 @@ __device__ __forceinline__ void route_token(const float (&v)[4], int E, int k, i
 // experts per lane.  Also scans the packed widths of the clipped weight
 // layout: an expert whose block would end past packed_limit is treated as
 // k_e = 0.  Fills off[], kk_s[], ch0[] and zeroes run[]; returns P.
-template <typename CountFn>
-__device__ __forceinline__ int expert_offsets(CountFn count, const int32_t* __restrict__ keep, int E,
-                                              int I, int packed_limit, int* off, int* kk_s, int* ch0,
-                                              int* run) {
+template <typename CountFn, typename KeepFn>
+__device__ __forceinline__ int expert_offsets(CountFn count, KeepFn keep, int E, int I, int packed_limit,
+                                              int* off, int* kk_s, int* ch0, int* run) {
     const int lane = threadIdx.x & 63;
     int k4[4], w4 = 0;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
         const int e = lane * 4 + q;
-        k4[q] = e < E ? min(max(keep[e], 0), I) : 0;
+        k4[q] = e < E ? min(max(keep(e), 0), I) : 0;
         w4 += packed_width(k4[q]);
     }
     // packed channel offsets (a prefix of at most 256 * 2^20 fits in int)
@@ -164,10 +163,12 @@ __device__ __forceinline__ int expert_offsets(CountFn count, const int32_t* __re
             off[e] = base;
             kk_s[e] = k4[q];
             run[e] = 0;
+        } else {
+            kk_s[e] = -1;  // below every width: the down-order ranking counts no such entry
         }
         base += c4[q];
     }
-    return __shfl(inc, 63, 64);
+    return lane63(inc);
 }
 
 // One wave: segment table (shared expert first: its tiles carry the longest
@@ -226,19 +227,19 @@ __device__ void write_tables(CountFn count, const int* off, const int* kk_s, con
             m.rt0 = s < hs ? 0 : c4 + i4 - n4;
             seg[s] = m;
         }
-        c1 += __shfl(i1, 63, 64);
-        c3 += __shfl(i3, 63, 64);
-        c4 += __shfl(i4, 63, 64);
+        c1 += lane63(i1);
+        c3 += lane63(i3);
+        c4 += lane63(i4);
     }
     // The down GEMM's tile order: the shared expert, then the routed experts
     // by decreasing width k_e (ties: lower id first), so that the longest
     // reductions are handed out first.  The bucketed forward keeps its
     // plan's order (one launch per width group).
-    static_assert(kMaxExperts % 4 == 0, "the width reads below stay inside kk_s");
+    static_assert(kMaxExperts == 4 * 64, "expert_offsets fills all of kk_s (four entries per lane)");
     // Expert e's rank counts the experts ordered before it, reading the
     // widths four at a time (kk_s is 16-byte aligned and holds kMaxExperts
-    // entries, so the last read stays inside it; entries at or past E are
-    // masked).
+    // entries, so the last read stays inside it; entries at or past E hold
+    // -1, which no width is below, so the count needs no bound check).
     if (hs && lane == 0) {
         ordl[0] = 0;
         order2[0] = 0;
@@ -255,8 +256,7 @@ __device__ void write_tables(CountFn count, const int* off, const int* kk_s, con
                 const int4 v = *reinterpret_cast<const int4*>(&kk_s[q0]);
                 const int kq[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    r += q0 + i < E && (kq[i] > ks || (kq[i] == ks && q0 + i < e));
+                for (int i = 0; i < 4; ++i) r += (kq[i] > ks) + (kq[i] == ks && q0 + i < e);
             }
             pos = r;
         }
@@ -271,7 +271,7 @@ __device__ void write_tables(CountFn count, const int* off, const int* kk_s, con
         const int n2 = i < nseg ? n2s[ordl[i]] : 0;
         const int i2 = wave_incl_scan(n2);
         if (i < nseg) t2start[i] = c2 + i2 - n2;
-        c2 += __shfl(i2, 63, 64);
+        c2 += lane63(i2);
     }
     if (lane == 0) {
         offsets[E] = P;
@@ -400,7 +400,8 @@ __global__ __launch_bounds__(64) void dispatch_scatter_kernel(
     __shared__ int n2s[kMaxExperts + 1];
     __shared__ int ordl[kMaxExperts + 1];
     auto count = [&](int e) { return counts[e]; };
-    const int P = expert_offsets(count, keep, E, I, packed_limit, off, kk_s, ch0, run);
+    auto keep_of = [&](int e) { return keep[e]; };
+    const int P = expert_offsets(count, keep_of, E, I, packed_limit, off, kk_s, ch0, run);
     __syncthreads();
     if (blockIdx.x == 0)
         write_tables(count, off, kk_s, ch0, plan, P, T, E, I, I_shared, d, ts, n2s, ordl, offsets, seg, t1start,
@@ -436,8 +437,12 @@ __global__ __launch_bounds__(64 * kSmallWaves) void dispatch_small_kernel(
     __shared__ int ordl[kMaxExperts + 1];
     __shared__ int32_t sidx[kSmallAssign];
     __shared__ RouteScratch rs[kSmallWaves];
+    __shared__ int keep_s[kMaxExperts];
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     for (int e = lane; e < E; e += 64) hist[wave][e] = 0;
+    // the budget is read while the first wave routes
+    if (wave == kSmallWaves - 1)
+        for (int e = lane; e < E; e += 64) keep_s[e] = keep[e];
     __builtin_amdgcn_wave_barrier();
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
     const int per = ceil_div(T, kSmallWaves);
@@ -480,7 +485,8 @@ __global__ __launch_bounds__(64 * kSmallWaves) void dispatch_small_kernel(
     __syncthreads();
     if (wave == 0) {
         auto count = [&](int e) { return cnt[e]; };
-        const int P = expert_offsets(count, keep, E, I, packed_limit, off, kk_s, ch0, run);
+        auto keep_of = [&](int e) { return keep_s[e]; };
+        const int P = expert_offsets(count, keep_of, E, I, packed_limit, off, kk_s, ch0, run);
         __builtin_amdgcn_wave_barrier();
         __atomic_signal_fence(__ATOMIC_SEQ_CST);
         write_tables(count, off, kk_s, ch0, plan, P, T, E, I, I_shared, d, ts, n2s, ordl, offsets, seg, t1start,

@@ -189,6 +189,30 @@ def test_bf16_decode_with_shared_expert_every_output_written(T):
             assert np.array_equal(y, y_to_f64(fm.to_host(yb)))
 
 
+@pytest.mark.parametrize("T", [1, 2, 3, 5, 7, 8])
+def test_bf16_vector_alu_decode_tiles(T):
+    """Up to 8 tokens the 16-wide weight-streaming tiles run on the vector
+    ALUs: each segment's rows are a template bound of 1, 2, 4 or 8 (T = 3, 5,
+    7 leave rows past the segment's), d = 776 ends in a 256-deep K batch with
+    one 8-wide chunk, I = 264 and I_s = 520 end in partial 16-channel tiles,
+    and the widths cross every chunk and tile edge.  One pass sends every
+    token to expert 2 first, so a routed segment holds all T rows."""
+    E, I = 6, 264
+    cfg, x, lg, w, s = mini_layer("valu%d" % T, 8, 776, E, I, 2, 520, config_id=93)
+    x, lg = x[:T], lg[:T]
+    g = gpu_layer_for(cfg, w, s, max_tokens=8)
+    skew = np.ascontiguousarray(lg + np.array([0, 0, 50, 0, 0, 0], np.float32))
+    tables = (np.full(E, I, np.int32), np.array([1, 7, 9, 15, 17, 263], np.int32),
+              np.array([8, 16, 0, 255, 256, 257], np.int32))
+    for logits in (lg, skew):
+        for keep in tables:
+            say("valu T", T, "keep", keep.tolist())
+            y, r = g.forward(x, logits, keep)
+            ref, rr = oracle_ref(cfg, x, logits, w, s, keep)
+            check_route(r, rr)
+            check_y(y, ref, BF16_TOL)
+
+
 def test_all_tokens_on_one_expert_and_ties():
     cfg, x, lg, w, s = mini_layer("skew", 257, 128, 8, 128, 2, 0, config_id=71)
     g = gpu_layer_for(cfg, w, s)
