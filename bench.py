@@ -53,8 +53,9 @@ PEAK_F32_TFLOPS = 157.3      # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
 RIDGE = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
 DECODE_MAX_T = 64            # the library runs its weight-streaming GEMMs for T <= 64 (bf16)
-DECODE_WIDE_T = 16           # above this many tokens the routed experts' take 64-wide tiles once T*k >= 8*E
-DECODE_WIDE_SHARED_T = 5     # above this many tokens the shared expert's take them
+GEMV_MAX_T = 8               # up to this many tokens the routed experts' GEMMs run on the vector ALUs,
+                             # above it on 64-wide matrix-core tiles
+DECODE_WIDE_SHARED_T = 5     # above this many tokens the shared expert's take the 64-wide tiles
 HEADLINE = "mixtral_8x7b"
 EXTRAS = ("qwen2_prefill", "decode", "qwen15")
 
@@ -369,15 +370,13 @@ def gate_up_kernel_name(cfg, T):
         return "gemm1_f32_kernel"
     if T > DECODE_MAX_T:
         return "gemm1_big_kernel"
-    wide_rt = T > DECODE_WIDE_T and T * cfg.top_k >= 8 * cfg.E
-    wide_sh = T > DECODE_WIDE_SHARED_T
+    routed = "gemm1_decode_wide_kernel" if T > GEMV_MAX_T else "gemv1_kernel"
     if not cfg.I_shared:
-        return "gemm1_decode_wide_kernel" if wide_rt else "gemm1_decode_kernel"
-    names = {"gemm1_decode_wide_kernel" if wide_rt else "gemm1_decode_kernel",
-             "gemm1_decode_wide_kernel" if wide_sh else "gemm1_decode_kernel"}
-    if len(names) == 1:
-        return names.pop()
-    return "gemm1_decode_kernel for the routed experts, gemm1_decode_wide_kernel for the shared expert"
+        return routed
+    shared = "gemm1_decode_wide_kernel" if T > DECODE_WIDE_SHARED_T else "gemv1_kernel"
+    if routed == shared:
+        return routed
+    return "%s for the routed experts, %s for the shared expert" % (routed, shared)
 
 
 def roofline_of(wl, alg, kt, steps, bf16, workload, keep_label):

@@ -13,9 +13,12 @@ constexpr int kRouteTokens = 16;   // tokens per routing block (= dispatch chunk
 constexpr int kSmallAssign = 1024; // T * top_k at or below which one workgroup dispatches
                                    // (every decode-sized batch: T <= 64, top_k <= 16)
 constexpr int kSmallWaves = 16;    // waves of that workgroup
-constexpr int kSmallRouteT = 16;   // above this many tokens route_kernel routes first (one token
+constexpr int kSmallRouteT = 64;   // above this many tokens route_kernel routes first (one token
                                    // per wave on several compute units) and the workgroup only
-                                   // dispatches
+                                   // dispatches.  Up to 64 the workgroup also routes: submitted
+                                   // before the shared expert's GEMMs, it holds a compute unit,
+                                   // where a second kernel would wait for one behind their
+                                   // workgroups (1-2 % per decode step at 17-64 tokens)
 
 typedef uint16_t bf16_t;           // raw bf16 bits in memory
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));

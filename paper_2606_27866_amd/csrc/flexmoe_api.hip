@@ -111,10 +111,10 @@ constexpr int kSideWaves = 4;
 int shared_ks2(const flexmoe_layer_desc& D, int T) {
     if (D.I_shared <= 0 || D.dtype != FLEXMOE_BF16) return 0;
     // weight streaming: chunks of one routed expert's worth of channels, two
-    // above kDecodeWideT tokens, where the shared expert's wide down tiles
+    // above kSharedSplit2T tokens, where the shared expert's wide down tiles
     // compete with the routed experts' (fewer, longer tiles measured 1.3-2 %
     // faster per step there, 0.4-0.9 % slower at 1 and 8 tokens)
-    if (T <= kDecodeMaxT) return T > kDecodeWideT ? std::min(2 * D.I, D.I_shared) : D.I;
+    if (T <= kDecodeMaxT) return T > kSharedSplit2T ? std::min(2 * D.I, D.I_shared) : D.I;
     const long long sh_tiles = (long long)ceil_div(T, kBigBM2) * ceil_div(D.d, kBigBN2);
     if (sh_tiles >= kComputeUnits) return 0;
     const long long p = std::min<long long>(ceil_div(kComputeUnits, (int)sh_tiles), D.I_shared / kMinSplitK);
@@ -535,15 +535,14 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return hip_fail(e, "plan upload");
     }
-    // 64-wide weight-streaming tiles whose workgroup shares the token rows
-    // through LDS (16-wide tiles each re-read every row of their segment).
-    // The shared expert (T rows) takes them from 6 tokens on (measured on the
-    // Qwen2-57B shape: even at 4 tokens, 1.04x slower at 1 token, faster from
-    // 6); the routed experts above 16 tokens once they average 8 rows (fewer
-    // rows leave little to share, and the wider tiles hold more LDS per
-    // compute unit).
+    // Weight-streaming tiles: up to kGemvMaxT tokens the routed experts run
+    // 16-wide tiles on the vector ALUs; above, 64-wide tiles on the matrix
+    // cores, whose workgroups share the token rows through LDS (measured on
+    // the Qwen2-57B shape: 5-15 % faster per decode step from 9 to 48 tokens
+    // than 16-wide matrix-core tiles).  The shared expert (T rows) takes the
+    // wide tiles from kDecodeWideSharedT + 1 = 6 tokens on.
     const bool wide_sh = decode && T > kDecodeWideSharedT;
-    const bool wide_rt = decode && T > kDecodeWideT && (long long)T * D.top_k >= 8LL * D.E;
+    const bool wide_rt = decode && T > kGemvMaxT;
     const int dbn = wide_rt ? kDecWideBN : kDecBN;
     const TileShape ts = !bf16   ? TileShape{kF32BM, kF32BN, kF32BM, kF32BN, 0}
                          : decode ? TileShape{kDecodeMaxT, dbn, kDecodeMaxT, dbn, ks2}

@@ -12,9 +12,8 @@
 // that streams at about 7.1 TB/s against 6.3 for plain loads, while
 // non-temporal half-line reads fall to 5.8.
 //
-// Tiles are those of the MFMA weight-streaming kernels (16 channels or
-// output columns of one segment, every row of the segment), so both kernel
-// families run on the same dispatch tables.  The four waves split the
+// A tile is 16 channels (gate/up) or 16 output columns (down) of one
+// segment, for every row of the segment.  The four waves split the
 // reduction into 256-deep batches (wave q: batches q, q+4, ...).  In a
 // batch, lane l holds the 8 consecutive K elements of chunk l%32 of tile
 // rows 2i + l/32 (i < 8), and the same 8 elements of every token row, and
@@ -269,7 +268,7 @@ __global__ __launch_bounds__(64 * GV_WAVES, NR <= 4 ? 4 : 3) void gemv2_kernel(G
     }
 }
 
-hipError_t launch_gemv1_decode(const Gemm1Params<bf16_t>& p, int tiles, hipStream_t s) {
+hipError_t launch_gemm1_decode(const Gemm1Params<bf16_t>& p, int tiles, hipStream_t s) {
     if (tiles <= 0 || p.tokens <= 0 || p.tokens > kGemvMaxT) return hipSuccess;
     if (p.tokens <= 1) gemv1_kernel<1><<<tiles, 64 * GV_WAVES, 0, s>>>(p);
     else if (p.tokens <= 2) gemv1_kernel<2><<<tiles, 64 * GV_WAVES, 0, s>>>(p);
@@ -278,7 +277,7 @@ hipError_t launch_gemv1_decode(const Gemm1Params<bf16_t>& p, int tiles, hipStrea
     return hipGetLastError();
 }
 
-hipError_t launch_gemv2_decode(const Gemm2Params<bf16_t>& p, int tiles, hipStream_t s) {
+hipError_t launch_gemm2_decode(const Gemm2Params<bf16_t>& p, int tiles, hipStream_t s) {
     if (tiles <= 0 || p.tokens <= 0 || p.tokens > kGemvMaxT) return hipSuccess;
     if (p.tokens <= 1) gemv2_kernel<1><<<tiles, 64 * GV_WAVES, 0, s>>>(p);
     else if (p.tokens <= 2) gemv2_kernel<2><<<tiles, 64 * GV_WAVES, 0, s>>>(p);

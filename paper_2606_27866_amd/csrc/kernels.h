@@ -135,14 +135,16 @@ __device__ __forceinline__ bool tile_of(const P& p, int L, int& s, SegMeta& sm, 
 constexpr int kF32BM = 64, kF32BN = 64;
 constexpr int kBigBM1 = 256, kBigBN1 = 128, kBigBM2 = 256, kBigBN2 = 256;
 constexpr int kDecodeMaxT = 64;     // T at or below which the weight-streaming kernels run
-constexpr int kDecBN = 16;          // their channels / output columns per tile
-constexpr int kDecodeWideT = 16;    // above this many tokens the routed experts' weight-streaming
-                                    // GEMMs may take (once T * k >= 8 E)
-constexpr int kDecodeWideSharedT = 5;  // above this many tokens the shared expert's take
-constexpr int kDecWideBN = 64;      // tiles of this many channels / output columns whose token
-                                    // rows are shared through LDS (launch_gemm*_decode_wide)
-constexpr int kGemvMaxT = 8;        // T at or below which the 16-wide weight-streaming tiles run
-                                    // on the vector ALUs (launch_gemv*_decode)
+constexpr int kGemvMaxT = 8;        // T at or below which the routed experts' weight-streaming
+                                    // GEMMs run on the vector ALUs, in tiles of kDecBN channels /
+                                    // output columns (launch_gemm*_decode); above, in tiles of
+                                    // kDecWideBN on the matrix cores (launch_gemm*_decode_wide)
+constexpr int kDecBN = 16;
+constexpr int kDecWideBN = 64;
+constexpr int kDecodeWideSharedT = 5;  // above this many tokens the shared expert takes the wide
+                                       // tiles too
+constexpr int kSharedSplit2T = 16;  // above this many (decode) tokens the shared expert's down
+                                    // reduction is split into chunks of 2 I channels, else of I
 
 __global__ void route_kernel(const float* logits, int T, int E, int k, int norm_topk, int32_t* idx,
                              float* wts, int32_t* blockcnt, int NB);
@@ -174,13 +176,11 @@ hipError_t launch_gemm1_big(const Gemm1Params<bf16_t>& p, int grid, hipStream_t 
 // alone: no other launch runs beside this one (the shared expert is not on
 // the side stream); the kernel then takes all of a compute unit's LDS.
 hipError_t launch_gemm2_big(const Gemm2Params<bf16_t>& p, int grid, hipStream_t s, bool alone);
+// T <= kGemvMaxT: 16-wide tiles on the vector ALUs (gemv_decode.hip).
 hipError_t launch_gemm1_decode(const Gemm1Params<bf16_t>& p, int tiles, hipStream_t s);
 hipError_t launch_gemm2_decode(const Gemm2Params<bf16_t>& p, int tiles, hipStream_t s);
-// T <= kGemvMaxT: the same tiles on the vector ALUs (launch_gemm*_decode
-// hands them over).
-hipError_t launch_gemv1_decode(const Gemm1Params<bf16_t>& p, int tiles, hipStream_t s);
-hipError_t launch_gemv2_decode(const Gemm2Params<bf16_t>& p, int tiles, hipStream_t s);
-// kDecodeWideT < T <= kDecodeMaxT: tiles of kDecWideBN channels / output columns.
+// T <= kDecodeMaxT: tiles of kDecWideBN channels / output columns on the
+// matrix cores (gemm_decode.hip).
 hipError_t launch_gemm1_decode_wide(const Gemm1Params<bf16_t>& p, int tiles, hipStream_t s);
 hipError_t launch_gemm2_decode_wide(const Gemm2Params<bf16_t>& p, int tiles, hipStream_t s);
 hipError_t launch_gemm1_f32(const Gemm1Params<float>& p, int grid, hipStream_t s);

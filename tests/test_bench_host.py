@@ -124,7 +124,7 @@ def test_kernel_thresholds_match_the_library():
         return int(m.group(1))
 
     assert bench.DECODE_MAX_T == const("kDecodeMaxT")
-    assert bench.DECODE_WIDE_T == const("kDecodeWideT")
+    assert bench.GEMV_MAX_T == const("kGemvMaxT")
     assert bench.DECODE_WIDE_SHARED_T == const("kDecodeWideSharedT")
 
 
@@ -158,9 +158,10 @@ def test_step_stats_are_order_statistics_of_the_steps():
     assert st["mean"] == pytest.approx(ms.mean())
 
 
-@pytest.mark.parametrize("T,name", [(1, "gemm1_decode_kernel"), (5, "gemm1_decode_kernel"),
-                                    (8, "gemm1_decode_kernel for the routed experts, gemm1_decode_wide_kernel "
+@pytest.mark.parametrize("T,name", [(1, "gemv1_kernel"), (5, "gemv1_kernel"),
+                                    (8, "gemv1_kernel for the routed experts, gemm1_decode_wide_kernel "
                                         "for the shared expert"),
+                                    (9, "gemm1_decode_wide_kernel"),
                                     (64, "gemm1_decode_wide_kernel"), (65, "gemm1_big_kernel")])
 def test_gate_up_kernel_named_from_the_library_thresholds(T, name):
     cfg = synth.CONFIGS["qwen2_57b_a14b_decode"]
