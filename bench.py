@@ -106,7 +106,7 @@ def parse(argv=None):
 
 def kernel_src_hash():
     h = hashlib.sha256()
-    for f in ("gemm_bf16_big.hip", "gemm_decode.hip", "common.h", "kernels.h", "mfma_tile.h"):
+    for f in ("gemm_bf16_big.hip", "gemm_decode.hip", "gemv_decode.hip", "common.h", "kernels.h", "mfma_tile.h"):
         h.update(open(os.path.join(ROOT, "paper_2606_27866_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
 
