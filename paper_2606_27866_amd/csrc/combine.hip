@@ -116,7 +116,7 @@ __global__ __launch_bounds__(256) void combine_bf16_kernel(const bf16_t* __restr
     uint32_t u[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-        u[i] = (uint32_t)f32_to_bf16(acc[2 * i]) | ((uint32_t)f32_to_bf16(acc[2 * i + 1]) << 16);
+        u[i] = pack_bf16x2(acc[2 * i], acc[2 * i + 1]);
     *reinterpret_cast<uint4*>(y + (size_t)t * d + n) = make_uint4(u[0], u[1], u[2], u[3]);
 }
 
@@ -133,8 +133,8 @@ __global__ __launch_bounds__(256) void combine_kernel(const OutT* __restrict__ O
         if constexpr (sizeof(OutT) == 4) {
             *reinterpret_cast<float4*>(y + (size_t)t * d + n) = acc;
         } else {
-            const uint32_t lo = (uint32_t)f32_to_bf16(acc.x) | ((uint32_t)f32_to_bf16(acc.y) << 16);
-            const uint32_t hi = (uint32_t)f32_to_bf16(acc.z) | ((uint32_t)f32_to_bf16(acc.w) << 16);
+            const uint32_t lo = pack_bf16x2(acc.x, acc.y);
+            const uint32_t hi = pack_bf16x2(acc.z, acc.w);
             *reinterpret_cast<uint2*>(y + (size_t)t * d + n) = make_uint2(lo, hi);
         }
     }

@@ -28,19 +28,24 @@ __device__ __forceinline__ float bf16_to_f32(bf16_t b) {
     return __uint_as_float(((uint32_t)b) << 16);
 }
 
-// Round to nearest even; NaN becomes a quiet NaN.
+// Round to nearest even (v_cvt_pk_bf16_f32, which also keeps NaNs NaN and
+// fp32 denormals as bf16 denormals: the kernels run with denormals
+// preserved).
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float float2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ bf16_t f32_to_bf16(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return (bf16_t)(u >> 16);
+    return __builtin_bit_cast(bf16_t, (__bf16)f);
+}
+// Two values rounded as above in one instruction: lo in bits 0-15.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(float2_t{lo, hi}, bf16x2_t));
 }
 
-// x * sigmoid(x) in fp32 via the hardware exp2.  For x -> -inf the quotient
-// tends to -0, for x -> +inf to x.
+// x * sigmoid(x) in fp32 via the hardware exp2 and reciprocal (1 ulp each).
+// For x -> -inf the product tends to -0, for x -> +inf to x.
 __device__ __forceinline__ float silu_fast(float x) {
-    float e = __builtin_amdgcn_exp2f(-x * 1.4426950408889634f);
-    return x / (1.0f + e);
+    const float e = __builtin_amdgcn_exp2f(-x * 1.4426950408889634f);
+    return x * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
 __host__ __device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }

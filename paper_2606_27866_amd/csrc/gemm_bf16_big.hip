@@ -359,9 +359,9 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
                         const int v = q * 4 + h * 2;
                         const float g0 = acc[i][jj][v], u0 = acc[i][jj + NF / 2][v];
                         const float g1 = acc[i][jj][v + 1], u1 = acc[i][jj + NF / 2][v + 1];
-                        const uint32_t lo = ch + h * 2 < sm.kk ? f32_to_bf16(silu_fast(g0) * u0) : 0u;
-                        const uint32_t hi = ch + h * 2 + 1 < sm.kk ? f32_to_bf16(silu_fast(g1) * u1) : 0u;
-                        w[h] = lo | (hi << 16);
+                        const float lo = ch + h * 2 < sm.kk ? silu_fast(g0) * u0 : 0.f;
+                        const float hi = ch + h * 2 + 1 < sm.kk ? silu_fast(g1) * u1 : 0.f;
+                        w[h] = pack_bf16x2(lo, hi);
                     }
                     *reinterpret_cast<uint2*>(hr + ch) = make_uint2(w[0], w[1]);
                 }
@@ -386,10 +386,8 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
 #pragma unroll
                             for (int h = 0; h < 2; ++h) {
                                 const int v = q * 4 + h * 2;
-                                gw[h] = (uint32_t)f32_to_bf16(acc[i][jj][v]) |
-                                        ((uint32_t)f32_to_bf16(acc[i][jj][v + 1]) << 16);
-                                uw[h] = (uint32_t)f32_to_bf16(acc[i][jj + NF / 2][v]) |
-                                        ((uint32_t)f32_to_bf16(acc[i][jj + NF / 2][v + 1]) << 16);
+                                gw[h] = pack_bf16x2(acc[i][jj][v], acc[i][jj][v + 1]);
+                                uw[h] = pack_bf16x2(acc[i][jj + NF / 2][v], acc[i][jj + NF / 2][v + 1]);
                             }
                             const size_t off = frag_blocked(rbase + row, ch, ldh);
                             *reinterpret_cast<uint2*>(Gb + off) = make_uint2(gw[0], gw[1]);
@@ -417,10 +415,8 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
                     for (int q = 0; q < 4; ++q) {
                         const int n = ntile * BN + wn * WCOL + j * 32 + q * 8 + sub;
                         if (n >= d) continue;
-                        const uint32_t w0 = (uint32_t)f32_to_bf16(acc[i][j][q * 4]) |
-                                            ((uint32_t)f32_to_bf16(acc[i][j][q * 4 + 1]) << 16);
-                        const uint32_t w1 = (uint32_t)f32_to_bf16(acc[i][j][q * 4 + 2]) |
-                                            ((uint32_t)f32_to_bf16(acc[i][j][q * 4 + 3]) << 16);
+                        const uint32_t w0 = pack_bf16x2(acc[i][j][q * 4], acc[i][j][q * 4 + 1]);
+                        const uint32_t w1 = pack_bf16x2(acc[i][j][q * 4 + 2], acc[i][j][q * 4 + 3]);
                         *reinterpret_cast<uint2*>(orow + n) = make_uint2(w0, w1);
                     }
             }

@@ -237,7 +237,7 @@ __device__ __forceinline__ void wide_tile(const Gemm1Params<bf16_t>& p1, const G
                     lo = acc[0][f][2 * h];
                     hi = acc[0][f][2 * h + 1];
                 }
-                v[h] = (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+                v[h] = pack_bf16x2(lo, hi);
             }
             bf16_t* dst;
             if constexpr (kGateUp)

@@ -75,7 +75,7 @@ __global__ __launch_bounds__(256) void train_prep_kernel(const float* __restrict
     uint32_t pk[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-        pk[i] = (uint32_t)f32_to_bf16(w * v[2 * i]) | ((uint32_t)f32_to_bf16(w * v[2 * i + 1]) << 16);
+        pk[i] = pack_bf16x2(w * v[2 * i], w * v[2 * i + 1]);
     *reinterpret_cast<uint4*>(out) = make_uint4(pk[0], pk[1], pk[2], pk[3]);
 }
 
