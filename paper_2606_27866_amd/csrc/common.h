@@ -143,16 +143,22 @@ namespace flexmoe {
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // Segment owning tile L: the largest s with tstart[s] <= L (segments with no
-// tiles share their start with the next one and are skipped).  The table is
-// uniform across the block, so this runs on scalar loads.
+// tiles share their start with the next one and are skipped).  tstart is
+// non-decreasing, so that is one less than the number of entries <= L: each
+// lane reads entries lane, lane + 64, ... all at once and ballots count them
+// -- one memory round trip at the start of every GEMM workgroup, where a
+// binary search took log2(nseg) dependent ones.  All 64 lanes must be active
+// (every caller runs it first thing, workgroup-uniform).
 __device__ __forceinline__ int find_segment(const int32_t* tstart, int nseg, int L) {
-    int lo = 0, hi = nseg - 1;
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (tstart[mid] <= L) lo = mid;
-        else hi = mid - 1;
-    }
-    return lo;
+    constexpr int NJ = (kMaxExperts + 1 + 63) / 64;  // segments: the experts and a shared expert
+    const int lane = threadIdx.x & 63;
+    int v[NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) v[j] = tstart[min(j * 64 + lane, nseg)];  // tstart holds nseg + 1 entries
+    int cnt = 0;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) cnt += __popcll(__ballot(j * 64 + lane < nseg && v[j] <= L));
+    return cnt - 1;
 }
 
 // Fragment-blocked layout of a [rows][C] bf16 matrix (C a multiple of 8):

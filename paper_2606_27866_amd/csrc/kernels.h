@@ -121,8 +121,9 @@ __device__ __forceinline__ bool tile_of(const P& p, int L, int& s, SegMeta& sm, 
         local = L;
         return true;
     }
-    L += p.tstart[p.seg_lo];
-    if (L >= p.tstart[p.seg_hi]) return false;
+    const int t_lo = p.tstart[p.seg_lo], t_hi = p.tstart[p.seg_hi];  // both requested before either is used
+    L += t_lo;
+    if (L >= t_hi) return false;
     const int i = find_segment(p.tstart, p.nseg, L);
     s = order_of(p, i);
     sm = p.seg[s];
