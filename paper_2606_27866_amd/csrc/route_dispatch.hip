@@ -176,8 +176,9 @@ __device__ __forceinline__ int expert_offsets(CountFn count, KeepFn keep, int E,
 // tile counts in segment order, and the down GEMM's tile order (order2, see
 // Gemm2Params::order) with its tile counts scanned in that order, 64
 // segments per round.  n2s and ordl are LDS scratch of nseg entries.
-template <typename CountFn>
-__device__ void write_tables(CountFn count, const int* off, const int* kk_s, const int* ch0,
+// rank(e): the number of experts ordered before expert e (see below).
+template <typename CountFn, typename RankFn>
+__device__ void write_tables(CountFn count, RankFn rank, const int* off, const int* kk_s, const int* ch0,
                              const int32_t* __restrict__ plan, int P, int T, int E, int I,
                              int I_shared, int d, TileShape ts, int* n2s, int* ordl,
                              int32_t* __restrict__ offsets, SegMeta* __restrict__ seg,
@@ -235,11 +236,6 @@ __device__ void write_tables(CountFn count, const int* off, const int* kk_s, con
     // by decreasing width k_e (ties: lower id first), so that the longest
     // reductions are handed out first.  The bucketed forward keeps its
     // plan's order (one launch per width group).
-    static_assert(kMaxExperts == 4 * 64, "expert_offsets fills all of kk_s (four entries per lane)");
-    // Expert e's rank counts the experts ordered before it, reading the
-    // widths four at a time (kk_s is 16-byte aligned and holds kMaxExperts
-    // entries, so the last read stays inside it; entries at or past E hold
-    // -1, which no width is below, so the count needs no bound check).
     if (hs && lane == 0) {
         ordl[0] = 0;
         order2[0] = 0;
@@ -247,19 +243,7 @@ __device__ void write_tables(CountFn count, const int* off, const int* kk_s, con
     for (int e0 = 0; e0 < E; e0 += 64) {
         const int e = e0 + lane;
         if (e >= E) continue;
-        int pos = e;
-        if (!plan) {
-            const int ks = kk_s[e];
-            int r = 0;
-#pragma unroll 4
-            for (int q0 = 0; q0 < E; q0 += 4) {
-                const int4 v = *reinterpret_cast<const int4*>(&kk_s[q0]);
-                const int kq[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-                for (int i = 0; i < 4; ++i) r += (kq[i] > ks) + (kq[i] == ks && q0 + i < e);
-            }
-            pos = r;
-        }
+        const int pos = plan ? e : rank(e);
         ordl[hs + pos] = hs + e;
         order2[hs + pos] = hs + e;
     }
@@ -278,6 +262,18 @@ __device__ void write_tables(CountFn count, const int* off, const int* kk_s, con
         t1start[nseg] = c1;
         t2start[nseg] = c2;
     }
+}
+
+// Expert e's place in the down GEMM's order counts the experts ordered
+// before it: wider ones, and equal widths with a lower id.  width_rank4 adds
+// the experts q0 .. q0+3, read as one 16-byte LDS access (kk_s is 16-byte
+// aligned and holds kMaxExperts entries; entries at or past E hold -1, which
+// no width is below, so the count needs no bound check).
+static_assert(kMaxExperts == 4 * 64, "expert_offsets fills all of kk_s (four entries per lane)");
+__device__ __forceinline__ int width_rank4(const int* kk_s, int q0, int ks, int e) {
+    const int4 v = *reinterpret_cast<const int4*>(&kk_s[q0]);
+    return (v.x > ks) + (v.x == ks && q0 < e) + (v.y > ks) + (v.y == ks && q0 + 1 < e) + (v.z > ks) +
+           (v.z == ks && q0 + 2 < e) + (v.w > ks) + (v.w == ks && q0 + 3 < e);
 }
 
 // One wave: stable placement of assignments [a0, a1) in rounds of 64.  The
@@ -403,9 +399,17 @@ __global__ __launch_bounds__(64) void dispatch_scatter_kernel(
     auto keep_of = [&](int e) { return keep[e]; };
     const int P = expert_offsets(count, keep_of, E, I, packed_limit, off, kk_s, ch0, run);
     __syncthreads();
-    if (blockIdx.x == 0)
-        write_tables(count, off, kk_s, ch0, plan, P, T, E, I, I_shared, d, ts, n2s, ordl, offsets, seg, t1start,
-                     t2start, order2);
+    if (blockIdx.x == 0) {
+        auto rank = [&](int e) {
+            const int ks = kk_s[e];
+            int r = 0;
+#pragma unroll 4
+            for (int q0 = 0; q0 < E; q0 += 4) r += width_rank4(kk_s, q0, ks, e);
+            return r;
+        };
+        write_tables(count, rank, off, kk_s, ch0, plan, P, T, E, I, I_shared, d, ts, n2s, ordl, offsets, seg,
+                     t1start, t2start, order2);
+    }
     const int a0 = blockIdx.x * kRouteTokens * k;
     const int a1 = min((blockIdx.x + 1) * kRouteTokens, T) * k;
     auto base = [&](int e) { return off[e] + blockbase[(size_t)e * NB + blockIdx.x]; };
@@ -438,6 +442,7 @@ __global__ __launch_bounds__(64 * kSmallWaves) void dispatch_small_kernel(
     __shared__ int32_t sidx[kSmallAssign];
     __shared__ RouteScratch rs[kSmallWaves];
     __shared__ int keep_s[kMaxExperts];
+    __shared__ int part[kSmallWaves][kMaxExperts];  // per-wave partial counts of the width ranks
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     for (int e = lane; e < E; e += 64) hist[wave][e] = 0;
     // the budget is read while the first wave routes
@@ -483,14 +488,35 @@ __global__ __launch_bounds__(64 * kSmallWaves) void dispatch_small_kernel(
         counts[e] = c;
     }
     __syncthreads();
+    auto count = [&](int e) { return cnt[e]; };
+    int P = 0;
     if (wave == 0) {
-        auto count = [&](int e) { return cnt[e]; };
         auto keep_of = [&](int e) { return keep_s[e]; };
-        const int P = expert_offsets(count, keep_of, E, I, packed_limit, off, kk_s, ch0, run);
-        __builtin_amdgcn_wave_barrier();
-        __atomic_signal_fence(__ATOMIC_SEQ_CST);
-        write_tables(count, off, kk_s, ch0, plan, P, T, E, I, I_shared, d, ts, n2s, ordl, offsets, seg, t1start,
-                     t2start, order2);
+        P = expert_offsets(count, keep_of, E, I, packed_limit, off, kk_s, ch0, run);
+    }
+    __syncthreads();
+    // the down GEMM's order: every wave counts, for each expert, the experts
+    // of its share of the width table ordered before it (wave w: entries 4w
+    // .. 4w+3, then 64 further on, ...); the first wave adds the shares
+    if (!plan) {
+        for (int e0 = 0; e0 < E; e0 += 64) {
+            const int e = e0 + lane;
+            const int ks = kk_s[min(e, kMaxExperts - 1)];
+            int r = 0;
+            for (int q0 = wave * 4; q0 < E; q0 += kSmallWaves * 4) r += width_rank4(kk_s, q0, ks, e);
+            if (e < E) part[wave][e] = r;
+        }
+    }
+    __syncthreads();
+    if (wave == 0) {
+        auto rank = [&](int e) {
+            int r = 0;
+#pragma unroll
+            for (int w = 0; w < kSmallWaves; ++w) r += part[w][e];
+            return r;
+        };
+        write_tables(count, rank, off, kk_s, ch0, plan, P, T, E, I, I_shared, d, ts, n2s, ordl, offsets, seg,
+                     t1start, t2start, order2);
     }
     __syncthreads();
     // this wave's running position inside each expert starts at its base
