@@ -18,7 +18,9 @@
 //     XOR-swizzled by bits 1..3 of the row index, so the 16 lanes served in
 //     one LDS cycle of a fragment read hit 64 distinct banks.
 //   - two LDS stages of 64 KB: the loads of K tile t+1 are in flight while
-//     tile t is multiplied.  MFMA operand fragments are read from LDS one
+//     tile t is multiplied (a launch with the GPU to itself takes a third
+//     token-row stage, 160 KB in all, so that half of each tile's DMAs
+//     leave before the barrier).  MFMA operand fragments are read from LDS one
 //     16-deep step ahead of their use.  This keeps the kernel near 200 VGPRs:
 //     its two waves per SIMD then leave room on every compute unit for the
 //     small routing kernels of a concurrently dispatched batch, which a
@@ -58,7 +60,7 @@ constexpr int WM = 2, WN = NWAVE / WM;      // wave grid
 static_assert(BM == WM * 128, "a full tile gives each M-wave four 32-row fragments");
 constexpr int NF = BN / (WN * 32);          // 32-column fragments per wave
 constexpr int WCOL = BN / WN;               // weight rows per wave
-constexpr int NSTAGE = 2;                   // LDS stages of BK-deep token-row (A) tiles
+constexpr int NSB = 2;                      // LDS stages of BK-deep weight (B) tiles
 constexpr int NSTEP = BK / 16;              // 16-deep MFMA steps per K tile
 static_assert(NSTEP == 4, "the K-loop schedule is laid out for four steps per K tile");
 constexpr int RPI = 64 / CHUNKS;            // LDS rows filled per DMA instruction
@@ -67,10 +69,10 @@ constexpr int NI = ROWS_PER_WAVE / RPI;     // DMA instructions per wave per ope
 constexpr int LOADS_PER_TILE = 2 * NI;      // DMA instructions per lane per K tile
 constexpr int STAGE_A = BM * ROWB;          // 32 KB
 constexpr int STAGE_B = BN * ROWB;          // 32 KB
-// LDS of a workgroup with NSB stages of weight (B) tiles: 128 KB for two,
+// LDS of a workgroup with NSA stages of token-row (A) tiles: 128 KB for two,
 // 160 KB -- all of a compute unit's LDS -- for three.
-template <int NSB>
-constexpr int smem_bytes() { return NSTAGE * STAGE_A + NSB * STAGE_B; }
+template <int NSA>
+constexpr int smem_bytes() { return NSA * STAGE_A + NSB * STAGE_B; }
 static_assert(smem_bytes<3>() <= 160 * 1024, "the stages fit the compute unit's LDS");
 constexpr int XCD_GROUP = 8;                // consecutive tiles kept on one XCD
 constexpr int ROW_GROUP = 4;                // row tiles of a segment walked before the next column
@@ -123,9 +125,10 @@ __device__ __forceinline__ void train_store_h_transposed(const Gemm1Params<bf16_
 // kTrain: 0 = inference; 1 = also g and u of the routed rows
 // (fragment-blocked) and their h transposed (channel saliency); 2 = also g
 // and u of every row, fragment-blocked (the masked layer's training backward).
-// NSB: LDS stages of weight tiles (2, or 3: the weights of K tile kt+3 are
-// requested with the token rows of kt+2, two tiles ahead of their use).
-template <bool kGateUp, int kTrain = 0, int NSB = 2>
+// NSA: LDS stages of token-row tiles (2, or 3: token-row tile kt+2 is then
+// requested during the first MFMA step of tile kt instead of after the
+// barrier, so each barrier releases half as many DMAs).
+template <bool kGateUp, int kTrain = 0, int NSA = 2>
 __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Gemm2Params<bf16_t>& p2,
                                          unsigned char* smem) {
     const int d = kGateUp ? p1.d : p2.d;
@@ -230,7 +233,7 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
         for (int i = 0; i < NI; ++i) load_lds16(ra, acol[i] < lim ? aoff[i] : kOOB, soff, sa + i * RPI * ROWB);
     };
     auto issue_b = [&](int kt, int stage) {
-        unsigned char* sb = smem + NSTAGE * STAGE_A + stage * STAGE_B + wave * ROWS_PER_WAVE * ROWB;
+        unsigned char* sb = smem + NSA * STAGE_A + stage * STAGE_B + wave * ROWS_PER_WAVE * ROWB;
         const int lim = K - kt * BK;
         const uint32_t soff = (uint32_t)(kt * BK) * 2u;
 #pragma unroll
@@ -264,8 +267,8 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
                 for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
         bf16x8 a[2][MFW], b[2][NF];  // fragment buffers of alternate steps
         auto read_frags = [&](int kt, int ks, int buf) {
-            const unsigned char* sa = smem + (kt % NSTAGE) * STAGE_A;
-            const unsigned char* sb = smem + NSTAGE * STAGE_A + (kt % NSB) * STAGE_B;
+            const unsigned char* sa = smem + (kt % NSA) * STAGE_A;
+            const unsigned char* sb = smem + NSA * STAGE_A + (kt % NSB) * STAGE_B;
             const int chunk = ks * 2 + (lane >> 5);
 #pragma unroll
             for (int i = 0; i < MFW; ++i) a[buf][i] = lds_frag(sa, wm * WR + i * 32 + (lane & 31), chunk);
@@ -280,49 +283,53 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[buf][j], a[buf][i], acc[i][j], 0, 0, 0);
         };
 
-        // Two LDS stages, fragments one step ahead:
+        // Two weight stages, fragments one step ahead:
         //   steps s < 3: read (kt, s+1) | MFMA (kt, s)
         //   wait for tile kt+1 and this wave's reads, barrier
-        //   DMA tile kt+2 into the stage of tile kt | read (kt+1, 0) | MFMA (kt, 3)
+        //   DMA tile kt+2 into the stages of tile kt | read (kt+1, 0) | MFMA (kt, 3)
         // At the barrier every wave has finished reading tile kt (its last
-        // fragments are in registers), so its stage can be refilled, and tile
-        // kt+1 has landed, so its fragments can be read.  Every iteration
-        // issues one tile's DMAs (zero-page loads once past the end), so at
-        // the wait no later tile's loads are outstanding (two stages).
-        // With three B stages the weight tile kt+3 is requested together
-        // with token-row tile kt+2, two K tiles before its use: per
-        // iteration the loads go out as [A(kt+2), B(kt+3)], so at the wait
-        // only B(kt+2) -- issued last -- may still be outstanding.
-        // With three weight stages, weight tile kt+3 is requested after
-        // token-row tile kt+2: at the wait below only that last request may
-        // still be outstanding.
-        constexpr int AHEAD = NSB - NSTAGE;  // weight tiles further ahead (0 or 1)
-        static_assert(AHEAD == 0 || AHEAD == 1, "two or three weight stages");
+        // fragments are in registers), so its stages can be refilled, and
+        // tile kt+1 has landed, so its fragments can be read.  Every
+        // iteration issues one tile's DMAs (zero-page loads once past the
+        // end), so at the wait no later tile's loads are outstanding.
+        // With three token-row stages, token-row tile kt+2 goes into the
+        // stage of tile kt-1 (free since the previous barrier) beside the
+        // MFMAs of step 0, and only the weight tile's DMAs follow the
+        // barrier: the 64 DMAs a barrier used to release at once (8 waves x
+        // 8) queue behind the MFMAs of one step, halved, they do not (the
+        // Mixtral-shaped gate/up GEMM runs 3 % faster).  At the wait that
+        // token-row tile may still be outstanding.
+        static_assert(NSA == 2 || NSA == 3, "two or three token-row stages");
+        constexpr int EARLY = NSA == 3 ? NI : 0;  // DMAs issued before the barrier
         issue_a(0, 0);
         issue_b(0, 0);
         issue_a(1, 1);
         issue_b(1, 1);
-        if constexpr (AHEAD) issue_b(2, 2);
-        __builtin_amdgcn_s_waitcnt(waitcnt_vm((2 + AHEAD) * NI));  // tile 0 in
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * NI));  // tile 0 in
         barrier_no_fence();
         read_frags(0, 0, 0);
         for (int kt = 0; kt < nk; ++kt) {
+            read_frags(kt, 1, 1);
+            if constexpr (NSA == 3) issue_a(kt + 2, (kt + 2) % 3);
+            mfma_step(0);
+            sched_interleave<NMF, EARLY, NRD>();
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int st = 0; st < NSTEP - 1; ++st) {
+            for (int st = 1; st < NSTEP - 1; ++st) {
                 read_frags(kt, st + 1, (st + 1) & 1);
                 mfma_step(st & 1);
                 sched_interleave<NMF, 0, NRD>();
                 __builtin_amdgcn_sched_barrier(0);
             }
-            __builtin_amdgcn_s_waitcnt(waitcnt_vm(AHEAD * NI) & kWaitLgkm0);  // tile kt+1 in; own reads done
+            __builtin_amdgcn_s_waitcnt(waitcnt_vm(EARLY) & kWaitLgkm0);  // tile kt+1 in; own reads done
             barrier_no_fence();  // all waves are done reading tile kt: its stages are free
             __builtin_amdgcn_sched_barrier(0);
-            issue_a(kt + NSTAGE, kt % NSTAGE);
-            issue_b(kt + NSB, kt % NSB);
+            if constexpr (NSA == 2) issue_a(kt + 2, kt % 2);
+            issue_b(kt + 2, kt % 2);
             // after the last tile this reads stale stages, whose values go unused
             read_frags(kt + 1, 0, 0);
             mfma_step((NSTEP - 1) & 1);
-            sched_interleave<NMF, LOADS_PER_TILE, NRD>();
+            sched_interleave<NMF, LOADS_PER_TILE - EARLY, NRD>();
             __builtin_amdgcn_sched_barrier(0);
         }
         __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // no DMA may outlive the workgroup's LDS
@@ -430,9 +437,12 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
     else run(std::integral_constant<int, 1>{});
 }
 
+// NSA = 3 when the launch has the compute units to itself (its 160 KB of LDS
+// leave no room for a concurrent launch's workgroups).
+template <int NSA>
 __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void gemm1_big_kernel(Gemm1Params<bf16_t> p) {
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[smem_bytes<2>()];
-    big_tile<true>(p, Gemm2Params<bf16_t>{}, smem);
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[smem_bytes<NSA>()];
+    big_tile<true, 0, NSA>(p, Gemm2Params<bf16_t>{}, smem);
 }
 
 // The gate/up GEMM of the training forward: the same tiles, plus the
@@ -449,19 +459,19 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void gemm1_big_train_rm_ke
     big_tile<true, 2>(p, Gemm2Params<bf16_t>{}, smem);
 }
 
-// NSB = 3 when the launch has the compute units to itself (its 160 KB of LDS
-// leave no room for a concurrent launch's workgroups): the down GEMM's long
-// reductions then run 2-3 % faster on the Mixtral and Qwen2-57B shapes.
-template <int NSB>
+// NSA = 3 as for the gate/up GEMM: the down GEMM's long reductions then run
+// 4 % faster on the Mixtral and Qwen2-57B shapes.
+template <int NSA>
 __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void gemm2_big_kernel(Gemm2Params<bf16_t> p) {
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[smem_bytes<NSB>()];
-    big_tile<false, 0, NSB>(Gemm1Params<bf16_t>{}, p, smem);
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[smem_bytes<NSA>()];
+    big_tile<false, 0, NSA>(Gemm1Params<bf16_t>{}, p, smem);
 }
 
-hipError_t launch_gemm1_big(const Gemm1Params<bf16_t>& p, int grid, hipStream_t s) {
+hipError_t launch_gemm1_big(const Gemm1Params<bf16_t>& p, int grid, hipStream_t s, bool alone) {
     if (grid <= 0) return hipSuccess;
     const int g = (grid + 8 * XCD_GROUP - 1) / (8 * XCD_GROUP) * (8 * XCD_GROUP);
-    gemm1_big_kernel<<<g, THREADS, 0, s>>>(p);
+    if (alone) gemm1_big_kernel<3><<<g, THREADS, 0, s>>>(p);
+    else gemm1_big_kernel<2><<<g, THREADS, 0, s>>>(p);
     return hipGetLastError();
 }
 

@@ -173,9 +173,9 @@ __global__ void dispatch_small_kernel(const float* logits, int T, int E, int k, 
 __global__ void set_keep_kernel(int32_t* keep, KeepArgs t, int E);
 
 // Launchers (defined next to their kernels).  Each returns the launch status.
-hipError_t launch_gemm1_big(const Gemm1Params<bf16_t>& p, int grid, hipStream_t s);
 // alone: no other launch runs beside this one (the shared expert is not on
 // the side stream); the kernel then takes all of a compute unit's LDS.
+hipError_t launch_gemm1_big(const Gemm1Params<bf16_t>& p, int grid, hipStream_t s, bool alone);
 hipError_t launch_gemm2_big(const Gemm2Params<bf16_t>& p, int grid, hipStream_t s, bool alone);
 // T <= kGemvMaxT: 16-wide tiles on the vector ALUs (gemv_decode.hip).
 hipError_t launch_gemm1_decode(const Gemm1Params<bf16_t>& p, int tiles, hipStream_t s);
