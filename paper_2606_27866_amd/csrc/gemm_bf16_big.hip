@@ -18,8 +18,8 @@
 //     XOR-swizzled by bits 1..3 of the row index, so the 16 lanes served in
 //     one LDS cycle of a fragment read hit 64 distinct banks.
 //   - two LDS stages of 64 KB: the loads of K tile t+1 are in flight while
-//     tile t is multiplied (a launch with the GPU to itself takes a third
-//     token-row stage, 160 KB in all, so that half of each tile's DMAs
+//     tile t is multiplied (a launch that may take all of the LDS takes a
+//     third token-row stage, 160 KB in all, so that half of each tile's DMAs
 //     leave before the barrier).  MFMA operand fragments are read from LDS one
 //     16-deep step ahead of their use.  This keeps the kernel near 200 VGPRs:
 //     its two waves per SIMD then leave room on every compute unit for the
@@ -437,8 +437,8 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
     else run(std::integral_constant<int, 1>{});
 }
 
-// NSA = 3 when the launch has the compute units to itself (its 160 KB of LDS
-// leave no room for a concurrent launch's workgroups).
+// NSA = 3 (160 KB of LDS) except for the shared expert's side-stream
+// launches, which must leave room for the routing kernels beside them.
 template <int NSA>
 __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void gemm1_big_kernel(Gemm1Params<bf16_t> p) {
     __shared__ __attribute__((aligned(1024))) unsigned char smem[smem_bytes<NSA>()];
@@ -467,10 +467,10 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void gemm2_big_kernel(Gemm
     big_tile<false, 0, NSA>(Gemm1Params<bf16_t>{}, p, smem);
 }
 
-hipError_t launch_gemm1_big(const Gemm1Params<bf16_t>& p, int grid, hipStream_t s, bool alone) {
+hipError_t launch_gemm1_big(const Gemm1Params<bf16_t>& p, int grid, hipStream_t s, bool full_lds) {
     if (grid <= 0) return hipSuccess;
     const int g = (grid + 8 * XCD_GROUP - 1) / (8 * XCD_GROUP) * (8 * XCD_GROUP);
-    if (alone) gemm1_big_kernel<3><<<g, THREADS, 0, s>>>(p);
+    if (full_lds) gemm1_big_kernel<3><<<g, THREADS, 0, s>>>(p);
     else gemm1_big_kernel<2><<<g, THREADS, 0, s>>>(p);
     return hipGetLastError();
 }
@@ -489,10 +489,10 @@ hipError_t launch_gemm1_big_train_rm(const Gemm1Params<bf16_t>& p, int grid, hip
     return hipGetLastError();
 }
 
-hipError_t launch_gemm2_big(const Gemm2Params<bf16_t>& p, int grid, hipStream_t s, bool alone) {
+hipError_t launch_gemm2_big(const Gemm2Params<bf16_t>& p, int grid, hipStream_t s, bool full_lds) {
     if (grid <= 0) return hipSuccess;
     const int g = (grid + 8 * XCD_GROUP - 1) / (8 * XCD_GROUP) * (8 * XCD_GROUP);
-    if (alone) gemm2_big_kernel<3><<<g, THREADS, 0, s>>>(p);
+    if (full_lds) gemm2_big_kernel<3><<<g, THREADS, 0, s>>>(p);
     else gemm2_big_kernel<2><<<g, THREADS, 0, s>>>(p);
     return hipGetLastError();
 }

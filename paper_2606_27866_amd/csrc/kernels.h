@@ -173,10 +173,13 @@ __global__ void dispatch_small_kernel(const float* logits, int T, int E, int k, 
 __global__ void set_keep_kernel(int32_t* keep, KeepArgs t, int E);
 
 // Launchers (defined next to their kernels).  Each returns the launch status.
-// alone: no other launch runs beside this one (the shared expert is not on
-// the side stream); the kernel then takes all of a compute unit's LDS.
-hipError_t launch_gemm1_big(const Gemm1Params<bf16_t>& p, int grid, hipStream_t s, bool alone);
-hipError_t launch_gemm2_big(const Gemm2Params<bf16_t>& p, int grid, hipStream_t s, bool alone);
+// full_lds: the launch takes all of a compute unit's LDS (a third token-row
+// stage).  Not for the shared expert's side-stream launches, which start
+// beside the routing kernels and would lock them out of the compute units;
+// the routed launches that follow the routing may (they and the side-stream
+// launches cannot share a compute unit's LDS either way).
+hipError_t launch_gemm1_big(const Gemm1Params<bf16_t>& p, int grid, hipStream_t s, bool full_lds);
+hipError_t launch_gemm2_big(const Gemm2Params<bf16_t>& p, int grid, hipStream_t s, bool full_lds);
 // T <= kGemvMaxT: 16-wide tiles on the vector ALUs (gemv_decode.hip).
 hipError_t launch_gemm1_decode(const Gemm1Params<bf16_t>& p, int tiles, hipStream_t s);
 hipError_t launch_gemm2_decode(const Gemm2Params<bf16_t>& p, int tiles, hipStream_t s);
