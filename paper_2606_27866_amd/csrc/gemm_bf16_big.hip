@@ -292,13 +292,13 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
         // tile kt+1 has landed, so its fragments can be read.  Every
         // iteration issues one tile's DMAs (zero-page loads once past the
         // end), so at the wait no later tile's loads are outstanding.
-        // With three token-row stages, token-row tile kt+2 goes into the
-        // stage of tile kt-1 (free since the previous barrier) beside the
-        // MFMAs of step 0, and only the weight tile's DMAs follow the
-        // barrier: the 64 DMAs a barrier used to release at once (8 waves x
-        // 8) queue behind the MFMAs of one step, halved, they do not (the
-        // Mixtral-shaped gate/up GEMM runs 3 % faster).  At the wait that
-        // token-row tile may still be outstanding.
+        // With two stages each wave issues all 8 of its DMAs right after the
+        // barrier, 64 per compute unit at once, and the MFMAs behind them
+        // wait for issue.  With three token-row stages, token-row tile kt+2
+        // goes into the stage of tile kt-1 (free since the previous barrier)
+        // beside the MFMAs of step 0 and only the weight tile's DMAs follow
+        // the barrier (the Mixtral-shaped gate/up GEMM runs 3 % faster); at
+        // the wait that token-row tile may still be outstanding.
         static_assert(NSA == 2 || NSA == 3, "two or three token-row stages");
         constexpr int EARLY = NSA == 3 ? NI : 0;  // DMAs issued before the barrier
         issue_a(0, 0);
