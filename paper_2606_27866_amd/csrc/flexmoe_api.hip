@@ -603,7 +603,7 @@ int forward_impl(const flexmoe_layer_desc* desc, int32_t T, const void* x, const
                     : decode     ? launch_gemm1_decode(p1, (int)n1, st)
                     : train == 1 ? launch_gemm1_big_train(p1, (int)n1, st)
                     : train == 2 ? launch_gemm1_big_train_rm(p1, (int)n1, st)
-                                 : launch_gemm1_big(p1, (int)n1, st, !sh);
+                                 : launch_gemm1_big(p1, (int)n1, st, !sh, !use_side);
             }
             if (e != hipSuccess) return hip_fail(e, "gate/up GEMM launch");
             // the masked layer's down GEMM reduces over the kept channels only

@@ -74,7 +74,7 @@ constexpr int STAGE_B = BN * ROWB;          // 32 KB
 template <int NSA>
 constexpr int smem_bytes() { return NSA * STAGE_A + NSB * STAGE_B; }
 static_assert(smem_bytes<3>() <= 160 * 1024, "the stages fit the compute unit's LDS");
-constexpr int XCD_GROUP = 8;                // consecutive tiles kept on one XCD
+constexpr int XCD_GROUP = 8;                // consecutive tiles kept on one XCD (default)
 constexpr int ROW_GROUP = 4;                // row tiles of a segment walked before the next column
 }  // namespace
 
@@ -128,14 +128,16 @@ __device__ __forceinline__ void train_store_h_transposed(const Gemm1Params<bf16_
 // NSA: LDS stages of token-row tiles (2, or 3: token-row tile kt+2 is then
 // requested during the first MFMA step of tile kt instead of after the
 // barrier, so each barrier releases half as many DMAs).
-template <bool kGateUp, int kTrain = 0, int NSA = 2>
+// XG: consecutive tiles kept on one XCD (XCD_GROUP, or 32 for a gate/up
+// launch with the GPU to itself, see gemm1_big_kernel).
+template <bool kGateUp, int kTrain = 0, int NSA = 2, int XG = XCD_GROUP>
 __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Gemm2Params<bf16_t>& p2,
                                          unsigned char* smem) {
     const int d = kGateUp ? p1.d : p2.d;
 
-    // tile numbering: XCD x = b % 8 takes groups of XCD_GROUP consecutive tiles
+    // tile numbering: XCD x = b % 8 takes runs of XG consecutive tiles
     const int jb = blockIdx.x >> 3;
-    const int L = (jb / XCD_GROUP) * (8 * XCD_GROUP) + (blockIdx.x & 7) * XCD_GROUP + jb % XCD_GROUP;
+    const int L = (jb / XG) * (8 * XG) + (blockIdx.x & 7) * XG + jb % XG;
     int s, local;
     SegMeta sm;
     if (!(kGateUp ? tile_of(p1, L, s, sm, local) : tile_of(p2, L, s, sm, local))) return;
@@ -144,11 +146,12 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
     // reduction chunk, chunk `split` after chunk split-1.  Inside a grid the
     // tiles go in groups of ROW_GROUP row tiles: all columns of a group, each
     // column's row tiles consecutive, then the next group.  An XCD's 32
-    // concurrent tiles (four runs of 8, from consecutive rounds over the 8
-    // XCDs) then share about ROW_GROUP token-row panels and 8 weight panels
-    // through its L2, instead of needing up to 32 token-row panels and 4
-    // weight panels: the L2 misses of the Mixtral-shaped gate/up launch drop
-    // from 13.3 GB to about 5 GB.
+    // concurrent tiles (four runs of 8 from consecutive rounds over the 8
+    // XCDs, or one run of 32) then share about ROW_GROUP token-row panels
+    // and 8 weight panels through its L2, instead of needing up to 32
+    // token-row panels and 4 weight panels: the L2 misses of the
+    // Mixtral-shaped gate/up launch drop from 13.3 GB (one row tile after
+    // another) to 9.5 GB with runs of 8 and 6.8 GB with runs of 32.
     const int mt = ceil_div(sm.rows, BM);
     const int nt = kGateUp ? ceil_div(sm.kg, BN / 2) : ceil_div(d, BN);
     const int split = kGateUp ? 0 : local / (mt * nt);
@@ -439,10 +442,15 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
 
 // NSA = 3 (160 KB of LDS) except for the shared expert's side-stream
 // launches, which must leave room for the routing kernels beside them.
-template <int NSA>
+// XG = 32 when no side-stream launch runs at all: the L2 misses drop by 29 %
+// and the layer step by about 1 % (Mixtral and Qwen2-57B shapes); beside a
+// side-stream launch the longer runs were 0.5 % slower.  The down GEMM keeps
+// runs of 8: its segments' reductions differ, and longer runs left the XCDs
+// unevenly loaded at the end.
+template <int NSA, int XG>
 __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void gemm1_big_kernel(Gemm1Params<bf16_t> p) {
     __shared__ __attribute__((aligned(1024))) unsigned char smem[smem_bytes<NSA>()];
-    big_tile<true, 0, NSA>(p, Gemm2Params<bf16_t>{}, smem);
+    big_tile<true, 0, NSA, XG>(p, Gemm2Params<bf16_t>{}, smem);
 }
 
 // The gate/up GEMM of the training forward: the same tiles, plus the
@@ -467,11 +475,13 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void gemm2_big_kernel(Gemm
     big_tile<false, 0, NSA>(Gemm1Params<bf16_t>{}, p, smem);
 }
 
-hipError_t launch_gemm1_big(const Gemm1Params<bf16_t>& p, int grid, hipStream_t s, bool full_lds) {
+hipError_t launch_gemm1_big(const Gemm1Params<bf16_t>& p, int grid, hipStream_t s, bool full_lds, bool alone) {
     if (grid <= 0) return hipSuccess;
-    const int g = (grid + 8 * XCD_GROUP - 1) / (8 * XCD_GROUP) * (8 * XCD_GROUP);
-    if (full_lds) gemm1_big_kernel<3><<<g, THREADS, 0, s>>>(p);
-    else gemm1_big_kernel<2><<<g, THREADS, 0, s>>>(p);
+    const int xg = alone ? 32 : XCD_GROUP;
+    const int g = (grid + 8 * xg - 1) / (8 * xg) * (8 * xg);
+    if (alone) gemm1_big_kernel<3, 32><<<g, THREADS, 0, s>>>(p);
+    else if (full_lds) gemm1_big_kernel<3, XCD_GROUP><<<g, THREADS, 0, s>>>(p);
+    else gemm1_big_kernel<2, XCD_GROUP><<<g, THREADS, 0, s>>>(p);
     return hipGetLastError();
 }
 

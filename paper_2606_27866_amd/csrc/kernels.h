@@ -178,7 +178,8 @@ __global__ void set_keep_kernel(int32_t* keep, KeepArgs t, int E);
 // beside the routing kernels and would lock them out of the compute units;
 // the routed launches that follow the routing may (they and the side-stream
 // launches cannot share a compute unit's LDS either way).
-hipError_t launch_gemm1_big(const Gemm1Params<bf16_t>& p, int grid, hipStream_t s, bool full_lds);
+// alone (gate/up): no side-stream launch runs at all; implies full_lds.
+hipError_t launch_gemm1_big(const Gemm1Params<bf16_t>& p, int grid, hipStream_t s, bool full_lds, bool alone);
 hipError_t launch_gemm2_big(const Gemm2Params<bf16_t>& p, int grid, hipStream_t s, bool full_lds);
 // T <= kGemvMaxT: 16-wide tiles on the vector ALUs (gemv_decode.hip).
 hipError_t launch_gemm1_decode(const Gemm1Params<bf16_t>& p, int tiles, hipStream_t s);
