@@ -456,15 +456,15 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void gemm1_big_kernel(Gemm
 // The gate/up GEMM of the training forward: the same tiles, plus the
 // transposed g, u and h copies of the routed segments (Gemm1Params).
 __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void gemm1_big_train_kernel(Gemm1Params<bf16_t> p) {
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[smem_bytes<2>()];
-    big_tile<true, 1>(p, Gemm2Params<bf16_t>{}, smem);
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[smem_bytes<3>()];
+    big_tile<true, 1, 3>(p, Gemm2Params<bf16_t>{}, smem);
 }
 
 // The gate/up GEMM of the masked layer's training forward: the same tiles,
 // plus g and u of every row (Gemm1Params).
 __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void gemm1_big_train_rm_kernel(Gemm1Params<bf16_t> p) {
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[smem_bytes<2>()];
-    big_tile<true, 2>(p, Gemm2Params<bf16_t>{}, smem);
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[smem_bytes<3>()];
+    big_tile<true, 2, 3>(p, Gemm2Params<bf16_t>{}, smem);
 }
 
 // NSA = 3 as for the gate/up GEMM: the down GEMM's long reductions then run
