@@ -21,6 +21,8 @@
 //   wgrad: A = x^T or dO^T [d][ldt], B = dG^T, dU^T or h^T [I][ldt], with a
 //          segment's rows as K (columns prow0 .. prow0 + rows of the
 //          transposed copies, zero-padded to a multiple of 8).
+#include <type_traits>
+
 #include "mfma_tile.h"
 #include "saliency.h"
 #include "train.h"
@@ -43,7 +45,8 @@ constexpr int ROWS_PER_WAVE = BM / NWAVE;   // A rows (and B rows) each wave loa
 constexpr int NI = ROWS_PER_WAVE / RPI;     // DMA instructions per wave per operand
 constexpr int LOADS_PER_TILE = 2 * NI;
 constexpr int STAGE_A = BM * ROWB;
-constexpr int STAGE = STAGE_A + BN * ROWB;
+constexpr int STAGE_B = BN * ROWB;
+constexpr int STAGE = STAGE_A + STAGE_B;
 constexpr int XCD_GROUP = 8;
 static_assert(BM == kSalTile && BN == kSalTile, "host tile counts use kSalTile");
 
@@ -73,6 +76,19 @@ __device__ __forceinline__ void nt_rows(int wave, int lane, int row_base, int va
     }
 }
 
+// Tail of a K loop that needs nothing after its last K tile: zero-page loads
+// keep the count of outstanding DMAs the schedule waits on.
+struct ZeroTail {
+    __amdgpu_buffer_rsrc_t r;
+    __device__ __forceinline__ void operator()(int, unsigned char* sa, unsigned char* sb) const {
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            load_lds16(r, kOOB, 0, sa + i * RPI * ROWB);
+            load_lds16(r, kOOB, 0, sb + i * RPI * ROWB);
+        }
+    }
+};
+
 // The K loop of one tile whose waves multiply MFW 32-row A fragments each:
 // acc[i][j] = A rows wm*32*MFW + i*32 .. x B rows wn*WCOL + j*32 ...  The
 // schedule is the forward's (two LDS stages, fragments one step ahead).  The
@@ -82,7 +98,12 @@ __device__ __forceinline__ void nt_rows(int wave, int lane, int row_base, int va
 // kSwap: the A fragment is the MFMA's first operand (lane -> B row, registers
 // -> runs of 4 A rows); otherwise the B fragment is (lane -> A row, registers
 // -> runs of 4 B rows).  zero = false continues accumulating into acc.
-template <int MFW, bool kSwap = true, typename Tail>
+// kThreeA: three A stages and two B stages (all 160 KB of LDS; the A stages
+// first, then the B stages) instead of two combined stages; A tile kt+2 is
+// requested beside the first MFMA step of tile kt, so each barrier releases
+// only the B tile's DMAs (as in the forward GEMMs).  The K tiles past the
+// end are zero-page loads, so `tail` must be a ZeroTail.
+template <int MFW, bool kSwap = true, bool kThreeA = false, typename Tail>
 __device__ __forceinline__ void nt_mainloop(unsigned char* smem, const NTOperands& op, int wave, int lane,
                                             floatx16 (&acc)[MFW][NF], Tail&& tail, bool zero = true) {
     constexpr int WR = 32 * MFW;
@@ -118,8 +139,8 @@ __device__ __forceinline__ void nt_mainloop(unsigned char* smem, const NTOperand
     };
     bf16x8 a[2][MFW], b[2][NF];
     auto read_frags = [&](int kt, int ks, int buf) {
-        const unsigned char* sa = smem + (kt % NSTAGE) * STAGE;
-        const unsigned char* sb = sa + STAGE_A;
+        const unsigned char* sa = kThreeA ? smem + (kt % 3) * STAGE_A : smem + (kt % NSTAGE) * STAGE;
+        const unsigned char* sb = kThreeA ? smem + 3 * STAGE_A + (kt % 2) * STAGE_B : sa + STAGE_A;
         const int chunk = ks * 2 + (lane >> 5);
 #pragma unroll
         for (int i = 0; i < MFW; ++i) a[buf][i] = lds_frag(sa, wm * WR + i * 32 + (lane & 31), chunk);
@@ -134,43 +155,77 @@ __device__ __forceinline__ void nt_mainloop(unsigned char* smem, const NTOperand
                 acc[i][j] = kSwap ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][i], b[buf][j], acc[i][j], 0, 0, 0)
                                   : __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[buf][j], a[buf][i], acc[i][j], 0, 0, 0);
     };
-    issue(0, 0);
-    issue(1, 1);
-    __builtin_amdgcn_s_waitcnt(waitcnt_vm(LOADS_PER_TILE));
-    barrier_no_fence();
-    read_frags(0, 0, 0);
-    for (int kt = 0; kt < nk; ++kt) {
+    if constexpr (kThreeA) {
+        static_assert(std::is_same<std::decay_t<Tail>, ZeroTail>::value, "three A stages: zero-page tail only");
+        // DMA of K tile kt's A part into A stage kt % 3, or its B part into
+        // B stage kt % 2 (masked past K and past the end)
+        auto issue_part = [&](int kt, bool part_a) {
+            unsigned char* dst = (part_a ? smem + (kt % 3) * STAGE_A : smem + 3 * STAGE_A + (kt % 2) * STAGE_B) +
+                                 wave * ROWS_PER_WAVE * ROWB;
+            const int lim = op.K - kt * BK;
+            const uint32_t soff = (uint32_t)(kt * BK) * 2u;
 #pragma unroll
-        for (int st = 0; st < NSTEP - 1; ++st) {
-            read_frags(kt, st + 1, (st + 1) & 1);
-            mfma_step(st & 1);
-            sched_interleave<NMF, 0, NRD>();
+            for (int i = 0; i < NI; ++i) {
+                const bool kin = op.acol[i] < lim;
+                if (part_a) load_lds16(op.ra, kin ? op.aoff[i] : kOOB, soff, dst + i * RPI * ROWB);
+                else load_lds16(op.rb, kin ? op.boff[i] : kOOB, soff, dst + i * RPI * ROWB);
+            }
+        };
+        issue_part(0, true);
+        issue_part(0, false);
+        issue_part(1, true);
+        issue_part(1, false);
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * NI));  // tile 0 in
+        barrier_no_fence();
+        read_frags(0, 0, 0);
+        for (int kt = 0; kt < nk; ++kt) {
+            read_frags(kt, 1, 1);
+            issue_part(kt + 2, true);  // into the A stage of tile kt-1, free since the last barrier
+            mfma_step(0);
+            sched_interleave<NMF, NI, NRD>();
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int st = 1; st < NSTEP - 1; ++st) {
+                read_frags(kt, st + 1, (st + 1) & 1);
+                mfma_step(st & 1);
+                sched_interleave<NMF, 0, NRD>();
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            __builtin_amdgcn_s_waitcnt(waitcnt_vm(NI) & kWaitLgkm0);  // tile kt+1 in; own reads done
+            barrier_no_fence();
+            __builtin_amdgcn_sched_barrier(0);
+            issue_part(kt + 2, false);
+            read_frags(kt + 1, 0, 0);
+            mfma_step((NSTEP - 1) & 1);
+            sched_interleave<NMF, NI, NRD>();
             __builtin_amdgcn_sched_barrier(0);
         }
-        __builtin_amdgcn_s_waitcnt(waitcnt_vm(0) & kWaitLgkm0);
+    } else {
+        issue(0, 0);
+        issue(1, 1);
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm(LOADS_PER_TILE));
         barrier_no_fence();
-        __builtin_amdgcn_sched_barrier(0);
-        issue(kt + NSTAGE, kt % NSTAGE);
-        read_frags(kt + 1, 0, 0);
-        mfma_step((NSTEP - 1) & 1);
-        sched_interleave<NMF, LOADS_PER_TILE, NRD>();
-        __builtin_amdgcn_sched_barrier(0);
+        read_frags(0, 0, 0);
+        for (int kt = 0; kt < nk; ++kt) {
+#pragma unroll
+            for (int st = 0; st < NSTEP - 1; ++st) {
+                read_frags(kt, st + 1, (st + 1) & 1);
+                mfma_step(st & 1);
+                sched_interleave<NMF, 0, NRD>();
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            __builtin_amdgcn_s_waitcnt(waitcnt_vm(0) & kWaitLgkm0);
+            barrier_no_fence();
+            __builtin_amdgcn_sched_barrier(0);
+            issue(kt + NSTAGE, kt % NSTAGE);
+            read_frags(kt + 1, 0, 0);
+            mfma_step((NSTEP - 1) & 1);
+            sched_interleave<NMF, LOADS_PER_TILE, NRD>();
+            __builtin_amdgcn_sched_barrier(0);
+        }
     }
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // no DMA may outlive the workgroup's LDS
 }
-
-// Tail of a K loop that needs nothing after its last K tile: zero-page loads
-// keep the count of outstanding DMAs the schedule waits on.
-struct ZeroTail {
-    __amdgpu_buffer_rsrc_t r;
-    __device__ __forceinline__ void operator()(int, unsigned char* sa, unsigned char* sb) const {
-#pragma unroll
-        for (int i = 0; i < NI; ++i) {
-            load_lds16(r, kOOB, 0, sa + i * RPI * ROWB);
-            load_lds16(r, kOOB, 0, sb + i * RPI * ROWB);
-        }
-    }
-};
 
 // Runs `body` with the fragment count for a tile of `rows` A rows (the two
 // M-waves cover 64*MFW rows).
@@ -341,7 +396,9 @@ __device__ __forceinline__ bool train_tile(const SegMeta* seg, int hs, int nseg,
 //     padding rows -- for the weight-gradient GEMMs.
 constexpr int DG_PITCH = BN / 2 + 8;                  // staged row (bf16): 272 bytes, 16-byte aligned
 constexpr int DG_STAGE = BM * DG_PITCH * 2;           // one staged array
-constexpr int DG_SMEM = (2 * DG_STAGE > NSTAGE * STAGE) ? 2 * DG_STAGE : NSTAGE * STAGE;
+constexpr int SMEM3 = 3 * STAGE_A + 2 * STAGE_B;        // the K loop's LDS with three A stages
+static_assert(SMEM3 <= 160 * 1024, "three A stages and two B stages fit one compute unit");
+constexpr int DG_SMEM = (2 * DG_STAGE > SMEM3) ? 2 * DG_STAGE : SMEM3;
 constexpr int DG_TPITCH = BM + 8;                     // transposed staging row (bf16): 4 rows = 16 banks
 static_assert(2 * (BN / 2) * DG_TPITCH * 2 <= DG_SMEM, "the transposed staging fits");
 static_assert(DG_SMEM <= 160 * 1024, "the dgrad LDS fits one compute unit");
@@ -381,7 +438,7 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void dgrad_kernel(ActDgrad
     by_rows(sm.rows - mtile * BM, [&](auto tag) {
         constexpr int MFW = decltype(tag)::value;
         floatx16 acc[MFW][NF];
-        nt_mainloop<MFW, false>(smem, op, wave, lane, acc, ZeroTail{op.ra});
+        nt_mainloop<MFW, false, true>(smem, op, wave, lane, acc, ZeroTail{op.ra});
         // the stages are free once every wave is past its last fragment read
         __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
         barrier_no_fence();
@@ -488,7 +545,7 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void dgrad_kernel(ActDgrad
 // dX = dG W_gate + dU W_up over the kept channels; tile = 256 rows x 256
 // hidden units, two K loops into one accumulator.
 __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void act_dx_kernel(ActDxParams p) {
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[NSTAGE * STAGE];
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[SMEM3];
     SegMeta sm;
     int mtile, ntile;
     if (!train_tile(p.seg, p.hs, p.nseg, p.T, p.Is, p.nD, p.nD, xcd_tile(dgrad_group(p.nD)), sm, mtile, ntile))
@@ -522,11 +579,11 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void act_dx_kernel(ActDxPa
     by_rows(sm.rows - mtile * BM, [&](auto tag) {
         constexpr int MFW = decltype(tag)::value;
         floatx16 acc[MFW][NF];
-        nt_mainloop<MFW, false>(smem, og, wave, lane, acc, ZeroTail{og.ra});
+        nt_mainloop<MFW, false, true>(smem, og, wave, lane, acc, ZeroTail{og.ra});
         // every wave is past its last LDS read before the second loop refills the stages
         __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
         barrier_no_fence();
-        nt_mainloop<MFW, false>(smem, ou, wave, lane, acc, ZeroTail{ou.ra}, false);
+        nt_mainloop<MFW, false, true>(smem, ou, wave, lane, acc, ZeroTail{ou.ra}, false);
         // epilogue: lane -> row, registers -> runs of 4 hidden units
 #pragma unroll
         for (int i = 0; i < MFW; ++i) {
