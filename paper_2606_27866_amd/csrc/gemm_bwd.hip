@@ -47,6 +47,8 @@ constexpr int LOADS_PER_TILE = 2 * NI;
 constexpr int STAGE_A = BM * ROWB;
 constexpr int STAGE_B = BN * ROWB;
 constexpr int STAGE = STAGE_A + STAGE_B;
+constexpr int SMEM3 = 3 * STAGE_A + 2 * STAGE_B;  // the K loop's LDS with three A stages
+static_assert(SMEM3 <= 160 * 1024, "three A stages and two B stages fit one compute unit");
 constexpr int XCD_GROUP = 8;
 static_assert(BM == kSalTile && BN == kSalTile, "host tile counts use kSalTile");
 
@@ -87,6 +89,11 @@ struct ZeroTail {
             load_lds16(r, kOOB, 0, sb + i * RPI * ROWB);
         }
     }
+    // one part (A or B) of a K-tile slot past the end, with three A stages
+    __device__ __forceinline__ void operator()(int, bool, unsigned char* dst) const {
+#pragma unroll
+        for (int i = 0; i < NI; ++i) load_lds16(r, kOOB, 0, dst + i * RPI * ROWB);
+    }
 };
 
 // The K loop of one tile whose waves multiply MFW 32-row A fragments each:
@@ -101,8 +108,9 @@ struct ZeroTail {
 // kThreeA: three A stages and two B stages (all 160 KB of LDS; the A stages
 // first, then the B stages) instead of two combined stages; A tile kt+2 is
 // requested beside the first MFMA step of tile kt, so each barrier releases
-// only the B tile's DMAs (as in the forward GEMMs).  The K tiles past the
-// end are zero-page loads, so `tail` must be a ZeroTail.
+// only the B tile's DMAs (as in the forward GEMMs).  The slots past the end
+// then go to tail(h, part_a, dst) once per part: NI loads into this wave's
+// rows of A stage (nk + h) % 3 or of B stage (nk + h) % 2.
 template <int MFW, bool kSwap = true, bool kThreeA = false, typename Tail>
 __device__ __forceinline__ void nt_mainloop(unsigned char* smem, const NTOperands& op, int wave, int lane,
                                             floatx16 (&acc)[MFW][NF], Tail&& tail, bool zero = true) {
@@ -156,12 +164,15 @@ __device__ __forceinline__ void nt_mainloop(unsigned char* smem, const NTOperand
                                   : __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[buf][j], a[buf][i], acc[i][j], 0, 0, 0);
     };
     if constexpr (kThreeA) {
-        static_assert(std::is_same<std::decay_t<Tail>, ZeroTail>::value, "three A stages: zero-page tail only");
         // DMA of K tile kt's A part into A stage kt % 3, or its B part into
-        // B stage kt % 2 (masked past K and past the end)
+        // B stage kt % 2 (masked past K)
         auto issue_part = [&](int kt, bool part_a) {
             unsigned char* dst = (part_a ? smem + (kt % 3) * STAGE_A : smem + 3 * STAGE_A + (kt % 2) * STAGE_B) +
                                  wave * ROWS_PER_WAVE * ROWB;
+            if (kt >= nk) {
+                tail(kt - nk, part_a, dst);
+                return;
+            }
             const int lim = op.K - kt * BK;
             const uint32_t soff = (uint32_t)(kt * BK) * 2u;
 #pragma unroll
@@ -256,7 +267,7 @@ __device__ __forceinline__ float hi_bf16(uint32_t w) { return __uint_as_float(w 
 // ---- wgrad + saliency: one tile = 256 hidden units x 256 channels of one
 // (matrix, expert) ----------------------------------------------------------
 __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void sal_wgrad_kernel(SalWgradParams p) {
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[NSTAGE * STAGE];
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[SMEM3];
     // all tiles of one (matrix, expert) on one XCD: they share its x^T (or
     // dO^T) rows and its dG^T (dU^T, h^T) rows
     const int L = xcd_tile(p.nI * p.nM);
@@ -293,29 +304,29 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void sal_wgrad_kernel(SalW
     nt_rows(wave, lane, ntile * BN, p.I, p.ldt, op.boff, bcol);
 
     // theta = W[c][m] of the tile's 256 channels x 256 hidden units (gate, up
-    // or the transposed down weight), brought into the two operand stages by
-    // the loop's last two DMA slots, while its last K tiles are multiplied.
-    // Stage (nk + h) % 2 holds channels h*128 .. +128, one 512-byte row each,
-    // 16-byte chunk pos of row r holding hidden units 8 * (pos ^ (r % 32)) ..
+    // or the transposed down weight), brought into the operand stages by the
+    // loop's last two DMA slots, while its last K tiles are multiplied.
+    // Slot h holds channels h*128 .. +128, one 512-byte row each: rows 0..63
+    // in A stage (nk + h) % 3, rows 64..127 in B stage (nk + h) % 2; 16-byte
+    // chunk pos of row r holds hidden units 8 * (pos ^ (r % 32)) ..
     const bf16_t* W = p.w[mat] + (size_t)e * p.I * p.d;
     const __amdgpu_buffer_rsrc_t rw = make_rsrc(W, (size_t)p.I * p.d);
-    auto theta_tail = [&](int h, unsigned char* sa, unsigned char* sb) {
+    auto theta_tail = [&](int h, bool part_a, unsigned char* dst) {
+        const int part = part_a ? 0 : 1;
 #pragma unroll
-        for (int i = 0; i < NI; ++i)
-#pragma unroll
-            for (int part = 0; part < 2; ++part) {
-                const int tr = part * 64 + wave * 8 + 2 * i + (lane >> 5);  // theta row of the stage
-                const int c = ntile * BN + h * 128 + tr;
-                const int m = mtile * BM + ((lane & 31) ^ (tr & 31)) * 8;
-                const uint32_t off = c < p.I && m < p.d ? (uint32_t)(((size_t)c * p.d + m) * 2) : kOOB;
-                load_lds16(rw, off, 0, (part ? sb : sa) + i * RPI * ROWB);
-            }
+        for (int i = 0; i < NI; ++i) {
+            const int tr = part * 64 + wave * 8 + 2 * i + (lane >> 5);  // theta row of the slot
+            const int c = ntile * BN + h * 128 + tr;
+            const int m = mtile * BM + ((lane & 31) ^ (tr & 31)) * 8;
+            const uint32_t off = c < p.I && m < p.d ? (uint32_t)(((size_t)c * p.d + m) * 2) : kOOB;
+            load_lds16(rw, off, 0, dst + i * RPI * ROWB);
+        }
     };
     const int nk = ceil_div(op.K, BK);
     by_rows(p.d - mtile * BM, [&](auto tag) {
         constexpr int MFW = decltype(tag)::value;
         floatx16 acc[MFW][NF];
-        nt_mainloop<MFW>(smem, op, wave, lane, acc, theta_tail);
+        nt_mainloop<MFW, true, true>(smem, op, wave, lane, acc, theta_tail);
         barrier_no_fence();  // every wave's theta DMAs have landed
         // epilogue: lane -> channel c, register v -> hidden unit
         // 8(v/4) + 4(lane/32) + v%4 of a fragment; (theta * dW)^2 summed
@@ -324,7 +335,10 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void sal_wgrad_kernel(SalW
         for (int j = 0; j < NF; ++j) {
             part[j] = 0.f;
             const int cl = wn * WCOL + j * 32 + (lane & 31);  // channel within the tile
-            const unsigned char* trow = smem + ((nk + (cl >> 7)) & 1) * STAGE + (cl & 127) * 512;
+            const int h = cl >> 7, tr = cl & 127;
+            const unsigned char* trow = (tr < 64 ? smem + ((nk + h) % 3) * STAGE_A
+                                                 : smem + 3 * STAGE_A + ((nk + h) % 2) * STAGE_B) +
+                                        (tr & 63) * 512;
 #pragma unroll
             for (int i = 0; i < MFW; ++i)
 #pragma unroll
@@ -396,8 +410,6 @@ __device__ __forceinline__ bool train_tile(const SegMeta* seg, int hs, int nseg,
 //     padding rows -- for the weight-gradient GEMMs.
 constexpr int DG_PITCH = BN / 2 + 8;                  // staged row (bf16): 272 bytes, 16-byte aligned
 constexpr int DG_STAGE = BM * DG_PITCH * 2;           // one staged array
-constexpr int SMEM3 = 3 * STAGE_A + 2 * STAGE_B;        // the K loop's LDS with three A stages
-static_assert(SMEM3 <= 160 * 1024, "three A stages and two B stages fit one compute unit");
 constexpr int DG_SMEM = (2 * DG_STAGE > SMEM3) ? 2 * DG_STAGE : SMEM3;
 constexpr int DG_TPITCH = BM + 8;                     // transposed staging row (bf16): 4 rows = 16 banks
 static_assert(2 * (BN / 2) * DG_TPITCH * 2 <= DG_SMEM, "the transposed staging fits");
