@@ -12,8 +12,8 @@
 //
 // All are "NT" GEMMs: A rows and B rows are contiguous in K, staged by the
 // same LDS pipeline as the forward's big tiles (mfma_tile.h: 256 x 256 x 64
-// tiles, 8 waves as 2 x 4, direct-to-LDS DMA, two stages, fragments one step
-// ahead).  In the wgrad the MFMA takes the A fragment first, so a lane's
+// tiles, 8 waves as 2 x 4, direct-to-LDS DMA, three A and two B stages,
+// fragments one step ahead).  In the wgrad the MFMA takes the A fragment first, so a lane's
 // accumulator holds one B row (a channel) and runs of 4 consecutive A rows,
 // and the weight reads of its epilogue are 8-byte accesses.
 //   dgrad: A = dO [A][d] (a segment's rows), B = W_down^T [E][I][d] (a
@@ -37,16 +37,13 @@ constexpr int WAVES_PER_SIMD = NWAVE / 4;
 constexpr int WM = 2, WN = NWAVE / WM;      // wave grid
 constexpr int NF = BN / (WN * 32);          // 32-row B fragments per wave
 constexpr int WCOL = BN / WN;               // B rows per wave
-constexpr int NSTAGE = 2;
 constexpr int NSTEP = BK / 16;
 static_assert(NSTEP == 4, "the K-loop schedule is laid out for four steps per K tile");
 constexpr int RPI = 64 / CHUNKS;            // LDS rows filled per DMA instruction
 constexpr int ROWS_PER_WAVE = BM / NWAVE;   // A rows (and B rows) each wave loads
 constexpr int NI = ROWS_PER_WAVE / RPI;     // DMA instructions per wave per operand
-constexpr int LOADS_PER_TILE = 2 * NI;
 constexpr int STAGE_A = BM * ROWB;
 constexpr int STAGE_B = BN * ROWB;
-constexpr int STAGE = STAGE_A + STAGE_B;
 constexpr int SMEM3 = 3 * STAGE_A + 2 * STAGE_B;  // the K loop's LDS with three A stages
 static_assert(SMEM3 <= 160 * 1024, "three A stages and two B stages fit one compute unit");
 constexpr int XCD_GROUP = 8;
@@ -82,14 +79,7 @@ __device__ __forceinline__ void nt_rows(int wave, int lane, int row_base, int va
 // keep the count of outstanding DMAs the schedule waits on.
 struct ZeroTail {
     __amdgpu_buffer_rsrc_t r;
-    __device__ __forceinline__ void operator()(int, unsigned char* sa, unsigned char* sb) const {
-#pragma unroll
-        for (int i = 0; i < NI; ++i) {
-            load_lds16(r, kOOB, 0, sa + i * RPI * ROWB);
-            load_lds16(r, kOOB, 0, sb + i * RPI * ROWB);
-        }
-    }
-    // one part (A or B) of a K-tile slot past the end, with three A stages
+    // one part (A or B) of a K-tile slot past the end
     __device__ __forceinline__ void operator()(int, bool, unsigned char* dst) const {
 #pragma unroll
         for (int i = 0; i < NI; ++i) load_lds16(r, kOOB, 0, dst + i * RPI * ROWB);
@@ -98,20 +88,17 @@ struct ZeroTail {
 
 // The K loop of one tile whose waves multiply MFW 32-row A fragments each:
 // acc[i][j] = A rows wm*32*MFW + i*32 .. x B rows wn*WCOL + j*32 ...  The
-// schedule is the forward's (two LDS stages, fragments one step ahead).  The
-// last two DMA slots of the loop (K tiles nk and nk+1, past the end) go to
-// tail(h, sa, sb) for h = 0, 1, which must issue exactly NI loads into each
-// of this wave's A and B parts of the freed stage (nk + h) % 2.
+// schedule is the forward's: three A stages and two B stages (all 160 KB of
+// LDS; the A stages first, then the B stages), fragments read one step ahead,
+// A tile kt+2 requested beside the first MFMA step of tile kt, so each
+// barrier releases only the B tile's DMAs.  The last two DMA slots of each
+// part (K tiles nk and nk+1, past the end) go to tail(h, part_a, dst) for
+// h = 0, 1, which must issue exactly NI loads into this wave's rows `dst` of
+// A stage (nk + h) % 3 or of B stage (nk + h) % 2.
 // kSwap: the A fragment is the MFMA's first operand (lane -> B row, registers
 // -> runs of 4 A rows); otherwise the B fragment is (lane -> A row, registers
 // -> runs of 4 B rows).  zero = false continues accumulating into acc.
-// kThreeA: three A stages and two B stages (all 160 KB of LDS; the A stages
-// first, then the B stages) instead of two combined stages; A tile kt+2 is
-// requested beside the first MFMA step of tile kt, so each barrier releases
-// only the B tile's DMAs (as in the forward GEMMs).  The slots past the end
-// then go to tail(h, part_a, dst) once per part: NI loads into this wave's
-// rows of A stage (nk + h) % 3 or of B stage (nk + h) % 2.
-template <int MFW, bool kSwap = true, bool kThreeA = false, typename Tail>
+template <int MFW, bool kSwap = true, typename Tail>
 __device__ __forceinline__ void nt_mainloop(unsigned char* smem, const NTOperands& op, int wave, int lane,
                                             floatx16 (&acc)[MFW][NF], Tail&& tail, bool zero = true) {
     constexpr int WR = 32 * MFW;
@@ -128,27 +115,10 @@ __device__ __forceinline__ void nt_mainloop(unsigned char* smem, const NTOperand
     }
 
     const int nk = ceil_div(op.K, BK);
-    auto issue = [&](int kt, int stage) {
-        unsigned char* sa = smem + stage * STAGE + wave * ROWS_PER_WAVE * ROWB;
-        unsigned char* sb = sa + STAGE_A;
-        if (kt >= nk) {
-            tail(kt - nk, sa, sb);
-            return;
-        }
-        const int k0 = kt * BK;
-        const int lim = op.K - k0;
-        const uint32_t soff = (uint32_t)k0 * 2u;
-#pragma unroll
-        for (int i = 0; i < NI; ++i) {
-            const bool kin = op.acol[i] < lim;
-            load_lds16(op.ra, kin ? op.aoff[i] : kOOB, soff, sa + i * RPI * ROWB);
-            load_lds16(op.rb, kin ? op.boff[i] : kOOB, soff, sb + i * RPI * ROWB);
-        }
-    };
     bf16x8 a[2][MFW], b[2][NF];
     auto read_frags = [&](int kt, int ks, int buf) {
-        const unsigned char* sa = kThreeA ? smem + (kt % 3) * STAGE_A : smem + (kt % NSTAGE) * STAGE;
-        const unsigned char* sb = kThreeA ? smem + 3 * STAGE_A + (kt % 2) * STAGE_B : sa + STAGE_A;
+        const unsigned char* sa = smem + (kt % 3) * STAGE_A;
+        const unsigned char* sb = smem + 3 * STAGE_A + (kt % 2) * STAGE_B;
         const int chunk = ks * 2 + (lane >> 5);
 #pragma unroll
         for (int i = 0; i < MFW; ++i) a[buf][i] = lds_frag(sa, wm * WR + i * 32 + (lane & 31), chunk);
@@ -163,77 +133,52 @@ __device__ __forceinline__ void nt_mainloop(unsigned char* smem, const NTOperand
                 acc[i][j] = kSwap ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][i], b[buf][j], acc[i][j], 0, 0, 0)
                                   : __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[buf][j], a[buf][i], acc[i][j], 0, 0, 0);
     };
-    if constexpr (kThreeA) {
-        // DMA of K tile kt's A part into A stage kt % 3, or its B part into
-        // B stage kt % 2 (masked past K)
-        auto issue_part = [&](int kt, bool part_a) {
-            unsigned char* dst = (part_a ? smem + (kt % 3) * STAGE_A : smem + 3 * STAGE_A + (kt % 2) * STAGE_B) +
-                                 wave * ROWS_PER_WAVE * ROWB;
-            if (kt >= nk) {
-                tail(kt - nk, part_a, dst);
-                return;
-            }
-            const int lim = op.K - kt * BK;
-            const uint32_t soff = (uint32_t)(kt * BK) * 2u;
+    // DMA of K tile kt's A part into A stage kt % 3, or its B part into
+    // B stage kt % 2 (masked past K)
+    auto issue_part = [&](int kt, bool part_a) {
+        unsigned char* dst = (part_a ? smem + (kt % 3) * STAGE_A : smem + 3 * STAGE_A + (kt % 2) * STAGE_B) +
+                             wave * ROWS_PER_WAVE * ROWB;
+        if (kt >= nk) {
+            tail(kt - nk, part_a, dst);
+            return;
+        }
+        const int lim = op.K - kt * BK;
+        const uint32_t soff = (uint32_t)(kt * BK) * 2u;
 #pragma unroll
-            for (int i = 0; i < NI; ++i) {
-                const bool kin = op.acol[i] < lim;
-                if (part_a) load_lds16(op.ra, kin ? op.aoff[i] : kOOB, soff, dst + i * RPI * ROWB);
-                else load_lds16(op.rb, kin ? op.boff[i] : kOOB, soff, dst + i * RPI * ROWB);
-            }
-        };
-        issue_part(0, true);
-        issue_part(0, false);
-        issue_part(1, true);
-        issue_part(1, false);
-        __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * NI));  // tile 0 in
-        barrier_no_fence();
-        read_frags(0, 0, 0);
-        for (int kt = 0; kt < nk; ++kt) {
-            read_frags(kt, 1, 1);
-            issue_part(kt + 2, true);  // into the A stage of tile kt-1, free since the last barrier
-            mfma_step(0);
-            sched_interleave<NMF, NI, NRD>();
-            __builtin_amdgcn_sched_barrier(0);
+        for (int i = 0; i < NI; ++i) {
+            const bool kin = op.acol[i] < lim;
+            if (part_a) load_lds16(op.ra, kin ? op.aoff[i] : kOOB, soff, dst + i * RPI * ROWB);
+            else load_lds16(op.rb, kin ? op.boff[i] : kOOB, soff, dst + i * RPI * ROWB);
+        }
+    };
+    issue_part(0, true);
+    issue_part(0, false);
+    issue_part(1, true);
+    issue_part(1, false);
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * NI));  // tile 0 in
+    barrier_no_fence();
+    read_frags(0, 0, 0);
+    for (int kt = 0; kt < nk; ++kt) {
+        read_frags(kt, 1, 1);
+        issue_part(kt + 2, true);  // into the A stage of tile kt-1, free since the last barrier
+        mfma_step(0);
+        sched_interleave<NMF, NI, NRD>();
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int st = 1; st < NSTEP - 1; ++st) {
-                read_frags(kt, st + 1, (st + 1) & 1);
-                mfma_step(st & 1);
-                sched_interleave<NMF, 0, NRD>();
-                __builtin_amdgcn_sched_barrier(0);
-            }
-            __builtin_amdgcn_s_waitcnt(waitcnt_vm(NI) & kWaitLgkm0);  // tile kt+1 in; own reads done
-            barrier_no_fence();
-            __builtin_amdgcn_sched_barrier(0);
-            issue_part(kt + 2, false);
-            read_frags(kt + 1, 0, 0);
-            mfma_step((NSTEP - 1) & 1);
-            sched_interleave<NMF, NI, NRD>();
+        for (int st = 1; st < NSTEP - 1; ++st) {
+            read_frags(kt, st + 1, (st + 1) & 1);
+            mfma_step(st & 1);
+            sched_interleave<NMF, 0, NRD>();
             __builtin_amdgcn_sched_barrier(0);
         }
-    } else {
-        issue(0, 0);
-        issue(1, 1);
-        __builtin_amdgcn_s_waitcnt(waitcnt_vm(LOADS_PER_TILE));
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm(NI) & kWaitLgkm0);  // tile kt+1 in; own reads done
         barrier_no_fence();
-        read_frags(0, 0, 0);
-        for (int kt = 0; kt < nk; ++kt) {
-#pragma unroll
-            for (int st = 0; st < NSTEP - 1; ++st) {
-                read_frags(kt, st + 1, (st + 1) & 1);
-                mfma_step(st & 1);
-                sched_interleave<NMF, 0, NRD>();
-                __builtin_amdgcn_sched_barrier(0);
-            }
-            __builtin_amdgcn_s_waitcnt(waitcnt_vm(0) & kWaitLgkm0);
-            barrier_no_fence();
-            __builtin_amdgcn_sched_barrier(0);
-            issue(kt + NSTAGE, kt % NSTAGE);
-            read_frags(kt + 1, 0, 0);
-            mfma_step((NSTEP - 1) & 1);
-            sched_interleave<NMF, LOADS_PER_TILE, NRD>();
-            __builtin_amdgcn_sched_barrier(0);
-        }
+        __builtin_amdgcn_sched_barrier(0);
+        issue_part(kt + 2, false);
+        read_frags(kt + 1, 0, 0);
+        mfma_step((NSTEP - 1) & 1);
+        sched_interleave<NMF, NI, NRD>();
+        __builtin_amdgcn_sched_barrier(0);
     }
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // no DMA may outlive the workgroup's LDS
 }
@@ -326,7 +271,7 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void sal_wgrad_kernel(SalW
     by_rows(p.d - mtile * BM, [&](auto tag) {
         constexpr int MFW = decltype(tag)::value;
         floatx16 acc[MFW][NF];
-        nt_mainloop<MFW, true, true>(smem, op, wave, lane, acc, theta_tail);
+        nt_mainloop<MFW, true>(smem, op, wave, lane, acc, theta_tail);
         barrier_no_fence();  // every wave's theta DMAs have landed
         // epilogue: lane -> channel c, register v -> hidden unit
         // 8(v/4) + 4(lane/32) + v%4 of a fragment; (theta * dW)^2 summed
@@ -450,7 +395,7 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void dgrad_kernel(ActDgrad
     by_rows(sm.rows - mtile * BM, [&](auto tag) {
         constexpr int MFW = decltype(tag)::value;
         floatx16 acc[MFW][NF];
-        nt_mainloop<MFW, false, true>(smem, op, wave, lane, acc, ZeroTail{op.ra});
+        nt_mainloop<MFW, false>(smem, op, wave, lane, acc, ZeroTail{op.ra});
         // the stages are free once every wave is past its last fragment read
         __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
         barrier_no_fence();
@@ -591,11 +536,11 @@ __global__ __launch_bounds__(THREADS, WAVES_PER_SIMD) void act_dx_kernel(ActDxPa
     by_rows(sm.rows - mtile * BM, [&](auto tag) {
         constexpr int MFW = decltype(tag)::value;
         floatx16 acc[MFW][NF];
-        nt_mainloop<MFW, false, true>(smem, og, wave, lane, acc, ZeroTail{og.ra});
+        nt_mainloop<MFW, false>(smem, og, wave, lane, acc, ZeroTail{og.ra});
         // every wave is past its last LDS read before the second loop refills the stages
         __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
         barrier_no_fence();
-        nt_mainloop<MFW, false, true>(smem, ou, wave, lane, acc, ZeroTail{ou.ra}, false);
+        nt_mainloop<MFW, false>(smem, ou, wave, lane, acc, ZeroTail{ou.ra}, false);
         // epilogue: lane -> row, registers -> runs of 4 hidden units
 #pragma unroll
         for (int i = 0; i < MFW; ++i) {
