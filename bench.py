@@ -104,10 +104,17 @@ def parse(argv=None):
     return ap.parse_args(argv)
 
 
-def kernel_src_hash():
+def kernel_src_hash(read=None):
+    """Hash of the gate/up kernels' sources with // comments and blank lines
+    removed, so that an edit of a comment keeps the counter records valid.
+    `read(name)` returns a file's text (default: the working tree)."""
+    read = read or (lambda f: open(os.path.join(ROOT, "paper_2606_27866_amd", "csrc", f)).read())
     h = hashlib.sha256()
     for f in ("gemm_bf16_big.hip", "gemm_decode.hip", "gemv_decode.hip", "common.h", "kernels.h", "mfma_tile.h"):
-        h.update(open(os.path.join(ROOT, "paper_2606_27866_amd", "csrc", f), "rb").read())
+        for line in read(f).splitlines():
+            code = line.split("//", 1)[0].rstrip()
+            if code:
+                h.update(code.encode() + b"\n")
     return h.hexdigest()[:16]
 
 

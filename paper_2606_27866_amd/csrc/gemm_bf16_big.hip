@@ -29,10 +29,10 @@
 //   - tiles are numbered segment-major (shared expert first: its reductions
 //     are the longest), inside a segment in groups of four row tiles (all
 //     columns of a group, a column's row tiles consecutive); runs of 8
-//     consecutive tiles go to one XCD (workgroup b runs on XCD b % 8),
-//     interleaving the XCDs every 8 tiles, so that the tiles an XCD runs at
-//     once share token-row and weight panels in its L2 while the work stays
-//     balanced.
+//     consecutive tiles (32 for a gate/up launch with no concurrent launch
+//     beside it) go to one XCD (workgroup b runs on XCD b % 8), interleaving
+//     the XCDs run by run, so that the tiles an XCD runs at once share
+//     token-row and weight panels in its L2 while the work stays balanced.
 // gate/up: a workgroup tile is 256 rows x 128 channels; its B tile holds the
 //   128 gate rows then the 128 up rows of those channels, and wave (wm, wn)
 //   multiplies gate rows [wn*32, wn*32+32) and the matching up rows, so the

@@ -108,6 +108,25 @@ def test_traffic_record_is_used_only_for_the_same_kernels_table_and_T(tmp_path, 
     assert bench.load_traffic("qwen15_moe_a27b", 4096, "own") == expect
 
 
+def test_kernel_hash_ignores_comments_but_not_code():
+    """A comment edit keeps the counter records valid; a code edit does not."""
+    src = {}
+
+    def read(f):
+        if f not in src:
+            src[f] = open(os.path.join(bench.ROOT, "paper_2606_27866_amd", "csrc", f)).read()
+        return src[f]
+
+    base = bench.kernel_src_hash(read)
+    assert base == bench.kernel_src_hash()
+    text = read("gemm_bf16_big.hip")
+    src["gemm_bf16_big.hip"] = "// a new comment line\n\n" + text.replace("namespace flexmoe {", "namespace flexmoe {  // note", 1)
+    assert bench.kernel_src_hash(read) == base
+    src["gemm_bf16_big.hip"] = text.replace("constexpr int NSB = 2;", "constexpr int NSB = 3;", 1)
+    assert src["gemm_bf16_big.hip"] != text
+    assert bench.kernel_src_hash(read) != base
+
+
 def test_missing_traffic_record_gives_null(tmp_path, monkeypatch):
     monkeypatch.setattr(bench, "traffic_file", lambda workload, T: str(tmp_path / "absent.json"))
     assert bench.load_traffic("qwen15_moe_a27b", 4096, "own") is None
