@@ -718,7 +718,7 @@ def action_section(wl, args):
     out = dict(tokens=T, steps_timed=steps, ms_per_step=ms_s, tokens_per_s=T / (ms_s / 1e3),
                tflops=f_all / (ms_s / 1e3) / 1e12, frac_mfma=f_all / (ms_s / 1e3) / 1e12 / PEAK_BF16_TFLOPS,
                flops_per_step=f_all, mean_kept_fraction=nk / A_I, ratios=list(ratios),
-               roofline_dgrad=dict(kernel="dgrad + SwiGLU backward + mask gradient (act_dgrad_kernel)",
+               roofline_dgrad=dict(kernel="dgrad + SwiGLU backward + mask gradient (dgrad_kernel<2>)",
                                    bound="mfma", achieved=f_dgrad / (dg_ms / 1e3) / 1e12, peak=PEAK_BF16_TFLOPS,
                                    unit="TFLOP/s", frac=f_dgrad / (dg_ms / 1e3) / 1e12 / PEAK_BF16_TFLOPS,
                                    avg_launch_ms=dg_ms, flops_per_launch=f_dgrad),
