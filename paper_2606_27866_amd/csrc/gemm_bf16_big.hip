@@ -185,19 +185,27 @@ __device__ __forceinline__ void big_tile(const Gemm1Params<bf16_t>& p1, const Ge
         const bf16_t* W = (wave * ROWS_PER_WAVE < BN / 2 ? (shared ? p1.sg : p1.wg) : (shared ? p1.su : p1.wu)) + rw.base;
         ra = make_rsrc(p1.x, (size_t)p1.tokens * d);
         rb = make_rsrc(W, (size_t)rw.rows * d);
+        // token of each A row: every lane loads its rows' entries of the
+        // permutation (rows past the segment read its last row's, unused), so
+        // the NI loads are in flight together rather than one after another
+        int tok[NI];
+        const int row_l = mtile * BM + wave * ROWS_PER_WAVE + lane / CHUNKS;
+        if (shared) {
+#pragma unroll
+            for (int i = 0; i < NI; ++i) tok[i] = row_l + i * RPI;
+        } else {
+            const int32_t* pr = p1.perm + sm.row0;
+#pragma unroll
+            for (int i = 0; i < NI; ++i) tok[i] = pr[min(row_l + i * RPI, sm.rows - 1)];
+        }
 #pragma unroll
         for (int i = 0; i < NI; ++i) {
             const int r = wave * ROWS_PER_WAVE + i * RPI + lane / CHUNKS;
             const int row = mtile * BM + r;
             const int c = swz(r, pos) * 8;
             acol[i] = c;
-            aoff[i] = kOOB;
-            if (row < sm.rows) {
-                const int t = shared ? row
-                                     : (int)min((unsigned)(p1.perm[sm.row0 + row] / p1.top_k),
-                                                (unsigned)(p1.tokens - 1));
-                aoff[i] = (uint32_t)(((size_t)t * d + c) * 2);
-            }
+            const int t = shared ? tok[i] : (int)min((unsigned)(tok[i] / p1.top_k), (unsigned)(p1.tokens - 1));
+            aoff[i] = row < sm.rows ? (uint32_t)(((size_t)t * d + c) * 2) : kOOB;
             const int ch = ntile * (BN / 2) + (r & (BN / 2 - 1));
             boff[i] = ch < sm.kg ? (uint32_t)(((size_t)ch * d + c) * 2) : kOOB;
         }

@@ -120,18 +120,25 @@ __device__ __forceinline__ void wide_tile(const Gemm1Params<bf16_t>& p1, const G
     const int pos = lane % WCHUNKS;
     uint32_t aoff[NDMA], woff[WW_DMA];
     int acol[NDMA], wcol[WW_DMA];
+    // source row of each token row: the routed gate/up rows are gathered
+    // through perm; every lane loads its entries (rows past the segment read
+    // its last row's, unused), so the NDMA loads are in flight together
+    int src[NDMA];
+#pragma unroll
+    for (int i = 0; i < NDMA; ++i) src[i] = WRPI * (wave * NDMA + i) + lane / WCHUNKS;
+    if (kGateUp && !shared) {
+        const int32_t* pr = p1.perm + sm.row0;
+#pragma unroll
+        for (int i = 0; i < NDMA; ++i) src[i] = pr[max(min(src[i], R - 1), 0)];
+#pragma unroll
+        for (int i = 0; i < NDMA; ++i) src[i] = (int)min((unsigned)(src[i] / p1.top_k), (unsigned)(p1.tokens - 1));
+    }
 #pragma unroll
     for (int i = 0; i < NDMA; ++i) {
         const int r = WRPI * (wave * NDMA + i) + lane / WCHUNKS;
         const int c = pos ^ (r & 15);
         acol[i] = c * 8;
-        aoff[i] = kOOB;
-        if (r < R) {
-            int src = r;
-            if (kGateUp && !shared)
-                src = (int)min((unsigned)(p1.perm[sm.row0 + r] / p1.top_k), (unsigned)(p1.tokens - 1));
-            aoff[i] = (uint32_t)(((size_t)src * lda + c * 8) * 2);
-        }
+        aoff[i] = r < R ? (uint32_t)(((size_t)src[i] * lda + c * 8) * 2) : kOOB;
     }
 #pragma unroll
     for (int i = 0; i < WW_DMA; ++i) {

@@ -136,12 +136,21 @@ __global__ __launch_bounds__(64 * GV_WAVES, NR <= 2 ? 4 : NR == 4 ? 3 : 2) void 
     // byte offsets of the lane's chunk of batch 0 (the batch start is the
     // scalar offset); kOOB (the load returns zeros) for rows past the GEMM
     uint32_t xoff[NR], woff[GV_NI];
+    // token of each row: routed rows are gathered through perm, all NR
+    // entries requested together (rows past the segment read its last
+    // row's, unused)
+    int tok[NR];
 #pragma unroll
-    for (int r = 0; r < NR; ++r) {
-        const int t = shared ? r : (int)min((unsigned)(p.perm[sm.row0 + max(min(r, R - 1), 0)] / p.top_k),
-                                            (unsigned)(p.tokens - 1));
-        xoff[r] = r < R ? (uint32_t)(((size_t)t * d + ck) * 2) : kOOB;
+    for (int r = 0; r < NR; ++r) tok[r] = r;
+    if (!shared) {
+        const int32_t* pr = p.perm + sm.row0;
+#pragma unroll
+        for (int r = 0; r < NR; ++r) tok[r] = pr[max(min(r, R - 1), 0)];
+#pragma unroll
+        for (int r = 0; r < NR; ++r) tok[r] = (int)min((unsigned)(tok[r] / p.top_k), (unsigned)(p.tokens - 1));
     }
+#pragma unroll
+    for (int r = 0; r < NR; ++r) xoff[r] = r < R ? (uint32_t)(((size_t)tok[r] * d + ck) * 2) : kOOB;
 #pragma unroll
     for (int i = 0; i < GV_NI; ++i) {
         const int c = ntile * GV_ROWS + 2 * i + half;  // channel; the GEMM computes c < kg

@@ -116,8 +116,14 @@ template <typename P>
 __device__ __forceinline__ bool tile_of(const P& p, int L, int& s, SegMeta& sm, int& local) {
     if (p.part == kPartShared) {
         if (L >= p.shared_tiles) return false;
+        // the argument values are pinned in scalar registers here: otherwise
+        // the compiler may merge the read of `tokens` with the routed path's
+        // read of seg[s].rows into one generic (flat) load, one more memory
+        // round trip at the start of every tile
+        int tokens = p.tokens, is = p.Is;
+        asm volatile("" : "+s"(tokens), "+s"(is));
         s = 0;
-        sm = SegMeta{0, p.tokens, p.Is, 0, p.Is, -1, 0, 0};
+        sm = SegMeta{0, tokens, is, 0, is, -1, 0, 0};
         local = L;
         return true;
     }
