@@ -71,7 +71,7 @@ def test_workspace_monotone_in_T():
 
 
 @pytest.mark.parametrize("shape", [
-    dict(d=2048, E=60, I=1408, top_k=4, I_shared=5632),   # split at T < 8193
+    dict(d=2048, E=60, I=1408, top_k=4, I_shared=5632),   # split at T <= 3840
     dict(d=256, E=8, I=128, top_k=2, I_shared=3080),      # split 3 ways, ragged chunk
     dict(d=4096, E=8, I=14336, top_k=2, I_shared=0),
     dict(d=256, E=8, I=128, top_k=2, I_shared=3080, dtype=fm.FLEXMOE_F32),
