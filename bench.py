@@ -36,6 +36,8 @@ the device channel saliency of Eq. 2 and one action-learning step).
 reaches on the same GPU.
 """
 import argparse
+import contextlib
+import gc
 import hashlib
 import json
 import os
@@ -102,6 +104,21 @@ def parse(argv=None):
                     help="after timing, copy this many MiB device-to-device once, so that a "
                          "counter run sees a plain copy of known size (HBM byte calibration)")
     return ap.parse_args(argv)
+
+
+@contextlib.contextmanager
+def no_gc():
+    """Run a timed region with Python's cyclic garbage collector paused, as
+    the standard library's timeit does: a full collection inside a loop of
+    decode-sized steps stalls the host that feeds the GPU for milliseconds,
+    and the GPU idles meanwhile."""
+    was = gc.isenabled()
+    gc.disable()
+    try:
+        yield
+    finally:
+        if was:
+            gc.enable()
 
 
 def kernel_src_hash(read=None):
@@ -255,11 +272,12 @@ class Workload:
         torch.cuda.synchronize()
         ev0 = torch.cuda.Event(enable_timing=True)
         ev1 = torch.cuda.Event(enable_timing=True)
-        ev0.record()
-        for i in range(steps):
-            self._step(i, keep_names, mode)
-        ev1.record()
-        torch.cuda.synchronize()
+        with no_gc():
+            ev0.record()
+            for i in range(steps):
+                self._step(i, keep_names, mode)
+            ev1.record()
+            torch.cuda.synchronize()
         ms = ev0.elapsed_time(ev1)
         kt = None
         if with_kernel_times:
@@ -273,11 +291,12 @@ class Workload:
         mode = mode or ("upload" if len(keep_names) > 1 else "fixed")
         torch.cuda.synchronize()
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
-        for i in range(steps):
-            ev[i].record()
-            self._step(i, keep_names, mode)
-        ev[steps].record()
-        torch.cuda.synchronize()
+        with no_gc():
+            for i in range(steps):
+                ev[i].record()
+                self._step(i, keep_names, mode)
+            ev[steps].record()
+            torch.cuda.synchronize()
         return [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
 
     def warm(self, args, keep_names, mode=None, min_steps=None, warm_s=None):
@@ -315,11 +334,12 @@ class Workload:
         torch.cuda.synchronize()
         ev0 = torch.cuda.Event(enable_timing=True)
         ev1 = torch.cuda.Event(enable_timing=True)
-        ev0.record()
-        for i in range(steps):
-            self.graphs[i % len(self.graphs)].replay()
-        ev1.record()
-        torch.cuda.synchronize()
+        with no_gc():
+            ev0.record()
+            for i in range(steps):
+                self.graphs[i % len(self.graphs)].replay()
+            ev1.record()
+            torch.cuda.synchronize()
         return ev0.elapsed_time(ev1)
 
     def run_bucketed(self, steps, table_name, k_align):
@@ -330,13 +350,14 @@ class Workload:
         torch.cuda.synchronize()
         ev0 = torch.cuda.Event(enable_timing=True)
         ev1 = torch.cuda.Event(enable_timing=True)
-        ev0.record()
-        for i in range(steps):
-            self.use_copy(i)
-            x, lg = self.xd[i % len(self.xd)]
-            self.layer.forward(x, lg, y=self.y, bucketed=(keep, k_align))
-        ev1.record()
-        torch.cuda.synchronize()
+        with no_gc():
+            ev0.record()
+            for i in range(steps):
+                self.use_copy(i)
+                x, lg = self.xd[i % len(self.xd)]
+                self.layer.forward(x, lg, y=self.y, bucketed=(keep, k_align))
+            ev1.record()
+            torch.cuda.synchronize()
         return ev0.elapsed_time(ev1)
 
     def export_clipped(self, table_name):
@@ -355,13 +376,14 @@ class Workload:
         torch.cuda.synchronize()
         ev0 = torch.cuda.Event(enable_timing=True)
         ev1 = torch.cuda.Event(enable_timing=True)
-        ev0.record()
-        for i in range(steps):
-            self.use_copy(i)  # shared expert of this copy
-            x, lg = self.xd[i % len(self.xd)]
-            self.layer.forward(x, lg, y=self.y, clipped=cws[i % len(cws)])
-        ev1.record()
-        torch.cuda.synchronize()
+        with no_gc():
+            ev0.record()
+            for i in range(steps):
+                self.use_copy(i)  # shared expert of this copy
+                x, lg = self.xd[i % len(self.xd)]
+                self.layer.forward(x, lg, y=self.y, clipped=cws[i % len(cws)])
+            ev1.record()
+            torch.cuda.synchronize()
         return ev0.elapsed_time(ev1)
 
     def release(self):
@@ -858,18 +880,20 @@ def decode_section(args):
         # host latency of one flexmoe_set_budget call through the binding
         torch.cuda.synchronize()
         nh = 500
-        h0 = time.perf_counter()
-        for i in range(nh):
-            wl.layer.set_budget(wl.tables[names[i % len(names)]])
-        host_us = (time.perf_counter() - h0) / nh * 1e6
-        torch.cuda.synchronize()
+        with no_gc():
+            h0 = time.perf_counter()
+            for i in range(nh):
+                wl.layer.set_budget(wl.tables[names[i % len(names)]])
+            host_us = (time.perf_counter() - h0) / nh * 1e6
+            torch.cuda.synchronize()
         # GPU time of the upload kernel: a burst of launches on an idle stream
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for i in range(nh):
-            wl.layer.set_budget(wl.tables[names[i % len(names)]])
-        e1.record()
-        torch.cuda.synchronize()
+        with no_gc():
+            e0.record()
+            for i in range(nh):
+                wl.layer.set_budget(wl.tables[names[i % len(names)]])
+            e1.record()
+            torch.cuda.synchronize()
         gpu_us = e0.elapsed_time(e1) / nh * 1e3
         cost = dict(set_budget_host_us=host_us, set_keep_kernel_gpu_us_burst=gpu_us,
                     cycling_minus_fixed_us=(sw["step_ms"]["median"] - fixed_med) * 1e3,
