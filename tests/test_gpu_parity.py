@@ -92,6 +92,9 @@ MINIS = [
     # chunks (2 of 1024 channels; 3 of 1088, 1088 and 904)
     ("m_shared_split2", 300, 256, 8, 128, 2, 2048, 1),
     ("m_shared_split3", 200, 128, 4, 64, 2, 3080, 0),
+    # 10 chunks of 1024: the combine adds the shared row sets in two batches
+    # of 8 (the prefill combine's top-2 variant)
+    ("m_shared_split10", 200, 128, 4, 64, 2, 10240, 1),
     # a shared expert with 16 x 64 = 1024 gate/up tiles fills the GPU on its
     # own: it runs as segment 0 of the routed experts' launches (no side
     # stream), and its down reduction is split into 8 chunks
